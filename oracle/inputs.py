@@ -1,0 +1,82 @@
+"""Host-side inputs for the oracle, regenerated from the seeded generator package.
+
+TEST INFRASTRUCTURE ONLY (see kvprm_oracle). Every tensor is produced by
+``synth`` on the host from (seed, stream, element index) and decoded exactly to
+float64. Nothing here comes from the GPU library.
+
+Weights are generated one layer at a time on demand (with a small cache), and
+cache pages one physical page at a time, so that full-size workloads only ever
+hold one layer of weights and the pages of the candidates actually scored.
+"""
+from __future__ import annotations
+
+from functools import lru_cache
+from typing import Optional
+
+import numpy as np
+
+import synth
+from . import kvprm_oracle as ko
+
+_DT = {"f32": synth.DT_F32, "bf16": synth.DT_BF16, "f64": synth.DT_F64}
+
+
+def _gen_tensor(name, kind, dims, seed, layer, wdtype, shape):
+    mean, std = synth.tensor_mean_std(name, dims)
+    n = int(np.prod(dims))
+    raw = synth.host_normal(n, seed, synth.stream_id(layer, kind), 0, mean, std, _DT[wdtype])
+    return ko.decode_storage(raw, wdtype).reshape(dims)
+
+
+def readout_from_synth(shape: synth.ModelShape, seed: int, layer_cache: int = 2) -> ko.Readout:
+    """Readout weights of a synthetic model (weights in the stored precision, widened)."""
+    wdt = shape.weight_dtype
+
+    @lru_cache(maxsize=layer_cache)
+    def layer(l: int) -> ko.LayerWeights:
+        t = {name: _gen_tensor(name, kind, dims, seed, l, wdt, shape)
+             for name, kind, dims in synth.layer_tensors(shape)}
+        return ko.LayerWeights(**t)
+
+    g = {name: _gen_tensor(name, kind, dims, seed, synth.GLOBAL, wdt, shape)
+         for name, kind, dims in synth.global_tensors(shape)}
+    return ko.Readout(layer, g["verify_embed"], g["final_norm"], g["reward_w"], 0.0)
+
+
+def cache_from_synth(w: synth.Workload, nan_pages=(), page_cache: int = 4096) -> ko.PagedCache:
+    """Paged pools of a workload, one physical page per call, decoded to float64."""
+    s = w.shape
+    nkv, ps, d = s.num_kv_heads, s.page_size, s.head_dim
+    T = s.tile_elems
+    eb = s.kv_elem_bytes
+
+    @lru_cache(maxsize=page_cache)
+    def tiles(layer: int, which: str, page: int) -> np.ndarray:
+        stream = synth.kv_stream(layer, which)
+        std = w.k_std if which == "k" else w.v_std
+        if s.kv_dtype == "fp8":
+            codes, scales = synth.host_fp8_tiles(nkv, T, w.seed, stream, page * nkv)
+            vals = ko.e4m3fn_to_f64(codes).reshape(nkv, T) * scales.astype(np.float64)[:, None]
+        else:
+            raw = synth.host_normal(nkv * T, w.seed, stream, page * nkv * T, 0.0, std,
+                                    _DT[s.kv_dtype])
+            vals = ko.decode_storage(raw, s.kv_dtype).reshape(nkv, T)
+        out = np.empty((nkv, ps, d))
+        for j in range(nkv):
+            if which == "k":
+                out[j] = ko.k_tile_to_tokens(vals[j], ps, d, eb)
+            else:
+                out[j] = ko.v_tile_to_tokens(vals[j], ps, d)
+        return out
+
+    return ko.PagedCache(tiles)
+
+
+def score_workload(w: synth.Workload, candidates=None, return_hidden: bool = False):
+    """Oracle scores (z, P(+)) of the listed candidates (default: all) of a workload."""
+    cand = list(range(w.batch)) if candidates is None else list(candidates)
+    ro = readout_from_synth(w.shape, w.seed)
+    cache = cache_from_synth(w)
+    lens = [w.lengths[b] for b in cand]
+    pt = [w.page_table[b] for b in cand]
+    return ko.verify_pass(w.shape, ro, cache, lens, pt, return_hidden=return_hidden)

@@ -1,0 +1,390 @@
+"""Seeded synthetic inputs for KV-PRM verify-token scoring.
+
+This package is the only thing the fp64 oracle and the GPU path share. It
+holds no arithmetic of the scoring method: it produces model shapes, the
+per-candidate cache lengths, the scattered page tables, and the values of
+every weight and cache tensor, addressed by (seed, stream, element index).
+
+Value generation has two implementations of one definition
+(``csrc/synth_host.c`` for host memory, ``csrc/synth_device.hip`` for device
+memory) that agree bit for bit; see the header of ``synth_host.c``.
+
+Workloads stand in for the paper's generator caches (Qwen3 models on math
+reasoning trajectories; section 5.1): only shapes, lengths and value
+statistics are reproduced, since neither the datasets nor the weights exist
+here. Integer recipes (lengths, page permutations, token ids) use the same
+SplitMix64 counter words, evaluated in Python.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+HOST_LIB = os.path.join(_HERE, "libsynth_host.so")
+DEVICE_LIB = os.path.join(_HERE, "libsynth_device.so")
+
+MASK64 = (1 << 64) - 1
+GAMMA = 0x9E3779B97F4A7C15
+
+# storage dtype codes shared by both generator implementations
+DT_F32, DT_BF16, DT_F64 = 0, 1, 2
+
+# stream ids: per-layer tensors are (layer << 8) | kind
+K_ATTN_NORM, K_WQ, K_WK, K_WV, K_WO, K_FFN_NORM, K_WGATE, K_WUP, K_WDOWN, K_KPOOL, K_VPOOL = range(11)
+GLOBAL = 0xFFFF
+G_VERIFY_EMBED, G_FINAL_NORM, G_REWARD_W, G_EMBED_TABLE = range(4)
+RECIPE = 0xFFFE
+R_LENGTHS, R_PERM, R_TOKENS, R_SUFFIX = range(4)
+ADAPTER_SEED_OFFSET = 0x100000  # weights theta' of the verify token in the mixed re-encode check
+
+
+def stream_id(layer: int, kind: int) -> int:
+    return (layer << 8) | kind
+
+
+# --------------------------------------------------------------------------------------------
+# integer counter words (Python twin of synth_words in synth_host.c)
+
+
+def _mix(z: int) -> int:
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & MASK64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & MASK64
+    return z ^ (z >> 31)
+
+
+def key(seed: int, stream: int) -> int:
+    return _mix((_mix((seed + GAMMA) & MASK64) + stream * GAMMA) & MASK64)
+
+
+def word(k: int, n: int) -> int:
+    return _mix((k + (n + 1) * GAMMA) & MASK64)
+
+
+def uniform_int(k: int, n: int, lo: int, hi: int) -> int:
+    """Integer in [lo, hi] from word n: lo + floor(u53 * (hi - lo + 1) / 2^53)."""
+    u = word(k, n) >> 11
+    return lo + (u * (hi - lo + 1)) // (1 << 53)
+
+
+def permutation(seed: int, stream: int, n: int) -> List[int]:
+    """Fisher-Yates shuffle of range(n) driven by counter words."""
+    k = key(seed, stream)
+    p = list(range(n))
+    c = 0
+    for i in range(n - 1, 0, -1):
+        j = uniform_int(k, c, 0, i)
+        c += 1
+        p[i], p[j] = p[j], p[i]
+    return p
+
+
+# --------------------------------------------------------------------------------------------
+# value generation (ctypes over the two C implementations)
+
+_host = None
+_dev = None
+
+
+def _load_host():
+    global _host
+    if _host is None:
+        if not os.path.exists(HOST_LIB):
+            raise RuntimeError(f"{HOST_LIB} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(HOST_LIB)
+        lib.synth_fill_normal.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
+                                          ctypes.c_uint64, ctypes.c_int64, ctypes.c_double,
+                                          ctypes.c_double, ctypes.c_int]
+        lib.synth_fill_normal.restype = None
+        lib.synth_fill_fp8_tiles.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                             ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint64,
+                                             ctypes.c_int64]
+        lib.synth_fill_fp8_tiles.restype = None
+        lib.synth_words.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
+                                    ctypes.c_uint64, ctypes.c_int64]
+        lib.synth_words.restype = None
+        _host = lib
+    return _host
+
+
+def _load_dev():
+    global _dev
+    if _dev is None:
+        if not os.path.exists(DEVICE_LIB):
+            raise RuntimeError(f"{DEVICE_LIB} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(DEVICE_LIB)
+        lib.synth_dev_fill_normal.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
+                                              ctypes.c_uint64, ctypes.c_int64, ctypes.c_double,
+                                              ctypes.c_double, ctypes.c_int, ctypes.c_void_p]
+        lib.synth_dev_fill_normal.restype = ctypes.c_int
+        lib.synth_dev_fill_fp8_tiles.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                                 ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint64,
+                                                 ctypes.c_int64, ctypes.c_void_p]
+        lib.synth_dev_fill_fp8_tiles.restype = ctypes.c_int
+        _dev = lib
+    return _dev
+
+
+_NP_OF = {DT_F32: np.float32, DT_BF16: np.uint16, DT_F64: np.float64}
+
+
+def host_normal(n: int, seed: int, stream: int, offset: int = 0, mean: float = 0.0,
+                std: float = 1.0, dtype: int = DT_F64) -> np.ndarray:
+    """value(offset .. offset+n) in host memory (bf16 returned as raw uint16 bits)."""
+    out = np.empty(n, dtype=_NP_OF[dtype])
+    if n:
+        _load_host().synth_fill_normal(out.ctypes.data, n, seed, stream, offset, mean, std, dtype)
+    return out
+
+
+def host_fp8_tiles(ntiles: int, tile: int, seed: int, stream: int, tile0: int = 0):
+    """(codes uint8 [ntiles*tile], scales fp32 [ntiles]) for tiles tile0 .. tile0+ntiles."""
+    codes = np.empty(ntiles * tile, dtype=np.uint8)
+    scales = np.empty(ntiles, dtype=np.float32)
+    if ntiles:
+        _load_host().synth_fill_fp8_tiles(codes.ctypes.data, scales.ctypes.data, ntiles, tile,
+                                          seed, stream, tile0)
+    return codes, scales
+
+
+def device_normal(ptr: int, n: int, seed: int, stream: int, offset: int = 0, mean: float = 0.0,
+                  std: float = 1.0, dtype: int = DT_F32, hip_stream: int = 0) -> None:
+    """Write value(offset .. offset+n) into device memory at ptr (asynchronous on hip_stream)."""
+    rc = _load_dev().synth_dev_fill_normal(ptr, n, seed, stream, offset, mean, std, dtype,
+                                           hip_stream)
+    if rc != 0:
+        raise RuntimeError(f"synth_dev_fill_normal failed with hipError {rc}")
+
+
+def device_fp8_tiles(codes_ptr: int, scales_ptr: int, ntiles: int, tile: int, seed: int,
+                     stream: int, tile0: int = 0, hip_stream: int = 0) -> None:
+    rc = _load_dev().synth_dev_fill_fp8_tiles(codes_ptr, scales_ptr, ntiles, tile, seed, stream,
+                                              tile0, hip_stream)
+    if rc != 0:
+        raise RuntimeError(f"synth_dev_fill_fp8_tiles failed with hipError {rc}")
+
+
+# --------------------------------------------------------------------------------------------
+# workload recipes
+
+
+@dataclass(frozen=True)
+class ModelShape:
+    num_layers: int
+    hidden: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    ffn_dim: int
+    rope_theta: float = 1.0e6
+    rms_eps: float = 1.0e-6
+    weight_dtype: str = "bf16"  # "f32" | "bf16"
+    kv_dtype: str = "bf16"  # "f32" | "bf16" | "fp8"
+    page_size: int = 16
+
+    @property
+    def group(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+    @property
+    def kv_elem_bytes(self) -> int:
+        return {"f32": 4, "bf16": 2, "fp8": 1, "f64": 8}[self.kv_dtype]
+
+    @property
+    def w_elem_bytes(self) -> int:
+        return {"f32": 4, "bf16": 2}[self.weight_dtype]
+
+    @property
+    def tile_elems(self) -> int:
+        """Elements of one (page, kv-head) tile of K or V."""
+        return self.page_size * self.head_dim
+
+
+@dataclass
+class Workload:
+    """One synthetic scoring batch: model shape, value seeds, lengths and page table."""
+
+    name: str
+    shape: ModelShape
+    seed: int
+    lengths: List[int]
+    page_table: List[List[int]]  # physical page ids, rows padded with -1 to max_pages
+    num_pages: int
+    group_start: List[int] = field(default_factory=list)  # prefix-sharing hint (may be empty)
+    group_prefix_len: List[int] = field(default_factory=list)
+    k_std: float = 1.0  # test variants scale K to make the softmax peaked
+    v_std: float = 1.0
+
+    @property
+    def batch(self) -> int:
+        return len(self.lengths)
+
+    @property
+    def max_pages(self) -> int:
+        return max([len(r) for r in self.page_table] + [1])
+
+    def used_pages(self) -> List[int]:
+        s = set()
+        for b, row in enumerate(self.page_table):
+            npg = -(-self.lengths[b] // self.shape.page_size)
+            s.update(row[:npg])
+        return sorted(s)
+
+    def page_table_array(self) -> np.ndarray:
+        mp = self.max_pages
+        a = np.full((self.batch, mp), -1, dtype=np.int32)
+        for b, row in enumerate(self.page_table):
+            a[b, : len(row)] = row
+        return a
+
+    def unique_tokens(self) -> int:
+        """Cached tokens counted once per physical page slot (shared prefix counted once)."""
+        ps = self.shape.page_size
+        seen = {}
+        for b, row in enumerate(self.page_table):
+            L = self.lengths[b]
+            for i in range(-(-L // ps)):
+                n = min(ps, L - i * ps)
+                seen[row[i]] = max(seen.get(row[i], 0), n)
+        return sum(seen.values())
+
+
+# weight stream descriptions: (kind, rows, cols, is_norm_gain)
+def layer_tensors(s: ModelShape):
+    H, d, nq, nkv, F = s.hidden, s.head_dim, s.num_q_heads, s.num_kv_heads, s.ffn_dim
+    return [
+        ("attn_norm", K_ATTN_NORM, (H,)),
+        ("wq", K_WQ, (nq * d, H)),
+        ("wk", K_WK, (nkv * d, H)),
+        ("wv", K_WV, (nkv * d, H)),
+        ("wo", K_WO, (H, nq * d)),
+        ("ffn_norm", K_FFN_NORM, (H,)),
+        ("w_gate", K_WGATE, (F, H)),
+        ("w_up", K_WUP, (F, H)),
+        ("w_down", K_WDOWN, (H, F)),
+    ]
+
+
+def tensor_mean_std(name: str, dims) -> tuple:
+    """Value statistics of the synthetic weights.
+
+    Matrices are N(0, std = 1/sqrt(fan_in)) (fan_in = the input width, the
+    second dimension of an [out, in] matrix); norm gains are 1 + 0.1 N(0, 1)
+    so that a dropped gain is visible; the verify embedding is N(0, 1); the
+    reward vector is N(0, 1/sqrt(H)).
+    """
+    if name in ("attn_norm", "ffn_norm", "final_norm"):
+        return 1.0, 0.1
+    if name in ("verify_embed", "embed_table"):
+        return 0.0, 1.0
+    if name == "reward_w":
+        return 0.0, 1.0 / math.sqrt(dims[0])
+    return 0.0, 1.0 / math.sqrt(dims[1])
+
+
+def global_tensors(s: ModelShape):
+    H = s.hidden
+    return [
+        ("verify_embed", G_VERIFY_EMBED, (H,)),
+        ("final_norm", G_FINAL_NORM, (H,)),
+        ("reward_w", G_REWARD_W, (H,)),
+    ]
+
+
+def _assign_pages(seed: int, lengths: Sequence[int], ps: int, shared_prefix_pages: int = 0):
+    """Scatter logical pages over a pool 1.25x the unique page count (Fisher-Yates)."""
+    B = len(lengths)
+    priv = [-(-max(L - shared_prefix_pages * ps, 0) // ps) for L in lengths]
+    unique = shared_prefix_pages + sum(priv)
+    num_pages = max(1, math.ceil(1.25 * unique))
+    perm = permutation(seed, stream_id(RECIPE, R_PERM), num_pages)
+    rows = []
+    nxt = shared_prefix_pages
+    for b in range(B):
+        row = [perm[i] for i in range(shared_prefix_pages)]
+        for _ in range(priv[b]):
+            row.append(perm[nxt])
+            nxt += 1
+        rows.append(row)
+    mp = max([len(r) for r in rows] + [1])
+    rows = [r + [-1] * (mp - len(r)) for r in rows]
+    return rows, num_pages
+
+
+TINY = ModelShape(2, 256, 4, 2, 64, 1024, weight_dtype="f32", kv_dtype="f32")
+B7 = ModelShape(28, 3584, 28, 4, 128, 18944)
+LARGE_FP8 = ModelShape(64, 8192, 64, 8, 128, 28672, kv_dtype="fp8")
+
+
+def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional[int] = None,
+                  lengths: Optional[Sequence[int]] = None, seed: Optional[int] = None,
+                  k_std: float = 1.0) -> Workload:
+    """The five workloads of the benchmark plan, plus custom ones for tests.
+
+    tiny_fp32    B=4, 2 layers, H=256, 4/2 heads, d_h=64, FFN 1024, fp32, L=512 each
+    b7_bf16      B=16, 28 layers, H=3584, 28/4 heads, d_h=128, FFN 18944, bf16, L=4096
+    ragged_32k   7B shape, B=8, L_b ~ U[16384, 32768]
+    beam_prefix  7B shape, B=64, one shared 16384-token prefix + private U[512, 2048]
+    large_fp8    B=16, 64 layers, H=8192, 64/8 heads, FFN 28672, bf16 weights,
+                 e4m3 K/V with per-(layer, page, kv-head) scales, L_b ~ U[8192, 16384]
+    custom       any shape with explicit lengths (tests)
+    """
+    presets = {
+        "tiny_fp32": (TINY, 1000),
+        "b7_bf16": (B7, 1001),
+        "ragged_32k": (B7, 1002),
+        "beam_prefix": (B7, 1003),
+        "large_fp8": (LARGE_FP8, 1004),
+    }
+    if name in presets:
+        shp, sd = presets[name]
+        shape = shape or shp
+        seed = sd if seed is None else seed
+    if shape is None or seed is None:
+        raise ValueError(f"unknown workload {name!r} without explicit shape and seed")
+    ps = shape.page_size
+    klen = key(seed, stream_id(RECIPE, R_LENGTHS))
+    groups_start: List[int] = []
+    groups_prefix: List[int] = []
+    prefix_pages = 0
+    if lengths is not None:
+        lens = [int(x) for x in lengths]
+    elif name == "tiny_fp32":
+        lens = [512] * (batch or 4)
+    elif name == "b7_bf16":
+        lens = [4096] * (batch or 16)
+    elif name == "ragged_32k":
+        lens = [uniform_int(klen, i, 16384, 32768) for i in range(batch or 8)]
+    elif name == "beam_prefix":
+        B = batch or 64
+        prefix = 16384
+        prefix_pages = prefix // ps
+        lens = [prefix + uniform_int(klen, i, 512, 2048) for i in range(B)]
+        groups_start, groups_prefix = [0, B], [prefix]
+    elif name == "large_fp8":
+        lens = [uniform_int(klen, i, 8192, 16384) for i in range(batch or 16)]
+    else:
+        raise ValueError(f"workload {name!r} needs explicit lengths")
+    rows, num_pages = _assign_pages(seed, lens, ps, prefix_pages)
+    return Workload(name, shape, seed, lens, rows, num_pages, groups_start, groups_prefix,
+                    k_std=k_std)
+
+
+def token_ids(seed: int, n: int, vocab: int = 1000) -> List[int]:
+    """Random token ids in [0, vocab) for the re-encode workload."""
+    k = key(seed, stream_id(RECIPE, R_TOKENS))
+    return [uniform_int(k, i, 0, vocab - 1) for i in range(n)]
+
+
+def kv_pool_elems(shape: ModelShape, num_pages: int) -> int:
+    """Elements of one layer's K (or V) pool: [num_pages][n_kv][page_size][head_dim]."""
+    return num_pages * shape.num_kv_heads * shape.tile_elems
+
+
+def kv_stream(layer: int, which: str) -> int:
+    return stream_id(layer, K_KPOOL if which == "k" else K_VPOOL)

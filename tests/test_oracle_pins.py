@@ -1,0 +1,429 @@
+"""Pins of the fp64 oracle against closed forms, invariants, library routines and brute
+force (CPU only). Each test names the property it fixes; together they are chosen so that a
+dropped term, a wrong sign or index, or a transposed operand in the oracle fails one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import synth
+from oracle import kvprm_oracle as ko
+from oracle import inputs
+
+RNG = np.random.default_rng(1234)
+
+
+# ------------------------------------------------------------------------ number formats
+
+
+def test_e4m3_all_256_codes_against_torch():
+    codes = np.arange(256, dtype=np.uint8)
+    ours = ko.e4m3fn_to_f64(codes)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert nan.sum() == 2  # 0x7F and 0xFF
+    assert np.array_equal(ours[~nan], ref[~nan])
+    assert ours[0x7E] == 448.0 and ours[0x01] == 2.0 ** -9 and ours[0x08] == 2.0 ** -6
+
+
+def test_bf16_decode_against_torch():
+    bits = np.arange(0, 65536, 7, dtype=np.uint32).astype(np.uint16)
+    ours = ko.bf16_bits_to_f64(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    fin = np.isfinite(ref)
+    assert np.array_equal(ours[fin], ref[fin])
+
+
+# ------------------------------------------------------------------------ attention
+
+
+def test_attention_one_key_returns_its_value():
+    for d in (4, 64, 128):
+        q, k, v = RNG.normal(size=d) * 5, RNG.normal(size=(1, d)), RNG.normal(size=(1, d))
+        assert np.allclose(ko.attention(q, k, v), v[0], rtol=0, atol=1e-14)
+
+
+def test_attention_identical_keys_give_mean_of_values():
+    d, n = 64, 37
+    q = RNG.normal(size=d)
+    K = np.tile(RNG.normal(size=d), (n, 1))
+    V = RNG.normal(size=(n, d))
+    assert np.allclose(ko.attention(q, K, V), V.mean(axis=0), rtol=0, atol=1e-14)
+    # a zero query sees equal logits for any keys
+    assert np.allclose(ko.attention(np.zeros(d), RNG.normal(size=(n, d)), V), V.mean(axis=0),
+                       rtol=0, atol=1e-14)
+
+
+def test_attention_two_keys_closed_form():
+    """Keys along q with q.k1 - q.k2 = delta: weight of key 1 is sigmoid(delta / sqrt(d))."""
+    d = 16
+    q = RNG.normal(size=d)
+    qq = q @ q
+    a, b = 3.0, -1.5
+    K = np.stack([a * q / qq, b * q / qq])
+    V = RNG.normal(size=(2, d))
+    w1 = scipy.special.expit((a - b) / math.sqrt(d))
+    assert np.allclose(ko.attention(q, K, V), w1 * V[0] + (1 - w1) * V[1], rtol=0, atol=1e-14)
+
+
+def test_attention_brute_force_against_torch_sdpa():
+    d, n = 64, 300
+    q = RNG.normal(size=d) * 2
+    K, V = RNG.normal(size=(n, d)), RNG.normal(size=(n, d))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None, None, None, :], torch.from_numpy(K)[None, None],
+        torch.from_numpy(V)[None, None]).numpy()[0, 0, 0]
+    assert np.allclose(ko.attention(q, K, V), ref, rtol=0, atol=1e-13)
+
+
+def test_attention_invariances():
+    d, n = 32, 50
+    q = RNG.normal(size=d)
+    K, V = RNG.normal(size=(n, d)), RNG.normal(size=(n, d))
+    o = ko.attention(q, K, V)
+    perm = RNG.permutation(n)
+    assert np.allclose(ko.attention(q, K[perm], V[perm]), o, rtol=0, atol=1e-14)
+    # adding one vector w to every key shifts all logits by q.w / sqrt(d): no effect
+    w = RNG.normal(size=d) * 10
+    assert np.allclose(ko.attention(q, K + w, V), o, rtol=0, atol=1e-13)
+    # huge logits stay finite (max subtraction)
+    o2 = ko.attention(q * 1e4, K, V)
+    assert np.all(np.isfinite(o2))
+    s = K @ q
+    assert np.allclose(o2, V[np.argmax(s)], atol=1e-12)
+
+
+# ------------------------------------------------------------------------ rotary, norms, FFN
+
+
+def test_rope_position_zero_is_identity_and_norm_preserving():
+    y = RNG.normal(size=(3, 64))
+    assert np.array_equal(ko.rope(y, 0, 1e6), y)
+    r = ko.rope(y, 12345, 1e6)
+    assert np.allclose(np.linalg.norm(r, axis=1), np.linalg.norm(y, axis=1), atol=1e-12)
+
+
+def test_rope_relative_position():
+    q, k = RNG.normal(size=(1, 128)), RNG.normal(size=(1, 128))
+    for m, n, c in [(5, 3, 100), (30000, 17, 2345), (0, 4096, 7)]:
+        a = ko.rope(q, m, 1e6) @ ko.rope(k, n, 1e6).T
+        b = ko.rope(q, m + c, 1e6) @ ko.rope(k, n + c, 1e6).T
+        assert np.allclose(a, b, rtol=0, atol=1e-10)
+
+
+def test_rope_basis_vectors_closed_form():
+    """e_i rotates in the (i, i + d/2) plane by pos * theta^(-2i/d)."""
+    d, th, pos = 8, 1e6, 7
+    for i in range(d // 2):
+        e = np.zeros((1, d))
+        e[0, i] = 1.0
+        r = ko.rope(e, pos, th)[0]
+        ang = pos * th ** (-2 * i / d)
+        expect = np.zeros(d)
+        expect[i], expect[i + d // 2] = math.cos(ang), math.sin(ang)
+        assert np.allclose(r, expect, atol=1e-15)
+
+
+def test_rope_matches_transformers_rotate_half():
+    from transformers.models.llama.modeling_llama import apply_rotary_pos_emb
+    d, th = 64, 1e6
+    pos = np.array([0, 1, 7, 300, 511])
+    q = RNG.normal(size=(1, 2, len(pos), d))
+    inv = 1.0 / th ** (np.arange(0, d, 2) / d)
+    emb = np.concatenate([np.outer(pos, inv)] * 2, axis=-1)
+    cos, sin = torch.from_numpy(np.cos(emb))[None], torch.from_numpy(np.sin(emb))[None]
+    ref, _ = apply_rotary_pos_emb(torch.from_numpy(q), torch.from_numpy(q), cos, sin)
+    for t, p in enumerate(pos):
+        assert np.allclose(ko.rope(q[0, :, t], int(p), th), ref.numpy()[0, :, t], atol=1e-13)
+
+
+def test_rmsnorm_scale_invariance_and_unit_rms():
+    x = RNG.normal(size=(4, 256)) * 3
+    g = np.ones(256)
+    a = ko.rms_norm(x, g, 0.0)
+    assert np.allclose(ko.rms_norm(x * 7.5, g, 0.0), a, atol=1e-14)
+    assert np.allclose(np.mean(a * a, axis=1), 1.0, atol=1e-14)
+    gam = RNG.normal(size=256)
+    assert np.allclose(ko.rms_norm(x, gam, 0.0), a * gam, atol=1e-14)
+    # eps enters under the root: x = c * ones gives c / sqrt(c^2 + eps)
+    c, eps = 1e-3, 1e-6
+    assert np.allclose(ko.rms_norm(np.full(8, c), np.ones(8), eps), c / math.sqrt(c * c + eps))
+
+
+def test_swiglu_closed_form_and_orientation():
+    # scalar case: w_d * silu(w_g u) * (w_u u), silu(a) = a * sigmoid(a)
+    u, wg, wu, wd = 0.7, 1.3, -0.4, 2.0
+    a = wg * u
+    expect = wd * a * scipy.special.expit(a) * (wu * u)
+    got = ko.swiglu_ffn(np.array([u]), np.array([[wg]]), np.array([[wu]]), np.array([[wd]]))
+    assert np.allclose(got, expect, atol=1e-15)
+    # matrix case against torch's silu with [out, in] weights (nn.Linear convention)
+    H, F = 6, 10
+    U = RNG.normal(size=H)
+    Wg, Wu, Wd = RNG.normal(size=(F, H)), RNG.normal(size=(F, H)), RNG.normal(size=(H, F))
+    t = lambda m: torch.from_numpy(m)
+    ref = torch.nn.functional.linear(
+        torch.nn.functional.silu(torch.nn.functional.linear(t(U), t(Wg))) *
+        torch.nn.functional.linear(t(U), t(Wu)), t(Wd)).numpy()
+    assert np.allclose(ko.swiglu_ffn(U, Wg, Wu, Wd), ref, atol=1e-13)
+
+
+def test_two_logit_softmax_equals_sigmoid_head():
+    zm = RNG.normal(size=1000) * 10
+    zp = RNG.normal(size=1000) * 10
+    ref = scipy.special.softmax(np.stack([zm, zp], axis=1), axis=1)[:, 1]
+    assert np.allclose(ko.judgment_probability(zm, zp), ref, rtol=0, atol=1e-15)
+    assert np.allclose(ko.sigmoid(zp - zm), ref, rtol=0, atol=1e-15)
+    big = np.array([-800.0, -40.0, 0.0, 40.0, 800.0])
+    assert np.allclose(ko.sigmoid(big), scipy.special.expit(big), rtol=1e-15, atol=0)
+
+
+# ------------------------------------------------------------------------ cache layout
+
+
+def test_cache_tile_layouts():
+    ps, d = 16, 128
+    tok = np.arange(ps * d).reshape(ps, d)  # value = slot * d + dim
+    for eb in (4, 2, 1):
+        x = 16 // eb
+        stored = np.empty(ps * d, dtype=np.int64)
+        for s in range(ps):
+            for m in range(d):
+                stored[((m // x) * ps + s) * x + m % x] = tok[s, m]
+        assert np.array_equal(ko.k_tile_to_tokens(stored, ps, d, eb), tok)
+    stored_v = np.empty(ps * d, dtype=np.int64)
+    for s in range(ps):
+        for m in range(d):
+            stored_v[m * ps + s] = tok[s, m]
+    assert np.array_equal(ko.v_tile_to_tokens(stored_v, ps, d), tok)
+
+
+# ------------------------------------------------------------------------ model-level pins
+
+TINY = synth.TINY
+
+
+def _tiny_small(layers=2, **kw):
+    return synth.ModelShape(layers, 64, 4, 2, 16, 96, weight_dtype="f32", kv_dtype="f32", **kw)
+
+
+def _dense_cache(K, V, ps):
+    """Paged cache over dense per-candidate K/V ([B][n_kv... as [L][n_kv][n][d]]), pages
+    laid out in logical order, physical ids given by page tables built here."""
+    B = len(K)
+    tiles = {}
+    page_table = []
+    nxt = 0
+    for b in range(B):
+        NL, nkv, n, d = K[b].shape
+        npg = -(-n // ps)
+        row = []
+        for i in range(npg):
+            phys = 1000 + 3 * nxt  # arbitrary physical ids
+            nxt += 1
+            row.append(phys)
+            for l in range(NL):
+                kt = np.full((nkv, ps, d), np.nan)
+                vt = np.full((nkv, ps, d), np.nan)
+                cnt = min(ps, n - i * ps)
+                kt[:, :cnt] = K[b][l][:, i * ps: i * ps + cnt]
+                vt[:, :cnt] = V[b][l][:, i * ps: i * ps + cnt]
+                tiles[(l, "k", phys)] = kt
+                tiles[(l, "v", phys)] = vt
+        page_table.append(row)
+    return ko.PagedCache(lambda l, w, p: tiles[(l, w, p)]), page_table
+
+
+def _readout(shape, seed):
+    return inputs.readout_from_synth(shape, seed, layer_cache=64)
+
+
+def _embed(shape, seed, vocab=1000):
+    return synth.host_normal(vocab * shape.hidden, seed, synth.stream_id(synth.GLOBAL,
+                             synth.G_EMBED_TABLE)).reshape(vocab, shape.hidden)
+
+
+@pytest.mark.parametrize("mixed", [False, True])
+def test_verify_pass_equals_causal_reencode(mixed):
+    """Re-encode equivalence: the verify pass over the cache a causal forward wrote equals
+    that forward's last position; with mixed=True the verify token alone uses other weights
+    (adapter on for the verify token only)."""
+    shape = _tiny_small()
+    seed = 77
+    base = _readout(shape, seed)
+    ver = _readout(shape, seed + synth.ADAPTER_SEED_OFFSET) if mixed else base
+    E = _embed(shape, seed)
+    Ks, Vs, zs, hs, lens = [], [], [], [], []
+    for b, n in enumerate([40, 16, 1, 23]):
+        toks = synth.token_ids(seed + b, n)
+        z, p, h, K, V = ko.reencode(shape, base.layer, ver.layer, E, toks, ver.verify_embed,
+                                    ver.final_norm, ver.reward_w)
+        Ks.append(K), Vs.append(V), zs.append(z), hs.append(h), lens.append(n)
+    cache, pt = _dense_cache(Ks, Vs, shape.page_size)
+    z2, p2, h2 = ko.verify_pass(shape, ver, cache, lens, pt, return_hidden=True)
+    assert np.allclose(z2, zs, rtol=0, atol=1e-12)
+    assert np.allclose(h2, np.stack(hs), rtol=0, atol=1e-12)
+    assert np.allclose(p2, ko.sigmoid(np.array(zs)), rtol=0, atol=1e-12)
+
+
+def test_empty_cache_is_one_token_forward():
+    shape = _tiny_small()
+    ro = _readout(shape, 5)
+    E = _embed(shape, 5)
+    z, p, h, _, _ = ko.reencode(shape, ro.layer, ro.layer, E, [], ro.verify_embed, ro.final_norm,
+                                ro.reward_w)
+    cache = ko.PagedCache(lambda l, w, pg: (_ for _ in ()).throw(AssertionError("read")))
+    z2, p2 = ko.verify_pass(shape, ro, cache, [0], [[-1]])
+    assert abs(z2[0] - z) < 1e-14
+
+
+def test_gqa_equals_mha_with_replicated_kv_heads():
+    """n_kv = 2, g = 2 equals n_kv = 4 (MHA) with each kv-head's projection rows and cache
+    replicated for its g query heads."""
+    shape = _tiny_small(layers=1)
+    ro = _readout(shape, 9)
+    d, nkv, g = shape.head_dim, shape.num_kv_heads, shape.group
+    W = ro.layer(0)
+    rep = lambda M: np.concatenate([M[(j // g) * d:(j // g + 1) * d] for j in range(nkv * g)])
+    Wm = ko.LayerWeights(W.attn_norm, W.wq, rep(W.wk), rep(W.wv), W.wo, W.ffn_norm, W.w_gate,
+                         W.w_up, W.w_down)
+    mha = synth.ModelShape(1, 64, 4, 4, 16, 96, weight_dtype="f32", kv_dtype="f32")
+    ro_m = ko.Readout(lambda l: Wm, ro.verify_embed, ro.final_norm, ro.reward_w)
+    n = 37
+    K = RNG.normal(size=(1, nkv, n, d))
+    V = RNG.normal(size=(1, nkv, n, d))
+    c1, pt1 = _dense_cache([K], [V], 16)
+    c2, pt2 = _dense_cache([np.repeat(K, g, axis=1)], [np.repeat(V, g, axis=1)], 16)
+    z1, _ = ko.verify_pass(shape, ro, c1, [n], pt1)
+    z2, _ = ko.verify_pass(mha, ro_m, c2, [n], pt2)
+    assert abs(z1[0] - z2[0]) < 1e-13
+
+
+def test_page_permutation_nan_slots_and_candidate_independence():
+    w = synth.make_workload("custom", shape=_tiny_small(), lengths=[0, 1, 15, 16, 17, 70],
+                            seed=31)
+    ro = _readout(w.shape, w.seed)
+    base = inputs.cache_from_synth(w)
+    ps = w.shape.page_size
+
+    # NaN in every slot at or beyond each candidate's length, and in every unused page
+    valid = {}
+    for b, row in enumerate(w.page_table):
+        L = w.lengths[b]
+        for i in range(-(-L // ps)):
+            valid[row[i]] = min(ps, L - i * ps)
+
+    def poisoned(l, which, page):
+        t = base.tiles(l, which, page).copy() if page in valid else np.full(
+            (w.shape.num_kv_heads, ps, w.shape.head_dim), np.nan)
+        if page in valid:
+            t[:, valid[page]:] = np.nan
+        return t
+
+    z, p = ko.verify_pass(w.shape, ro, base, w.lengths, w.page_table)
+    z_nan, _ = ko.verify_pass(w.shape, ro, ko.PagedCache(poisoned), w.lengths, w.page_table)
+    assert np.all(np.isfinite(z_nan)) and np.array_equal(z, z_nan)
+
+    # relabel physical pages
+    perm = {pg: 5000 + 7 * i for i, pg in enumerate(sorted(valid))}
+    inv = {v: k for k, v in perm.items()}
+    relab = ko.PagedCache(lambda l, wh, pg: base.tiles(l, wh, inv[pg]))
+    pt2 = [[perm.get(x, -1) for x in row] for row in w.page_table]
+    z2, _ = ko.verify_pass(w.shape, ro, relab, w.lengths, pt2)
+    assert np.array_equal(z, z2)
+
+    # one candidate alone scores the same as inside the batch
+    for b in (0, 3, 5):
+        zb, _ = ko.verify_pass(w.shape, ro, base, [w.lengths[b]], [w.page_table[b]])
+        assert abs(zb[0] - z[b]) < 1e-14  # BLAS blocking may differ with batch width
+
+
+def test_cached_length_changes_the_score():
+    """The cache is really read: dropping the last cached token changes z."""
+    w = synth.make_workload("custom", shape=_tiny_small(), lengths=[33, 32], seed=4)
+    ro = _readout(w.shape, w.seed)
+    c = inputs.cache_from_synth(w)
+    z, _ = ko.verify_pass(w.shape, ro, c, w.lengths, w.page_table)
+    z2, _ = ko.verify_pass(w.shape, ro, c, [32], [w.page_table[0]])
+    assert abs(z[0] - z2[0]) > 1e-6
+
+
+# ------------------------------------------------------------------------ library decoder
+
+
+def _hf_model(shape, ro, E):
+    from transformers import LlamaConfig, LlamaForCausalLM
+    cfg = LlamaConfig(hidden_size=shape.hidden, intermediate_size=shape.ffn_dim,
+                      num_hidden_layers=shape.num_layers, num_attention_heads=shape.num_q_heads,
+                      num_key_value_heads=shape.num_kv_heads, head_dim=shape.head_dim,
+                      rms_norm_eps=shape.rms_eps, rope_theta=shape.rope_theta,
+                      vocab_size=E.shape[0], attention_bias=False, mlp_bias=False,
+                      tie_word_embeddings=False)
+    cfg._attn_implementation = "eager"
+    m = LlamaForCausalLM(cfg).to(torch.float64).eval()
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a))
+    with torch.no_grad():
+        m.model.embed_tokens.weight.copy_(t(E))
+        for l, layer in enumerate(m.model.layers):
+            W = ro.layer(l)
+            layer.input_layernorm.weight.copy_(t(W.attn_norm))
+            layer.self_attn.q_proj.weight.copy_(t(W.wq))
+            layer.self_attn.k_proj.weight.copy_(t(W.wk))
+            layer.self_attn.v_proj.weight.copy_(t(W.wv))
+            layer.self_attn.o_proj.weight.copy_(t(W.wo))
+            layer.post_attention_layernorm.weight.copy_(t(W.ffn_norm))
+            layer.mlp.gate_proj.weight.copy_(t(W.w_gate))
+            layer.mlp.up_proj.weight.copy_(t(W.w_up))
+            layer.mlp.down_proj.weight.copy_(t(W.w_down))
+        m.model.norm.weight.copy_(t(ro.final_norm))
+        # two judgment rows: "+" = reward vector, "-" = zero
+        m.lm_head.weight.zero_()
+        m.lm_head.weight[1].copy_(t(ro.reward_w))
+    return m
+
+
+@pytest.mark.parametrize("mixed", [False, True])
+def test_verify_pass_against_transformers_llama_with_kv_cache(mixed):
+    """A library decoder (transformers' Llama block: pre-norm RMSNorm, rotate-half rotary,
+    grouped-query attention, SwiGLU) encodes the trajectory with base weights, then runs the
+    verify token against its own KV cache with the verify weights. The oracle's verify pass
+    over that same cache must agree. The library computes norms, rotary angles and softmax in
+    fp32, hence the 1e-5 tolerance."""
+    shape = synth.ModelShape(2, 256, 4, 2, 64, 1024, weight_dtype="f32", kv_dtype="f32")
+    seed = 1000
+    base = _readout(shape, seed)
+    ver = _readout(shape, seed + synth.ADAPTER_SEED_OFFSET) if mixed else base
+    E = _embed(shape, seed).copy()
+    vid = 999
+    E_v = E.copy()
+    E_v[vid] = ver.verify_embed
+    mb = _hf_model(shape, base, E)
+    mv = _hf_model(shape, ver, E_v)
+    n = 48
+    toks = torch.tensor([synth.token_ids(seed, n)])
+    with torch.no_grad():
+        out = mb(input_ids=toks, use_cache=True)
+        pkv = out.past_key_values
+        out2 = mv(input_ids=torch.tensor([[vid]]), past_key_values=pkv, use_cache=True,
+                  output_hidden_states=True)
+    h_ref = out2.hidden_states[-1][0, -1].numpy()
+    z_ref = out2.logits[0, -1, 1].item() - out2.logits[0, -1, 0].item()
+    # the cache the library wrote during the prefix pass: [layers][n_kv][n][d] after rotation
+    Ks = np.stack([pkv.layers[l].keys[0, :, :n].numpy() for l in range(shape.num_layers)])
+    Vs = np.stack([pkv.layers[l].values[0, :, :n].numpy() for l in range(shape.num_layers)])
+    cache, pt = _dense_cache([Ks], [Vs], shape.page_size)
+    z, p, h = ko.verify_pass(shape, ver, cache, [n], pt, return_hidden=True)
+    assert np.max(np.abs(h[0] - h_ref)) < 1e-5
+    assert abs(z[0] - z_ref) < 1e-5
+    # and the full causal re-encode of [x; v] in the library equals the oracle's re-encode
+    if not mixed:
+        with torch.no_grad():
+            full = mv(input_ids=torch.cat([toks, torch.tensor([[vid]])], dim=1),
+                      output_hidden_states=True)
+        zr, _, hr, _, _ = ko.reencode(shape, base.layer, base.layer, E, toks[0].tolist(),
+                                      base.verify_embed, base.final_norm, base.reward_w)
+        assert np.max(np.abs(hr - full.hidden_states[-1][0, -1].numpy())) < 1e-5
