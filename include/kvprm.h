@@ -1,0 +1,170 @@
+/*
+ * kvprm.h - C ABI of the KV-PRM verify-token scoring library for AMD Instinct MI355X (gfx950).
+ *
+ * KV-PRM (section 4.1, Eq. (score)) scores a candidate trajectory by pushing one appended
+ * "verify" token through the adapter-merged decoder f_{theta+dtheta}, conditioned on the key/
+ * value cache the generator already produced for that trajectory, and reading two judgment
+ * logits: P(+) = softmax([z_-, z_+]) at the "+" entry = sigmoid(z_+ - z_-). The cost is one
+ * query against L cached positions per layer (Eq. (cost_kv)), O(d L) instead of the O(d L^2)
+ * re-encode of the text (Eq. (1)).
+ *
+ * Conventions for every entry point
+ *   - All tensor pointers are DEVICE pointers unless the name ends in _host. The caller owns
+ *     every buffer; the library never frees, never writes the cache, the page table or the
+ *     weights, and never allocates device memory inside kvprm_score / kvprm_attention (the
+ *     caller passes a workspace sized by kvprm_workspace_size).
+ *   - Calls only enqueue work on `stream` (a hipStream_t; NULL = the null stream) and never
+ *     synchronise the host. Outputs are valid once the stream reaches that point.
+ *   - Arguments are validated on the host before anything is enqueued; on any error nothing
+ *     is enqueued. The returned status says what failed; kvprm_last_error() has the text.
+ *   - A handle is immutable after kvprm_create. Concurrent calls on one handle are safe when
+ *     they use distinct workspaces and outputs.
+ *   - Out-of-range physical page ids in the page table are undefined behaviour (they are not
+ *     checked on the device).
+ *
+ * Model structure (the paper names only "decoder-only transformer"; the block follows the
+ * Qwen3/Llama family it evaluates): pre-norm RMSNorm -> Q/K/V projections -> rotate-half
+ * rotary embedding at the verify position -> grouped-query attention (q-head h reads kv-head
+ * floor(h / g), g = n_q / n_kv) -> output projection -> residual; RMSNorm -> SwiGLU FFN ->
+ * residual; final RMSNorm -> reward vector. No biases. All matrices are row-major [out, in].
+ */
+#ifndef KVPRM_H
+#define KVPRM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct kvprm_handle_s *kvprm_handle;
+
+typedef enum {
+  KVPRM_OK = 0,
+  KVPRM_E_INVALID = 1,     /* a null pointer, a negative size, inconsistent arguments */
+  KVPRM_E_UNSUPPORTED = 2, /* a valid configuration this build does not implement */
+  KVPRM_E_WORKSPACE = 3,   /* workspace pointer null or smaller than kvprm_workspace_size */
+  KVPRM_E_HIP = 4,         /* a HIP runtime call or kernel launch failed */
+  KVPRM_E_INTERNAL = 5
+} kvprm_status;
+
+typedef enum { KVPRM_F32 = 0, KVPRM_BF16 = 1, KVPRM_FP8_E4M3 = 2 } kvprm_dtype;
+
+/* Model shape. Supported: head_dim in {64, 128}; page_size == 16; num_q_heads a multiple of
+ * num_kv_heads; weight_dtype F32 with kv_dtype F32, or weight_dtype BF16 with kv_dtype BF16 or
+ * FP8_E4M3 (OCP E4M3FN: bias 7, max 448, no infinities). */
+typedef struct {
+  int32_t num_layers;   /* N_L */
+  int32_t hidden;       /* H, a multiple of 64 */
+  int32_t num_q_heads;  /* n_q */
+  int32_t num_kv_heads; /* n_kv */
+  int32_t head_dim;     /* d_h */
+  int32_t ffn_dim;      /* F, a multiple of 64 */
+  float rope_theta;     /* rotary base theta; angle of pair i at position p is p * theta^(-2i/d_h) */
+  float rms_eps;        /* RMSNorm epsilon: y = x / sqrt(mean(x^2) + eps) * gamma */
+  kvprm_dtype weight_dtype;
+  kvprm_dtype kv_dtype;
+  int32_t page_size; /* tokens per cache page; must be 16 */
+} kvprm_model_desc;
+
+/* One decoder layer of the readout weights theta + dtheta (the LoRA update is merged into the
+ * base weights by the caller: W' = W + (alpha / r) B A; section 4.1 and the hyperparameter
+ * table). Element type weight_dtype; row-major [out, in]. */
+typedef struct {
+  const void *attn_norm; /* [H]                gain of the attention RMSNorm */
+  const void *wq;        /* [n_q * d_h, H]     head h occupies rows [h d_h, (h+1) d_h) */
+  const void *wk;        /* [n_kv * d_h, H] */
+  const void *wv;        /* [n_kv * d_h, H] */
+  const void *wo;        /* [H, n_q * d_h] */
+  const void *ffn_norm;  /* [H]                gain of the FFN RMSNorm */
+  const void *w_gate;    /* [F, H] */
+  const void *w_up;      /* [F, H] */
+  const void *w_down;    /* [H, F] */
+} kvprm_layer_weights;
+
+typedef struct {
+  const kvprm_layer_weights *layers; /* HOST array [num_layers] of device pointers */
+  const void *verify_embed;          /* [H] embedding row of the verify token (weight_dtype) */
+  const void *final_norm;            /* [H] gain of the final RMSNorm (weight_dtype) */
+  const void *reward_w;              /* [H] W_out[+] - W_out[-] (weight_dtype) */
+  float reward_b;                    /* b[+] - b[-] */
+} kvprm_readout_weights;
+
+/* Paged KV cache written by the generator (adapter off; section 4.1). Keys are stored after
+ * the rotary embedding of their own position; values are not rotated.
+ *   pool layout: [num_layers][num_pages][num_kv_heads][tile]
+ *   K tile (page_size x d_h values): [d_h / x][page_size][x], x = 16 bytes / element size
+ *            (x = 4 fp32, 8 bf16, 16 fp8): element (slot s, dim m) at ((m / x) * 16 + s) * x + m % x
+ *   V tile: [d_h][page_size]: element (slot s, dim m) at m * 16 + s
+ * For FP8_E4M3 pools the stored code is multiplied by a per-(layer, page, kv-head) fp32 scale:
+ *   k_scale, v_scale: [num_layers][num_pages][num_kv_heads]; NULL for other dtypes. */
+typedef struct {
+  const void *k_pages;
+  const void *v_pages;
+  const float *k_scale;
+  const float *v_scale;
+  int32_t num_pages;
+} kvprm_kv_cache;
+
+/* The candidates to score. Candidate b has L_b = lengths[b] cached tokens at positions
+ * 0..L_b-1; token t sits in logical page t / 16, slot t % 16, and logical page i maps to
+ * physical page page_table[b * max_pages + i]. Slots at or beyond L_b in the last page and
+ * table entries beyond ceil(L_b / 16) are never read (they may hold garbage or -1).
+ * The verify token sits at position L_b and attends to the L_b cached keys and its own key.
+ *
+ * Prefix-sharing hint (optional, a pure performance hint: results are defined by the page
+ * table alone): candidates [group_start_host[g], group_start_host[g+1]) share their first
+ * group_prefix_len_host[g] tokens, which must be a multiple of 16, at most every member's
+ * length, and held by the same physical pages in every member's row. Groups tile [0, B). */
+typedef struct {
+  int32_t batch;                        /* B >= 0 */
+  const int32_t *page_table;            /* device [B][max_pages] */
+  int32_t max_pages;                    /* >= 1 */
+  const int32_t *lengths;               /* device [B], 0 <= L_b <= max_pages * 16 */
+  const int32_t *lengths_host;          /* optional host mirror of lengths (validation) */
+  int32_t num_groups;                   /* 0 = no prefix-sharing hint */
+  const int32_t *group_start_host;      /* [num_groups + 1] */
+  const int32_t *group_prefix_len_host; /* [num_groups] */
+} kvprm_batch;
+
+/* Create a handle for one model shape. Returns KVPRM_E_UNSUPPORTED for shapes outside the list
+ * above. *out is set only on success. */
+kvprm_status kvprm_create(const kvprm_model_desc *desc, kvprm_handle *out);
+
+/* Release a handle (NULL is accepted). */
+kvprm_status kvprm_destroy(kvprm_handle h);
+
+/* Bytes of device workspace kvprm_score and kvprm_attention need for this batch (it depends on
+ * batch and max_pages only). */
+kvprm_status kvprm_workspace_size(kvprm_handle h, const kvprm_batch *batch, size_t *bytes);
+
+/* Eq. (score) for every candidate: scores[b] = P(+) in [0, 1] and, if logits != NULL,
+ * logits[b] = z_b = w_r . RMSNorm(x_b) + b_r (fp32, device [B]). The residual stream, queries,
+ * softmax state and accumulators are fp32; weights and cache are read at their stored
+ * precision. B = 0 returns KVPRM_OK and enqueues nothing. The workspace (device, 256-byte
+ * aligned, >= kvprm_workspace_size bytes) is scratch owned by the call until the stream
+ * passes it; its contents on entry do not matter. */
+kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *batch,
+                         const kvprm_readout_weights *weights, void *workspace, size_t ws_bytes,
+                         float *scores, float *logits, void *stream);
+
+/* The attention step of one layer alone (for tests and diagnostics): for every candidate b and
+ * q-head h, o[b][h] = softmax(q K^T / sqrt(d_h)) V over the L_b cached keys/values of `layer`
+ * and the extra key/value k_self[b][h / g], v_self[b][h / g] (the verify token's own).
+ * q: device fp32 [B][n_q][d_h] (already rotated); k_self, v_self: device fp32 [B][n_kv][d_h];
+ * o: device fp32 [B][n_q][d_h]. The prefix-sharing hint is honoured as in kvprm_score. */
+kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *batch,
+                             int32_t layer, const float *q, const float *k_self,
+                             const float *v_self, void *workspace, size_t ws_bytes, float *o,
+                             void *stream);
+
+/* Text of the last error on the calling thread ("" if none). Valid until the next call on
+ * this thread. */
+const char *kvprm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVPRM_H */

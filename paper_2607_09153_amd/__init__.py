@@ -1,0 +1,177 @@
+"""Python binding of libkvprm (KV-PRM verify-token scoring on MI355X).
+
+Argument marshalling only: every step of the scoring pass runs in the HIP kernels of
+``libkvprm.so``; this module maps the C structures of ``include/kvprm.h`` onto ctypes and
+raises on a non-OK status. Device memory and streams are the caller's (torch tensors and
+streams are the usual source; pass their ``data_ptr()`` and ``cuda_stream``).
+There is no fallback: if the library is not built, importing the binding raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvprm.so")
+
+KVPRM_OK, KVPRM_E_INVALID, KVPRM_E_UNSUPPORTED, KVPRM_E_WORKSPACE, KVPRM_E_HIP, KVPRM_E_INTERNAL = range(6)
+KVPRM_F32, KVPRM_BF16, KVPRM_FP8_E4M3 = 0, 1, 2
+DTYPE_CODE = {"f32": KVPRM_F32, "bf16": KVPRM_BF16, "fp8": KVPRM_FP8_E4M3}
+
+EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
+            "kvprm_attention", "kvprm_last_error"]
+
+
+class ModelDesc(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("rope_theta", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                ("weight_dtype", ctypes.c_int), ("kv_dtype", ctypes.c_int),
+                ("page_size", ctypes.c_int32)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")]
+
+
+class ReadoutWeights(ctypes.Structure):
+    _fields_ = [("layers", ctypes.POINTER(LayerWeights)), ("verify_embed", ctypes.c_void_p),
+                ("final_norm", ctypes.c_void_p), ("reward_w", ctypes.c_void_p),
+                ("reward_b", ctypes.c_float)]
+
+
+class KVCache(ctypes.Structure):
+    _fields_ = [("k_pages", ctypes.c_void_p), ("v_pages", ctypes.c_void_p),
+                ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p),
+                ("num_pages", ctypes.c_int32)]
+
+
+class Batch(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("page_table", ctypes.c_void_p),
+                ("max_pages", ctypes.c_int32), ("lengths", ctypes.c_void_p),
+                ("lengths_host", ctypes.POINTER(ctypes.c_int32)),
+                ("num_groups", ctypes.c_int32),
+                ("group_start_host", ctypes.POINTER(ctypes.c_int32)),
+                ("group_prefix_len_host", ctypes.POINTER(ctypes.c_int32))]
+
+
+class KvprmError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"kvprm status {status}: {msg}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built (run __graft_entry__.build()); "
+                          "the scoring pass has no non-GPU implementation")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    lib.kvprm_create.argtypes = [ctypes.POINTER(ModelDesc), ctypes.POINTER(vp)]
+    lib.kvprm_destroy.argtypes = [vp]
+    lib.kvprm_workspace_size.argtypes = [vp, ctypes.POINTER(Batch), ctypes.POINTER(sz)]
+    lib.kvprm_score.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
+                                ctypes.POINTER(ReadoutWeights), vp, sz, vp, vp, vp]
+    lib.kvprm_attention.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
+                                    ctypes.c_int32, vp, vp, vp, vp, sz, vp, vp]
+    for f in ("kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
+              "kvprm_attention"):
+        getattr(lib, f).restype = ctypes.c_int
+    lib.kvprm_last_error.argtypes = []
+    lib.kvprm_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load()
+
+
+def _check(st: int):
+    if st != KVPRM_OK:
+        raise KvprmError(st, lib.kvprm_last_error().decode())
+
+
+def kvprm_last_error() -> str:
+    return lib.kvprm_last_error().decode()
+
+
+def make_desc(num_layers, hidden, num_q_heads, num_kv_heads, head_dim, ffn_dim,
+              rope_theta=1.0e6, rms_eps=1.0e-6, weight_dtype="bf16", kv_dtype="bf16",
+              page_size=16) -> ModelDesc:
+    return ModelDesc(num_layers, hidden, num_q_heads, num_kv_heads, head_dim, ffn_dim,
+                     rope_theta, rms_eps, DTYPE_CODE[weight_dtype], DTYPE_CODE[kv_dtype],
+                     page_size)
+
+
+def kvprm_create(desc: ModelDesc) -> int:
+    h = ctypes.c_void_p()
+    _check(lib.kvprm_create(ctypes.byref(desc), ctypes.byref(h)))
+    return h.value
+
+
+def kvprm_destroy(handle: int) -> None:
+    _check(lib.kvprm_destroy(handle))
+
+
+def make_batch(batch: int, page_table_ptr: int, max_pages: int, lengths_ptr: int,
+               lengths_host: Optional[Sequence[int]] = None,
+               group_start: Optional[Sequence[int]] = None,
+               group_prefix_len: Optional[Sequence[int]] = None) -> Batch:
+    """Batch descriptor; host arrays are copied into ctypes buffers kept alive on the struct."""
+    b = Batch()
+    b.batch, b.page_table, b.max_pages, b.lengths = batch, page_table_ptr, max_pages, lengths_ptr
+    keep = []
+    if lengths_host is not None:
+        arr = (ctypes.c_int32 * len(lengths_host))(*lengths_host)
+        keep.append(arr)
+        b.lengths_host = ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))
+    if group_start:
+        gs = (ctypes.c_int32 * len(group_start))(*group_start)
+        gp = (ctypes.c_int32 * len(group_prefix_len))(*group_prefix_len)
+        keep += [gs, gp]
+        b.num_groups = len(group_prefix_len)
+        b.group_start_host = ctypes.cast(gs, ctypes.POINTER(ctypes.c_int32))
+        b.group_prefix_len_host = ctypes.cast(gp, ctypes.POINTER(ctypes.c_int32))
+    b._keep = keep
+    return b
+
+
+def make_cache(k_ptr: int, v_ptr: int, num_pages: int, k_scale_ptr: int = 0,
+               v_scale_ptr: int = 0) -> KVCache:
+    return KVCache(k_ptr, v_ptr, k_scale_ptr or None, v_scale_ptr or None, num_pages)
+
+
+def make_readout(layers: Sequence[dict], verify_embed: int, final_norm: int, reward_w: int,
+                 reward_b: float = 0.0) -> ReadoutWeights:
+    """layers: per layer a dict of device pointers with the LayerWeights field names."""
+    arr = (LayerWeights * len(layers))()
+    for i, d in enumerate(layers):
+        for name, _ in LayerWeights._fields_:
+            setattr(arr[i], name, d[name])
+    r = ReadoutWeights(ctypes.cast(arr, ctypes.POINTER(LayerWeights)), verify_embed, final_norm,
+                       reward_w, reward_b)
+    r._keep = arr
+    return r
+
+
+def kvprm_workspace_size(handle: int, batch: Batch) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.kvprm_workspace_size(handle, ctypes.byref(batch), ctypes.byref(n)))
+    return n.value
+
+
+def kvprm_score(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeights,
+                workspace_ptr: int, ws_bytes: int, scores_ptr: int, logits_ptr: int = 0,
+                stream: int = 0) -> None:
+    _check(lib.kvprm_score(handle, ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(weights),
+                           workspace_ptr, ws_bytes, scores_ptr, logits_ptr or None, stream or None))
+
+
+def kvprm_attention(handle: int, cache: KVCache, batch: Batch, layer: int, q_ptr: int,
+                    k_self_ptr: int, v_self_ptr: int, workspace_ptr: int, ws_bytes: int,
+                    o_ptr: int, stream: int = 0) -> None:
+    _check(lib.kvprm_attention(handle, ctypes.byref(cache), ctypes.byref(batch), layer, q_ptr,
+                               k_self_ptr, v_self_ptr, workspace_ptr, ws_bytes, o_ptr,
+                               stream or None))

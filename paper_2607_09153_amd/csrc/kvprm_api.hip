@@ -1,0 +1,242 @@
+// C ABI of libkvprm: argument validation, workspace carving and launch sequencing of the
+// verify-token pass. Nothing here allocates device memory or synchronises the host.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+
+#include "../../include/kvprm.h"
+#include "kvprm_internal.h"
+
+using namespace kvprm;
+
+struct kvprm_handle_s {
+  kvprm_model_desc desc;
+  Dims dm;
+};
+
+static thread_local std::string g_err;
+
+static kvprm_status fail(kvprm_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+static kvprm_status fail(kvprm_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+static kvprm_status ok() {
+  g_err.clear();
+  return KVPRM_OK;
+}
+
+#define HIP_TRY(expr, what)                                                                  \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(KVPRM_E_HIP, "%s: %s", what, hipGetErrorString(e_)); \
+  } while (0)
+
+extern "C" {
+
+const char *kvprm_last_error(void) { return g_err.c_str(); }
+
+kvprm_status kvprm_create(const kvprm_model_desc *d, kvprm_handle *out) {
+  if (!d || !out) return fail(KVPRM_E_INVALID, "kvprm_create: null argument");
+  if (d->num_layers < 1 || d->hidden < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1 ||
+      d->head_dim < 1 || d->ffn_dim < 1)
+    return fail(KVPRM_E_INVALID, "kvprm_create: sizes must be positive");
+  if (d->num_q_heads % d->num_kv_heads != 0)
+    return fail(KVPRM_E_INVALID, "kvprm_create: num_q_heads %% num_kv_heads != 0");
+  if (!(d->rms_eps >= 0.f) || !(d->rope_theta > 0.f))
+    return fail(KVPRM_E_INVALID, "kvprm_create: rms_eps must be >= 0 and rope_theta > 0");
+  if (d->page_size != 16) return fail(KVPRM_E_UNSUPPORTED, "kvprm_create: page_size must be 16");
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(KVPRM_E_UNSUPPORTED, "kvprm_create: head_dim must be 64 or 128");
+  if (d->num_q_heads / d->num_kv_heads > 16)
+    return fail(KVPRM_E_UNSUPPORTED, "kvprm_create: at most 16 query heads per kv-head");
+  if (d->hidden % 64 != 0 || d->ffn_dim % 64 != 0 || (d->num_q_heads * d->head_dim) % 64 != 0)
+    return fail(KVPRM_E_UNSUPPORTED, "kvprm_create: hidden, ffn_dim, n_q*d_h must be multiples of 64");
+  const bool f32 = d->weight_dtype == KVPRM_F32 && d->kv_dtype == KVPRM_F32;
+  const bool bf = d->weight_dtype == KVPRM_BF16 &&
+                  (d->kv_dtype == KVPRM_BF16 || d->kv_dtype == KVPRM_FP8_E4M3);
+  if (!f32 && !bf)
+    return fail(KVPRM_E_UNSUPPORTED,
+                "kvprm_create: dtype pair must be (F32, F32), (BF16, BF16) or (BF16, FP8_E4M3)");
+  kvprm_handle h = new (std::nothrow) kvprm_handle_s;
+  if (!h) return fail(KVPRM_E_INTERNAL, "kvprm_create: out of host memory");
+  h->desc = *d;
+  Dims &m = h->dm;
+  m.layers = d->num_layers;
+  m.H = d->hidden;
+  m.nq = d->num_q_heads;
+  m.nkv = d->num_kv_heads;
+  m.d = d->head_dim;
+  m.F = d->ffn_dim;
+  m.g = d->num_q_heads / d->num_kv_heads;
+  m.theta = d->rope_theta;
+  m.eps = d->rms_eps;
+  m.wdt = d->weight_dtype == KVPRM_BF16 ? 1 : 0;
+  m.kvdt = d->kv_dtype == KVPRM_F32 ? 0 : (d->kv_dtype == KVPRM_BF16 ? 1 : 2);
+  *out = h;
+  return ok();
+}
+
+kvprm_status kvprm_destroy(kvprm_handle h) {
+  delete h;
+  return ok();
+}
+
+static kvprm_status check_batch(const kvprm_handle h, const kvprm_batch *b, const char *fn) {
+  if (!b) return fail(KVPRM_E_INVALID, "%s: null batch", fn);
+  if (b->batch < 0) return fail(KVPRM_E_INVALID, "%s: batch < 0", fn);
+  if (b->batch == 0) return KVPRM_OK;
+  if (b->batch > 256) return fail(KVPRM_E_UNSUPPORTED, "%s: at most 256 candidates per call", fn);
+  if (!b->page_table || !b->lengths) return fail(KVPRM_E_INVALID, "%s: null page_table or lengths", fn);
+  if (b->max_pages < 1) return fail(KVPRM_E_INVALID, "%s: max_pages < 1", fn);
+  const int cap = b->max_pages * h->desc.page_size;
+  if (b->lengths_host)
+    for (int i = 0; i < b->batch; ++i)
+      if (b->lengths_host[i] < 0 || b->lengths_host[i] > cap)
+        return fail(KVPRM_E_INVALID, "%s: lengths[%d] = %d outside [0, %d]", fn, i,
+                    b->lengths_host[i], cap);
+  if (b->num_groups < 0) return fail(KVPRM_E_INVALID, "%s: num_groups < 0", fn);
+  if (b->num_groups > 0) {
+    const int *s = b->group_start_host, *pl = b->group_prefix_len_host;
+    if (!s || !pl) return fail(KVPRM_E_INVALID, "%s: null group arrays", fn);
+    if (s[0] != 0 || s[b->num_groups] != b->batch)
+      return fail(KVPRM_E_INVALID, "%s: groups must tile [0, batch)", fn);
+    for (int g = 0; g < b->num_groups; ++g) {
+      if (s[g + 1] <= s[g]) return fail(KVPRM_E_INVALID, "%s: group %d is empty or unordered", fn, g);
+      if (pl[g] < 0 || pl[g] % h->desc.page_size != 0 || pl[g] > cap)
+        return fail(KVPRM_E_INVALID, "%s: group %d prefix %d not a page multiple in [0, %d]", fn,
+                    g, pl[g], cap);
+      if (b->lengths_host)
+        for (int i = s[g]; i < s[g + 1]; ++i)
+          if (b->lengths_host[i] < pl[g])
+            return fail(KVPRM_E_INVALID, "%s: candidate %d shorter than its group prefix", fn, i);
+    }
+  }
+  return KVPRM_OK;
+}
+
+static kvprm_status check_cache(const kvprm_handle h, const kvprm_kv_cache *c, const char *fn) {
+  if (!c || !c->k_pages || !c->v_pages) return fail(KVPRM_E_INVALID, "%s: null cache pool", fn);
+  if (c->num_pages < 1) return fail(KVPRM_E_INVALID, "%s: num_pages < 1", fn);
+  if (h->dm.kvdt == 2 && (!c->k_scale || !c->v_scale))
+    return fail(KVPRM_E_INVALID, "%s: fp8 cache needs k_scale and v_scale", fn);
+  return KVPRM_OK;
+}
+
+static size_t ws_bytes_for(const kvprm_handle h, const kvprm_batch *b) {
+  Plan p = make_plan(h->dm, b->batch, b->max_pages);
+  return carve(h->dm, p, nullptr).bytes;
+}
+
+kvprm_status kvprm_workspace_size(kvprm_handle h, const kvprm_batch *b, size_t *bytes) {
+  if (!h || !bytes) return fail(KVPRM_E_INVALID, "kvprm_workspace_size: null argument");
+  kvprm_status st = check_batch(h, b, "kvprm_workspace_size");
+  if (st != KVPRM_OK) return st;
+  *bytes = b->batch == 0 ? 0 : ws_bytes_for(h, b);
+  return ok();
+}
+
+static kvprm_status check_ws(const kvprm_handle h, const kvprm_batch *b, void *ws, size_t n,
+                             const char *fn) {
+  const size_t need = ws_bytes_for(h, b);
+  if (!ws || n < need)
+    return fail(KVPRM_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                ws ? n : (size_t)0);
+  if (((uintptr_t)ws & 255) != 0) return fail(KVPRM_E_WORKSPACE, "%s: workspace not 256-byte aligned", fn);
+  return KVPRM_OK;
+}
+
+static GroupTable group_table(const kvprm_batch *) {
+  GroupTable gt;
+  memset(&gt, 0, sizeof gt);
+  return gt;
+}
+
+kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                         const kvprm_readout_weights *wts, void *workspace, size_t ws_bytes,
+                         float *scores, float *logits, void *stream) {
+  const char *fn = "kvprm_score";
+  if (!h) return fail(KVPRM_E_INVALID, "%s: null handle", fn);
+  kvprm_status st = check_batch(h, b, fn);
+  if (st != KVPRM_OK) return st;
+  if (b->batch == 0) return ok();
+  if ((st = check_cache(h, cache, fn)) != KVPRM_OK) return st;
+  if (!wts || !wts->layers || !wts->verify_embed || !wts->final_norm || !wts->reward_w)
+    return fail(KVPRM_E_INVALID, "%s: null readout weights", fn);
+  for (int l = 0; l < h->dm.layers; ++l) {
+    const kvprm_layer_weights &W = wts->layers[l];
+    if (!W.attn_norm || !W.wq || !W.wk || !W.wv || !W.wo || !W.ffn_norm || !W.w_gate ||
+        !W.w_up || !W.w_down)
+      return fail(KVPRM_E_INVALID, "%s: null weight in layer %d", fn, l);
+  }
+  if (!scores) return fail(KVPRM_E_INVALID, "%s: null scores", fn);
+  if ((st = check_ws(h, b, workspace, ws_bytes, fn)) != KVPRM_OK) return st;
+
+  const Dims &dm = h->dm;
+  hipStream_t s = (hipStream_t)stream;
+  const Plan p = make_plan(dm, b->batch, b->max_pages);
+  const Workspace w = carve(dm, p, workspace);
+  const GroupTable gt = group_table(b);
+  HIP_TRY(launch_init(dm, p, w, wts->verify_embed, s), "init");
+  for (int l = 0; l < dm.layers; ++l) {
+    const kvprm_layer_weights &W = wts->layers[l];
+    GemvSegs qkv{{W.wq, W.wk, W.wv}, {dm.nq * dm.d, dm.nkv * dm.d, dm.nkv * dm.d}, 3};
+    HIP_TRY(launch_gemv(dm, p, qkv, dm.H, p.kslice_qkv, p.ks_qkv, w.x, W.attn_norm, w.ss, w.part, s),
+            "qkv projection");
+    HIP_TRY(launch_qkv_finish(dm, p, w, b->lengths, s), "rotary");
+    HIP_TRY(launch_attention(dm, p, w, l, cache->k_pages, cache->v_pages, cache->k_scale,
+                             cache->v_scale, cache->num_pages, b->page_table, b->lengths, gt, w.q,
+                             w.kself, w.vself, w.o, s),
+            "attention");
+    GemvSegs wo{{W.wo, nullptr, nullptr}, {dm.H, 0, 0}, 1};
+    HIP_TRY(launch_gemv(dm, p, wo, dm.nq * dm.d, p.kslice_o, p.ks_o, w.o, nullptr, nullptr, w.part, s),
+            "output projection");
+    HIP_TRY(launch_residual(dm, p, w, p.ks_o, s), "residual");
+    GemvSegs gu{{W.w_gate, W.w_up, nullptr}, {dm.F, dm.F, 0}, 2};
+    HIP_TRY(launch_gemv(dm, p, gu, dm.H, p.kslice_gu, p.ks_gu, w.x, W.ffn_norm, w.ss, w.part, s),
+            "gate/up projection");
+    HIP_TRY(launch_swiglu(dm, p, w, p.ks_gu, s), "swiglu");
+    GemvSegs dn{{W.w_down, nullptr, nullptr}, {dm.H, 0, 0}, 1};
+    HIP_TRY(launch_gemv(dm, p, dn, dm.F, p.kslice_d, p.ks_d, w.hffn, nullptr, nullptr, w.part, s),
+            "down projection");
+    HIP_TRY(launch_residual(dm, p, w, p.ks_d, s), "residual");
+  }
+  HIP_TRY(launch_head(dm, p, w, wts->final_norm, wts->reward_w, wts->reward_b, scores, logits, s),
+          "reward head");
+  return ok();
+}
+
+kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                             int32_t layer, const float *q, const float *k_self,
+                             const float *v_self, void *workspace, size_t ws_bytes, float *o,
+                             void *stream) {
+  const char *fn = "kvprm_attention";
+  if (!h) return fail(KVPRM_E_INVALID, "%s: null handle", fn);
+  kvprm_status st = check_batch(h, b, fn);
+  if (st != KVPRM_OK) return st;
+  if (b->batch == 0) return ok();
+  if ((st = check_cache(h, cache, fn)) != KVPRM_OK) return st;
+  if (layer < 0 || layer >= h->dm.layers)
+    return fail(KVPRM_E_INVALID, "%s: layer %d outside [0, %d)", fn, layer, h->dm.layers);
+  if (!q || !k_self || !v_self || !o) return fail(KVPRM_E_INVALID, "%s: null q/k_self/v_self/o", fn);
+  if ((st = check_ws(h, b, workspace, ws_bytes, fn)) != KVPRM_OK) return st;
+  const Dims &dm = h->dm;
+  const Plan p = make_plan(dm, b->batch, b->max_pages);
+  const Workspace w = carve(dm, p, workspace);
+  HIP_TRY(launch_attention(dm, p, w, layer, cache->k_pages, cache->v_pages, cache->k_scale,
+                           cache->v_scale, cache->num_pages, b->page_table, b->lengths,
+                           group_table(b), q, k_self, v_self, o, (hipStream_t)stream),
+          "attention");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,601 @@
+// HIP kernels of the verify-token pass (gfx950). Vector-ALU versions for every dtype; the
+// matrix-core (MFMA) kernels for bf16 weights and bf16/fp8 caches live in kvprm_mfma.hip.
+//
+// Per layer the pass runs: RMSNorm+QKV projection (split-K partials) -> sum partials + rotary
+// -> split-L paged attention partials -> log-sum-exp merge with the token's own key -> output
+// projection -> residual add -> RMSNorm+gate/up projection -> SwiGLU -> down projection ->
+// residual add; after the last layer the final RMSNorm and the reward head.
+// Every reduction has a fixed order, so results are bitwise reproducible run to run.
+#include <math.h>
+
+#include "kvprm_internal.h"
+
+namespace kvprm {
+
+// ------------------------------------------------------------------------------- helpers
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+__device__ __forceinline__ float load_scalar(const void *p, size_t i, int wdt) {
+  return wdt ? bf16_bits_to_f32(((const uint16_t *)p)[i]) : ((const float *)p)[i];
+}
+
+// OCP E4M3FN code -> fp32 (exact). Exponent 0: subnormal m/8 * 2^-6.
+__device__ __forceinline__ float e4m3_to_f32(uint32_t c) {
+  uint32_t s = (c & 0x80u) << 24;
+  uint32_t e = (c >> 3) & 0xFu;
+  uint32_t m = c & 0x7u;
+  float v;
+  if (e == 0) {
+    v = (float)m * 0.001953125f;  // m * 2^-9
+  } else {
+    v = __uint_as_float(((e + 120u) << 23) | (m << 20));
+  }
+  if (e == 15u && m == 7u) v = __uint_as_float(0x7FC00000u);
+  return __uint_as_float(__float_as_uint(v) | s);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// Sum over a 256-thread block; every thread gets the result. red must hold 4 floats.
+__device__ __forceinline__ float block_sum256(float v, float *red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// ------------------------------------------------------------------------------- plan
+
+Plan make_plan(const Dims &dm, int B, int max_pages) {
+  Plan p{};
+  p.B = B;
+  p.max_pages = max_pages;
+  p.nch = (max_pages + kChunkPages - 1) / kChunkPages;
+  p.nss = (dm.H + 255) / 256;
+  // split-K slices: the activation slice of all B candidates is staged in LDS (<= 32 KiB)
+  auto slice = [&](int K) {
+    int s = (8192 / (B > 0 ? B : 1)) & ~63;
+    if (s < 64) s = 64;
+    if (s > K) s = K;
+    return s;
+  };
+  p.kslice_qkv = slice(dm.H);
+  p.kslice_o = slice(dm.nq * dm.d);
+  p.kslice_gu = slice(dm.H);
+  p.kslice_d = slice(dm.F);
+  p.ks_qkv = (dm.H + p.kslice_qkv - 1) / p.kslice_qkv;
+  p.ks_o = (dm.nq * dm.d + p.kslice_o - 1) / p.kslice_o;
+  p.ks_gu = (dm.H + p.kslice_gu - 1) / p.kslice_gu;
+  p.ks_d = (dm.F + p.kslice_d - 1) / p.kslice_d;
+  size_t a = (size_t)p.ks_qkv * (dm.nq + 2 * dm.nkv) * dm.d;
+  size_t b2 = (size_t)p.ks_o * dm.H;
+  size_t c = (size_t)p.ks_gu * 2 * dm.F;
+  size_t e = (size_t)p.ks_d * dm.H;
+  size_t m = a > b2 ? a : b2;
+  m = m > c ? m : c;
+  m = m > e ? m : e;
+  p.part_elems = m * (size_t)B;
+  return p;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+Workspace carve(const Dims &dm, const Plan &p, void *base) {
+  Workspace w{};
+  char *c = (char *)base;
+  size_t off = 0;
+  auto take = [&](size_t elems) {
+    float *r = base ? (float *)(c + off) : nullptr;
+    off += align256(elems * sizeof(float));
+    return r;
+  };
+  const size_t B = (size_t)p.B;
+  w.x = take(B * dm.H);
+  w.ss = take((size_t)p.nss * B);
+  w.part = take(p.part_elems);
+  w.q = take(B * dm.nq * dm.d);
+  w.kself = take(B * dm.nkv * dm.d);
+  w.vself = take(B * dm.nkv * dm.d);
+  w.apart = take(B * dm.nq * (size_t)p.nch * (dm.d + 2));
+  w.o = take(B * dm.nq * dm.d);
+  w.hffn = take(B * dm.F);
+  w.bytes = off;
+  return w;
+}
+
+// ------------------------------------------------------------------------------- init
+
+// x[b] = e_v for every candidate (the verify token's embedding); ss = its sum of squares per
+// 256-row block.
+__global__ __launch_bounds__(256) void k_init(float *x, float *ss, const void *ev, int wdt, int B,
+                                              int H) {
+  __shared__ float red[4];
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  float v = (r < H) ? load_scalar(ev, r, wdt) : 0.f;
+  if (r < H)
+    for (int b = 0; b < B; ++b) x[(size_t)b * H + r] = v;
+  float t = block_sum256(v * v, red);
+  if (threadIdx.x == 0)
+    for (int b = 0; b < B; ++b) ss[(size_t)blockIdx.x * B + b] = t;
+}
+
+hipError_t launch_init(const Dims &dm, const Plan &p, const Workspace &w, const void *verify_embed,
+                       hipStream_t s) {
+  hipLaunchKernelGGL(k_init, dim3(p.nss), dim3(256), 0, s, w.x, w.ss, verify_embed, dm.wdt, p.B,
+                     dm.H);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------- GEMV (VALU)
+
+// One thread per output row; the block's K-slice of the (normalised) activations of all
+// candidates sits in LDS and is read as broadcasts. Partials: part[ks][row][b].
+template <int WDT>
+__global__ __launch_bounds__(256) void k_gemv_valu(GemvSegs segs, int rows_total, int K, int kslice,
+                                                   const float *in, const void *gamma,
+                                                   const float *ss, int nss, float eps, int B,
+                                                   float *part) {
+  extern __shared__ float u_s[];  // [B][kslice]
+  __shared__ float inv_s[256];
+  const int k0 = blockIdx.y * kslice;
+  const int kn = min(kslice, K - k0);
+  if (gamma) {
+    for (int b = threadIdx.x; b < B; b += 256) {
+      float t = 0.f;
+      for (int i = 0; i < nss; ++i) t += ss[(size_t)i * B + b];
+      inv_s[b] = 1.0f / sqrtf(t / (float)K + eps);
+    }
+    __syncthreads();
+  }
+  for (int i = threadIdx.x; i < B * kn; i += 256) {
+    const int b = i / kn, k = i - b * kn;
+    float v = in[(size_t)b * K + k0 + k];
+    if (gamma) v = v * inv_s[b] * load_scalar(gamma, k0 + k, WDT);
+    u_s[b * kslice + k] = v;
+  }
+  __syncthreads();
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= rows_total) return;
+  int seg = 0, base = 0;
+  while (seg < segs.nseg - 1 && r >= base + segs.rows[seg]) base += segs.rows[seg++];
+  const size_t roff = (size_t)(r - base) * K + k0;
+  constexpr int NB = 8;
+  for (int b0 = 0; b0 < B; b0 += NB) {
+    float acc[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[j] = 0.f;
+    if (WDT == 1) {
+      const uint4 *wp = (const uint4 *)((const uint16_t *)segs.w[seg] + roff);
+      for (int k = 0; k < kn; k += 8) {
+        uint4 wv = wp[k >> 3];
+        float wf[8] = {bf16_bits_to_f32(wv.x & 0xFFFF), bf16_bits_to_f32(wv.x >> 16),
+                       bf16_bits_to_f32(wv.y & 0xFFFF), bf16_bits_to_f32(wv.y >> 16),
+                       bf16_bits_to_f32(wv.z & 0xFFFF), bf16_bits_to_f32(wv.z >> 16),
+                       bf16_bits_to_f32(wv.w & 0xFFFF), bf16_bits_to_f32(wv.w >> 16)};
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          if (b0 + j < B) {
+            const float *u = u_s + (b0 + j) * kslice + k;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[j] += wf[e] * u[e];
+          }
+        }
+      }
+    } else {
+      const float4 *wp = (const float4 *)((const float *)segs.w[seg] + roff);
+      for (int k = 0; k < kn; k += 4) {
+        float4 wv = wp[k >> 2];
+        float wf[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          if (b0 + j < B) {
+            const float *u = u_s + (b0 + j) * kslice + k;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[j] += wf[e] * u[e];
+          }
+        }
+      }
+    }
+    float *out = part + ((size_t)blockIdx.y * rows_total + r) * B;
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      if (b0 + j < B) out[b0 + j] = acc[j];
+  }
+}
+
+hipError_t launch_gemv(const Dims &dm, const Plan &p, const GemvSegs &segs, int K, int kslice,
+                       int ksplit, const float *in, const void *gamma, const float *ss,
+                       float *part, hipStream_t s) {
+  int rows = 0;
+  for (int i = 0; i < segs.nseg; ++i) rows += segs.rows[i];
+  dim3 grid((rows + 255) / 256, ksplit);
+  size_t lds = (size_t)p.B * kslice * sizeof(float);
+  if (dm.wdt == 1)
+    hipLaunchKernelGGL(k_gemv_valu<1>, grid, dim3(256), lds, s, segs, rows, K, kslice, in, gamma,
+                       ss, p.nss, dm.eps, p.B, part);
+  else
+    hipLaunchKernelGGL(k_gemv_valu<0>, grid, dim3(256), lds, s, segs, rows, K, kslice, in, gamma,
+                       ss, p.nss, dm.eps, p.B, part);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------- q/k/v + rotary
+
+// Sums the split-K partials of the fused q|k|v projection and rotates q and k at position L_b
+// (rotate-half: pair (i, i + d/2) by angle L_b * theta^(-2i/d), evaluated in fp64).
+__global__ void k_qkv_finish(const float *part, int ksplit, int rows_total, int B, int nq, int nkv,
+                             int d, float theta, const int32_t *lengths, float *q, float *ks,
+                             float *vs) {
+  const int b = blockIdx.x, head = blockIdx.y, i = threadIdx.x;  // i < d/2
+  const int r0 = head * d + i, r1 = r0 + d / 2;
+  float a = 0.f, c = 0.f;
+  for (int k = 0; k < ksplit; ++k) {
+    a += part[((size_t)k * rows_total + r0) * B + b];
+    c += part[((size_t)k * rows_total + r1) * B + b];
+  }
+  float oa = a, oc = c;
+  if (head < nq + nkv) {
+    const double pos = (double)lengths[b];
+    const double inv = pow((double)theta, (-2.0 * (double)i) / (double)d);
+    double sn, cs;
+    sincos(pos * inv, &sn, &cs);
+    oa = (float)((double)a * cs - (double)c * sn);
+    oc = (float)((double)c * cs + (double)a * sn);
+  }
+  float *dst;
+  if (head < nq)
+    dst = q + ((size_t)b * nq + head) * d;
+  else if (head < nq + nkv)
+    dst = ks + ((size_t)b * nkv + (head - nq)) * d;
+  else
+    dst = vs + ((size_t)b * nkv + (head - nq - nkv)) * d;
+  dst[i] = oa;
+  dst[i + d / 2] = oc;
+}
+
+hipError_t launch_qkv_finish(const Dims &dm, const Plan &p, const Workspace &w,
+                             const int32_t *lengths, hipStream_t s) {
+  const int rows = (dm.nq + 2 * dm.nkv) * dm.d;
+  hipLaunchKernelGGL(k_qkv_finish, dim3(p.B, dm.nq + 2 * dm.nkv), dim3(dm.d / 2), 0, s, w.part,
+                     p.ks_qkv, rows, p.B, dm.nq, dm.nkv, dm.d, dm.theta, lengths, w.q, w.kself,
+                     w.vself);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------- attention (VALU)
+
+template <int KVT>
+__device__ __forceinline__ float kv_elem(const void *tile, int idx) {
+  if (KVT == 0) return ((const float *)tile)[idx];
+  if (KVT == 1) return bf16_bits_to_f32(((const uint16_t *)tile)[idx]);
+  return e4m3_to_f32(((const uint8_t *)tile)[idx]);
+}
+
+// One block per (chunk of kChunkPages pages, kv-head j, candidate b) over the candidate's
+// private pages [first_page, npages). Writes unnormalised partials for the g q-heads of j:
+// acc = sum_t e^{s_t - m} V_t, m = max_t s_t, l = sum_t e^{s_t - m}; an empty chunk writes
+// m = -inf, l = 0.
+template <int KVT, int D>
+__global__ __launch_bounds__(256) void k_attn_valu(const void *kpool, const void *vpool,
+                                                   const float *kscale, const float *vscale,
+                                                   int nkv, int g, const int32_t *page_table,
+                                                   int max_pages, const int32_t *lengths,
+                                                   GroupTable gt, int nch, const float *q,
+                                                   float *apart, int nq) {
+  constexpr int EB = KVT == 0 ? 4 : (KVT == 1 ? 2 : 1);
+  constexpr int X = 16 / EB;
+  constexpr int T = kChunkPages * kPage;  // tokens per chunk
+  constexpr int NT = 256 / D;             // token groups in the PV phase
+  __shared__ float q_s[16][D];
+  __shared__ float s_s[16][T];
+  __shared__ float acc_s[NT][16][D];
+  __shared__ float ml_s[16][2];
+  __shared__ int phys_s[kChunkPages];
+  __shared__ float ksc_s[kChunkPages], vsc_s[kChunkPages];
+
+  const int c = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  const int L = lengths[b];
+  const int npages = (L + kPage - 1) / kPage;
+  int first = 0;
+  for (int gi = 0; gi < gt.n; ++gi)
+    if (b >= gt.start[gi] && b < gt.start[gi + 1]) first = gt.prefix_pages[gi];
+  const int p0 = first + c * kChunkPages;
+  float *outbase = apart + (((size_t)b * nq + (size_t)j * g) * nch + c) * (D + 2);
+  const size_t hstride = (size_t)nch * (D + 2);
+  if (p0 >= npages) {
+    for (int i = threadIdx.x; i < g * (D + 2); i += 256) {
+      const int h = i / (D + 2), e = i - h * (D + 2);
+      outbase[h * hstride + e] = (e == D) ? -INFINITY : 0.f;
+    }
+    return;
+  }
+  const int p1 = min(npages, p0 + kChunkPages);
+  const int tok0 = p0 * kPage;
+  const int ntok = min(L, p1 * kPage) - tok0;
+  for (int i = threadIdx.x; i < g * D; i += 256) {
+    const int h = i / D, m = i - h * D;
+    q_s[h][m] = q[((size_t)b * nq + j * g + h) * D + m];
+  }
+  for (int i = threadIdx.x; i < p1 - p0; i += 256) {
+    const int ph = page_table[(size_t)b * max_pages + p0 + i];
+    phys_s[i] = ph;
+    if (KVT == 2) {
+      ksc_s[i] = kscale[(size_t)ph * nkv + j];
+      vsc_s[i] = vscale[(size_t)ph * nkv + j];
+    }
+  }
+  __syncthreads();
+  const float rs = 1.0f / sqrtf((float)D);
+  // scores
+  for (int t = threadIdx.x; t < T; t += 256) {
+    float s[16];
+#pragma unroll
+    for (int h = 0; h < 16; ++h) s[h] = 0.f;
+    if (t < ntok) {
+      const int pg = t / kPage, slot = t % kPage;
+      const char *tile = (const char *)kpool + ((size_t)phys_s[pg] * nkv + j) * (kPage * D) * EB;
+      for (int m0 = 0; m0 < D; m0 += X) {
+#pragma unroll
+        for (int e = 0; e < X; ++e) {
+          const float kv = kv_elem<KVT>(tile, ((m0 / X) * kPage + slot) * X + e);
+#pragma unroll
+          for (int h = 0; h < 16; ++h)
+            if (h < g) s[h] += q_s[h][m0 + e] * kv;
+        }
+      }
+      const float sc = (KVT == 2) ? ksc_s[pg] * rs : rs;
+#pragma unroll
+      for (int h = 0; h < 16; ++h)
+        if (h < g) s_s[h][t] = s[h] * sc;
+    } else {
+#pragma unroll
+      for (int h = 0; h < 16; ++h)
+        if (h < g) s_s[h][t] = -INFINITY;
+    }
+  }
+  __syncthreads();
+  // softmax statistics per head: one wave per head
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int h = wv; h < g; h += 4) {
+    float m = -INFINITY;
+    for (int t = lane; t < T; t += 64) m = fmaxf(m, s_s[h][t]);
+    m = wave_max(m);
+    float l = 0.f;
+    for (int t = lane; t < T; t += 64) {
+      const float pv = (t < ntok) ? expf(s_s[h][t] - m) : 0.f;
+      s_s[h][t] = pv;
+      l += pv;
+    }
+    l = wave_sum(l);
+    if (lane == 0) {
+      ml_s[h][0] = m;
+      ml_s[h][1] = l;
+    }
+  }
+  __syncthreads();
+  // P V: thread (dim m, token group tg)
+  {
+    const int m = threadIdx.x % D, tg = threadIdx.x / D;
+    float acc[16];
+#pragma unroll
+    for (int h = 0; h < 16; ++h) acc[h] = 0.f;
+    const int npg = p1 - p0;
+    for (int pg = tg; pg < npg; pg += NT) {
+      const char *tile = (const char *)vpool + ((size_t)phys_s[pg] * nkv + j) * (kPage * D) * EB;
+      const float vsc = (KVT == 2) ? vsc_s[pg] : 1.f;
+      const int nslot = min(kPage, ntok - pg * kPage);
+      for (int sl = 0; sl < nslot; ++sl) {
+        const float v = kv_elem<KVT>(tile, m * kPage + sl) * vsc;
+        const int t = pg * kPage + sl;
+#pragma unroll
+        for (int h = 0; h < 16; ++h)
+          if (h < g) acc[h] += s_s[h][t] * v;
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < 16; ++h)
+      if (h < g) acc_s[tg][h][m] = acc[h];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < g * D; i += 256) {
+    const int h = i / D, m = i - h * D;
+    float a = 0.f;
+    for (int tg = 0; tg < NT; ++tg) a += acc_s[tg][h][m];
+    outbase[h * hstride + m] = a;
+  }
+  if (threadIdx.x < g) {
+    outbase[threadIdx.x * hstride + D] = ml_s[threadIdx.x][0];
+    outbase[threadIdx.x * hstride + D + 1] = ml_s[threadIdx.x][1];
+  }
+}
+
+// Log-sum-exp merge of the chunk partials with the token's own key/value:
+// m = max(m_c, s_self), o = (sum_c e^{m_c - m} acc_c + e^{s_self - m} v_self) /
+//                           (sum_c e^{m_c - m} l_c + e^{s_self - m}).
+template <int D>
+__global__ __launch_bounds__(D) void k_merge(const float *apart, int nch, GroupTable gt,
+                                             const float *q,
+                                             const float *kself, const float *vself,
+                                             const int32_t *lengths, float *o, int nq, int nkv,
+                                             int g) {
+  __shared__ float red[2];
+  const int b = blockIdx.x, h = blockIdx.y, m = threadIdx.x;
+  const int j = h / g;
+  float prod = q[((size_t)b * nq + h) * D + m] * kself[((size_t)b * nkv + j) * D + m];
+  prod = wave_sum(prod);
+  if (D > 64) {
+    if ((m & 63) == 0) red[m >> 6] = prod;
+    __syncthreads();
+    prod = red[0] + red[1];
+  }
+  const float s_self = prod * (1.0f / sqrtf((float)D));
+  const int L = lengths[b];
+  const int npages = (L + kPage - 1) / kPage;
+  int first = 0;
+  for (int gi = 0; gi < gt.n; ++gi)
+    if (b >= gt.start[gi] && b < gt.start[gi + 1]) first = gt.prefix_pages[gi];
+  const int nc = (npages - first + kChunkPages - 1) / kChunkPages;
+  const float *pb = apart + ((size_t)b * nq + h) * nch * (D + 2);
+  float mx = s_self;
+  for (int c = 0; c < nc; ++c) mx = fmaxf(mx, pb[(size_t)c * (D + 2) + D]);
+  float es = expf(s_self - mx);
+  float l = es;
+  float acc = es * vself[((size_t)b * nkv + j) * D + m];
+  for (int c = 0; c < nc; ++c) {
+    const float *pc = pb + (size_t)c * (D + 2);
+    const float f = expf(pc[D] - mx);
+    l += f * pc[D + 1];
+    acc += f * pc[m];
+  }
+  o[((size_t)b * nq + h) * D + m] = acc / l;
+}
+
+hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, int layer,
+                            const void *kpool, const void *vpool, const float *kscale,
+                            const float *vscale, int num_pages, const int32_t *page_table,
+                            const int32_t *lengths, const GroupTable &gt, const float *q,
+                            const float *kself, const float *vself, float *o, hipStream_t s) {
+  const int EB = dm.kvdt == 0 ? 4 : (dm.kvdt == 1 ? 2 : 1);
+  const size_t layer_elems = (size_t)num_pages * dm.nkv * kPage * dm.d;
+  const char *kp = (const char *)kpool + layer_elems * EB * layer;
+  const char *vp = (const char *)vpool + layer_elems * EB * layer;
+  const float *ksc = kscale ? kscale + (size_t)layer * num_pages * dm.nkv : nullptr;
+  const float *vsc = vscale ? vscale + (size_t)layer * num_pages * dm.nkv : nullptr;
+  dim3 grid(p.nch, dm.nkv, p.B);
+#define KVPRM_ATT(KVT, D)                                                                     \
+  hipLaunchKernelGGL((k_attn_valu<KVT, D>), grid, dim3(256), 0, s, kp, vp, ksc, vsc, dm.nkv, \
+                     dm.g, page_table, p.max_pages, lengths, gt, p.nch, q, w.apart, dm.nq)
+  if (dm.d == 64) {
+    if (dm.kvdt == 0) KVPRM_ATT(0, 64);
+    else if (dm.kvdt == 1) KVPRM_ATT(1, 64);
+    else KVPRM_ATT(2, 64);
+  } else {
+    if (dm.kvdt == 0) KVPRM_ATT(0, 128);
+    else if (dm.kvdt == 1) KVPRM_ATT(1, 128);
+    else KVPRM_ATT(2, 128);
+  }
+#undef KVPRM_ATT
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (dm.d == 64)
+    hipLaunchKernelGGL(k_merge<64>, dim3(p.B, dm.nq), dim3(64), 0, s, w.apart, p.nch, gt, q,
+                       kself, vself, lengths, o, dm.nq, dm.nkv, dm.g);
+  else
+    hipLaunchKernelGGL(k_merge<128>, dim3(p.B, dm.nq), dim3(128), 0, s, w.apart, p.nch, gt, q,
+                       kself, vself, lengths, o, dm.nq, dm.nkv, dm.g);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------- residual
+
+// x[b][r] += sum_ks part[ks][r][b]; ss[blk][b] = sum over the block's rows of x^2.
+__global__ __launch_bounds__(256) void k_residual(float *x, const float *part, int ksplit, float *ss,
+                                                  int B, int H) {
+  __shared__ float red[4][64];
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int b0 = 0; b0 < B; b0 += 64) {
+    for (int bb = 0; bb < 64 && b0 + bb < B; ++bb) {
+      const int b = b0 + bb;
+      float v = 0.f;
+      if (r < H) {
+        float a = 0.f;
+        for (int k = 0; k < ksplit; ++k) a += part[((size_t)k * H + r) * B + b];
+        v = x[(size_t)b * H + r] + a;
+        x[(size_t)b * H + r] = v;
+      }
+      const float t = wave_sum(v * v);
+      if (lane == 0) red[wv][bb] = t;
+    }
+    __syncthreads();
+    if (threadIdx.x < 64 && b0 + threadIdx.x < B)
+      ss[(size_t)blockIdx.x * B + b0 + threadIdx.x] =
+          (red[0][threadIdx.x] + red[1][threadIdx.x]) + (red[2][threadIdx.x] + red[3][threadIdx.x]);
+    __syncthreads();
+  }
+}
+
+hipError_t launch_residual(const Dims &dm, const Plan &p, const Workspace &w, int ksplit,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(k_residual, dim3(p.nss), dim3(256), 0, s, w.x, w.part, ksplit, w.ss, p.B,
+                     dm.H);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------- SwiGLU
+
+// h[b][f] = silu(gate) * up, gate/up = sums of the split-K partials of rows f and F + f.
+__global__ __launch_bounds__(256) void k_swiglu(const float *part, int ksplit, float *h, int B,
+                                                int F) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)B * F) return;
+  const int f = (int)(i / B), b = (int)(i - (size_t)f * B);
+  float gs = 0.f, us = 0.f;
+  for (int k = 0; k < ksplit; ++k) {
+    gs += part[((size_t)k * 2 * F + f) * B + b];
+    us += part[((size_t)k * 2 * F + F + f) * B + b];
+  }
+  h[(size_t)b * F + f] = gs / (1.0f + expf(-gs)) * us;
+}
+
+hipError_t launch_swiglu(const Dims &dm, const Plan &p, const Workspace &w, int ksplit,
+                         hipStream_t s) {
+  const size_t n = (size_t)p.B * dm.F;
+  hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, w.part, ksplit,
+                     w.hffn, p.B, dm.F);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------- reward head
+
+// z_b = w_r . (x_b / sqrt(mean(x_b^2) + eps) * gamma_f) + b_r; P(+) = sigmoid(z_b).
+__global__ __launch_bounds__(256) void k_head(const float *x, int H, float eps, const void *gam,
+                                              const void *wr, int wdt, float rb, float *scores,
+                                              float *logits) {
+  __shared__ float red[4];
+  const int b = blockIdx.x;
+  const float *xb = x + (size_t)b * H;
+  float sq = 0.f;
+  for (int r = threadIdx.x; r < H; r += 256) sq += xb[r] * xb[r];
+  sq = block_sum256(sq, red);
+  const float inv = 1.0f / sqrtf(sq / (float)H + eps);
+  float dot = 0.f;
+  for (int r = threadIdx.x; r < H; r += 256)
+    dot += (xb[r] * inv * load_scalar(gam, r, wdt)) * load_scalar(wr, r, wdt);
+  dot = block_sum256(dot, red);
+  if (threadIdx.x == 0) {
+    const float z = dot + rb;
+    float pz;
+    if (z >= 0.f) {
+      pz = 1.0f / (1.0f + expf(-z));
+    } else {
+      const float ez = expf(z);
+      pz = ez / (1.0f + ez);
+    }
+    scores[b] = pz;
+    if (logits) logits[b] = z;
+  }
+}
+
+hipError_t launch_head(const Dims &dm, const Plan &p, const Workspace &w, const void *final_norm,
+                       const void *reward_w, float reward_b, float *scores, float *logits,
+                       hipStream_t s) {
+  hipLaunchKernelGGL(k_head, dim3(p.B), dim3(256), 0, s, w.x, dm.H, dm.eps, final_norm, reward_w,
+                     dm.wdt, reward_b, scores, logits);
+  return hipGetLastError();
+}
+
+}  // namespace kvprm

@@ -1,0 +1,143 @@
+"""C ABI of libkvprm on the CPU: the library loads, exports every declared entry point, and
+rejects bad arguments with the documented status before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_09153_amd as kv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "kvprm.h")).read()
+    return sorted(set(re.findall(r"\b(kvprm_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert set(names) == set(kv.EXPORTED)
+    lib = ctypes.CDLL(kv.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _desc(**over):
+    d = dict(num_layers=2, hidden=256, num_q_heads=4, num_kv_heads=2, head_dim=64, ffn_dim=1024,
+             weight_dtype="f32", kv_dtype="f32")
+    d.update(over)
+    return kv.make_desc(**d)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(head_dim=96), kv.KVPRM_E_UNSUPPORTED),
+    (dict(page_size=32), kv.KVPRM_E_UNSUPPORTED),
+    (dict(num_q_heads=5), kv.KVPRM_E_INVALID),
+    (dict(hidden=0), kv.KVPRM_E_INVALID),
+    (dict(hidden=250), kv.KVPRM_E_UNSUPPORTED),
+    (dict(weight_dtype="f32", kv_dtype="bf16"), kv.KVPRM_E_UNSUPPORTED),
+    (dict(weight_dtype="bf16", kv_dtype="f32"), kv.KVPRM_E_UNSUPPORTED),
+    (dict(num_q_heads=34, num_kv_heads=2), kv.KVPRM_E_UNSUPPORTED),
+])
+def test_create_rejects(over, status):
+    with pytest.raises(kv.KvprmError) as e:
+        kv.kvprm_create(_desc(**over))
+    assert e.value.status == status
+    assert kv.kvprm_last_error()
+
+
+def test_create_accepts_supported_shapes():
+    for over in ({}, dict(weight_dtype="bf16", kv_dtype="bf16", head_dim=128, num_q_heads=28,
+                          num_kv_heads=4, hidden=3584, ffn_dim=18944),
+                 dict(weight_dtype="bf16", kv_dtype="fp8", head_dim=128)):
+        h = kv.kvprm_create(_desc(**over))
+        kv.kvprm_destroy(h)
+    kv.kvprm_destroy(None)
+
+
+FAKE = 0x10000  # never dereferenced: validation fails before anything is enqueued
+
+
+def _cache(**o):
+    c = dict(k_ptr=FAKE, v_ptr=FAKE, num_pages=4)
+    c.update(o)
+    return kv.make_cache(**c)
+
+
+def _weights(nl=2, null_layer=None):
+    layers = []
+    for l in range(nl):
+        d = {n: FAKE for n, _ in kv.LayerWeights._fields_}
+        if l == null_layer:
+            d["w_up"] = 0
+        layers.append(d)
+    return kv.make_readout(layers, FAKE, FAKE, FAKE)
+
+
+def _score(h, batch, cache=None, weights=None, ws=FAKE, ws_bytes=1 << 40, scores=FAKE):
+    kv.kvprm_score(h, cache or _cache(), batch, weights or _weights(), ws, ws_bytes, scores, 0, 0)
+
+
+@pytest.fixture
+def handle():
+    h = kv.kvprm_create(_desc())
+    yield h
+    kv.kvprm_destroy(h)
+
+
+def test_score_validation_errors(handle):
+    h = handle
+    ok_batch = kv.make_batch(2, FAKE, 4, FAKE, [10, 64])
+    cases = [
+        (kv.make_batch(-1, FAKE, 4, FAKE), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(2, 0, 4, FAKE), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(2, FAKE, 0, FAKE), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(2, FAKE, 4, FAKE, [10, 65]), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(2, FAKE, 4, FAKE, [10, -1]), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(300, FAKE, 4, FAKE), {}, kv.KVPRM_E_UNSUPPORTED),
+        (kv.make_batch(2, FAKE, 4, FAKE, [32, 40], [0, 1], [16]), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(2, FAKE, 4, FAKE, [32, 40], [0, 2], [8]), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(2, FAKE, 4, FAKE, [16, 40], [0, 2], [32]), {}, kv.KVPRM_E_INVALID),
+        (ok_batch, dict(cache=_cache(k_ptr=0)), kv.KVPRM_E_INVALID),
+        (ok_batch, dict(cache=_cache(num_pages=0)), kv.KVPRM_E_INVALID),
+        (ok_batch, dict(weights=_weights(null_layer=1)), kv.KVPRM_E_INVALID),
+        (ok_batch, dict(scores=0), kv.KVPRM_E_INVALID),
+        (ok_batch, dict(ws=0), kv.KVPRM_E_WORKSPACE),
+        (ok_batch, dict(ws_bytes=1000), kv.KVPRM_E_WORKSPACE),
+        (ok_batch, dict(ws=FAKE + 8), kv.KVPRM_E_WORKSPACE),
+    ]
+    for batch, kw, status in cases:
+        with pytest.raises(kv.KvprmError) as e:
+            _score(h, batch, **kw)
+        assert e.value.status == status, (kw, kv.kvprm_last_error())
+
+
+def test_fp8_cache_needs_scales():
+    h = kv.kvprm_create(_desc(weight_dtype="bf16", kv_dtype="fp8"))
+    try:
+        with pytest.raises(kv.KvprmError) as e:
+            _score(h, kv.make_batch(1, FAKE, 4, FAKE), cache=_cache())
+        assert e.value.status == kv.KVPRM_E_INVALID and "scale" in kv.kvprm_last_error()
+    finally:
+        kv.kvprm_destroy(h)
+
+
+def test_batch_zero_is_noop_and_workspace_sizes(handle):
+    _score(handle, kv.make_batch(0, 0, 1, 0), ws=0, ws_bytes=0, scores=0)
+    assert kv.kvprm_workspace_size(handle, kv.make_batch(0, 0, 1, 0)) == 0
+    a = kv.kvprm_workspace_size(handle, kv.make_batch(4, FAKE, 32, FAKE))
+    b = kv.kvprm_workspace_size(handle, kv.make_batch(4, FAKE, 64, FAKE))
+    c = kv.kvprm_workspace_size(handle, kv.make_batch(8, FAKE, 64, FAKE))
+    assert 0 < a <= b < c
+
+
+def test_attention_validation(handle):
+    batch = kv.make_batch(1, FAKE, 4, FAKE)
+    with pytest.raises(kv.KvprmError) as e:
+        kv.kvprm_attention(handle, _cache(), batch, 2, FAKE, FAKE, FAKE, FAKE, 1 << 40, FAKE)
+    assert e.value.status == kv.KVPRM_E_INVALID
+    with pytest.raises(kv.KvprmError) as e:
+        kv.kvprm_attention(handle, _cache(), batch, 0, 0, FAKE, FAKE, FAKE, 1 << 40, FAKE)
+    assert e.value.status == kv.KVPRM_E_INVALID

@@ -1,0 +1,155 @@
+"""GPU parity of libkvprm against the fp64 oracle on identical seeded inputs.
+
+Tolerances: fp32 weights and cache, max |dP(+)| <= 1e-5; bf16 weights (bf16 or fp8 cache),
+max |dP(+)| <= 2e-3. The logit z is also checked, so that a saturated sigmoid cannot hide an
+error. The attention step alone is compared element by element.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import inputs as oin
+from oracle import kvprm_oracle as ko
+from synth.device import DeviceWorkload
+
+from gpu_common import host_activations, kv, run_attention, run_score
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def test_device_generator_matches_host_bits():
+    _say("case: device generator vs host")
+    n = 1 << 20
+    for dt, tdt in ((synth.DT_F32, torch.float32), (synth.DT_BF16, torch.bfloat16),
+                    (synth.DT_F64, torch.float64)):
+        t = torch.empty(n, dtype=tdt, device="cuda")
+        synth.device_normal(t.data_ptr(), n, 17, 5, 1000, 0.5, 0.25, dt, 0)
+        torch.cuda.synchronize()
+        host = synth.host_normal(n, 17, 5, 1000, 0.5, 0.25, dt)
+        dev = t.cpu()
+        if dt == synth.DT_BF16:
+            dev = dev.view(torch.int16).numpy().view(np.uint16)
+        else:
+            dev = dev.numpy()
+        assert np.array_equal(dev.view(np.uint8), host.view(np.uint8))
+    T, nt = 2048, 333
+    codes = torch.empty(nt * T, dtype=torch.uint8, device="cuda")
+    scales = torch.empty(nt, dtype=torch.float32, device="cuda")
+    synth.device_fp8_tiles(codes.data_ptr(), scales.data_ptr(), nt, T, 9, 3, 50, 0)
+    torch.cuda.synchronize()
+    hc, hs = synth.host_fp8_tiles(nt, T, 9, 3, 50)
+    assert np.array_equal(codes.cpu().numpy(), hc)
+    assert np.array_equal(scales.cpu().numpy(), hs)
+
+
+ATTN_CASES = [
+    # name, lengths (incl. empty, one token, page edges, ragged tails), K scale
+    ("tiny_fp32", [512, 0, 1, 15, 16, 17, 700, 1025], 1.0),
+    ("b7_bf16", [4096, 0, 1, 17, 5000, 9000], 1.0),
+    ("b7_bf16_spiky", [3000, 33, 16], 30.0),
+    ("fp8", [2049, 0, 31, 8192], 1.0),
+]
+
+
+def _shape(name):
+    import dataclasses
+    if name == "tiny_fp32":
+        return synth.TINY
+    if name.startswith("b7"):
+        return dataclasses.replace(synth.B7, num_layers=2)
+    if name == "fp8":
+        return dataclasses.replace(synth.LARGE_FP8, num_layers=2)
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("name,lengths,k_std", ATTN_CASES)
+def test_attention_parity(name, lengths, k_std):
+    _say(f"case: attention {name} lengths={lengths}")
+    shape = _shape(name)
+    w = synth.make_workload("custom", shape=shape, lengths=lengths, seed=4242, k_std=k_std)
+    dw = DeviceWorkload(w, nan_unused_pages=True, fill_weights=False)
+    q, ks, vs = host_activations(w, 0xABC, scale=1.0)
+    layer = 1
+    o = run_attention(dw, layer, q, ks, vs)
+    cache = oin.cache_from_synth(w)
+    ref = ko.attention_layer(shape, cache, layer, w.lengths, w.page_table, q.astype(np.float64),
+                             ks.astype(np.float64), vs.astype(np.float64))
+    assert np.all(np.isfinite(o))
+    err = np.max(np.abs(o - ref))
+    scale = max(1.0, float(np.max(np.abs(ref))))
+    _say(f"  max|do| = {err:.3e} (max|o| = {np.max(np.abs(ref)):.3e})")
+    assert err <= 2e-5 * scale
+
+
+def _parity(w, tol_p, tol_z, **kw):
+    dw = DeviceWorkload(w, nan_unused_pages=True)
+    p, z = run_score(dw, **kw)
+    zr, pr = oin.score_workload(w)
+    dp, dz = np.max(np.abs(p - pr)), np.max(np.abs(z - zr))
+    _say(f"  max|dP| = {dp:.3e}  max|dz| = {dz:.3e}  P = {np.round(p, 4)}")
+    assert np.all(np.isfinite(p)) and np.all(np.isfinite(z))
+    assert dp <= tol_p and dz <= tol_z
+    return p, z
+
+
+def test_score_parity_tiny_fp32():
+    _say("case: score tiny_fp32 (B=4, L=512)")
+    _parity(synth.make_workload("tiny_fp32"), 1e-5, 4e-5)
+
+
+def test_score_parity_tiny_ragged_and_empty():
+    _say("case: score tiny ragged lengths incl. 0")
+    w = synth.make_workload("custom", shape=synth.TINY, lengths=[0, 1, 15, 16, 17, 511, 2000],
+                            seed=77)
+    _parity(w, 1e-5, 4e-5)
+
+
+def test_score_parity_tiny_spiky_keys():
+    _say("case: score tiny, K scaled x30 (peaked softmax)")
+    w = synth.make_workload("custom", shape=synth.TINY, lengths=[300, 64, 129], seed=78,
+                            k_std=30.0)
+    _parity(w, 1e-5, 4e-5)
+
+
+def test_score_parity_7b_two_layers_bf16():
+    _say("case: score 7B shape, 2 layers, bf16, ragged")
+    import dataclasses
+    shape = dataclasses.replace(synth.B7, num_layers=2)
+    w = synth.make_workload("custom", shape=shape, lengths=[4096, 0, 17, 3001, 1200], seed=79)
+    _parity(w, 2e-3, 2e-2)
+
+
+def test_score_deterministic_and_batch_zero():
+    _say("case: determinism + B=0")
+    w = synth.make_workload("custom", shape=synth.TINY, lengths=[100, 513, 7], seed=80)
+    dw = DeviceWorkload(w)
+    a = run_score(dw)
+    b = run_score(dw)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    m = kv()
+    h = m.kvprm_create(dw.desc(m))
+    try:
+        empty = m.make_batch(0, 0, 1, 0)
+        assert m.kvprm_workspace_size(h, empty) == 0
+        m.kvprm_score(h, dw.cache(m), empty, dw.readout(m), 0, 0, 0, 0, 0)
+    finally:
+        m.kvprm_destroy(h)
+
+
+def test_cache_and_weights_unchanged():
+    _say("case: inputs are read-only")
+    w = synth.make_workload("custom", shape=synth.TINY, lengths=[100, 37], seed=81)
+    dw = DeviceWorkload(w)
+    kc, vc = dw.k_pool.clone(), dw.v_pool.clone()
+    wq = dw.layers[0]["wq"].clone()
+    run_score(dw)
+    assert torch.equal(kc, dw.k_pool) and torch.equal(vc, dw.v_pool)
+    assert torch.equal(wq, dw.layers[0]["wq"])
