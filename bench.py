@@ -1,0 +1,196 @@
+"""Benchmark of KV-PRM verify-token scoring on one MI355X.
+
+One step = one kvprm_score call over the whole hot path (all layers, projections, paged
+attention, merge, FFN, reward head) for the ragged long-context batch: the 7B-class shape in
+bf16 (28 layers, H=3584, 28/4 heads, d_h=128, FFN 18944), B=8 candidates with cached lengths
+L_b ~ U[16384, 32768] on 16-token pages scattered over a pool. Inputs are synthetic (seeded
+generator) and resident in HBM before the timed region.
+
+Prints one JSON line: scores/s (value), the end-to-end KV-read rate, the roofline of the
+dominant kernel (the split-L attention step, timed live with HIP events on its stream) and the
+fp64 CPU oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(w, dw):
+    s = w.shape
+    kv_bytes = s.num_layers * w.unique_tokens() * 2 * s.num_kv_heads * s.head_dim * s.kv_elem_bytes
+    if s.kv_dtype == "fp8":
+        kv_bytes += s.num_layers * len(w.used_pages()) * s.num_kv_heads * 2 * 4
+    return kv_bytes, dw.weight_bytes()
+
+
+def time_attention_step(kv, dw, h, batch, ws, n, reps):
+    """Average duration of the attention step (split-L partial kernel + merge kernel) of one
+    layer, measured with HIP events on the stream the kernels are launched on."""
+    import torch
+    w = dw.w
+    s = w.shape
+    q = torch.randn(w.batch, s.num_q_heads, s.head_dim, device="cuda")
+    ks = torch.randn(w.batch, s.num_kv_heads, s.head_dim, device="cuda")
+    vs = torch.randn(w.batch, s.num_kv_heads, s.head_dim, device="cuda")
+    o = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+    cache = dw.cache(kv)
+
+    def call(layer):
+        kv.kvprm_attention(h, cache, batch, layer, q.data_ptr(), ks.data_ptr(), vs.data_ptr(),
+                           ws.data_ptr(), n, o.data_ptr(), stream.cuda_stream)
+
+    for l in range(s.num_layers):
+        call(l)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for i, (a, b) in enumerate(evs):
+        a.record(stream)
+        call(i % s.num_layers)
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = [a.elapsed_time(b) for a, b in evs]
+    return sum(ms) / len(ms)
+
+
+def cpu_baseline(w, layers_sample):
+    """The fp64 oracle, untuned, on all candidates of the workload through its first
+    `layers_sample` layers; input generation is done before the clock starts. Scaled to
+    scores/s of the full-depth model."""
+    import dataclasses
+
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import inputs as oin
+    from oracle import kvprm_oracle as ko
+
+    s = w.shape
+    sub = dataclasses.replace(s, num_layers=layers_sample)
+    ro = oin.readout_from_synth(sub, w.seed, layer_cache=layers_sample)
+    npages = sum(-(-L // s.page_size) for L in w.lengths)
+    cache = oin.cache_from_synth(w, page_cache=2 * layers_sample * npages + 16)
+    for l in range(layers_sample):  # materialise inputs outside the timed region
+        ro.layer(l)
+        for b in range(w.batch):
+            for i in range(-(-w.lengths[b] // s.page_size)):
+                cache.tiles(l, "k", w.page_table[b][i])
+                cache.tiles(l, "v", w.page_table[b][i])
+    t0 = time.perf_counter()
+    ko.verify_pass(sub, ro, cache, w.lengths, w.page_table)
+    dt = time.perf_counter() - t0
+    per_call = dt * s.num_layers / layers_sample
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": w.batch / per_call, "unit": "scores/s", "cores": threads, "kind": "oracle",
+            "sample": (f"{w.name}: all {w.batch} candidates through the first {layers_sample} of "
+                       f"{s.num_layers} layers in {dt:.1f} s (fp64 numpy, inputs pre-generated), "
+                       f"scaled by {s.num_layers}/{layers_sample} to one full call")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="ragged_32k")
+    ap.add_argument("--cpu-layers", type=int, default=2,
+                    help="layers of the oracle sample for the CPU baseline (0 = skip)")
+    ap.add_argument("--attn-reps", type=int, default=56)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from synth.device import DeviceWorkload
+    import paper_2607_09153_amd as kv
+
+    torch.cuda.set_device(0)
+    w = synth.make_workload(args.workload)
+    _log(f"workload {w.name}: B={w.batch} lengths={w.lengths} pages={w.num_pages}")
+    t0 = time.time()
+    dw = DeviceWorkload(w)
+    torch.cuda.synchronize()
+    _log(f"inputs generated in HBM in {time.time() - t0:.1f} s")
+    kv_bytes, w_bytes = algorithmic_bytes(w, dw)
+
+    h = kv.kvprm_create(dw.desc(kv))
+    batch = dw.batch(kv)
+    n = kv.kvprm_workspace_size(h, batch)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    scores = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    cache, readout = dw.cache(kv), dw.readout(kv)
+
+    def step():
+        kv.kvprm_score(h, cache, batch, readout, ws.data_ptr(), n, scores.data_ptr(), 0,
+                       stream.cuda_stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    _log(f"warmup done ({args.warmup} steps)")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms = dt * 1e3 / args.steps
+    _log(f"timed {args.steps} steps: {ms:.3f} ms/step")
+
+    attn_ms = time_attention_step(kv, dw, h, batch, ws, n, args.attn_reps)
+    kv_per_layer = kv_bytes / w.shape.num_layers
+    achieved = kv_per_layer / (attn_ms * 1e-3) / 1e9
+    _log(f"attention step: {attn_ms * 1e3:.1f} us/layer, {achieved:.0f} GB/s")
+    kv.kvprm_destroy(h)
+
+    out = {
+        "metric": "verify-token scores/sec + achieved KV-read HBM GB/s at L=32k, B=8",
+        "value": w.batch / (ms * 1e-3),
+        "unit": "scores/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "layers": w.shape.num_layers,
+                   "hidden": w.shape.hidden, "heads": [w.shape.num_q_heads, w.shape.num_kv_heads],
+                   "head_dim": w.shape.head_dim, "ffn": w.shape.ffn_dim,
+                   "kv_dtype": w.shape.kv_dtype, "cached_tokens": sum(w.lengths),
+                   "mean_length": sum(w.lengths) / w.batch},
+        "kv_read_gbps": kv_bytes / (ms * 1e-3) / 1e9,
+        "end_to_end_gbps": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9,
+        "bytes_per_call": {"kv": kv_bytes, "weights": w_bytes},
+        "roofline": {"kernel": "split-L paged attention step (partials + merge), one layer",
+                     "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "avg_us": attn_ms * 1e3, "bytes_per_launch": kv_per_layer},
+    }
+    if args.cpu_layers > 0:
+        _log("timing the oracle on the CPU sample ...")
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -96,6 +96,8 @@ static kvprm_status check_batch(const kvprm_handle h, const kvprm_batch *b, cons
   if (b->batch < 0) return fail(KVPRM_E_INVALID, "%s: batch < 0", fn);
   if (b->batch == 0) return KVPRM_OK;
   if (b->batch > 256) return fail(KVPRM_E_UNSUPPORTED, "%s: at most 256 candidates per call", fn);
+  if (h->dm.wdt == 1 && b->batch > 64)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: at most 64 candidates per call with bf16 weights", fn);
   if (!b->page_table || !b->lengths) return fail(KVPRM_E_INVALID, "%s: null page_table or lengths", fn);
   if (b->max_pages < 1) return fail(KVPRM_E_INVALID, "%s: max_pages < 1", fn);
   const int cap = b->max_pages * h->desc.page_size;
@@ -190,7 +192,7 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   for (int l = 0; l < dm.layers; ++l) {
     const kvprm_layer_weights &W = wts->layers[l];
     GemvSegs qkv{{W.wq, W.wk, W.wv}, {dm.nq * dm.d, dm.nkv * dm.d, dm.nkv * dm.d}, 3};
-    HIP_TRY(launch_gemv(dm, p, qkv, dm.H, p.kslice_qkv, p.ks_qkv, w.x, W.attn_norm, w.ss, w.part, s),
+    HIP_TRY(launch_gemv(dm, p, qkv, dm.H, p.kslice_qkv, p.ks_qkv, w.x, W.attn_norm, w.ss, w.part, w.act, s),
             "qkv projection");
     HIP_TRY(launch_qkv_finish(dm, p, w, b->lengths, s), "rotary");
     HIP_TRY(launch_attention(dm, p, w, l, cache->k_pages, cache->v_pages, cache->k_scale,
@@ -198,15 +200,15 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
                              w.kself, w.vself, w.o, s),
             "attention");
     GemvSegs wo{{W.wo, nullptr, nullptr}, {dm.H, 0, 0}, 1};
-    HIP_TRY(launch_gemv(dm, p, wo, dm.nq * dm.d, p.kslice_o, p.ks_o, w.o, nullptr, nullptr, w.part, s),
+    HIP_TRY(launch_gemv(dm, p, wo, dm.nq * dm.d, p.kslice_o, p.ks_o, w.o, nullptr, nullptr, w.part, w.act, s),
             "output projection");
     HIP_TRY(launch_residual(dm, p, w, p.ks_o, s), "residual");
     GemvSegs gu{{W.w_gate, W.w_up, nullptr}, {dm.F, dm.F, 0}, 2};
-    HIP_TRY(launch_gemv(dm, p, gu, dm.H, p.kslice_gu, p.ks_gu, w.x, W.ffn_norm, w.ss, w.part, s),
+    HIP_TRY(launch_gemv(dm, p, gu, dm.H, p.kslice_gu, p.ks_gu, w.x, W.ffn_norm, w.ss, w.part, w.act, s),
             "gate/up projection");
     HIP_TRY(launch_swiglu(dm, p, w, p.ks_gu, s), "swiglu");
     GemvSegs dn{{W.w_down, nullptr, nullptr}, {dm.H, 0, 0}, 1};
-    HIP_TRY(launch_gemv(dm, p, dn, dm.F, p.kslice_d, p.ks_d, w.hffn, nullptr, nullptr, w.part, s),
+    HIP_TRY(launch_gemv(dm, p, dn, dm.F, p.kslice_d, p.ks_d, w.hffn, nullptr, nullptr, w.part, w.act, s),
             "down projection");
     HIP_TRY(launch_residual(dm, p, w, p.ks_d, s), "residual");
   }

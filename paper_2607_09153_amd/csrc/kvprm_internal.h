@@ -37,6 +37,7 @@ struct Workspace {
   float *apart;    // attention partials [B][nq][nch][d + 2] (acc..., m, l)
   float *o;        // [B][nq * d]
   float *hffn;     // [B][F]
+  uint4 *act;      // activation operand of the MFMA GEMV (bf16 hi/lo, B-operand order)
   size_t bytes;
 };
 
@@ -46,7 +47,13 @@ struct Plan {
   int ks_qkv, ks_o, ks_gu, ks_d;  // split-K counts
   int kslice_qkv, kslice_o, kslice_gu, kslice_d;
   size_t part_elems;
+  size_t act_bytes;
 };
+
+// MFMA GEMV helpers (kvprm_mfma.hip)
+int gemv_nt(int B);
+int gemv_bp(int B);
+void gemv_split(int rows, int K, int B, int &kslice, int &ksplit);
 
 Plan make_plan(const Dims &dm, int B, int max_pages);
 Workspace carve(const Dims &dm, const Plan &p, void *base);
@@ -63,7 +70,14 @@ struct GemvSegs {
 };
 hipError_t launch_gemv(const Dims &dm, const Plan &p, const GemvSegs &segs, int K, int kslice,
                        int ksplit, const float *in, const void *gamma, const float *ss,
-                       float *part, hipStream_t s);
+                       float *part, uint4 *actbuf, hipStream_t s);
+hipError_t launch_gemv_mfma(const Dims &dm, const Plan &p, const GemvSegs &segs, int K,
+                            int kslice, int ksplit, const float *in, const void *gamma,
+                            const float *ss, float *part, uint4 *actbuf, hipStream_t s);
+hipError_t launch_attn_mfma(const Dims &dm, const Plan &p, const char *kp, const char *vp,
+                            const float *ksc, const float *vsc, const int32_t *page_table,
+                            const int32_t *lengths, const GroupTable &gt, const float *q,
+                            float *apart, hipStream_t s);
 hipError_t launch_qkv_finish(const Dims &dm, const Plan &p, const Workspace &w,
                              const int32_t *lengths, hipStream_t s);
 hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, int layer,

@@ -65,21 +65,33 @@ Plan make_plan(const Dims &dm, int B, int max_pages) {
   p.max_pages = max_pages;
   p.nch = (max_pages + kChunkPages - 1) / kChunkPages;
   p.nss = (dm.H + 255) / 256;
-  // split-K slices: the activation slice of all B candidates is staged in LDS (<= 32 KiB)
-  auto slice = [&](int K) {
-    int s = (8192 / (B > 0 ? B : 1)) & ~63;
-    if (s < 64) s = 64;
-    if (s > K) s = K;
-    return s;
-  };
-  p.kslice_qkv = slice(dm.H);
-  p.kslice_o = slice(dm.nq * dm.d);
-  p.kslice_gu = slice(dm.H);
-  p.kslice_d = slice(dm.F);
-  p.ks_qkv = (dm.H + p.kslice_qkv - 1) / p.kslice_qkv;
-  p.ks_o = (dm.nq * dm.d + p.kslice_o - 1) / p.kslice_o;
-  p.ks_gu = (dm.H + p.kslice_gu - 1) / p.kslice_gu;
-  p.ks_d = (dm.F + p.kslice_d - 1) / p.kslice_d;
+  if (dm.wdt == 1) {
+    // matrix-core GEMV: split K only as far as needed to cover the chip
+    gemv_split((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B, p.kslice_qkv, p.ks_qkv);
+    gemv_split(dm.H, dm.nq * dm.d, B, p.kslice_o, p.ks_o);
+    gemv_split(2 * dm.F, dm.H, B, p.kslice_gu, p.ks_gu);
+    gemv_split(dm.H, dm.F, B, p.kslice_d, p.ks_d);
+    int kmax = dm.H > dm.F ? dm.H : dm.F;
+    if (dm.nq * dm.d > kmax) kmax = dm.nq * dm.d;
+    p.act_bytes = (size_t)(kmax / 32) * gemv_nt(B) * 64 * 16;
+  } else {
+    // vector-ALU GEMV: the activation slice of all B candidates is staged in LDS (<= 32 KiB)
+    auto slice = [&](int K) {
+      int s = (8192 / (B > 0 ? B : 1)) & ~63;
+      if (s < 64) s = 64;
+      if (s > K) s = K;
+      return s;
+    };
+    p.kslice_qkv = slice(dm.H);
+    p.kslice_o = slice(dm.nq * dm.d);
+    p.kslice_gu = slice(dm.H);
+    p.kslice_d = slice(dm.F);
+    p.ks_qkv = (dm.H + p.kslice_qkv - 1) / p.kslice_qkv;
+    p.ks_o = (dm.nq * dm.d + p.kslice_o - 1) / p.kslice_o;
+    p.ks_gu = (dm.H + p.kslice_gu - 1) / p.kslice_gu;
+    p.ks_d = (dm.F + p.kslice_d - 1) / p.kslice_d;
+    p.act_bytes = 0;
+  }
   size_t a = (size_t)p.ks_qkv * (dm.nq + 2 * dm.nkv) * dm.d;
   size_t b2 = (size_t)p.ks_o * dm.H;
   size_t c = (size_t)p.ks_gu * 2 * dm.F;
@@ -112,6 +124,7 @@ Workspace carve(const Dims &dm, const Plan &p, void *base) {
   w.apart = take(B * dm.nq * (size_t)p.nch * (dm.d + 2));
   w.o = take(B * dm.nq * dm.d);
   w.hffn = take(B * dm.F);
+  w.act = (uint4 *)take((p.act_bytes + 3) / 4);
   w.bytes = off;
   return w;
 }
@@ -218,7 +231,9 @@ __global__ __launch_bounds__(256) void k_gemv_valu(GemvSegs segs, int rows_total
 
 hipError_t launch_gemv(const Dims &dm, const Plan &p, const GemvSegs &segs, int K, int kslice,
                        int ksplit, const float *in, const void *gamma, const float *ss,
-                       float *part, hipStream_t s) {
+                       float *part, uint4 *actbuf, hipStream_t s) {
+  if (dm.wdt == 1)
+    return launch_gemv_mfma(dm, p, segs, K, kslice, ksplit, in, gamma, ss, part, actbuf, s);
   int rows = 0;
   for (int i = 0; i < segs.nseg; ++i) rows += segs.rows[i];
   dim3 grid((rows + 255) / 256, ksplit);
@@ -463,6 +478,18 @@ __global__ __launch_bounds__(D) void k_merge(const float *apart, int nch, GroupT
   o[((size_t)b * nq + h) * D + m] = acc / l;
 }
 
+static hipError_t launch_merge(const Dims &dm, const Plan &p, const Workspace &w,
+                               const GroupTable &gt, const int32_t *lengths, const float *q,
+                               const float *kself, const float *vself, float *o, hipStream_t s) {
+  if (dm.d == 64)
+    hipLaunchKernelGGL(k_merge<64>, dim3(p.B, dm.nq), dim3(64), 0, s, w.apart, p.nch, gt, q,
+                       kself, vself, lengths, o, dm.nq, dm.nkv, dm.g);
+  else
+    hipLaunchKernelGGL(k_merge<128>, dim3(p.B, dm.nq), dim3(128), 0, s, w.apart, p.nch, gt, q,
+                       kself, vself, lengths, o, dm.nq, dm.nkv, dm.g);
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, int layer,
                             const void *kpool, const void *vpool, const float *kscale,
                             const float *vscale, int num_pages, const int32_t *page_table,
@@ -474,6 +501,11 @@ hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, i
   const char *vp = (const char *)vpool + layer_elems * EB * layer;
   const float *ksc = kscale ? kscale + (size_t)layer * num_pages * dm.nkv : nullptr;
   const float *vsc = vscale ? vscale + (size_t)layer * num_pages * dm.nkv : nullptr;
+  if (dm.kvdt != 0) {
+    hipError_t e = launch_attn_mfma(dm, p, kp, vp, ksc, vsc, page_table, lengths, gt, q, w.apart, s);
+    if (e != hipSuccess) return e;
+    return launch_merge(dm, p, w, gt, lengths, q, kself, vself, o, s);
+  }
   dim3 grid(p.nch, dm.nkv, p.B);
 #define KVPRM_ATT(KVT, D)                                                                     \
   hipLaunchKernelGGL((k_attn_valu<KVT, D>), grid, dim3(256), 0, s, kp, vp, ksc, vsc, dm.nkv, \
@@ -490,13 +522,7 @@ hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, i
 #undef KVPRM_ATT
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (dm.d == 64)
-    hipLaunchKernelGGL(k_merge<64>, dim3(p.B, dm.nq), dim3(64), 0, s, w.apart, p.nch, gt, q,
-                       kself, vself, lengths, o, dm.nq, dm.nkv, dm.g);
-  else
-    hipLaunchKernelGGL(k_merge<128>, dim3(p.B, dm.nq), dim3(128), 0, s, w.apart, p.nch, gt, q,
-                       kself, vself, lengths, o, dm.nq, dm.nkv, dm.g);
-  return hipGetLastError();
+  return launch_merge(dm, p, w, gt, lengths, q, kself, vself, o, s);
 }
 
 // ------------------------------------------------------------------------------- residual
