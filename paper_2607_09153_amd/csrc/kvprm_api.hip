@@ -100,6 +100,8 @@ static kvprm_status check_batch(const kvprm_handle h, const kvprm_batch *b, cons
     return fail(KVPRM_E_UNSUPPORTED, "%s: at most 64 candidates per call with bf16 weights", fn);
   if (!b->page_table || !b->lengths) return fail(KVPRM_E_INVALID, "%s: null page_table or lengths", fn);
   if (b->max_pages < 1) return fail(KVPRM_E_INVALID, "%s: max_pages < 1", fn);
+  if (b->max_pages > kMaxChunks * kChunkPages)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: max_pages above %d", fn, kMaxChunks * kChunkPages);
   const int cap = b->max_pages * h->desc.page_size;
   if (b->lengths_host)
     for (int i = 0; i < b->batch; ++i)
@@ -188,11 +190,39 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   const Plan p = make_plan(dm, b->batch, b->max_pages);
   const Workspace w = carve(dm, p, workspace);
   const GroupTable gt = group_table(b);
+  const int EB = dm.kvdt == 0 ? 4 : (dm.kvdt == 1 ? 2 : 1);
+  const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * EB;
+  const size_t layer_scales = (size_t)cache->num_pages * dm.nkv;
+  if (dm.wdt == 1) {
+    // matrix-core pipeline: five launches per layer
+    HIP_TRY(launch_init_mx(dm, p, w, wts->verify_embed, wts->layers[0].attn_norm, b->lengths, s),
+            "init");
+    for (int l = 0; l < dm.layers; ++l) {
+      const kvprm_layer_weights &W = wts->layers[l];
+      HIP_TRY(launch_qkv_mx(dm, p, w, W.wq, W.wk, W.wv, s), "qkv projection");
+      HIP_TRY(launch_attn_mx(dm, p, w, (const char *)cache->k_pages + layer_bytes * l,
+                             (const char *)cache->v_pages + layer_bytes * l,
+                             cache->k_scale ? cache->k_scale + layer_scales * l : nullptr,
+                             cache->v_scale ? cache->v_scale + layer_scales * l : nullptr,
+                             b->page_table, b->lengths, gt, w.q, w.kself, w.vself, nullptr, w.opO,
+                             s),
+              "attention");
+      HIP_TRY(launch_oproj_mx(dm, p, w, W.wo, W.ffn_norm, s), "output projection");
+      HIP_TRY(launch_gateup_mx(dm, p, w, W.w_gate, W.w_up, s), "gate/up projection");
+      HIP_TRY(launch_down_mx(dm, p, w, W.w_down,
+                             l + 1 < dm.layers ? wts->layers[l + 1].attn_norm : nullptr, s),
+              "down projection");
+    }
+    HIP_TRY(launch_head(dm, p, w, wts->final_norm, wts->reward_w, wts->reward_b, scores, logits, s),
+            "reward head");
+    return ok();
+  }
+  // vector-ALU pipeline (fp32 weights)
   HIP_TRY(launch_init(dm, p, w, wts->verify_embed, s), "init");
   for (int l = 0; l < dm.layers; ++l) {
     const kvprm_layer_weights &W = wts->layers[l];
     GemvSegs qkv{{W.wq, W.wk, W.wv}, {dm.nq * dm.d, dm.nkv * dm.d, dm.nkv * dm.d}, 3};
-    HIP_TRY(launch_gemv(dm, p, qkv, dm.H, p.kslice_qkv, p.ks_qkv, w.x, W.attn_norm, w.ss, w.part, w.act, s),
+    HIP_TRY(launch_gemv(dm, p, qkv, dm.H, p.kslice_qkv, p.ks_qkv, w.x, W.attn_norm, w.ss, w.part, s),
             "qkv projection");
     HIP_TRY(launch_qkv_finish(dm, p, w, b->lengths, s), "rotary");
     HIP_TRY(launch_attention(dm, p, w, l, cache->k_pages, cache->v_pages, cache->k_scale,
@@ -200,15 +230,15 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
                              w.kself, w.vself, w.o, s),
             "attention");
     GemvSegs wo{{W.wo, nullptr, nullptr}, {dm.H, 0, 0}, 1};
-    HIP_TRY(launch_gemv(dm, p, wo, dm.nq * dm.d, p.kslice_o, p.ks_o, w.o, nullptr, nullptr, w.part, w.act, s),
+    HIP_TRY(launch_gemv(dm, p, wo, dm.nq * dm.d, p.kslice_o, p.ks_o, w.o, nullptr, nullptr, w.part, s),
             "output projection");
     HIP_TRY(launch_residual(dm, p, w, p.ks_o, s), "residual");
     GemvSegs gu{{W.w_gate, W.w_up, nullptr}, {dm.F, dm.F, 0}, 2};
-    HIP_TRY(launch_gemv(dm, p, gu, dm.H, p.kslice_gu, p.ks_gu, w.x, W.ffn_norm, w.ss, w.part, w.act, s),
+    HIP_TRY(launch_gemv(dm, p, gu, dm.H, p.kslice_gu, p.ks_gu, w.x, W.ffn_norm, w.ss, w.part, s),
             "gate/up projection");
     HIP_TRY(launch_swiglu(dm, p, w, p.ks_gu, s), "swiglu");
     GemvSegs dn{{W.w_down, nullptr, nullptr}, {dm.H, 0, 0}, 1};
-    HIP_TRY(launch_gemv(dm, p, dn, dm.F, p.kslice_d, p.ks_d, w.hffn, nullptr, nullptr, w.part, w.act, s),
+    HIP_TRY(launch_gemv(dm, p, dn, dm.F, p.kslice_d, p.ks_d, w.hffn, nullptr, nullptr, w.part, s),
             "down projection");
     HIP_TRY(launch_residual(dm, p, w, p.ks_d, s), "residual");
   }

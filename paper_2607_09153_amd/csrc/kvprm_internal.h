@@ -24,6 +24,7 @@ struct GroupTable {
 
 // Attention split: each work item covers kChunkPages pages of one (candidate, kv-head).
 constexpr int kChunkPages = 32;
+constexpr int kMaxChunks = 1024;  // chunk partials one merge handles: max_pages <= 32768
 constexpr int kPage = 16;
 
 // Workspace carve-up (all offsets 256-byte aligned).
@@ -34,26 +35,38 @@ struct Workspace {
   float *q;        // [B][nq][d]
   float *kself;    // [B][nkv][d]
   float *vself;    // [B][nkv][d]
-  float *apart;    // attention partials [B][nq][nch][d + 2] (acc..., m, l)
+  float *apart;    // attention partials: [B][nq][nch][d + 2] (vector-ALU path) or
+                   // [B][nq][d + 2][nch rounded up to 4] (matrix-core path)
   float *o;        // [B][nq * d]
-  float *hffn;     // [B][F]
-  uint4 *act;      // activation operand of the MFMA GEMV (bf16 hi/lo, B-operand order)
+  float *hffn;     // [B][F] (vector-ALU path)
+  // matrix-core path
+  float *rope;       // [B][d/2][2] cos, sin of the verify position
+  uint16_t *opA;     // GEMV operands (bf16 hi/lo): QKV and gate/up input (K = H)
+  uint16_t *opO;     //   output projection input (K = n_q d)
+  uint16_t *opD;     //   down projection input (K = F)
   size_t bytes;
+};
+
+struct GemvPlan {
+  int rows, K, kslice, ksplit;
 };
 
 struct Plan {
   int B, max_pages, nch;      // nch = chunks per (candidate, kv-head) at max_pages
-  int nss;                    // blocks of 256 rows in H
+  int nss;                    // row blocks of H that carry partial sums of squares
+  int rb;                     // rows per such block
+  // vector-ALU path
   int ks_qkv, ks_o, ks_gu, ks_d;  // split-K counts
   int kslice_qkv, kslice_o, kslice_gu, kslice_d;
+  // matrix-core path
+  int nt, bp;                 // operand column tiles and padded batch
+  GemvPlan g_qkv, g_o, g_gu, g_d;
   size_t part_elems;
-  size_t act_bytes;
 };
 
-// MFMA GEMV helpers (kvprm_mfma.hip)
+// matrix-core helpers (kvprm_mfma.hip)
 int gemv_nt(int B);
 int gemv_bp(int B);
-void gemv_split(int rows, int K, int B, int &kslice, int &ksplit);
 
 Plan make_plan(const Dims &dm, int B, int max_pages);
 Workspace carve(const Dims &dm, const Plan &p, void *base);
@@ -70,14 +83,23 @@ struct GemvSegs {
 };
 hipError_t launch_gemv(const Dims &dm, const Plan &p, const GemvSegs &segs, int K, int kslice,
                        int ksplit, const float *in, const void *gamma, const float *ss,
-                       float *part, uint4 *actbuf, hipStream_t s);
-hipError_t launch_gemv_mfma(const Dims &dm, const Plan &p, const GemvSegs &segs, int K,
-                            int kslice, int ksplit, const float *in, const void *gamma,
-                            const float *ss, float *part, uint4 *actbuf, hipStream_t s);
-hipError_t launch_attn_mfma(const Dims &dm, const Plan &p, const char *kp, const char *vp,
-                            const float *ksc, const float *vsc, const int32_t *page_table,
-                            const int32_t *lengths, const GroupTable &gt, const float *q,
-                            float *apart, hipStream_t s);
+                       float *part, hipStream_t s);
+// matrix-core pipeline (bf16 weights)
+hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *ev,
+                          const void *gamma0, const int32_t *lengths, hipStream_t s);
+hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
+                         const void *wk, const void *wv, hipStream_t s);
+hipError_t launch_oproj_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
+                           const void *gamma_ffn, hipStream_t s);
+hipError_t launch_gateup_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
+                            const void *wu, hipStream_t s);
+hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
+                          const void *gamma_next, hipStream_t s);
+hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
+                          const char *vp, const float *ksc, const float *vsc,
+                          const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,
+                          const float *q, const float *kself, const float *vself, float *o,
+                          uint16_t *op, hipStream_t s);
 hipError_t launch_qkv_finish(const Dims &dm, const Plan &p, const Workspace &w,
                              const int32_t *lengths, hipStream_t s);
 hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, int layer,

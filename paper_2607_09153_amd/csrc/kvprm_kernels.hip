@@ -59,23 +59,46 @@ __device__ __forceinline__ float block_sum256(float v, float *red) {
 
 // ------------------------------------------------------------------------------- plan
 
+// Split-K plan of a matrix-core GEMV: split K only as far as needed for about 2048 waves, in
+// whole 32-wide blocks.
+static GemvPlan gemv_plan(int rows, int K, int B) {
+  GemvPlan g;
+  g.rows = rows;
+  g.K = K;
+  const int mt = gemv_nt(B) >= 2 ? 2 : 1;
+  const int waves = (rows / 16 + mt - 1) / mt;
+  int want = (2048 + waves - 1) / waves;
+  const int nkb = K / 32;
+  if (want < 1) want = 1;
+  if (want > nkb) want = nkb;
+  const int kb_per = (nkb + want - 1) / want;
+  g.kslice = kb_per * 32;
+  g.ksplit = (K + g.kslice - 1) / g.kslice;
+  return g;
+}
+
 Plan make_plan(const Dims &dm, int B, int max_pages) {
   Plan p{};
   p.B = B;
   p.max_pages = max_pages;
   p.nch = (max_pages + kChunkPages - 1) / kChunkPages;
-  p.nss = (dm.H + 255) / 256;
+  size_t m = 0;
   if (dm.wdt == 1) {
-    // matrix-core GEMV: split K only as far as needed to cover the chip
-    gemv_split((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B, p.kslice_qkv, p.ks_qkv);
-    gemv_split(dm.H, dm.nq * dm.d, B, p.kslice_o, p.ks_o);
-    gemv_split(2 * dm.F, dm.H, B, p.kslice_gu, p.ks_gu);
-    gemv_split(dm.H, dm.F, B, p.kslice_d, p.ks_d);
-    int kmax = dm.H > dm.F ? dm.H : dm.F;
-    if (dm.nq * dm.d > kmax) kmax = dm.nq * dm.d;
-    p.act_bytes = (size_t)(kmax / 32) * gemv_nt(B) * 64 * 16;
+    p.rb = 64;
+    p.nt = gemv_nt(B);
+    p.bp = gemv_bp(B);
+    p.g_qkv = gemv_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B);
+    p.g_o = gemv_plan(dm.H, dm.nq * dm.d, B);
+    p.g_gu = gemv_plan(2 * dm.F, dm.H, B);
+    p.g_d = gemv_plan(dm.H, dm.F, B);
+    const GemvPlan *gs[4] = {&p.g_qkv, &p.g_o, &p.g_gu, &p.g_d};
+    for (const GemvPlan *g : gs) {
+      const size_t e = (size_t)((g->ksplit + 3) & ~3) * g->rows;
+      if (e > m) m = e;
+    }
   } else {
     // vector-ALU GEMV: the activation slice of all B candidates is staged in LDS (<= 32 KiB)
+    p.rb = 256;
     auto slice = [&](int K) {
       int s = (8192 / (B > 0 ? B : 1)) & ~63;
       if (s < 64) s = 64;
@@ -90,15 +113,11 @@ Plan make_plan(const Dims &dm, int B, int max_pages) {
     p.ks_o = (dm.nq * dm.d + p.kslice_o - 1) / p.kslice_o;
     p.ks_gu = (dm.H + p.kslice_gu - 1) / p.kslice_gu;
     p.ks_d = (dm.F + p.kslice_d - 1) / p.kslice_d;
-    p.act_bytes = 0;
+    const size_t e[4] = {(size_t)p.ks_qkv * (dm.nq + 2 * dm.nkv) * dm.d, (size_t)p.ks_o * dm.H,
+                         (size_t)p.ks_gu * 2 * dm.F, (size_t)p.ks_d * dm.H};
+    for (size_t v : e) m = v > m ? v : m;
   }
-  size_t a = (size_t)p.ks_qkv * (dm.nq + 2 * dm.nkv) * dm.d;
-  size_t b2 = (size_t)p.ks_o * dm.H;
-  size_t c = (size_t)p.ks_gu * 2 * dm.F;
-  size_t e = (size_t)p.ks_d * dm.H;
-  size_t m = a > b2 ? a : b2;
-  m = m > c ? m : c;
-  m = m > e ? m : e;
+  p.nss = (dm.H + p.rb - 1) / p.rb;
   p.part_elems = m * (size_t)B;
   return p;
 }
@@ -121,10 +140,16 @@ Workspace carve(const Dims &dm, const Plan &p, void *base) {
   w.q = take(B * dm.nq * dm.d);
   w.kself = take(B * dm.nkv * dm.d);
   w.vself = take(B * dm.nkv * dm.d);
-  w.apart = take(B * dm.nq * (size_t)p.nch * (dm.d + 2));
+  w.apart = take(B * dm.nq * (size_t)((p.nch + 3) & ~3) * (dm.d + 2));
   w.o = take(B * dm.nq * dm.d);
   w.hffn = take(B * dm.F);
-  w.act = (uint4 *)take((p.act_bytes + 3) / 4);
+  if (dm.wdt == 1) {
+    const size_t per_k = (size_t)p.nt * 64 * 8 / 32;  // bf16 elements per input of an operand
+    w.rope = take(B * dm.d);
+    w.opA = (uint16_t *)take((per_k * dm.H + 1) / 2);
+    w.opO = (uint16_t *)take((per_k * dm.nq * dm.d + 1) / 2);
+    w.opD = (uint16_t *)take((per_k * dm.F + 1) / 2);
+  }
   w.bytes = off;
   return w;
 }
@@ -231,9 +256,7 @@ __global__ __launch_bounds__(256) void k_gemv_valu(GemvSegs segs, int rows_total
 
 hipError_t launch_gemv(const Dims &dm, const Plan &p, const GemvSegs &segs, int K, int kslice,
                        int ksplit, const float *in, const void *gamma, const float *ss,
-                       float *part, uint4 *actbuf, hipStream_t s) {
-  if (dm.wdt == 1)
-    return launch_gemv_mfma(dm, p, segs, K, kslice, ksplit, in, gamma, ss, part, actbuf, s);
+                       float *part, hipStream_t s) {
   int rows = 0;
   for (int i = 0; i < segs.nseg; ++i) rows += segs.rows[i];
   dim3 grid((rows + 255) / 256, ksplit);
@@ -501,11 +524,9 @@ hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, i
   const char *vp = (const char *)vpool + layer_elems * EB * layer;
   const float *ksc = kscale ? kscale + (size_t)layer * num_pages * dm.nkv : nullptr;
   const float *vsc = vscale ? vscale + (size_t)layer * num_pages * dm.nkv : nullptr;
-  if (dm.kvdt != 0) {
-    hipError_t e = launch_attn_mfma(dm, p, kp, vp, ksc, vsc, page_table, lengths, gt, q, w.apart, s);
-    if (e != hipSuccess) return e;
-    return launch_merge(dm, p, w, gt, lengths, q, kself, vself, o, s);
-  }
+  if (dm.kvdt != 0)  // matrix-core kernels (bf16 and fp8 caches)
+    return launch_attn_mx(dm, p, w, kp, vp, ksc, vsc, page_table, lengths, gt, q, kself, vself, o,
+                          nullptr, s);
   dim3 grid(p.nch, dm.nkv, p.B);
 #define KVPRM_ATT(KVT, D)                                                                     \
   hipLaunchKernelGGL((k_attn_valu<KVT, D>), grid, dim3(256), 0, s, kp, vp, ksc, vsc, dm.nkv, \

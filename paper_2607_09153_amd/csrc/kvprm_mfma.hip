@@ -1,10 +1,20 @@
-// Matrix-core (MFMA, v_mfma_f32_16x16x32_bf16) kernels of the verify-token pass for gfx950:
-// the projection GEMVs over bf16 weights and the split-L paged attention over bf16 / fp8 caches.
+// Matrix-core (MFMA, v_mfma_f32_16x16x32_bf16) pipeline of the verify-token pass for gfx950,
+// used with bf16 weights and bf16 or fp8 (OCP e4m3) caches. Per layer:
+//
+//   QKV GEMV -> finish (RMSNorm scale + rotary -> q, k_self, v_self)
+//   attention (split-L paged partials) -> merge with the token's own key (-> o, as operand)
+//   O GEMV -> residual (x += .., sums of squares, operand x * gamma_ffn)
+//   gate/up GEMV -> SwiGLU (RMSNorm scale, silu(g) * u, operand of the down projection)
+//   down GEMV -> residual (x += .., sums of squares, operand x * gamma_attn of the next layer)
+//
+// GEMVs split K over blocks and store k-partials; the following small kernel sums them in a
+// fixed order, so results are bitwise reproducible. RMSNorm is applied as a per-candidate
+// scale after the product: W (x * gamma * r) = r * (W (x * gamma)), r = 1/sqrt(mean(x^2) + eps).
 //
 // Precision: weights and cache values enter the matrix cores exactly (bf16, or e4m3 widened to
-// bf16, which is exact). The fp32 operands on the other side (activations, queries, softmax
-// probabilities) are split as x = hi + lo with hi = bf16(x), lo = bf16(x - hi), and both halves
-// are multiplied, so products carry ~16 significant bits and accumulate in fp32.
+// bf16, which is exact). The fp32 operands on the other side are split into bf16 terms,
+// x = hi + lo (three terms for queries), and every term is multiplied, so products keep about
+// fp32 accuracy and accumulate in fp32.
 //
 // MFMA 16x16x32 operand layout used throughout (lane l, c = l / 16, n = l % 16):
 //   A (16 x 32): lane holds row n, reduction slots 8c .. 8c+7
@@ -12,7 +22,14 @@
 //   D (16 x 16): lane holds rows 4c .. 4c+3 of column n
 // Reduction slots are paired between A and B by (c, element), so any assignment of the
 // contracted index to slots is valid as long as both operands use the same one.
+//
+// Activation operand of a GEMV ("operand buffer"): for k-block kb (32 inputs), column tile t
+// and lane, 8 bf16 = inputs 32 kb + 8 (lane / 16) + i of column 16 t + lane % 16. Columns: with
+// Bp == 8 (batch <= 8, one tile) columns 0..7 hold the hi halves and 8..15 the lo halves of
+// candidates 0..7; otherwise columns [0, Bp) are hi and [Bp, 2 Bp) lo (Bp = batch rounded up
+// to 16). Columns of absent candidates only ever reach outputs that are discarded.
 #include <math.h>
+#include <string.h>
 
 #include "kvprm_internal.h"
 
@@ -40,81 +57,127 @@ __device__ __forceinline__ void split_hi_lo(float x, uint32_t &hi, uint32_t &lo)
 
 __device__ __forceinline__ uint32_t pack2(uint32_t a, uint32_t b) { return a | (b << 16); }
 
-// ------------------------------------------------------------------------------- GEMV operand
-
-// Activation operand of the projection GEMV, in B-operand order:
-//   buf[(kb * NT + t) * 64 + lane] = 8 bf16 for k = 32 kb + 8 (lane / 16) + i, column
-//   t * 16 + lane % 16.
-// Column -> (candidate, half): with Bp == 8 (NT == 1) columns 0..7 are the hi halves and 8..15
-// the lo halves of candidates 0..7; otherwise columns [0, Bp) are hi and [Bp, 2 Bp) lo.
-// u = in (optionally RMS-normalised: in * rsqrt(mean(in^2) + eps) * gamma, with the sum of
-// squares taken from the per-256-row partials ss).
-__global__ __launch_bounds__(256) void k_act_prep(const float *in, int K, const void *gamma,
-                                                  int wdt, const float *ss, int nss, float eps,
-                                                  int B, int Bp, int NT, uint4 *buf) {
-  const int idx = blockIdx.x * 256 + threadIdx.x;
-  const int total = (K / 32) * NT * 64;
-  if (idx >= total) return;
-  const int lane = idx & 63;
-  const int t = (idx >> 6) % NT;
-  const int kb = (idx >> 6) / NT;
-  const int col = t * 16 + (lane & 15);
-  const int lo_half = (col >= Bp) ? 1 : 0;
-  const int cand = col - lo_half * Bp;
-  uint32_t h16[8];
-  if (cand < B) {
-    float inv = 1.f;
-    if (gamma) {
-      float s = 0.f;
-      for (int i = 0; i < nss; ++i) s += ss[(size_t)i * B + cand];
-      inv = 1.0f / sqrtf(s / (float)K + eps);
-    }
-    const int k0 = kb * 32 + 8 * (lane >> 4);
-    const float *src = in + (size_t)cand * K + k0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      float u = src[i];
-      if (gamma) {
-        const float gm = wdt ? __uint_as_float((uint32_t)((const uint16_t *)gamma)[k0 + i] << 16)
-                             : ((const float *)gamma)[k0 + i];
-        u = u * inv * gm;
-      }
-      uint32_t hi, lo;
-      split_hi_lo(u, hi, lo);
-      h16[i] = lo_half ? lo : hi;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) h16[i] = 0;
-  }
-  buf[idx] = make_uint4(pack2(h16[0], h16[1]), pack2(h16[2], h16[3]), pack2(h16[4], h16[5]),
-                        pack2(h16[6], h16[7]));
+__device__ __forceinline__ float ld_w(const void *p, size_t i, int wdt) {
+  return wdt ? __uint_as_float((uint32_t)((const uint16_t *)p)[i] << 16) : ((const float *)p)[i];
 }
 
-// ------------------------------------------------------------------------------- GEMV (MFMA)
+// Store v for input k of candidate cand into an operand buffer (hi and lo halves).
+__device__ __forceinline__ void store_operand(uint16_t *op, int NT, int Bp, int k, int cand,
+                                              float v) {
+  uint32_t hi, lo;
+  split_hi_lo(v, hi, lo);
+  const int kb = k >> 5, c = (k >> 3) & 3, i = k & 7;
+  int col = cand;
+  op[((size_t)((kb * NT + (col >> 4)) * 64 + c * 16 + (col & 15))) * 8 + i] = (uint16_t)hi;
+  col = cand + Bp;
+  op[((size_t)((kb * NT + (col >> 4)) * 64 + c * 16 + (col & 15))) * 8 + i] = (uint16_t)lo;
+}
 
-// part[ks][row][b] = sum over the k-slice of W[row][k] u_b[k]. Each wave owns MT consecutive
+__device__ __forceinline__ float wsum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wmax(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// Deterministic 256-thread block reductions; every thread receives the result.
+__device__ __forceinline__ float bsum(float v, float *red) {
+  v = wsum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__device__ __forceinline__ float bmax(float v, float *red) {
+  v = wmax(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+int gemv_nt(int B) { return B <= 8 ? 1 : 2 * ((B + 15) / 16); }
+int gemv_bp(int B) { return B <= 8 ? 8 : 16 * ((B + 15) / 16); }
+
+// ------------------------------------------------------------------------------- init
+
+// x_b = e_v, the sums of squares per 64-row block, the QKV operand e_v * gamma_attn(0), and the
+// rotary table cos/sin(L_b theta^(-2i/d)) (angles in fp64).
+__global__ __launch_bounds__(256) void k_init_mx(float *x, float *ss, int RB, const void *ev,
+                                                 const void *gamma0, int wdt, int B, int H,
+                                                 uint16_t *opA, int NT, int Bp,
+                                                 const int32_t *lengths, float theta, int d,
+                                                 float *rope) {
+  __shared__ float red[4];
+  const int r0 = blockIdx.x * RB;
+  const int nr = min(RB, H - r0);
+  float sq = 0.f;
+  for (int i = threadIdx.x; i < nr; i += 256) {
+    const int r = r0 + i;
+    const float v = ld_w(ev, r, wdt);
+    sq += v * v;
+    const float u = v * ld_w(gamma0, r, wdt);
+    for (int b = 0; b < B; ++b) {
+      x[(size_t)b * H + r] = v;
+      store_operand(opA, NT, Bp, r, b, u);
+    }
+  }
+  sq = bsum(sq, red);
+  if (threadIdx.x < B) ss[(size_t)blockIdx.x * B + threadIdx.x] = sq;
+  if (blockIdx.x == 0) {
+    for (int e = threadIdx.x; e < B * (d / 2); e += 256) {
+      const int b = e / (d / 2), i = e - b * (d / 2);
+      const double inv = pow((double)theta, (-2.0 * (double)i) / (double)d);
+      double sn, cs;
+      sincos((double)lengths[b] * inv, &sn, &cs);
+      rope[2 * e] = (float)cs;
+      rope[2 * e + 1] = (float)sn;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------- GEMV
+
+struct GemvArgs {
+  const void *w[3];  // weight segments [rows_i][K], row-major, stacked in order
+  int seg_rows[3];
+  int nseg;
+  int rows, K, kslice, ksplit;
+  const uint4 *act;  // operand buffer of the input
+  int B;
+  float *part;  // [rows][B][ksp] k-partials, ksp = ksplit rounded up to 4
+  int ksp;
+};
+
+// part[row][b][ks] = sum over k-slice ks of W[row][k] u_b[k]. Each wave owns MT consecutive
 // 16-row tiles; per 32-wide k-block it loads MT weight tiles straight from HBM into A-operand
-// registers (16 bytes per lane, rows n, k 8c..8c+7) and NT activation tiles (L2-resident, 1 KiB
-// per wave-load), and issues MT * NT MFMAs. hi/lo halves are added in the epilogue.
+// registers (16 bytes per lane: row n, inputs 8c .. 8c+7) and NT operand tiles (L2-resident,
+// 1 KiB per wave-load) and issues MT * NT MFMAs. The hi and lo halves of each candidate are
+// added before the partial is stored.
 template <int MT, int NT>
-__global__ __launch_bounds__(256) void k_gemv_mfma(GemvSegs segs, int rows_total, int K, int kslice,
-                                                   const uint4 *act, int B, int Bp, float *part) {
+__global__ __launch_bounds__(256) void k_gemv_mx(GemvArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rt0 = (blockIdx.x * 4 + wave) * MT;
   const int ks = blockIdx.y;
-  const int k0 = ks * kslice;
-  const int nkb = min(kslice, K - k0) >> 5;
-  if (rt0 * 16 >= rows_total) return;
+  const int k0 = ks * a.kslice;
+  const int nkb = min(a.kslice, a.K - k0) >> 5;
+  const int tile0 = (blockIdx.x * 4 + wave) * MT;
+  const int B = a.B;
+  if (tile0 * 16 >= a.rows) return;
   const uint16_t *wrow[MT];
   bool valid[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
-    const int r = (rt0 + m) * 16 + (lane & 15);
-    valid[m] = (rt0 + m) * 16 < rows_total;
+    const int r = (tile0 + m) * 16 + (lane & 15);
+    valid[m] = (tile0 + m) * 16 < a.rows;
     int seg = 0, base = 0;
-    while (seg < segs.nseg - 1 && r >= base + segs.rows[seg]) base += segs.rows[seg++];
-    wrow[m] = (const uint16_t *)segs.w[seg] + (size_t)(valid[m] ? r - base : 0) * K + k0 +
+    while (seg < a.nseg - 1 && r >= base + a.seg_rows[seg]) base += a.seg_rows[seg++];
+    wrow[m] = (const uint16_t *)a.w[seg] + (size_t)(valid[m] ? r - base : 0) * a.K + k0 +
               8 * (lane >> 4);
   }
   floatx4 acc[MT][NT];
@@ -122,30 +185,30 @@ __global__ __launch_bounds__(256) void k_gemv_mfma(GemvSegs segs, int rows_total
   for (int m = 0; m < MT; ++m)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const uint4 *ap = act + (size_t)(k0 >> 5) * NT * 64 + lane;
+  const uint4 *ap = a.act + (size_t)(k0 >> 5) * NT * 64 + lane;
 #pragma unroll 4
   for (int kb = 0; kb < nkb; ++kb) {
-    uint4 a[MT], bv[NT];
+    uint4 av[MT], bv[NT];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
-      a[m] = valid[m] ? *(const uint4 *)(wrow[m] + kb * 32) : make_uint4(0, 0, 0, 0);
+      av[m] = valid[m] ? *(const uint4 *)(wrow[m] + kb * 32) : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int t = 0; t < NT; ++t) bv[t] = ap[(size_t)(kb * NT + t) * 64];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
-      for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(a[m], bv[t], acc[m][t]);
+      for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av[m], bv[t], acc[m][t]);
   }
   const int n = lane & 15, c4 = (lane >> 4) * 4;
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     if (!valid[m]) continue;
-    const int rbase = (rt0 + m) * 16 + c4;
+    const int rbase = (tile0 + m) * 16 + c4;
     if (NT == 1) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float v = acc[m][0][i] + __shfl_xor(acc[m][0][i], 8, 64);
-        if (n < 8 && n < B) part[((size_t)ks * rows_total + rbase + i) * B + n] = v;
+        if (n < 8 && n < B) a.part[((size_t)(rbase + i) * B + n) * a.ksp + ks] = v;
       }
     } else {
 #pragma unroll
@@ -154,57 +217,115 @@ __global__ __launch_bounds__(256) void k_gemv_mfma(GemvSegs segs, int rows_total
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float v = acc[m][t][i] + acc[m][t + NT / 2][i];
-          if (cand < B) part[((size_t)ks * rows_total + rbase + i) * B + cand] = v;
+          if (cand < B) a.part[((size_t)(rbase + i) * B + cand) * a.ksp + ks] = v;
         }
       }
     }
   }
 }
 
-int gemv_nt(int B) { return B <= 8 ? 1 : 2 * ((B + 15) / 16); }
-int gemv_bp(int B) { return B <= 8 ? 8 : 16 * ((B + 15) / 16); }
-
-// Split-K plan for the MFMA GEMV: enough waves to cover the chip, k-slices of whole 32-blocks.
-void gemv_split(int rows, int K, int B, int &kslice, int &ksplit) {
-  const int NT = gemv_nt(B);
-  const int MT = NT >= 2 ? 2 : 1;
-  const int waves_per_split = (rows / 16 + MT - 1) / MT;
-  const int target = 3072;
-  int want = (target + waves_per_split - 1) / waves_per_split;
-  const int nkb = K / 32;
-  if (want < 1) want = 1;
-  if (want > nkb) want = nkb;
-  const int kb_per = (nkb + want - 1) / want;
-  kslice = kb_per * 32;
-  ksplit = (K + kslice - 1) / kslice;
-}
-
-hipError_t launch_gemv_mfma(const Dims &dm, const Plan &p, const GemvSegs &segs, int K,
-                            int kslice, int ksplit, const float *in, const void *gamma,
-                            const float *ss, float *part, uint4 *actbuf, hipStream_t s) {
-  const int B = p.B, NT = gemv_nt(B), Bp = gemv_bp(B);
-  const int total = (K / 32) * NT * 64;
-  hipLaunchKernelGGL(k_act_prep, dim3((total + 255) / 256), dim3(256), 0, s, in, K, gamma, dm.wdt,
-                     ss, p.nss, dm.eps, B, Bp, NT, actbuf);
-  int rows = 0;
-  for (int i = 0; i < segs.nseg; ++i) rows += segs.rows[i];
-  const int rt = rows / 16;
-#define KVPRM_GEMV(MT_, NT_)                                                                  \
-  hipLaunchKernelGGL((k_gemv_mfma<MT_, NT_>), dim3((rt + 4 * MT_ - 1) / (4 * MT_), ksplit),   \
-                     dim3(256), 0, s, segs, rows, K, kslice, (const uint4 *)actbuf, B, Bp, part)
-  switch (NT) {
-    case 1: KVPRM_GEMV(1, 1); break;
-    case 2: KVPRM_GEMV(2, 2); break;
-    case 4: KVPRM_GEMV(2, 4); break;
-    case 6: KVPRM_GEMV(2, 6); break;
-    case 8: KVPRM_GEMV(2, 8); break;
-    default: return hipErrorInvalidValue;
+// Sum of the k-partials of output (r, b): contiguous, read with 16-byte loads, added in k order.
+__device__ __forceinline__ float ksum(const float *part, int ksp, int ksplit, int r, int B, int b) {
+  const float4 *pp = (const float4 *)(part + ((size_t)r * B + b) * ksp);
+  float s = 0.f;
+  for (int k4 = 0; k4 < (ksp >> 2); ++k4) {
+    const float4 v = pp[k4];
+    const int k = 4 * k4;
+    s += v.x;
+    if (k + 1 < ksplit) s += v.y;
+    if (k + 2 < ksplit) s += v.z;
+    if (k + 3 < ksplit) s += v.w;
   }
-#undef KVPRM_GEMV
-  return hipGetLastError();
+  return s;
 }
 
-// ------------------------------------------------------------------------------- attention (MFMA)
+// r_b = 1 / sqrt(mean(x_b^2) + eps) from the per-row-block sums of squares, into inv_s[b].
+__device__ __forceinline__ void load_inv_rms(const float *ss, int nss, int B, int H, float eps,
+                                             float *inv_s) {
+  for (int b = threadIdx.x; b < B; b += blockDim.x) {
+    float s = 0.f;
+    for (int i = 0; i < nss; ++i) s += ss[(size_t)i * B + b];
+    inv_s[b] = 1.0f / sqrtf(s / (float)H + eps);
+  }
+  __syncthreads();
+}
+
+// q, k_self, v_self from the QKV partials: scale by r_b (the attention RMSNorm, applied after
+// the product) and rotate q and k pairs (i, i + d/2) with the cos/sin table of position L_b.
+// One thread per (pair, candidate).
+__global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *part, int ksp, int ksplit,
+                                                    const float *ss, int nss, int H, float eps,
+                                                    int B, int nq, int nkv, int d,
+                                                    const float *rope, float *q, float *ks,
+                                                    float *vs) {
+  __shared__ float inv_s[64];
+  load_inv_rms(ss, nss, B, H, eps, inv_s);
+  const int hd = d / 2;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= (nq + 2 * nkv) * hd * B) return;
+  const int pr = e / B, b = e - pr * B;
+  const int head = pr / hd, i = pr - head * hd;
+  const int r = head * d + i;
+  const float inv = inv_s[b];
+  const float x1 = ksum(part, ksp, ksplit, r, B, b) * inv;
+  const float x2 = ksum(part, ksp, ksplit, r + hd, B, b) * inv;
+  float o1 = x1, o2 = x2;
+  if (head < nq + nkv) {
+    const float cs = rope[((size_t)b * hd + i) * 2], sn = rope[((size_t)b * hd + i) * 2 + 1];
+    o1 = x1 * cs - x2 * sn;
+    o2 = x2 * cs + x1 * sn;
+  }
+  float *dst;
+  if (head < nq)
+    dst = q + ((size_t)b * nq + head) * d;
+  else if (head < nq + nkv)
+    dst = ks + ((size_t)b * nkv + (head - nq)) * d;
+  else
+    dst = vs + ((size_t)b * nkv + (head - nq - nkv)) * d;
+  dst[i] = o1;
+  dst[i + hd] = o2;
+}
+
+// Residual add x += sum_k partials for a block of 64 rows, the rows' sums of squares per
+// candidate (ss[block][b], fixed order), and the next GEMV's operand x * gamma_next.
+__global__ __launch_bounds__(256) void k_resid_mx(float *x, const float *part, int ksp, int ksplit,
+                                                  float *ss, int B, int H, const void *gamma_next,
+                                                  int wdt, uint16_t *op, int NT, int Bp) {
+  __shared__ float sq_s[64][65];
+  const int r0 = blockIdx.x * 64;
+  const int nr = min(64, H - r0);
+  for (int e = threadIdx.x; e < nr * B; e += 256) {
+    const int rl = e / B, b = e - rl * B, r = r0 + rl;
+    const float xv = x[(size_t)b * H + r] + ksum(part, ksp, ksplit, r, B, b);
+    x[(size_t)b * H + r] = xv;
+    sq_s[rl][b] = xv * xv;
+    if (gamma_next) store_operand(op, NT, Bp, r, b, xv * ld_w(gamma_next, r, wdt));
+  }
+  __syncthreads();
+  if (threadIdx.x < B) {
+    float s = 0.f;
+    for (int rl = 0; rl < nr; ++rl) s += sq_s[rl][threadIdx.x];
+    ss[(size_t)blockIdx.x * B + threadIdx.x] = s;
+  }
+}
+
+// h = silu(r_b g) * (r_b u) for gate rows f and up rows F + f (the FFN RMSNorm applied after
+// the product), written as the down projection's operand. One thread per (feature, candidate).
+__global__ __launch_bounds__(256) void k_swiglu_mx(const float *part, int ksp, int ksplit,
+                                                   const float *ss, int nss, int H, float eps,
+                                                   int B, int F, uint16_t *op, int NT, int Bp) {
+  __shared__ float inv_s[64];
+  load_inv_rms(ss, nss, B, H, eps, inv_s);
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= F * B) return;
+  const int f = e / B, b = e - f * B;
+  const float inv = inv_s[b];
+  const float gv = ksum(part, ksp, ksplit, f, B, b) * inv;
+  const float uv = ksum(part, ksp, ksplit, F + f, B, b) * inv;
+  store_operand(op, NT, Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
+}
+
+// ------------------------------------------------------------------------------- attention
 
 template <bool HIGH>
 __device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t word) {
@@ -213,22 +334,33 @@ __device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t word) {
   return (__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xFFFF0000u);
 }
 
+struct AttnArgs {
+  const char *kp, *vp;     // this layer's pools
+  const float *ksc, *vsc;  // this layer's fp8 scales (or null)
+  int nkv, g, nq;
+  const int32_t *page_table;
+  int max_pages;
+  const int32_t *lengths;
+  GroupTable gt;
+  int nch;
+  const float *q, *kself, *vself;
+  float *apart;   // [B][nq][D + 2][nchp]: acc rows, then m, then l; chunk index innermost
+  int nchp;       // chunk slots per row (nch rounded up to 4)
+  float *o;       // [B][nq][D] fp32 output (may be null)
+  uint16_t *op;   // operand buffer of the output projection (may be null)
+  int NT, Bp;
+};
+
 // One block (4 waves) per (chunk of kChunkPages pages, kv-head j, candidate b) over the
 // candidate's private pages. Each wave takes page pairs (32 tokens): S = K Q^T on the matrix
 // cores (A = the K tile, 16 tokens x 32 dims; B = the g query heads as columns, in three bf16
-// terms),
-// online softmax per head in registers (a lane holds 4 tokens of one head per page), then
-// O^T += V^T P^T (A = V^T rows of 16 dims x 32 tokens read straight from the dimension-major V
-// tile, B = P^T hi and lo). The four waves merge through LDS and write one unnormalised partial
+// terms), online softmax per head in registers (a lane holds 4 tokens of one head per page),
+// then O^T += V^T P^T (A = V^T, 16 dims x 32 tokens, read straight from the dimension-major V
+// tile; B = P^T hi and lo). The four waves combine through LDS into one unnormalised partial
 // (acc, m, l) per q-head. Slots at or beyond L_b are masked in S and zeroed in V (they may hold
 // anything, NaN included).
 template <int KVT, int D>
-__global__ __launch_bounds__(256) void k_attn_mfma(const void *kpool, const void *vpool,
-                                                   const float *kscale, const float *vscale,
-                                                   int nkv, int g, const int32_t *page_table,
-                                                   int max_pages, const int32_t *lengths,
-                                                   GroupTable gt, int nch, const float *q,
-                                                   float *apart, int nq) {
+__global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
   constexpr int NKB = D / 32;  // 32-dim blocks of q.k
   constexpr int NDB = D / 16;  // 16-dim blocks of the output
   constexpr int EB = KVT == 1 ? 2 : 1;
@@ -239,28 +371,21 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const void *kpool, const void
   __shared__ float red_acc[4][D][17];
 
   const int c = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
-  const int L = lengths[b];
+  const int nkv = a.nkv, g = a.g, nq = a.nq;
+  const int L = a.lengths[b];
   const int npages = (L + kPage - 1) / kPage;
   int first = 0;
-  for (int gi = 0; gi < gt.n; ++gi)
-    if (b >= gt.start[gi] && b < gt.start[gi + 1]) first = gt.prefix_pages[gi];
+  for (int gi = 0; gi < a.gt.n; ++gi)
+    if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
   const int p0 = first + c * kChunkPages;
-  float *outbase = apart + (((size_t)b * nq + (size_t)j * g) * nch + c) * (D + 2);
-  const size_t hstride = (size_t)nch * (D + 2);
-  if (p0 >= npages) {
-    for (int i = threadIdx.x; i < g * (D + 2); i += 256) {
-      const int h = i / (D + 2), e = i - h * (D + 2);
-      outbase[h * hstride + e] = (e == D) ? -INFINITY : 0.f;
-    }
-    return;
-  }
+  if (p0 >= npages) return;
   const int np = min(npages, p0 + kChunkPages) - p0;
   if (threadIdx.x < np) {
-    const int ph = page_table[(size_t)b * max_pages + p0 + threadIdx.x];
+    const int ph = a.page_table[(size_t)b * a.max_pages + p0 + threadIdx.x];
     phys_s[threadIdx.x] = ph;
     if (KVT == 2) {
-      ksc_s[threadIdx.x] = kscale[(size_t)ph * nkv + j];
-      vsc_s[threadIdx.x] = vscale[(size_t)ph * nkv + j];
+      ksc_s[threadIdx.x] = a.ksc[(size_t)ph * nkv + j];
+      vsc_s[threadIdx.x] = a.vsc[(size_t)ph * nkv + j];
     }
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -270,7 +395,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const void *kpool, const void
   // scores keep fp32-level accuracy even for very large logits
   uint4 qhi[NKB], qmd[NKB], qlo[NKB];
   {
-    const float *qr = q + ((size_t)b * nq + (size_t)j * g + (n < g ? n : 0)) * D;
+    const float *qr = a.q + ((size_t)b * nq + (size_t)j * g + (n < g ? n : 0)) * D;
 #pragma unroll
     for (int kk = 0; kk < NKB; ++kk) {
       uint32_t h[8], md[8], l[8];
@@ -306,10 +431,10 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const void *kpool, const void
     const bool hasB = lb < np;
     const int pa = phys_s[la];
     const int pb = hasB ? phys_s[lb] : pa;
-    const char *kA = (const char *)kpool + ((size_t)pa * nkv + j) * TILE;
-    const char *kB = (const char *)kpool + ((size_t)pb * nkv + j) * TILE;
-    const char *vA = (const char *)vpool + ((size_t)pa * nkv + j) * TILE;
-    const char *vB = (const char *)vpool + ((size_t)pb * nkv + j) * TILE;
+    const char *kA = a.kp + ((size_t)pa * nkv + j) * TILE;
+    const char *kB = a.kp + ((size_t)pb * nkv + j) * TILE;
+    const char *vA = a.vp + ((size_t)pa * nkv + j) * TILE;
+    const char *vB = a.vp + ((size_t)pb * nkv + j) * TILE;
     // ---- loads
     uint4 KA[NKB], KB[NKB];
     uint2 VA[NDB], VB[NDB];
@@ -426,7 +551,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const void *kpool, const void
       acc[nb] = mfma16(vop, Plo, acc[nb]);
     }
   }
-  // ---- merge the four waves
+  // ---- combine the four waves into this chunk's partial
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
   if (lane < 16) {
@@ -438,42 +563,221 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const void *kpool, const void
 #pragma unroll
     for (int i = 0; i < 4; ++i) red_acc[wave][nb * 16 + 4 * cq + i][n] = acc[nb][i];
   __syncthreads();
+  const size_t hrow = (size_t)(D + 2) * a.nchp;
+  float *outbase = a.apart + ((size_t)b * nq + (size_t)j * g) * hrow + c;
   for (int e = threadIdx.x; e < g * D; e += 256) {
     const int h = e / D, d = e - h * D;
     float M = red_m[0][h];
 #pragma unroll
     for (int w = 1; w < 4; ++w) M = fmaxf(M, red_m[w][h]);
-    float a = 0.f, l = 0.f;
+    float av = 0.f, lv = 0.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const float f = (red_m[w][h] == -INFINITY) ? 0.f : expf(red_m[w][h] - M);
-      a += f * red_acc[w][d][h];
-      l += f * red_l[w][h];
+      av += f * red_acc[w][d][h];
+      lv += f * red_l[w][h];
     }
-    outbase[h * hstride + d] = a;
+    outbase[h * hrow + (size_t)d * a.nchp] = av;
     if (d == 0) {
-      outbase[h * hstride + D] = M;
-      outbase[h * hstride + D + 1] = l;
+      outbase[h * hrow + (size_t)D * a.nchp] = M;
+      outbase[h * hrow + (size_t)(D + 1) * a.nchp] = lv;
     }
   }
 }
 
-hipError_t launch_attn_mfma(const Dims &dm, const Plan &p, const char *kp, const char *vp,
-                            const float *ksc, const float *vsc, const int32_t *page_table,
-                            const int32_t *lengths, const GroupTable &gt, const float *q,
-                            float *apart, hipStream_t s) {
-  dim3 grid(p.nch, dm.nkv, p.B);
-#define KVPRM_ATTM(KVT, D)                                                                   \
-  hipLaunchKernelGGL((k_attn_mfma<KVT, D>), grid, dim3(256), 0, s, kp, vp, ksc, vsc, dm.nkv, \
-                     dm.g, page_table, p.max_pages, lengths, gt, p.nch, q, apart, dm.nq)
-  if (dm.kvdt == 1) {
-    if (dm.d == 64) KVPRM_ATTM(1, 64);
-    else KVPRM_ATTM(1, 128);
-  } else {
-    if (dm.d == 64) KVPRM_ATTM(2, 64);
-    else KVPRM_ATTM(2, 128);
+// Log-sum-exp merge of the chunk partials of one (candidate b, q-head h) with the token's own
+// key/value: m = max(s_self, m_c),
+//   o = (e^{s_self - m} v_self + sum_c e^{m_c - m} acc_c) / (e^{s_self - m} + sum_c e^{m_c - m} l_c).
+// One block of D threads per (b, h); each thread owns one output dimension and reads its
+// contiguous row of chunk partials with 16-byte loads. Writes o (fp32) and/or the operand of the
+// output projection.
+template <int D>
+__global__ __launch_bounds__(D) void k_merge_mx(AttnArgs a) {
+  __shared__ float m_s[kMaxChunks], f_s[kMaxChunks];
+  __shared__ float red[4];
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+  const int j = h / a.g;
+  const int L = a.lengths[b];
+  const int npages = (L + kPage - 1) / kPage;
+  int first = 0;
+  for (int gi = 0; gi < a.gt.n; ++gi)
+    if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
+  const int nc = (npages - first + kChunkPages - 1) / kChunkPages;
+  const size_t hrow = (size_t)(D + 2) * a.nchp;
+  const float *base = a.apart + ((size_t)b * a.nq + h) * hrow;
+  // own key: s_self = q . k_self / sqrt(D)
+  float dot = wsum(a.q[((size_t)b * a.nq + h) * D + t] * a.kself[((size_t)b * a.nkv + j) * D + t]);
+  if (D > 64) {
+    if ((t & 63) == 0) red[t >> 6] = dot;
+    __syncthreads();
+    dot = red[0] + red[1];
+    __syncthreads();
   }
-#undef KVPRM_ATTM
+  const float s_self = dot * (1.0f / sqrtf((float)D));
+  for (int c = t; c < nc; c += D) m_s[c] = base[(size_t)D * a.nchp + c];
+  __syncthreads();
+  float M = s_self;
+  for (int c = 0; c < nc; ++c) M = fmaxf(M, m_s[c]);
+  float lsum = 0.f;
+  for (int c = t; c < nc; c += D) {
+    const float f = expf(m_s[c] - M);
+    f_s[c] = f;
+    lsum += f * base[(size_t)(D + 1) * a.nchp + c];
+  }
+  lsum = wsum(lsum);
+  if (D > 64) {
+    if ((t & 63) == 0) red[2 + (t >> 6)] = lsum;
+    __syncthreads();
+    lsum = red[2] + red[3];
+  }
+  __syncthreads();
+  const float4 *row = (const float4 *)(base + (size_t)t * a.nchp);
+  float acc = 0.f;
+#pragma unroll 8
+  for (int c4 = 0; c4 < (nc + 3) >> 2; ++c4) {
+    const float4 v = row[c4];
+    const int c = 4 * c4;
+    acc += f_s[c] * v.x;
+    if (c + 1 < nc) acc += f_s[c + 1] * v.y;
+    if (c + 2 < nc) acc += f_s[c + 2] * v.z;
+    if (c + 3 < nc) acc += f_s[c + 3] * v.w;
+  }
+  const float es = expf(s_self - M);
+  const float ov = (acc + es * a.vself[((size_t)b * a.nkv + j) * D + t]) / (lsum + es);
+  if (a.o) a.o[((size_t)b * a.nq + h) * D + t] = ov;
+  if (a.op) store_operand(a.op, a.NT, a.Bp, h * D + t, b, ov);
+}
+
+// ------------------------------------------------------------------------------- launchers
+
+hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *ev,
+                          const void *gamma0, const int32_t *lengths, hipStream_t s) {
+  hipLaunchKernelGGL(k_init_mx, dim3(p.nss), dim3(256), 0, s, w.x, w.ss, p.rb, ev, gamma0, dm.wdt,
+                     p.B, dm.H, w.opA, p.nt, p.bp, lengths, dm.theta, dm.d, w.rope);
+  return hipGetLastError();
+}
+
+static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *w0, int r0,
+                                 const void *w1, int r1, const void *w2, int r2,
+                                 const uint16_t *act, float *part, hipStream_t s) {
+  GemvArgs a;
+  memset(&a, 0, sizeof a);
+  a.w[0] = w0;
+  a.w[1] = w1;
+  a.w[2] = w2;
+  a.seg_rows[0] = r0;
+  a.seg_rows[1] = r1;
+  a.seg_rows[2] = r2;
+  a.nseg = w2 ? 3 : (w1 ? 2 : 1);
+  a.rows = gp.rows;
+  a.K = gp.K;
+  a.kslice = gp.kslice;
+  a.ksplit = gp.ksplit;
+  a.act = (const uint4 *)act;
+  a.B = p.B;
+  a.part = part;
+  a.ksp = (gp.ksplit + 3) & ~3;
+  const int mt = p.nt >= 2 ? 2 : 1;
+  dim3 grid((gp.rows / 16 + 4 * mt - 1) / (4 * mt), gp.ksplit);
+#define KVPRM_G(MT_, NT_) hipLaunchKernelGGL((k_gemv_mx<MT_, NT_>), grid, dim3(256), 0, s, a)
+  switch (p.nt) {
+    case 1: KVPRM_G(1, 1); break;
+    case 2: KVPRM_G(2, 2); break;
+    case 4: KVPRM_G(2, 4); break;
+    case 6: KVPRM_G(2, 6); break;
+    case 8: KVPRM_G(2, 8); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef KVPRM_G
+  return hipGetLastError();
+}
+
+static int ksp_of(const GemvPlan &g) { return (g.ksplit + 3) & ~3; }
+
+hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
+                         const void *wk, const void *wv, hipStream_t s) {
+  hipError_t e = launch_gemv_mx(p, p.g_qkv, wq, dm.nq * dm.d, wk, dm.nkv * dm.d, wv, dm.nkv * dm.d,
+                                w.opA, w.part, s);
+  if (e != hipSuccess) return e;
+  const int n = (dm.nq + 2 * dm.nkv) * (dm.d / 2) * p.B;
+  hipLaunchKernelGGL(k_qkv_fin_mx, dim3((n + 255) / 256), dim3(256), 0, s, w.part, ksp_of(p.g_qkv),
+                     p.g_qkv.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.nq, dm.nkv, dm.d, w.rope,
+                     w.q, w.kself, w.vself);
+  return hipGetLastError();
+}
+
+hipError_t launch_oproj_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
+                           const void *gamma_ffn, hipStream_t s) {
+  hipError_t e = launch_gemv_mx(p, p.g_o, wo, dm.H, nullptr, 0, nullptr, 0, w.opO, w.part, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_resid_mx, dim3(p.nss), dim3(256), 0, s, w.x, w.part, ksp_of(p.g_o),
+                     p.g_o.ksplit, w.ss, p.B, dm.H, gamma_ffn, dm.wdt, w.opA, p.nt, p.bp);
+  return hipGetLastError();
+}
+
+hipError_t launch_gateup_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
+                            const void *wu, hipStream_t s) {
+  hipError_t e = launch_gemv_mx(p, p.g_gu, wg, dm.F, wu, dm.F, nullptr, 0, w.opA, w.part, s);
+  if (e != hipSuccess) return e;
+  const int n = dm.F * p.B;
+  hipLaunchKernelGGL(k_swiglu_mx, dim3((n + 255) / 256), dim3(256), 0, s, w.part, ksp_of(p.g_gu),
+                     p.g_gu.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.F, w.opD, p.nt, p.bp);
+  return hipGetLastError();
+}
+
+hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
+                          const void *gamma_next, hipStream_t s) {
+  hipError_t e = launch_gemv_mx(p, p.g_d, wd, dm.H, nullptr, 0, nullptr, 0, w.opD, w.part, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_resid_mx, dim3(p.nss), dim3(256), 0, s, w.x, w.part, ksp_of(p.g_d),
+                     p.g_d.ksplit, w.ss, p.B, dm.H, gamma_next, dm.wdt, w.opA, p.nt, p.bp);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
+                          const char *vp, const float *ksc, const float *vsc,
+                          const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,
+                          const float *q, const float *kself, const float *vself, float *o,
+                          uint16_t *op, hipStream_t s) {
+  AttnArgs a;
+  memset(&a, 0, sizeof a);
+  a.kp = kp;
+  a.vp = vp;
+  a.ksc = ksc;
+  a.vsc = vsc;
+  a.nkv = dm.nkv;
+  a.g = dm.g;
+  a.nq = dm.nq;
+  a.page_table = page_table;
+  a.max_pages = p.max_pages;
+  a.lengths = lengths;
+  a.gt = gt;
+  a.nch = p.nch;
+  a.q = q;
+  a.kself = kself;
+  a.vself = vself;
+  a.apart = w.apart;
+  a.nchp = (p.nch + 3) & ~3;
+  a.o = o;
+  a.op = op;
+  a.NT = p.nt;
+  a.Bp = p.bp;
+  dim3 grid(p.nch, dm.nkv, p.B);
+#define KVPRM_A(KVT, D) hipLaunchKernelGGL((k_attn_mx<KVT, D>), grid, dim3(256), 0, s, a)
+  if (dm.kvdt == 1) {
+    if (dm.d == 64) KVPRM_A(1, 64);
+    else KVPRM_A(1, 128);
+  } else {
+    if (dm.d == 64) KVPRM_A(2, 64);
+    else KVPRM_A(2, 128);
+  }
+#undef KVPRM_A
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (dm.d == 64)
+    hipLaunchKernelGGL(k_merge_mx<64>, dim3(p.B, dm.nq), dim3(64), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_merge_mx<128>, dim3(p.B, dm.nq), dim3(128), 0, s, a);
   return hipGetLastError();
 }
 
