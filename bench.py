@@ -66,6 +66,26 @@ def time_attention_step(kv, dw, h, batch, ws, n, reps):
     return sum(ms) / len(ms)
 
 
+def copy_bandwidth(nbytes=4 << 30, reps=10):
+    """Streaming reference on this GPU: a device-to-device copy of nbytes (read + write bytes
+    counted), timed with events; context for the HBM fraction, not a kernel of the path."""
+    import torch
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    del a, b
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
 def cpu_baseline(w, layers_sample):
     """The fp64 oracle, untuned, on all candidates of the workload through its first
     `layers_sample` layers; input generation is done before the clock starts. Scaled to
@@ -159,6 +179,8 @@ def main():
     achieved = kv_per_layer / (attn_ms * 1e-3) / 1e9
     _log(f"attention step: {attn_ms * 1e3:.1f} us/layer, {achieved:.0f} GB/s")
     kv.kvprm_destroy(h)
+    copy_gbps = copy_bandwidth()
+    _log(f"device copy reference: {copy_gbps:.0f} GB/s")
 
     out = {
         "metric": "verify-token scores/sec + achieved KV-read HBM GB/s at L=32k, B=8",
@@ -185,6 +207,7 @@ def main():
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
                      "avg_us": attn_ms * 1e3, "bytes_per_launch": kv_per_layer},
+        "copy_reference_gbps": copy_gbps,
     }
     if args.cpu_layers > 0:
         _log("timing the oracle on the CPU sample ...")

@@ -26,7 +26,8 @@
  * Qwen3/Llama family it evaluates): pre-norm RMSNorm -> Q/K/V projections -> rotate-half
  * rotary embedding at the verify position -> grouped-query attention (q-head h reads kv-head
  * floor(h / g), g = n_q / n_kv) -> output projection -> residual; RMSNorm -> SwiGLU FFN ->
- * residual; final RMSNorm -> reward vector. No biases. All matrices are row-major [out, in].
+ * residual; final RMSNorm -> reward vector. No biases. Matrices are [out, in] (layout: see
+ * kvprm_layer_weights).
  */
 #ifndef KVPRM_H
 #define KVPRM_H
@@ -70,7 +71,9 @@ typedef struct {
 
 /* One decoder layer of the readout weights theta + dtheta (the LoRA update is merged into the
  * base weights by the caller: W' = W + (alpha / r) B A; section 4.1 and the hyperparameter
- * table). Element type weight_dtype; row-major [out, in]. */
+ * table). Element type weight_dtype. Matrices are [out, in]: row-major for F32 weights; for BF16
+ * weights in the packed tile layout written by kvprm_pack_weight (so that the matrix cores
+ * stream them contiguously). Gains are plain vectors. */
 typedef struct {
   const void *attn_norm; /* [H]                gain of the attention RMSNorm */
   const void *wq;        /* [n_q * d_h, H]     head h occupies rows [h d_h, (h+1) d_h) */
@@ -94,9 +97,12 @@ typedef struct {
 /* Paged KV cache written by the generator (adapter off; section 4.1). Keys are stored after
  * the rotary embedding of their own position; values are not rotated.
  *   pool layout: [num_layers][num_pages][num_kv_heads][tile]
- *   K tile (page_size x d_h values): [d_h / x][page_size][x], x = 16 bytes / element size
- *            (x = 4 fp32, 8 bf16, 16 fp8): element (slot s, dim m) at ((m / x) * 16 + s) * x + m % x
- *   V tile: [d_h][page_size]: element (slot s, dim m) at m * 16 + s
+ *   x = 16 bytes / element size (4 fp32, 8 bf16, 16 fp8), r = x / 4
+ *   K tile (page_size x d_h values): [d_h / x][page_size][x]: element (slot s, dim m) at
+ *            ((m / x) * 16 + s) * x + m % x
+ *   V tile: [d_h / (16 r)][4][16][r][4]: element (slot s, dim m) at
+ *            ((((m / (16 r)) * 4 + s / 4) * 16 + m % 16) * r + (m / 16) % r) * 4 + s % 4
+ *            (each 16 bytes hold 4 consecutive slots of r dimensions 16 apart)
  * For FP8_E4M3 pools the stored code is multiplied by a per-(layer, page, kv-head) fp32 scale:
  *   k_scale, v_scale: [num_layers][num_pages][num_kv_heads]; NULL for other dtypes. */
 typedef struct {
@@ -158,6 +164,14 @@ kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const 
                              int32_t layer, const float *q, const float *k_self,
                              const float *v_self, void *workspace, size_t ws_bytes, float *o,
                              void *stream);
+
+/* Repack one bf16 weight matrix W [rows][K] from row-major order into the packed tile layout
+ * that kvprm_score reads for BF16 weights: blocks of 1 KiB, block kb * (rows / 16) + t holding
+ * rows 16t .. 16t+15 and inputs 32kb .. 32kb+31; inside a block, 16-byte group l (0..63) holds
+ * W[16t + l % 16][32kb + 8 (l / 16) + i], i = 0..7. src and dst are device pointers to rows * K
+ * bf16 values that must not overlap; rows % 16 == 0 and K % 32 == 0, else KVPRM_E_INVALID.
+ * Enqueued on `stream`; a one-time preparation of static weights, not part of scoring. */
+kvprm_status kvprm_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, void *stream);
 
 /* Text of the last error on the calling thread ("" if none). Valid until the next call on
  * this thread. */

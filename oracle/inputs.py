@@ -22,10 +22,14 @@ _DT = {"f32": synth.DT_F32, "bf16": synth.DT_BF16, "f64": synth.DT_F64}
 
 
 def _gen_tensor(name, kind, dims, seed, layer, wdtype, shape):
+    """One weight tensor in its storage order, widened; bf16 matrices are stored packed."""
     mean, std = synth.tensor_mean_std(name, dims)
     n = int(np.prod(dims))
     raw = synth.host_normal(n, seed, synth.stream_id(layer, kind), 0, mean, std, _DT[wdtype])
-    return ko.decode_storage(raw, wdtype).reshape(dims)
+    vals = ko.decode_storage(raw, wdtype)
+    if len(dims) == 2 and wdtype == "bf16":
+        return ko.unpack_tiled(vals, dims[0], dims[1])
+    return vals.reshape(dims)
 
 
 def readout_from_synth(shape: synth.ModelShape, seed: int, layer_cache: int = 2) -> ko.Readout:
@@ -66,7 +70,7 @@ def cache_from_synth(w: synth.Workload, nan_pages=(), page_cache: int = 4096) ->
             if which == "k":
                 out[j] = ko.k_tile_to_tokens(vals[j], ps, d, eb)
             else:
-                out[j] = ko.v_tile_to_tokens(vals[j], ps, d)
+                out[j] = ko.v_tile_to_tokens(vals[j], ps, d, eb)
         return out
 
     return ko.PagedCache(tiles)

@@ -78,9 +78,12 @@ def decode_storage(raw: np.ndarray, dtype: str) -> np.ndarray:
 # ---------------------------------------------------------------------------------------------
 # paged cache layout (the storage contract of the library's cache arguments)
 #
-# pool[layer][page][kv_head] is a tile of page_size x head_dim values.
-#   K tile: [head_dim / x][page_size][x], x = 16 bytes / element size
-#   V tile: [head_dim][page_size]           (dimension-major)
+# pool[layer][page][kv_head] is a tile of page_size (16) x head_dim values; x = 16 bytes /
+# element size values fill 16 bytes, r = x / 4.
+#   K tile: [head_dim / x][16 slots][x]: element (slot s, dim m) at ((m / x) * 16 + s) * x + m % x
+#   V tile: [head_dim / (16 r)][4][16][r][4]: element (s, m) at
+#           ((((m / (16 r)) * 4 + s / 4) * 16 + m % 16) * r + (m / 16) % r) * 4 + s % 4
+#   (16 bytes hold 4 consecutive slots of r dimensions 16 apart)
 
 
 def k_tile_to_tokens(tile: np.ndarray, page_size: int, head_dim: int, elem_bytes: int) -> np.ndarray:
@@ -89,9 +92,25 @@ def k_tile_to_tokens(tile: np.ndarray, page_size: int, head_dim: int, elem_bytes
     return tile.reshape(head_dim // x, page_size, x).transpose(1, 0, 2).reshape(page_size, head_dim)
 
 
-def v_tile_to_tokens(tile: np.ndarray, page_size: int, head_dim: int) -> np.ndarray:
+def v_tile_to_tokens(tile: np.ndarray, page_size: int, head_dim: int, elem_bytes: int) -> np.ndarray:
     """Reorder one stored V tile into [slot][dim]."""
-    return tile.reshape(head_dim, page_size).T
+    r = 16 // elem_bytes // 4
+    a = tile.reshape(head_dim // (16 * r), 4, 16, r, 4)  # [m // 16r][s // 4][m % 16][(m // 16) % r][s % 4]
+    return a.transpose(1, 4, 0, 3, 2).reshape(page_size, head_dim)
+
+
+# ---------------------------------------------------------------------------------------------
+# packed weight layout (the storage contract of bf16 weight matrices)
+#
+# A matrix W [rows][K] (rows and K multiples of 16 and 32) is stored as 1 KiB blocks, one per
+# (32-input block kb, 16-row tile t), block index kb * (rows / 16) + t; inside a block, 64 groups
+# of 8 values, group l holding W[16 t + l % 16][32 kb + 8 (l // 16) + i], i = 0..7.
+
+
+def unpack_tiled(stored: np.ndarray, rows: int, K: int) -> np.ndarray:
+    """Reorder packed storage into the row-major matrix [rows][K]."""
+    a = np.asarray(stored).reshape(K // 32, rows // 16, 4, 16, 8)  # [kb][t][l//16][l%16][i]
+    return a.transpose(1, 3, 0, 2, 4).reshape(rows, K)
 
 
 # ---------------------------------------------------------------------------------------------

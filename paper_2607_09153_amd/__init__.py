@@ -20,7 +20,7 @@ KVPRM_F32, KVPRM_BF16, KVPRM_FP8_E4M3 = 0, 1, 2
 DTYPE_CODE = {"f32": KVPRM_F32, "bf16": KVPRM_BF16, "fp8": KVPRM_FP8_E4M3}
 
 EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
-            "kvprm_attention", "kvprm_last_error"]
+            "kvprm_attention", "kvprm_pack_weight", "kvprm_last_error"]
 
 
 class ModelDesc(ctypes.Structure):
@@ -77,8 +77,9 @@ def _load():
                                 ctypes.POINTER(ReadoutWeights), vp, sz, vp, vp, vp]
     lib.kvprm_attention.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
                                     ctypes.c_int32, vp, vp, vp, vp, sz, vp, vp]
+    lib.kvprm_pack_weight.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, vp]
     for f in ("kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
-              "kvprm_attention"):
+              "kvprm_attention", "kvprm_pack_weight"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kvprm_last_error.argtypes = []
     lib.kvprm_last_error.restype = ctypes.c_char_p
@@ -167,6 +168,10 @@ def kvprm_score(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeigh
                 stream: int = 0) -> None:
     _check(lib.kvprm_score(handle, ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(weights),
                            workspace_ptr, ws_bytes, scores_ptr, logits_ptr or None, stream or None))
+
+
+def kvprm_pack_weight(src_ptr: int, dst_ptr: int, rows: int, K: int, stream: int = 0) -> None:
+    _check(lib.kvprm_pack_weight(src_ptr, dst_ptr, rows, K, stream or None))
 
 
 def kvprm_attention(handle: int, cache: KVCache, batch: Batch, layer: int, q_ptr: int,

@@ -59,6 +59,9 @@ kvprm_status kvprm_create(const kvprm_model_desc *d, kvprm_handle *out) {
     return fail(KVPRM_E_UNSUPPORTED, "kvprm_create: head_dim must be 64 or 128");
   if (d->num_q_heads / d->num_kv_heads > 16)
     return fail(KVPRM_E_UNSUPPORTED, "kvprm_create: at most 16 query heads per kv-head");
+  if (d->kv_dtype != KVPRM_F32 && d->num_kv_heads > kMaxKvHeadsMx)
+    return fail(KVPRM_E_UNSUPPORTED, "kvprm_create: at most %d kv-heads with bf16/fp8 caches",
+                kMaxKvHeadsMx);
   if (d->hidden % 64 != 0 || d->ffn_dim % 64 != 0 || (d->num_q_heads * d->head_dim) % 64 != 0)
     return fail(KVPRM_E_UNSUPPORTED, "kvprm_create: hidden, ffn_dim, n_q*d_h must be multiples of 64");
   const bool f32 = d->weight_dtype == KVPRM_F32 && d->kv_dtype == KVPRM_F32;
@@ -98,6 +101,8 @@ static kvprm_status check_batch(const kvprm_handle h, const kvprm_batch *b, cons
   if (b->batch > 256) return fail(KVPRM_E_UNSUPPORTED, "%s: at most 256 candidates per call", fn);
   if (h->dm.wdt == 1 && b->batch > 64)
     return fail(KVPRM_E_UNSUPPORTED, "%s: at most 64 candidates per call with bf16 weights", fn);
+  if (h->dm.wdt == 1 && ((h->dm.H + 63) / 64) * b->batch > kMaxSS)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: hidden * batch too large", fn);
   if (!b->page_table || !b->lengths) return fail(KVPRM_E_INVALID, "%s: null page_table or lengths", fn);
   if (b->max_pages < 1) return fail(KVPRM_E_INVALID, "%s: max_pages < 1", fn);
   if (b->max_pages > kMaxChunks * kChunkPages)
@@ -244,6 +249,19 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   }
   HIP_TRY(launch_head(dm, p, w, wts->final_norm, wts->reward_w, wts->reward_b, scores, logits, s),
           "reward head");
+  return ok();
+}
+
+kvprm_status kvprm_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, void *stream) {
+  const char *fn = "kvprm_pack_weight";
+  if (!src || !dst) return fail(KVPRM_E_INVALID, "%s: null pointer", fn);
+  if (rows <= 0 || K <= 0 || rows % 16 != 0 || K % 32 != 0)
+    return fail(KVPRM_E_INVALID, "%s: rows %% 16 and K %% 32 must be 0 (rows=%lld, K=%lld)", fn,
+                (long long)rows, (long long)K);
+  const uintptr_t a = (uintptr_t)src, b = (uintptr_t)dst, n = (uintptr_t)(rows * K * 2);
+  if (a < b + n && b < a + n) return fail(KVPRM_E_INVALID, "%s: src and dst overlap", fn);
+  if ((a | b) & 15) return fail(KVPRM_E_INVALID, "%s: pointers must be 16-byte aligned", fn);
+  HIP_TRY(launch_pack_weight(src, dst, rows, K, (hipStream_t)stream), "pack");
   return ok();
 }
 

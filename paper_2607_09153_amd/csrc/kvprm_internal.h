@@ -25,6 +25,8 @@ struct GroupTable {
 // Attention split: each work item covers kChunkPages pages of one (candidate, kv-head).
 constexpr int kChunkPages = 32;
 constexpr int kMaxChunks = 1024;  // chunk partials one merge handles: max_pages <= 32768
+constexpr int kMaxSS = 8192;
+constexpr int kMaxKvHeadsMx = 8;  // matrix-core attention: one wave per kv-head in a block      // sums-of-squares partials staged in LDS: (H / 64) * B
 constexpr int kPage = 16;
 
 // Workspace carve-up (all offsets 256-byte aligned).
@@ -35,8 +37,7 @@ struct Workspace {
   float *q;        // [B][nq][d]
   float *kself;    // [B][nkv][d]
   float *vself;    // [B][nkv][d]
-  float *apart;    // attention partials: [B][nq][nch][d + 2] (vector-ALU path) or
-                   // [B][nq][d + 2][nch rounded up to 4] (matrix-core path)
+  float *apart;    // attention partials [B][nq][nch][d + 2] (acc..., m, l)
   float *o;        // [B][nq * d]
   float *hffn;     // [B][F] (vector-ALU path)
   // matrix-core path
@@ -67,6 +68,8 @@ struct Plan {
 // matrix-core helpers (kvprm_mfma.hip)
 int gemv_nt(int B);
 int gemv_bp(int B);
+int gemv_mt(int nt);
+hipError_t launch_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, hipStream_t s);
 
 Plan make_plan(const Dims &dm, int B, int max_pages);
 Workspace carve(const Dims &dm, const Plan &p, void *base);

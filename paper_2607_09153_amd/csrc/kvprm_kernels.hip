@@ -59,19 +59,24 @@ __device__ __forceinline__ float block_sum256(float v, float *red) {
 
 // ------------------------------------------------------------------------------- plan
 
-// Split-K plan of a matrix-core GEMV: split K only as far as needed for about 2048 waves, in
-// whole 32-wide blocks.
+// Split-K plan of a matrix-core GEMV: split K only as far as needed for about 4096 waves (16
+// per CU), in whole 32-wide blocks, keeping at least 8 blocks per slice and the slice's operand
+// (staged in LDS, 1 KiB per block and column tile) within 64 KiB.
 static GemvPlan gemv_plan(int rows, int K, int B) {
   GemvPlan g;
   g.rows = rows;
   g.K = K;
-  const int mt = gemv_nt(B) >= 2 ? 2 : 1;
+  const int nt = gemv_nt(B);
+  const int mt = gemv_mt(nt);
   const int waves = (rows / 16 + mt - 1) / mt;
-  int want = (2048 + waves - 1) / waves;
+  int want = (4096 + waves - 1) / waves;
   const int nkb = K / 32;
+  if (want > nkb / 8) want = nkb / 8;
   if (want < 1) want = 1;
   if (want > nkb) want = nkb;
-  const int kb_per = (nkb + want - 1) / want;
+  int kb_per = (nkb + want - 1) / want;
+  const int kb_lds = 64 / nt;
+  if (kb_per > kb_lds) kb_per = kb_lds;
   g.kslice = kb_per * 32;
   g.ksplit = (K + g.kslice - 1) / g.kslice;
   return g;
@@ -140,7 +145,7 @@ Workspace carve(const Dims &dm, const Plan &p, void *base) {
   w.q = take(B * dm.nq * dm.d);
   w.kself = take(B * dm.nkv * dm.d);
   w.vself = take(B * dm.nkv * dm.d);
-  w.apart = take(B * dm.nq * (size_t)((p.nch + 3) & ~3) * (dm.d + 2));
+  w.apart = take(B * dm.nq * (size_t)p.nch * (dm.d + 2));
   w.o = take(B * dm.nq * dm.d);
   w.hffn = take(B * dm.F);
   if (dm.wdt == 1) {
@@ -435,8 +440,11 @@ __global__ __launch_bounds__(256) void k_attn_valu(const void *kpool, const void
       const char *tile = (const char *)vpool + ((size_t)phys_s[pg] * nkv + j) * (kPage * D) * EB;
       const float vsc = (KVT == 2) ? vsc_s[pg] : 1.f;
       const int nslot = min(kPage, ntok - pg * kPage);
+      constexpr int R = X / 4;
+      const int vbase = (((m / (16 * R)) * 4) * 16 + m % 16) * R + (m / 16) % R;
       for (int sl = 0; sl < nslot; ++sl) {
-        const float v = kv_elem<KVT>(tile, m * kPage + sl) * vsc;
+        // V tile: ((((m / 16R) * 4 + s / 4) * 16 + m % 16) * R + (m / 16) % R) * 4 + s % 4
+        const float v = kv_elem<KVT>(tile, (vbase + (sl / 4) * 16 * R) * 4 + sl % 4) * vsc;
         const int t = pg * kPage + sl;
 #pragma unroll
         for (int h = 0; h < 16; ++h)

@@ -103,6 +103,7 @@ __device__ __forceinline__ float bmax(float v, float *red) {
 }
 
 int gemv_nt(int B) { return B <= 8 ? 1 : 2 * ((B + 15) / 16); }
+int gemv_mt(int) { return 2; }
 int gemv_bp(int B) { return B <= 8 ? 8 : 16 * ((B + 15) / 16); }
 
 // ------------------------------------------------------------------------------- init
@@ -155,45 +156,74 @@ struct GemvArgs {
   int ksp;
 };
 
-// part[row][b][ks] = sum over k-slice ks of W[row][k] u_b[k]. Each wave owns MT consecutive
-// 16-row tiles; per 32-wide k-block it loads MT weight tiles straight from HBM into A-operand
-// registers (16 bytes per lane: row n, inputs 8c .. 8c+7) and NT operand tiles (L2-resident,
-// 1 KiB per wave-load) and issues MT * NT MFMAs. The hi and lo halves of each candidate are
+// part[row][b][ks] = sum over k-slice ks of W[row][k] u_b[k], W in the packed tile layout
+// (1 KiB per 32-input block and 16-row tile, input block major, in A-operand lane order): one
+// load instruction reads 1 KiB, and the waves working on one k-slice sweep a contiguous region
+// together, input block by input block. The block first copies its
+// k-slice of the operand (NT column tiles) into LDS; per batch of U k-blocks the MT * U weight
+// loads are issued before the MT * NT * U MFMAs. The hi and lo halves of each candidate are
 // added before the partial is stored.
-template <int MT, int NT>
+template <int MT, int NT, int U>
 __global__ __launch_bounds__(256) void k_gemv_mx(GemvArgs a) {
+  extern __shared__ uint4 act_s[];  // the block's k-slice of the operand: nkb * NT * 64 entries
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ks = blockIdx.y;
   const int k0 = ks * a.kslice;
   const int nkb = min(a.kslice, a.K - k0) >> 5;
   const int tile0 = (blockIdx.x * 4 + wave) * MT;
   const int B = a.B;
+  {
+    const uint4 *src = a.act + (size_t)(k0 >> 5) * NT * 64;
+    for (int i = threadIdx.x; i < nkb * NT * 64; i += 256) act_s[i] = src[i];
+  }
+  __syncthreads();
   if (tile0 * 16 >= a.rows) return;
-  const uint16_t *wrow[MT];
+  const uint4 *wt[MT];
+  size_t kstride[MT];  // uint4 entries between consecutive input blocks of a tile
   bool valid[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
-    const int r = (tile0 + m) * 16 + (lane & 15);
-    valid[m] = (tile0 + m) * 16 < a.rows;
+    const int tile = tile0 + m;
+    valid[m] = tile * 16 < a.rows;
     int seg = 0, base = 0;
-    while (seg < a.nseg - 1 && r >= base + a.seg_rows[seg]) base += a.seg_rows[seg++];
-    wrow[m] = (const uint16_t *)a.w[seg] + (size_t)(valid[m] ? r - base : 0) * a.K + k0 +
-              8 * (lane >> 4);
+    while (seg < a.nseg - 1 && tile * 16 >= base + a.seg_rows[seg]) base += a.seg_rows[seg++];
+    const int lt = valid[m] ? tile - base / 16 : 0;
+    const size_t ntiles = (size_t)a.seg_rows[seg] / 16;
+    kstride[m] = ntiles * 64;
+    wt[m] = (const uint4 *)a.w[seg] + ((size_t)(k0 >> 5) * ntiles + lt) * 64 + lane;
   }
   floatx4 acc[MT][NT];
 #pragma unroll
   for (int m = 0; m < MT; ++m)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const uint4 *ap = a.act + (size_t)(k0 >> 5) * NT * 64 + lane;
-#pragma unroll 4
-  for (int kb = 0; kb < nkb; ++kb) {
+  const uint4 *ap = act_s + lane;
+  // batches of U k-blocks: the weight loads of a batch are all issued before its MFMAs; the
+  // operand comes from LDS. Rows of an absent tile read tile 0 and are never stored.
+  int kb = 0;
+  for (; kb + U <= nkb; kb += U) {
+    uint4 av[U][MT];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) av[u][m] = wt[m][(size_t)(kb + u) * kstride[m]];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      uint4 bv[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) bv[t] = ap[((kb + u) * NT + t) * 64];
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av[u][m], bv[t], acc[m][t]);
+    }
+  }
+  for (; kb < nkb; ++kb) {
     uint4 av[MT], bv[NT];
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
-      av[m] = valid[m] ? *(const uint4 *)(wrow[m] + kb * 32) : make_uint4(0, 0, 0, 0);
+    for (int m = 0; m < MT; ++m) av[m] = wt[m][(size_t)kb * kstride[m]];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) bv[t] = ap[(size_t)(kb * NT + t) * 64];
+    for (int t = 0; t < NT; ++t) bv[t] = ap[(kb * NT + t) * 64];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -240,11 +270,14 @@ __device__ __forceinline__ float ksum(const float *part, int ksp, int ksplit, in
 }
 
 // r_b = 1 / sqrt(mean(x_b^2) + eps) from the per-row-block sums of squares, into inv_s[b].
+// The nss * B partial sums are staged in LDS (ss_s) with one round of parallel loads.
 __device__ __forceinline__ void load_inv_rms(const float *ss, int nss, int B, int H, float eps,
-                                             float *inv_s) {
+                                             float *ss_s, float *inv_s) {
+  for (int i = threadIdx.x; i < nss * B; i += blockDim.x) ss_s[i] = ss[i];
+  __syncthreads();
   for (int b = threadIdx.x; b < B; b += blockDim.x) {
     float s = 0.f;
-    for (int i = 0; i < nss; ++i) s += ss[(size_t)i * B + b];
+    for (int i = 0; i < nss; ++i) s += ss_s[i * B + b];
     inv_s[b] = 1.0f / sqrtf(s / (float)H + eps);
   }
   __syncthreads();
@@ -259,7 +292,8 @@ __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *part, int ksp, 
                                                     const float *rope, float *q, float *ks,
                                                     float *vs) {
   __shared__ float inv_s[64];
-  load_inv_rms(ss, nss, B, H, eps, inv_s);
+  __shared__ float ss_s[kMaxSS];
+  load_inv_rms(ss, nss, B, H, eps, ss_s, inv_s);
   const int hd = d / 2;
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= (nq + 2 * nkv) * hd * B) return;
@@ -315,7 +349,8 @@ __global__ __launch_bounds__(256) void k_swiglu_mx(const float *part, int ksp, i
                                                    const float *ss, int nss, int H, float eps,
                                                    int B, int F, uint16_t *op, int NT, int Bp) {
   __shared__ float inv_s[64];
-  load_inv_rms(ss, nss, B, H, eps, inv_s);
+  __shared__ float ss_s[kMaxSS];
+  load_inv_rms(ss, nss, B, H, eps, ss_s, inv_s);
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= F * B) return;
   const int f = e / B, b = e - f * B;
@@ -323,6 +358,30 @@ __global__ __launch_bounds__(256) void k_swiglu_mx(const float *part, int ksp, i
   const float gv = ksum(part, ksp, ksplit, f, B, b) * inv;
   const float uv = ksum(part, ksp, ksplit, F + f, B, b) * inv;
   store_operand(op, NT, Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
+}
+
+// Row-major [rows][K] -> packed tile layout: 16-byte group l of block kb * (rows/16) + t holds
+// W[16 t + l % 16][32 kb + 8 (l / 16) + i], i = 0..7. One thread per group.
+__global__ __launch_bounds__(256) void k_pack_weight(const uint4 *src, uint4 *dst, int64_t rows,
+                                                     int64_t K) {
+  const int64_t ngroups = rows * K / 8;
+  const int64_t ntiles = rows / 16;
+  for (int64_t gidx = (int64_t)blockIdx.x * 256 + threadIdx.x; gidx < ngroups;
+       gidx += (int64_t)gridDim.x * 256) {
+    const int64_t l = gidx & 63, blk = gidx >> 6;
+    const int64_t kb = blk / ntiles, t = blk - kb * ntiles;
+    const int64_t r = 16 * t + (l & 15), k = 32 * kb + 8 * (l >> 4);
+    dst[gidx] = src[(r * K + k) / 8];
+  }
+}
+
+hipError_t launch_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, hipStream_t s) {
+  const int64_t ngroups = rows * K / 8;
+  int64_t blocks = (ngroups + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(k_pack_weight, dim3((unsigned)blocks), dim3(256), 0, s, (const uint4 *)src,
+                     (uint4 *)dst, rows, K);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------------- attention
@@ -344,33 +403,29 @@ struct AttnArgs {
   GroupTable gt;
   int nch;
   const float *q, *kself, *vself;
-  float *apart;   // [B][nq][D + 2][nchp]: acc rows, then m, then l; chunk index innermost
-  int nchp;       // chunk slots per row (nch rounded up to 4)
+  float *apart;   // [B][nq][nch][D + 2]: per chunk the acc row, then m, then l
   float *o;       // [B][nq][D] fp32 output (may be null)
   uint16_t *op;   // operand buffer of the output projection (may be null)
   int NT, Bp;
 };
 
-// One block (4 waves) per (chunk of kChunkPages pages, kv-head j, candidate b) over the
-// candidate's private pages. Each wave takes page pairs (32 tokens): S = K Q^T on the matrix
-// cores (A = the K tile, 16 tokens x 32 dims; B = the g query heads as columns, in three bf16
+// One block per (chunk of kChunkPages pages, candidate b) over the candidate's private pages,
+// one wave per kv-head j, so the n_kv tiles of a page (contiguous in the pool) are read together.
+// Each wave walks the chunk two pages (32 tokens) at a time: S = K Q^T on the matrix cores
+// (A = the K tile, 16 tokens x 32 dims; B = the g query heads of j as columns, in three bf16
 // terms), online softmax per head in registers (a lane holds 4 tokens of one head per page),
-// then O^T += V^T P^T (A = V^T, 16 dims x 32 tokens, read straight from the dimension-major V
-// tile; B = P^T hi and lo). The four waves combine through LDS into one unnormalised partial
-// (acc, m, l) per q-head. Slots at or beyond L_b are masked in S and zeroed in V (they may hold
-// anything, NaN included).
+// then O^T += V^T P^T (A = V^T, 16 dims x 32 tokens; the V tile stores 4 consecutive slots of
+// a dimension together, so one 16-byte load per lane feeds 2 (bf16) or 4 (fp8) A operands; B =
+// P^T hi and lo). The wave writes its unnormalised partial (acc, m, l) per q-head.
+// Slots at or beyond L_b are masked in S and zeroed in V (they may hold anything, NaN included).
 template <int KVT, int D>
-__global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
+__global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   constexpr int NKB = D / 32;  // 32-dim blocks of q.k
   constexpr int NDB = D / 16;  // 16-dim blocks of the output
   constexpr int EB = KVT == 1 ? 2 : 1;
   constexpr size_t TILE = (size_t)kPage * D * EB;
-  __shared__ int phys_s[kChunkPages];
-  __shared__ float ksc_s[kChunkPages], vsc_s[kChunkPages];
-  __shared__ float red_m[4][16], red_l[4][16];
-  __shared__ float red_acc[4][D][17];
-
-  const int c = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  const int c = blockIdx.x, b = blockIdx.y;
+  const int j = threadIdx.x >> 6;
   const int nkv = a.nkv, g = a.g, nq = a.nq;
   const int L = a.lengths[b];
   const int npages = (L + kPage - 1) / kPage;
@@ -380,16 +435,59 @@ __global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
   const int p0 = first + c * kChunkPages;
   if (p0 >= npages) return;
   const int np = min(npages, p0 + kChunkPages) - p0;
-  if (threadIdx.x < np) {
-    const int ph = a.page_table[(size_t)b * a.max_pages + p0 + threadIdx.x];
-    phys_s[threadIdx.x] = ph;
-    if (KVT == 2) {
-      ksc_s[threadIdx.x] = a.ksc[(size_t)ph * nkv + j];
-      vsc_s[threadIdx.x] = a.vsc[(size_t)ph * nkv + j];
-    }
-  }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
   const int n = lane & 15, cq = lane >> 4;
+  // each wave reads the chunk's page ids itself into lane registers (lane i holds page i and,
+  // for fp8, its scales) and fetches them with cross-lane reads: no LDS, no barrier
+  const int ph_l = lane < np ? a.page_table[(size_t)b * a.max_pages + p0 + lane] : 0;
+  float ksc_l = 0.f, vsc_l = 0.f;
+  if (KVT == 2 && lane < np) {
+    ksc_l = a.ksc[(size_t)ph_l * nkv + j];
+    vsc_l = a.vsc[(size_t)ph_l * nkv + j];
+  }
+
+  // raw registers of one page pair; the next pair is loaded while the current one is computed
+  struct PairRaw {
+    uint4 k[2][NKB];      // K tiles of pages la, lb (fp8: first NKB / 2 entries)
+    uint4 v[2][NDB / 2];  // V: 16 bytes = 4 slots of 2 (bf16) or 4 (fp8) dimension blocks
+  };
+  const int npairs = (np + 1) >> 1;
+  auto load_pair = [&](int pp, PairRaw &r) {
+    // indices past the chunk are clamped to its last page: those tokens are masked anyway
+    const int pa = __shfl(ph_l, min(2 * pp, np - 1), 64);
+    const int pb = __shfl(ph_l, min(2 * pp + 1, np - 1), 64);
+    const char *kA = a.kp + ((size_t)pa * nkv + j) * TILE;
+    const char *kB = a.kp + ((size_t)pb * nkv + j) * TILE;
+    const char *vA = a.vp + ((size_t)pa * nkv + j) * TILE;
+    const char *vB = a.vp + ((size_t)pb * nkv + j) * TILE;
+    if (KVT == 1) {
+#pragma unroll
+      for (int kk = 0; kk < NKB; ++kk) {
+        r.k[0][kk] = *(const uint4 *)(kA + (size_t)(kk * 64 + lane) * 16);
+        r.k[1][kk] = *(const uint4 *)(kB + (size_t)(kk * 64 + lane) * 16);
+      }
+      // V tile (r = 2): 16-byte group (q, cq, n) holds slots 4cq..4cq+3 of dims 32q + n, 32q + 16 + n
+#pragma unroll
+      for (int q2 = 0; q2 < NDB / 2; ++q2) {
+        r.v[0][q2] = *(const uint4 *)(vA + (size_t)(q2 * 64 + lane) * 16);
+        r.v[1][q2] = *(const uint4 *)(vB + (size_t)(q2 * 64 + lane) * 16);
+      }
+    } else {
+#pragma unroll
+      for (int kp = 0; kp < NKB / 2; ++kp) {
+        r.k[0][kp] = *(const uint4 *)(kA + (size_t)(kp * 64 + lane) * 16);
+        r.k[1][kp] = *(const uint4 *)(kB + (size_t)(kp * 64 + lane) * 16);
+      }
+      // V tile (r = 4): 16-byte group (q, cq, n) holds slots 4cq..4cq+3 of dims 64q + 16j + n
+#pragma unroll
+      for (int q4 = 0; q4 < NDB / 4; ++q4) {
+        r.v[0][q4] = *(const uint4 *)(vA + (size_t)(q4 * 64 + lane) * 16);
+        r.v[1][q4] = *(const uint4 *)(vB + (size_t)(q4 * 64 + lane) * 16);
+      }
+    }
+  };
+  PairRaw r0, r1;
+  load_pair(0, r0);  // in flight while the queries are prepared
 
   // query operands of head n (zero columns for n >= g), split in three bf16 terms so that the
   // scores keep fp32-level accuracy even for very large logits
@@ -417,7 +515,6 @@ __global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
       qlo[kk] = make_uint4(pack2(l[0], l[1]), pack2(l[2], l[3]), pack2(l[4], l[5]), pack2(l[6], l[7]));
     }
   }
-  __syncthreads();
 
   const float rs = 1.0f / sqrtf((float)D);
   float m_run = -INFINITY, l_run = 0.f;
@@ -425,58 +522,46 @@ __global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
 #pragma unroll
   for (int nb = 0; nb < NDB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  const int npairs = (np + 1) >> 1;
-  for (int pp = wave; pp < npairs; pp += 4) {
-    const int la = 2 * pp, lb = 2 * pp + 1;
-    const bool hasB = lb < np;
-    const int pa = phys_s[la];
-    const int pb = hasB ? phys_s[lb] : pa;
-    const char *kA = a.kp + ((size_t)pa * nkv + j) * TILE;
-    const char *kB = a.kp + ((size_t)pb * nkv + j) * TILE;
-    const char *vA = a.vp + ((size_t)pa * nkv + j) * TILE;
-    const char *vB = a.vp + ((size_t)pb * nkv + j) * TILE;
-    // ---- loads
+  auto compute_pair = [&](int pp, const PairRaw &r) {
+    const int la = min(2 * pp, np - 1), lb = 2 * pp + 1;
+    const bool hasA = 2 * pp < np, hasB = lb < np;
     uint4 KA[NKB], KB[NKB];
     uint2 VA[NDB], VB[NDB];
     if (KVT == 1) {
 #pragma unroll
       for (int kk = 0; kk < NKB; ++kk) {
-        KA[kk] = *(const uint4 *)(kA + (size_t)(kk * 64 + lane) * 16);
-        KB[kk] = *(const uint4 *)(kB + (size_t)(kk * 64 + lane) * 16);
+        KA[kk] = r.k[0][kk];
+        KB[kk] = r.k[1][kk];
       }
 #pragma unroll
-      for (int nb = 0; nb < NDB; ++nb) {
-        VA[nb] = *(const uint2 *)(vA + (size_t)(nb * 16 + n) * 32 + cq * 8);
-        VB[nb] = *(const uint2 *)(vB + (size_t)(nb * 16 + n) * 32 + cq * 8);
+      for (int q2 = 0; q2 < NDB / 2; ++q2) {
+        VA[2 * q2] = make_uint2(r.v[0][q2].x, r.v[0][q2].y);
+        VA[2 * q2 + 1] = make_uint2(r.v[0][q2].z, r.v[0][q2].w);
+        VB[2 * q2] = make_uint2(r.v[1][q2].x, r.v[1][q2].y);
+        VB[2 * q2 + 1] = make_uint2(r.v[1][q2].z, r.v[1][q2].w);
       }
     } else {
-      uint4 ra[NKB / 2], rb[NKB / 2];
 #pragma unroll
       for (int kp = 0; kp < NKB / 2; ++kp) {
-        ra[kp] = *(const uint4 *)(kA + (size_t)(kp * 64 + lane) * 16);
-        rb[kp] = *(const uint4 *)(kB + (size_t)(kp * 64 + lane) * 16);
-      }
-      uint32_t wa[NDB], wb[NDB];
-#pragma unroll
-      for (int nb = 0; nb < NDB; ++nb) {
-        wa[nb] = *(const uint32_t *)(vA + (size_t)(nb * 16 + n) * 16 + cq * 4);
-        wb[nb] = *(const uint32_t *)(vB + (size_t)(nb * 16 + n) * 16 + cq * 4);
-      }
-#pragma unroll
-      for (int kp = 0; kp < NKB / 2; ++kp) {
-        KA[2 * kp] = make_uint4(fp8x2_to_bf16x2<false>(ra[kp].x), fp8x2_to_bf16x2<true>(ra[kp].x),
-                                fp8x2_to_bf16x2<false>(ra[kp].y), fp8x2_to_bf16x2<true>(ra[kp].y));
-        KA[2 * kp + 1] = make_uint4(fp8x2_to_bf16x2<false>(ra[kp].z), fp8x2_to_bf16x2<true>(ra[kp].z),
-                                    fp8x2_to_bf16x2<false>(ra[kp].w), fp8x2_to_bf16x2<true>(ra[kp].w));
-        KB[2 * kp] = make_uint4(fp8x2_to_bf16x2<false>(rb[kp].x), fp8x2_to_bf16x2<true>(rb[kp].x),
-                                fp8x2_to_bf16x2<false>(rb[kp].y), fp8x2_to_bf16x2<true>(rb[kp].y));
-        KB[2 * kp + 1] = make_uint4(fp8x2_to_bf16x2<false>(rb[kp].z), fp8x2_to_bf16x2<true>(rb[kp].z),
-                                    fp8x2_to_bf16x2<false>(rb[kp].w), fp8x2_to_bf16x2<true>(rb[kp].w));
+        const uint4 ra = r.k[0][kp], rb = r.k[1][kp];
+        KA[2 * kp] = make_uint4(fp8x2_to_bf16x2<false>(ra.x), fp8x2_to_bf16x2<true>(ra.x),
+                                fp8x2_to_bf16x2<false>(ra.y), fp8x2_to_bf16x2<true>(ra.y));
+        KA[2 * kp + 1] = make_uint4(fp8x2_to_bf16x2<false>(ra.z), fp8x2_to_bf16x2<true>(ra.z),
+                                    fp8x2_to_bf16x2<false>(ra.w), fp8x2_to_bf16x2<true>(ra.w));
+        KB[2 * kp] = make_uint4(fp8x2_to_bf16x2<false>(rb.x), fp8x2_to_bf16x2<true>(rb.x),
+                                fp8x2_to_bf16x2<false>(rb.y), fp8x2_to_bf16x2<true>(rb.y));
+        KB[2 * kp + 1] = make_uint4(fp8x2_to_bf16x2<false>(rb.z), fp8x2_to_bf16x2<true>(rb.z),
+                                    fp8x2_to_bf16x2<false>(rb.w), fp8x2_to_bf16x2<true>(rb.w));
       }
 #pragma unroll
-      for (int nb = 0; nb < NDB; ++nb) {
-        VA[nb] = make_uint2(fp8x2_to_bf16x2<false>(wa[nb]), fp8x2_to_bf16x2<true>(wa[nb]));
-        VB[nb] = make_uint2(fp8x2_to_bf16x2<false>(wb[nb]), fp8x2_to_bf16x2<true>(wb[nb]));
+      for (int q4 = 0; q4 < NDB / 4; ++q4) {
+        const uint32_t wa[4] = {r.v[0][q4].x, r.v[0][q4].y, r.v[0][q4].z, r.v[0][q4].w};
+        const uint32_t wb[4] = {r.v[1][q4].x, r.v[1][q4].y, r.v[1][q4].z, r.v[1][q4].w};
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          VA[4 * q4 + jj] = make_uint2(fp8x2_to_bf16x2<false>(wa[jj]), fp8x2_to_bf16x2<true>(wa[jj]));
+          VB[4 * q4 + jj] = make_uint2(fp8x2_to_bf16x2<false>(wb[jj]), fp8x2_to_bf16x2<true>(wb[jj]));
+        }
       }
     }
     // ---- scores: lane holds tokens 4cq + i of pages la and lb for head n
@@ -490,14 +575,14 @@ __global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
       sb = mfma16(KB[kk], qmd[kk], sb);
       sb = mfma16(KB[kk], qlo[kk], sb);
     }
-    const float sca = (KVT == 2) ? ksc_s[la] * rs : rs;
-    const float scb = (KVT == 2) ? ksc_s[hasB ? lb : la] * rs : rs;
+    const float sca = (KVT == 2) ? __shfl(ksc_l, la, 64) * rs : rs;
+    const float scb = (KVT == 2) ? __shfl(ksc_l, hasB ? lb : la, 64) * rs : rs;
     const int ta = (p0 + la) * kPage + 4 * cq, tb = (p0 + lb) * kPage + 4 * cq;
     float s[8];
     bool ok[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      ok[i] = ta + i < L;
+      ok[i] = hasA && (ta + i < L);
       ok[4 + i] = hasB && (tb + i < L);
       s[i] = ok[i] ? sa[i] * sca : -INFINITY;
       s[4 + i] = ok[4 + i] ? sb[i] * scb : -INFINITY;
@@ -507,7 +592,7 @@ __global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
     for (int i = 1; i < 8; ++i) mx = fmaxf(mx, s[i]);
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);  // finite: token 0 of page la is always valid
+    const float m_new = fmaxf(m_run, mx);  // finite: the first pair always has a valid token
     const float alpha = expf(m_run - m_new);
     m_run = m_new;
     float pv[8], psum = 0.f;
@@ -525,7 +610,7 @@ __global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
       acc[nb][3] *= alpha;
     }
     if (KVT == 2) {
-      const float va_s = vsc_s[la], vb_s = vsc_s[hasB ? lb : la];
+      const float va_s = __shfl(vsc_l, la, 64), vb_s = __shfl(vsc_l, hasB ? lb : la, 64);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         pv[i] *= va_s;
@@ -550,47 +635,35 @@ __global__ __launch_bounds__(256) void k_attn_mx(AttnArgs a) {
       acc[nb] = mfma16(vop, Phi, acc[nb]);
       acc[nb] = mfma16(vop, Plo, acc[nb]);
     }
+  };
+  // a branch-free loop over an even number of pairs: the pair past the end (if any) is fully
+  // masked, and loads past the end repeat the last page (an L2 hit), so that wait counts never
+  // cover the loads in flight for the next pair
+  for (int pp = 0; pp < npairs; pp += 2) {
+    load_pair(pp + 1, r1);
+    compute_pair(pp, r0);
+    load_pair(pp + 2, r0);
+    compute_pair(pp + 1, r1);
   }
-  // ---- combine the four waves into this chunk's partial
+  // ---- this wave's partial: lane holds acc rows d = 16 nb + 4 cq + i of head n, so each
+  // 16-byte store is contiguous with those of the 3 other lanes of the head (64 bytes)
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
-  if (lane < 16) {
-    red_m[wave][n] = m_run;
-    red_l[wave][n] = l_run;
-  }
+  if (n < g) {
+    float *hb = a.apart + (((size_t)b * nq + (size_t)j * g + n) * a.nch + c) * (D + 2);
 #pragma unroll
-  for (int nb = 0; nb < NDB; ++nb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) red_acc[wave][nb * 16 + 4 * cq + i][n] = acc[nb][i];
-  __syncthreads();
-  const size_t hrow = (size_t)(D + 2) * a.nchp;
-  float *outbase = a.apart + ((size_t)b * nq + (size_t)j * g) * hrow + c;
-  for (int e = threadIdx.x; e < g * D; e += 256) {
-    const int h = e / D, d = e - h * D;
-    float M = red_m[0][h];
-#pragma unroll
-    for (int w = 1; w < 4; ++w) M = fmaxf(M, red_m[w][h]);
-    float av = 0.f, lv = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float f = (red_m[w][h] == -INFINITY) ? 0.f : expf(red_m[w][h] - M);
-      av += f * red_acc[w][d][h];
-      lv += f * red_l[w][h];
-    }
-    outbase[h * hrow + (size_t)d * a.nchp] = av;
-    if (d == 0) {
-      outbase[h * hrow + (size_t)D * a.nchp] = M;
-      outbase[h * hrow + (size_t)(D + 1) * a.nchp] = lv;
-    }
+    for (int nb = 0; nb < NDB; ++nb)
+      *(float4 *)(hb + nb * 16 + 4 * cq) = make_float4(acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3]);
+    if (cq == 0) *(float2 *)(hb + D) = make_float2(m_run, l_run);
   }
 }
 
 // Log-sum-exp merge of the chunk partials of one (candidate b, q-head h) with the token's own
 // key/value: m = max(s_self, m_c),
 //   o = (e^{s_self - m} v_self + sum_c e^{m_c - m} acc_c) / (e^{s_self - m} + sum_c e^{m_c - m} l_c).
-// One block of D threads per (b, h); each thread owns one output dimension and reads its
-// contiguous row of chunk partials with 16-byte loads. Writes o (fp32) and/or the operand of the
-// output projection.
+// One block of D threads per (b, h), thread d owning output dimension d: the chunk maxima and
+// sums are staged in LDS, then each chunk's acc row is read coalesced by the block. Writes o
+// (fp32) and/or the operand of the output projection.
 template <int D>
 __global__ __launch_bounds__(D) void k_merge_mx(AttnArgs a) {
   __shared__ float m_s[kMaxChunks], f_s[kMaxChunks];
@@ -603,45 +676,40 @@ __global__ __launch_bounds__(D) void k_merge_mx(AttnArgs a) {
   for (int gi = 0; gi < a.gt.n; ++gi)
     if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
   const int nc = (npages - first + kChunkPages - 1) / kChunkPages;
-  const size_t hrow = (size_t)(D + 2) * a.nchp;
-  const float *base = a.apart + ((size_t)b * a.nq + h) * hrow;
+  const float *base = a.apart + ((size_t)b * a.nq + h) * a.nch * (D + 2);
+  for (int c = t; c < nc; c += D) {
+    m_s[c] = base[(size_t)c * (D + 2) + D];
+    f_s[c] = base[(size_t)c * (D + 2) + D + 1];  // l_c for now
+  }
   // own key: s_self = q . k_self / sqrt(D)
   float dot = wsum(a.q[((size_t)b * a.nq + h) * D + t] * a.kself[((size_t)b * a.nkv + j) * D + t]);
   if (D > 64) {
     if ((t & 63) == 0) red[t >> 6] = dot;
     __syncthreads();
     dot = red[0] + red[1];
-    __syncthreads();
   }
-  const float s_self = dot * (1.0f / sqrtf((float)D));
-  for (int c = t; c < nc; c += D) m_s[c] = base[(size_t)D * a.nchp + c];
   __syncthreads();
+  const float s_self = dot * (1.0f / sqrtf((float)D));
   float M = s_self;
   for (int c = 0; c < nc; ++c) M = fmaxf(M, m_s[c]);
   float lsum = 0.f;
   for (int c = t; c < nc; c += D) {
     const float f = expf(m_s[c] - M);
+    lsum += f * f_s[c];
     f_s[c] = f;
-    lsum += f * base[(size_t)(D + 1) * a.nchp + c];
   }
   lsum = wsum(lsum);
   if (D > 64) {
+    __syncthreads();
     if ((t & 63) == 0) red[2 + (t >> 6)] = lsum;
     __syncthreads();
     lsum = red[2] + red[3];
   }
   __syncthreads();
-  const float4 *row = (const float4 *)(base + (size_t)t * a.nchp);
   float acc = 0.f;
+  const float *col = base + t;
 #pragma unroll 8
-  for (int c4 = 0; c4 < (nc + 3) >> 2; ++c4) {
-    const float4 v = row[c4];
-    const int c = 4 * c4;
-    acc += f_s[c] * v.x;
-    if (c + 1 < nc) acc += f_s[c + 1] * v.y;
-    if (c + 2 < nc) acc += f_s[c + 2] * v.z;
-    if (c + 3 < nc) acc += f_s[c + 3] * v.w;
-  }
+  for (int c = 0; c < nc; ++c) acc += f_s[c] * col[(size_t)c * (D + 2)];
   const float es = expf(s_self - M);
   const float ov = (acc + es * a.vself[((size_t)b * a.nkv + j) * D + t]) / (lsum + es);
   if (a.o) a.o[((size_t)b * a.nq + h) * D + t] = ov;
@@ -677,15 +745,17 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
   a.B = p.B;
   a.part = part;
   a.ksp = (gp.ksplit + 3) & ~3;
-  const int mt = p.nt >= 2 ? 2 : 1;
+  const int mt = gemv_mt(p.nt);
   dim3 grid((gp.rows / 16 + 4 * mt - 1) / (4 * mt), gp.ksplit);
-#define KVPRM_G(MT_, NT_) hipLaunchKernelGGL((k_gemv_mx<MT_, NT_>), grid, dim3(256), 0, s, a)
+  const size_t lds = (size_t)(gp.kslice / 32) * p.nt * 64 * sizeof(uint4);
+#define KVPRM_G(MT_, NT_, U_) \
+  hipLaunchKernelGGL((k_gemv_mx<MT_, NT_, U_>), grid, dim3(256), lds, s, a)
   switch (p.nt) {
-    case 1: KVPRM_G(1, 1); break;
-    case 2: KVPRM_G(2, 2); break;
-    case 4: KVPRM_G(2, 4); break;
-    case 6: KVPRM_G(2, 6); break;
-    case 8: KVPRM_G(2, 8); break;
+    case 1: KVPRM_G(2, 1, 8); break;
+    case 2: KVPRM_G(2, 2, 4); break;
+    case 4: KVPRM_G(2, 4, 2); break;
+    case 6: KVPRM_G(2, 6, 2); break;
+    case 8: KVPRM_G(2, 8, 2); break;
     default: return hipErrorInvalidValue;
   }
 #undef KVPRM_G
@@ -757,13 +827,12 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   a.kself = kself;
   a.vself = vself;
   a.apart = w.apart;
-  a.nchp = (p.nch + 3) & ~3;
   a.o = o;
   a.op = op;
   a.NT = p.nt;
   a.Bp = p.bp;
-  dim3 grid(p.nch, dm.nkv, p.B);
-#define KVPRM_A(KVT, D) hipLaunchKernelGGL((k_attn_mx<KVT, D>), grid, dim3(256), 0, s, a)
+  dim3 grid(p.nch, p.B);
+#define KVPRM_A(KVT, D) hipLaunchKernelGGL((k_attn_mx<KVT, D>), grid, dim3(64 * dm.nkv), 0, s, a)
   if (dm.kvdt == 1) {
     if (dm.d == 64) KVPRM_A(1, 64);
     else KVPRM_A(1, 128);

@@ -141,3 +141,12 @@ def test_attention_validation(handle):
     with pytest.raises(kv.KvprmError) as e:
         kv.kvprm_attention(handle, _cache(), batch, 0, 0, FAKE, FAKE, FAKE, 1 << 40, FAKE)
     assert e.value.status == kv.KVPRM_E_INVALID
+
+
+def test_pack_weight_validation():
+    for args in [(0, FAKE, 16, 32), (FAKE, 0, 16, 32), (FAKE, FAKE * 4, 15, 32),
+                 (FAKE, FAKE * 4, 16, 48), (FAKE, FAKE * 4, 0, 32), (FAKE, FAKE + 64, 16, 32),
+                 (FAKE + 8, FAKE * 4, 16, 32)]:
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_pack_weight(*args)
+        assert e.value.status == kv.KVPRM_E_INVALID

@@ -153,3 +153,16 @@ def test_cache_and_weights_unchanged():
     run_score(dw)
     assert torch.equal(kc, dw.k_pool) and torch.equal(vc, dw.v_pool)
     assert torch.equal(wq, dw.layers[0]["wq"])
+
+
+def test_pack_weight_roundtrip():
+    _say("case: kvprm_pack_weight")
+    rows, K = 4608, 3584
+    raw = synth.host_normal(rows * K, 5, 77, 0, 0.0, 0.02, synth.DT_BF16)
+    src = torch.from_numpy(raw.view(np.int16)).cuda()
+    dst = torch.empty_like(src)
+    kv().kvprm_pack_weight(src.data_ptr(), dst.data_ptr(), rows, K,
+                           torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    back = ko.unpack_tiled(dst.cpu().numpy().view(np.uint16), rows, K)
+    assert np.array_equal(back, raw.reshape(rows, K))

@@ -195,11 +195,14 @@ def test_cache_tile_layouts():
             for m in range(d):
                 stored[((m // x) * ps + s) * x + m % x] = tok[s, m]
         assert np.array_equal(ko.k_tile_to_tokens(stored, ps, d, eb), tok)
-    stored_v = np.empty(ps * d, dtype=np.int64)
-    for s in range(ps):
-        for m in range(d):
-            stored_v[m * ps + s] = tok[s, m]
-    assert np.array_equal(ko.v_tile_to_tokens(stored_v, ps, d), tok)
+    for eb in (4, 2, 1):
+        r = 16 // eb // 4
+        stored_v = np.empty(ps * d, dtype=np.int64)
+        for s in range(ps):
+            for m in range(d):
+                idx = ((((m // (16 * r)) * 4 + s // 4) * 16 + m % 16) * r + (m // 16) % r) * 4 + s % 4
+                stored_v[idx] = tok[s, m]
+        assert np.array_equal(ko.v_tile_to_tokens(stored_v, ps, d, eb), tok)
 
 
 # ------------------------------------------------------------------------ model-level pins
@@ -427,3 +430,16 @@ def test_verify_pass_against_transformers_llama_with_kv_cache(mixed):
         zr, _, hr, _, _ = ko.reencode(shape, base.layer, base.layer, E, toks[0].tolist(),
                                       base.verify_embed, base.final_norm, base.reward_w)
         assert np.max(np.abs(hr - full.hidden_states[-1][0, -1].numpy())) < 1e-5
+
+
+def test_packed_weight_layout():
+    """Block kb * (rows/16) + t, group l, element i holds W[16 t + l % 16][32 kb + 8 (l // 16) + i]."""
+    rows, K = 48, 96
+    W = np.arange(rows * K).reshape(rows, K)
+    stored = np.empty(rows * K, dtype=np.int64)
+    for r in range(rows):
+        for k in range(K):
+            t, kb = r // 16, k // 32
+            l = (r % 16) + 16 * ((k % 32) // 8)
+            stored[((kb * (rows // 16) + t) * 64 + l) * 8 + k % 8] = W[r, k]
+    assert np.array_equal(ko.unpack_tiled(stored, rows, K), W)
