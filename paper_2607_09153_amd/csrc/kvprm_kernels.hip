@@ -59,9 +59,9 @@ __device__ __forceinline__ float block_sum256(float v, float *red) {
 
 // ------------------------------------------------------------------------------- plan
 
-// Split-K plan of a matrix-core GEMV: split K only as far as needed for about 4096 waves (16
-// per CU), in whole 32-wide blocks, keeping at least 8 blocks per slice and the slice's operand
-// (staged in LDS, 1 KiB per block and column tile) within 64 KiB.
+// Split-K plan of a matrix-core GEMV, in whole 32-wide input blocks: about 32 blocks per wave
+// (long contiguous weight streams), but at least ~2048 waves in all, at least 4 blocks per
+// slice, and the slice's operand (staged in LDS, 1 KiB per block and column tile) within 64 KiB.
 static GemvPlan gemv_plan(int rows, int K, int B) {
   GemvPlan g;
   g.rows = rows;
@@ -69,11 +69,12 @@ static GemvPlan gemv_plan(int rows, int K, int B) {
   const int nt = gemv_nt(B);
   const int mt = gemv_mt(nt);
   const int waves = (rows / 16 + mt - 1) / mt;
-  int want = (4096 + waves - 1) / waves;
   const int nkb = K / 32;
-  if (want > nkb / 8) want = nkb / 8;
+  int want = (nkb + 31) / 32;
+  const int want_par = (2048 + waves - 1) / waves;
+  if (want < want_par) want = want_par;
+  if (want > nkb / 4) want = nkb / 4;
   if (want < 1) want = 1;
-  if (want > nkb) want = nkb;
   int kb_per = (nkb + want - 1) / want;
   const int kb_lds = 64 / nt;
   if (kb_per > kb_lds) kb_per = kb_lds;

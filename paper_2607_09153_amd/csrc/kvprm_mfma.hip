@@ -103,7 +103,7 @@ __device__ __forceinline__ float bmax(float v, float *red) {
 }
 
 int gemv_nt(int B) { return B <= 8 ? 1 : 2 * ((B + 15) / 16); }
-int gemv_mt(int) { return 2; }
+int gemv_mt(int nt) { return nt >= 2 ? 2 : 1; }
 int gemv_bp(int B) { return B <= 8 ? 8 : 16 * ((B + 15) / 16); }
 
 // ------------------------------------------------------------------------------- init
@@ -751,7 +751,7 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
 #define KVPRM_G(MT_, NT_, U_) \
   hipLaunchKernelGGL((k_gemv_mx<MT_, NT_, U_>), grid, dim3(256), lds, s, a)
   switch (p.nt) {
-    case 1: KVPRM_G(2, 1, 8); break;
+    case 1: KVPRM_G(1, 1, 4); break;
     case 2: KVPRM_G(2, 2, 4); break;
     case 4: KVPRM_G(2, 4, 2); break;
     case 6: KVPRM_G(2, 6, 2); break;
