@@ -119,10 +119,14 @@ typedef struct {
  * table entries beyond ceil(L_b / 16) are never read (they may hold garbage or -1).
  * The verify token sits at position L_b and attends to the L_b cached keys and its own key.
  *
- * Prefix-sharing hint (optional, a pure performance hint: results are defined by the page
- * table alone): candidates [group_start_host[g], group_start_host[g+1]) share their first
- * group_prefix_len_host[g] tokens, which must be a multiple of 16, at most every member's
- * length, and held by the same physical pages in every member's row. Groups tile [0, B). */
+ * Prefix-sharing hint (optional; section 4.1: beam candidates that extend one prefix share its
+ * cached keys and values): candidates [group_start_host[g], group_start_host[g+1]) share their
+ * first group_prefix_len_host[g] tokens, which must be a multiple of 16 and at most every
+ * member's length (checked against lengths_host, which the hint requires), and be held by the
+ * same physical pages in every member's row (not checked: the shared part is read through the
+ * first member's row). Groups tile [0, B). With bf16 or fp8 caches and at most 64 groups the
+ * shared pages are read once per group instead of once per member; otherwise the hint is
+ * ignored. A valid hint changes results only by floating-point summation order. */
 typedef struct {
   int32_t batch;                        /* B >= 0 */
   const int32_t *page_table;            /* device [B][max_pages] */

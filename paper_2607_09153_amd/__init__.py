@@ -9,6 +9,7 @@ There is no fallback: if the library is not built, importing the binding raises.
 from __future__ import annotations
 
 import ctypes
+import importlib.util
 import os
 from typing import Optional, Sequence
 
@@ -64,7 +65,20 @@ class KvprmError(RuntimeError):
         self.status = status
 
 
+def _preload_hip_runtime():
+    """One HIP runtime per process: when torch is installed, load the runtime it ships with
+    before this library, so that the library binds to that copy (torch's streams and memory
+    are then valid here) rather than starting a second runtime beside torch's."""
+    spec = importlib.util.find_spec("torch")
+    for d in (spec.submodule_search_locations or []) if spec else []:
+        rt = os.path.join(d, "lib", "libamdhip64.so")
+        if os.path.exists(rt):
+            ctypes.CDLL(rt, mode=ctypes.RTLD_GLOBAL)
+            return
+
+
 def _load():
+    _preload_hip_runtime()
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built (run __graft_entry__.build()); "
                           "the scoring pass has no non-GPU implementation")

@@ -105,8 +105,9 @@ static kvprm_status check_batch(const kvprm_handle h, const kvprm_batch *b, cons
     return fail(KVPRM_E_UNSUPPORTED, "%s: hidden * batch too large", fn);
   if (!b->page_table || !b->lengths) return fail(KVPRM_E_INVALID, "%s: null page_table or lengths", fn);
   if (b->max_pages < 1) return fail(KVPRM_E_INVALID, "%s: max_pages < 1", fn);
-  if (b->max_pages > kMaxChunks * kChunkPages)
-    return fail(KVPRM_E_UNSUPPORTED, "%s: max_pages above %d", fn, kMaxChunks * kChunkPages);
+  // chunk slots per candidate: ceil(max_pages / 32), plus one where a shared prefix splits a chunk
+  if (b->max_pages > (kMaxChunks - 1) * kChunkPages)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: max_pages above %d", fn, (kMaxChunks - 1) * kChunkPages);
   const int cap = b->max_pages * h->desc.page_size;
   if (b->lengths_host)
     for (int i = 0; i < b->batch; ++i)
@@ -117,6 +118,8 @@ static kvprm_status check_batch(const kvprm_handle h, const kvprm_batch *b, cons
   if (b->num_groups > 0) {
     const int *s = b->group_start_host, *pl = b->group_prefix_len_host;
     if (!s || !pl) return fail(KVPRM_E_INVALID, "%s: null group arrays", fn);
+    if (!b->lengths_host)
+      return fail(KVPRM_E_INVALID, "%s: the prefix-sharing hint needs lengths_host", fn);
     if (s[0] != 0 || s[b->num_groups] != b->batch)
       return fail(KVPRM_E_INVALID, "%s: groups must tile [0, batch)", fn);
     for (int g = 0; g < b->num_groups; ++g) {
@@ -164,9 +167,41 @@ static kvprm_status check_ws(const kvprm_handle h, const kvprm_batch *b, void *w
   return KVPRM_OK;
 }
 
-static GroupTable group_table(const kvprm_batch *) {
+// Launch table of the attention kernels. The prefix-sharing hint is used by the matrix-core
+// attention only (fp32 caches take the vector-ALU path, which reads every page per candidate)
+// and only for up to kMaxGroups groups; otherwise it is ignored, which changes nothing but
+// speed. With lengths on the host, the chunk grid of the private pages is sized to the longest
+// private range instead of max_pages.
+static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b) {
   GroupTable gt;
   memset(&gt, 0, sizeof gt);
+  const bool share = h->dm.kvdt != 0 && b->num_groups > 0 && b->num_groups <= kMaxGroups;
+  if (share) {
+    gt.n = b->num_groups;
+    for (int i = 0; i <= gt.n; ++i) gt.start[i] = b->group_start_host[i];
+    const int cols_per_block = 16 * kPrefixWaves;
+    for (int i = 0; i < gt.n; ++i) {
+      const int pp = b->group_prefix_len_host[i] / kPage;
+      const int members = gt.start[i + 1] - gt.start[i];
+      gt.prefix_pages[i] = pp;
+      const int blocks = pp > 0 ? (members * h->dm.g + cols_per_block - 1) / cols_per_block : 0;
+      gt.colblock_start[i + 1] = gt.colblock_start[i] + blocks;
+      const int ch = (pp + kChunkPages - 1) / kChunkPages;
+      if (ch > gt.prefix_chunks) gt.prefix_chunks = ch;
+    }
+  }
+  if (b->lengths_host) {
+    int most = 1;
+    for (int i = 0; i < b->batch; ++i) {
+      int first = 0;
+      for (int k = 0; k < gt.n; ++k)
+        if (i >= gt.start[k] && i < gt.start[k + 1]) first = gt.prefix_pages[k];
+      const int priv = (b->lengths_host[i] + kPage - 1) / kPage - first;
+      const int ch = (priv + kChunkPages - 1) / kChunkPages;
+      if (ch > most) most = ch;
+    }
+    gt.private_chunks = most;
+  }
   return gt;
 }
 
@@ -194,7 +229,7 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   hipStream_t s = (hipStream_t)stream;
   const Plan p = make_plan(dm, b->batch, b->max_pages);
   const Workspace w = carve(dm, p, workspace);
-  const GroupTable gt = group_table(b);
+  const GroupTable gt = group_table(h, b);
   const int EB = dm.kvdt == 0 ? 4 : (dm.kvdt == 1 ? 2 : 1);
   const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * EB;
   const size_t layer_scales = (size_t)cache->num_pages * dm.nkv;
@@ -284,7 +319,7 @@ kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const 
   const Workspace w = carve(dm, p, workspace);
   HIP_TRY(launch_attention(dm, p, w, layer, cache->k_pages, cache->v_pages, cache->k_scale,
                            cache->v_scale, cache->num_pages, b->page_table, b->lengths,
-                           group_table(b), q, k_self, v_self, o, (hipStream_t)stream),
+                           group_table(h, b), q, k_self, v_self, o, (hipStream_t)stream),
           "attention");
   return ok();
 }

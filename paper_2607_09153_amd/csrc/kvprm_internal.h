@@ -16,15 +16,19 @@ struct Dims {
 
 // Prefix-sharing groups, passed by value to the attention kernels (no host->device copy).
 constexpr int kMaxGroups = 64;
+constexpr int kPrefixWaves = 8;  // waves per shared-prefix block (16 columns each)
 struct GroupTable {
-  int n;                         // 0 = no sharing
-  int start[kMaxGroups + 1];     // candidate ranges
-  int prefix_pages[kMaxGroups];  // shared pages of each group
+  int n;                               // 0 = no sharing
+  int start[kMaxGroups + 1];           // candidate ranges
+  int prefix_pages[kMaxGroups];        // shared pages of each group
+  int colblock_start[kMaxGroups + 1];  // shared-prefix column blocks of the groups, cumulative
+  int prefix_chunks;                   // chunks of the longest group prefix
+  int private_chunks;                  // chunk grid of the private pages (0 = ceil(max_pages / 32))
 };
 
 // Attention split: each work item covers kChunkPages pages of one (candidate, kv-head).
 constexpr int kChunkPages = 32;
-constexpr int kMaxChunks = 1024;  // chunk partials one merge handles: max_pages <= 32768
+constexpr int kMaxChunks = 1024;  // chunk partials one merge handles: max_pages <= 32736
 constexpr int kMaxSS = 8192;
 constexpr int kMaxKvHeadsMx = 8;  // matrix-core attention: one wave per kv-head in a block      // sums-of-squares partials staged in LDS: (H / 64) * B
 constexpr int kPage = 16;
@@ -53,7 +57,7 @@ struct GemvPlan {
 };
 
 struct Plan {
-  int B, max_pages, nch;      // nch = chunks per (candidate, kv-head) at max_pages
+  int B, max_pages, nch;      // nch = chunk slots per (candidate, q-head): ceil(max_pages / 32) + 1
   int nss;                    // row blocks of H that carry partial sums of squares
   int rb;                     // rows per such block
   // vector-ALU path

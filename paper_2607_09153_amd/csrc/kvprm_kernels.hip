@@ -87,7 +87,8 @@ Plan make_plan(const Dims &dm, int B, int max_pages) {
   Plan p{};
   p.B = B;
   p.max_pages = max_pages;
-  p.nch = (max_pages + kChunkPages - 1) / kChunkPages;
+  // one more slot than chunks of max_pages: a shared prefix that ends inside a chunk adds one
+  p.nch = (max_pages + kChunkPages - 1) / kChunkPages + 1;
   size_t m = 0;
   if (dm.wdt == 1) {
     p.rb = 64;

@@ -393,6 +393,184 @@ __device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t word) {
   return (__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xFFFF0000u);
 }
 
+// Raw registers of one page pair of one kv-head, in tile byte order (16 bytes per lane and
+// instruction): K tiles of pages A and B, then their V tiles. bf16 uses D/32 of each, fp8 D/64.
+template <int D>
+struct PairRaw {
+  uint4 k[2][D / 32];
+  uint4 v[2][D / 32];
+};
+
+// Loads a pair from tile base pointers (global memory or LDS).
+template <int KVT, int D>
+__device__ __forceinline__ void load_pair_raw(const uint4 *kA, const uint4 *kB, const uint4 *vA,
+                                              const uint4 *vB, int lane, PairRaw<D> &r) {
+  constexpr int N = KVT == 1 ? D / 32 : D / 64;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    r.k[0][i] = kA[i * 64 + lane];
+    r.k[1][i] = kB[i * 64 + lane];
+    r.v[0][i] = vA[i * 64 + lane];
+    r.v[1][i] = vB[i * 64 + lane];
+  }
+}
+
+// Raw pair -> bf16 MFMA operands. K: lane holds token lane % 16, 8 dims per 32-dim block
+// (bf16: dims 32kk + 8c + i; fp8: dims 16 (4 (kk/2) + c) + 8 (kk%2) + i). V (tile stores 4
+// consecutive slots of r dims 16 apart): VA[nb] = slots 4c..4c+3 of dim 16 nb + lane % 16.
+template <int KVT, int D>
+__device__ __forceinline__ void unpack_pair(const PairRaw<D> &r, uint4 *KA, uint4 *KB, uint2 *VA,
+                                            uint2 *VB) {
+  constexpr int NKB = D / 32, NDB = D / 16;
+  if (KVT == 1) {
+#pragma unroll
+    for (int kk = 0; kk < NKB; ++kk) {
+      KA[kk] = r.k[0][kk];
+      KB[kk] = r.k[1][kk];
+    }
+#pragma unroll
+    for (int q2 = 0; q2 < NDB / 2; ++q2) {
+      VA[2 * q2] = make_uint2(r.v[0][q2].x, r.v[0][q2].y);
+      VA[2 * q2 + 1] = make_uint2(r.v[0][q2].z, r.v[0][q2].w);
+      VB[2 * q2] = make_uint2(r.v[1][q2].x, r.v[1][q2].y);
+      VB[2 * q2 + 1] = make_uint2(r.v[1][q2].z, r.v[1][q2].w);
+    }
+  } else {
+#pragma unroll
+    for (int kp = 0; kp < NKB / 2; ++kp) {
+      const uint4 ra = r.k[0][kp], rb = r.k[1][kp];
+      KA[2 * kp] = make_uint4(fp8x2_to_bf16x2<false>(ra.x), fp8x2_to_bf16x2<true>(ra.x),
+                              fp8x2_to_bf16x2<false>(ra.y), fp8x2_to_bf16x2<true>(ra.y));
+      KA[2 * kp + 1] = make_uint4(fp8x2_to_bf16x2<false>(ra.z), fp8x2_to_bf16x2<true>(ra.z),
+                                  fp8x2_to_bf16x2<false>(ra.w), fp8x2_to_bf16x2<true>(ra.w));
+      KB[2 * kp] = make_uint4(fp8x2_to_bf16x2<false>(rb.x), fp8x2_to_bf16x2<true>(rb.x),
+                              fp8x2_to_bf16x2<false>(rb.y), fp8x2_to_bf16x2<true>(rb.y));
+      KB[2 * kp + 1] = make_uint4(fp8x2_to_bf16x2<false>(rb.z), fp8x2_to_bf16x2<true>(rb.z),
+                                  fp8x2_to_bf16x2<false>(rb.w), fp8x2_to_bf16x2<true>(rb.w));
+    }
+#pragma unroll
+    for (int q4 = 0; q4 < NDB / 4; ++q4) {
+      const uint32_t wa[4] = {r.v[0][q4].x, r.v[0][q4].y, r.v[0][q4].z, r.v[0][q4].w};
+      const uint32_t wb[4] = {r.v[1][q4].x, r.v[1][q4].y, r.v[1][q4].z, r.v[1][q4].w};
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        VA[4 * q4 + jj] = make_uint2(fp8x2_to_bf16x2<false>(wa[jj]), fp8x2_to_bf16x2<true>(wa[jj]));
+        VB[4 * q4 + jj] = make_uint2(fp8x2_to_bf16x2<false>(wb[jj]), fp8x2_to_bf16x2<true>(wb[jj]));
+      }
+    }
+  }
+}
+
+// Query operands of one column (zero when absent), split in three bf16 terms so that the
+// scores keep fp32-level accuracy even for very large logits. The dim order matches the K
+// operand of the cache dtype.
+template <int KVT, int D>
+__device__ __forceinline__ void load_query_ops(const float *qr, bool present, int cq, uint4 *qhi,
+                                               uint4 *qmd, uint4 *qlo) {
+  constexpr int NKB = D / 32;
+#pragma unroll
+  for (int kk = 0; kk < NKB; ++kk) {
+    uint32_t h[8], md[8], l[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int dim = (KVT == 1) ? kk * 32 + 8 * cq + i : 16 * (4 * (kk >> 1) + cq) + 8 * (kk & 1) + i;
+      const float v = present ? qr[dim] : 0.f;
+      uint32_t rest;
+      split_hi_lo(v, h[i], rest);
+      split_hi_lo(v - __uint_as_float(h[i] << 16), md[i], l[i]);
+    }
+    qhi[kk] = make_uint4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
+    qmd[kk] = make_uint4(pack2(md[0], md[1]), pack2(md[2], md[3]), pack2(md[4], md[5]),
+                         pack2(md[6], md[7]));
+    qlo[kk] = make_uint4(pack2(l[0], l[1]), pack2(l[2], l[3]), pack2(l[4], l[5]), pack2(l[6], l[7]));
+  }
+}
+
+// One online-softmax step over a page pair for the 16 columns of a wave: S = K Q^T (lane holds
+// tokens 4c + i of pages A and B for column lane % 16), running max / sum, then
+// O^T += V^T P^T with P split hi + lo. ok[] marks valid tokens (masked tokens get p = 0 and
+// their V entries are zeroed, since their slots may hold NaN). vsa / vsb scale P for fp8 V.
+template <int D>
+__device__ __forceinline__ void online_step(const uint4 *KA, const uint4 *KB, const uint2 *VA,
+                                            const uint2 *VB, const uint4 *qhi, const uint4 *qmd,
+                                            const uint4 *qlo, const bool *ok, float sca, float scb,
+                                            float vsa, float vsb, float &m_run, float &l_run,
+                                            floatx4 *acc) {
+  constexpr int NKB = D / 32, NDB = D / 16;
+  floatx4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < NKB; ++kk) {
+    sa = mfma16(KA[kk], qhi[kk], sa);
+    sa = mfma16(KA[kk], qmd[kk], sa);
+    sa = mfma16(KA[kk], qlo[kk], sa);
+    sb = mfma16(KB[kk], qhi[kk], sb);
+    sb = mfma16(KB[kk], qmd[kk], sb);
+    sb = mfma16(KB[kk], qlo[kk], sb);
+  }
+  float sv[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sv[i] = ok[i] ? sa[i] * sca : -INFINITY;
+    sv[4 + i] = ok[4 + i] ? sb[i] * scb : -INFINITY;
+  }
+  float mx = sv[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv[i]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(m_run, mx);  // finite once any valid token has been seen
+  const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
+  m_run = m_new;
+  float pv[8], psum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    pv[i] = ok[i] ? expf(sv[i] - m_new) : 0.f;
+    psum += pv[i];
+  }
+  l_run = l_run * alpha + psum;
+#pragma unroll
+  for (int nb = 0; nb < NDB; ++nb) {
+    acc[nb][0] *= alpha;
+    acc[nb][1] *= alpha;
+    acc[nb][2] *= alpha;
+    acc[nb][3] *= alpha;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    pv[i] *= vsa;
+    pv[4 + i] *= vsb;
+  }
+  uint32_t ph[8], pl[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) split_hi_lo(pv[i], ph[i], pl[i]);
+  const uint4 Phi = make_uint4(pack2(ph[0], ph[1]), pack2(ph[2], ph[3]), pack2(ph[4], ph[5]),
+                               pack2(ph[6], ph[7]));
+  const uint4 Plo = make_uint4(pack2(pl[0], pl[1]), pack2(pl[2], pl[3]), pack2(pl[4], pl[5]),
+                               pack2(pl[6], pl[7]));
+  const uint32_t ma0 = (ok[0] ? 0xFFFFu : 0u) | (ok[1] ? 0xFFFF0000u : 0u);
+  const uint32_t ma1 = (ok[2] ? 0xFFFFu : 0u) | (ok[3] ? 0xFFFF0000u : 0u);
+  const uint32_t mb0 = (ok[4] ? 0xFFFFu : 0u) | (ok[5] ? 0xFFFF0000u : 0u);
+  const uint32_t mb1 = (ok[6] ? 0xFFFFu : 0u) | (ok[7] ? 0xFFFF0000u : 0u);
+#pragma unroll
+  for (int nb = 0; nb < NDB; ++nb) {
+    const uint4 vop = make_uint4(VA[nb].x & ma0, VA[nb].y & ma1, VB[nb].x & mb0, VB[nb].y & mb1);
+    acc[nb] = mfma16(vop, Phi, acc[nb]);
+    acc[nb] = mfma16(vop, Plo, acc[nb]);
+  }
+}
+
+// Stores a wave's partial for column n (acc rows d = 16 nb + 4 cq + i; 64 bytes per head and
+// 16-dim block across the 4 lanes of the column) and its m, l.
+template <int D>
+__device__ __forceinline__ void store_partial(float *hb, int cq, const floatx4 *acc, float m_run,
+                                              float l_run) {
+  constexpr int NDB = D / 16;
+#pragma unroll
+  for (int nb = 0; nb < NDB; ++nb)
+    *(float4 *)(hb + nb * 16 + 4 * cq) = make_float4(acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3]);
+  if (cq == 0) *(float2 *)(hb + D) = make_float2(m_run, l_run);
+}
+
 struct AttnArgs {
   const char *kp, *vp;     // this layer's pools
   const float *ksc, *vsc;  // this layer's fp8 scales (or null)
@@ -403,7 +581,8 @@ struct AttnArgs {
   GroupTable gt;
   int nch;
   const float *q, *kself, *vself;
-  float *apart;   // [B][nq][nch][D + 2]: per chunk the acc row, then m, then l
+  float *apart;   // [B][nq][nch][D + 2]: per chunk the acc row, then m, then l; a candidate's
+                  // shared-prefix chunks come first, its private chunks after them
   float *o;       // [B][nq][D] fp32 output (may be null)
   uint16_t *op;   // operand buffer of the output projection (may be null)
   int NT, Bp;
@@ -432,6 +611,7 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   int first = 0;
   for (int gi = 0; gi < a.gt.n; ++gi)
     if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
+  const int ncp = (first + kChunkPages - 1) / kChunkPages;  // this candidate's prefix chunks
   const int p0 = first + c * kChunkPages;
   if (p0 >= npages) return;
   const int np = min(npages, p0 + kChunkPages) - p0;
@@ -445,196 +625,47 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
     ksc_l = a.ksc[(size_t)ph_l * nkv + j];
     vsc_l = a.vsc[(size_t)ph_l * nkv + j];
   }
-
-  // raw registers of one page pair; the next pair is loaded while the current one is computed
-  struct PairRaw {
-    uint4 k[2][NKB];      // K tiles of pages la, lb (fp8: first NKB / 2 entries)
-    uint4 v[2][NDB / 2];  // V: 16 bytes = 4 slots of 2 (bf16) or 4 (fp8) dimension blocks
-  };
   const int npairs = (np + 1) >> 1;
-  auto load_pair = [&](int pp, PairRaw &r) {
+  auto load_pair = [&](int pp, PairRaw<D> &r) {
     // indices past the chunk are clamped to its last page: those tokens are masked anyway
     const int pa = __shfl(ph_l, min(2 * pp, np - 1), 64);
     const int pb = __shfl(ph_l, min(2 * pp + 1, np - 1), 64);
-    const char *kA = a.kp + ((size_t)pa * nkv + j) * TILE;
-    const char *kB = a.kp + ((size_t)pb * nkv + j) * TILE;
-    const char *vA = a.vp + ((size_t)pa * nkv + j) * TILE;
-    const char *vB = a.vp + ((size_t)pb * nkv + j) * TILE;
-    if (KVT == 1) {
-#pragma unroll
-      for (int kk = 0; kk < NKB; ++kk) {
-        r.k[0][kk] = *(const uint4 *)(kA + (size_t)(kk * 64 + lane) * 16);
-        r.k[1][kk] = *(const uint4 *)(kB + (size_t)(kk * 64 + lane) * 16);
-      }
-      // V tile (r = 2): 16-byte group (q, cq, n) holds slots 4cq..4cq+3 of dims 32q + n, 32q + 16 + n
-#pragma unroll
-      for (int q2 = 0; q2 < NDB / 2; ++q2) {
-        r.v[0][q2] = *(const uint4 *)(vA + (size_t)(q2 * 64 + lane) * 16);
-        r.v[1][q2] = *(const uint4 *)(vB + (size_t)(q2 * 64 + lane) * 16);
-      }
-    } else {
-#pragma unroll
-      for (int kp = 0; kp < NKB / 2; ++kp) {
-        r.k[0][kp] = *(const uint4 *)(kA + (size_t)(kp * 64 + lane) * 16);
-        r.k[1][kp] = *(const uint4 *)(kB + (size_t)(kp * 64 + lane) * 16);
-      }
-      // V tile (r = 4): 16-byte group (q, cq, n) holds slots 4cq..4cq+3 of dims 64q + 16j + n
-#pragma unroll
-      for (int q4 = 0; q4 < NDB / 4; ++q4) {
-        r.v[0][q4] = *(const uint4 *)(vA + (size_t)(q4 * 64 + lane) * 16);
-        r.v[1][q4] = *(const uint4 *)(vB + (size_t)(q4 * 64 + lane) * 16);
-      }
-    }
+    load_pair_raw<KVT, D>((const uint4 *)(a.kp + ((size_t)pa * nkv + j) * TILE),
+                          (const uint4 *)(a.kp + ((size_t)pb * nkv + j) * TILE),
+                          (const uint4 *)(a.vp + ((size_t)pa * nkv + j) * TILE),
+                          (const uint4 *)(a.vp + ((size_t)pb * nkv + j) * TILE), lane, r);
   };
-  PairRaw r0, r1;
+  PairRaw<D> r0, r1;
   load_pair(0, r0);  // in flight while the queries are prepared
 
-  // query operands of head n (zero columns for n >= g), split in three bf16 terms so that the
-  // scores keep fp32-level accuracy even for very large logits
   uint4 qhi[NKB], qmd[NKB], qlo[NKB];
-  {
-    const float *qr = a.q + ((size_t)b * nq + (size_t)j * g + (n < g ? n : 0)) * D;
-#pragma unroll
-    for (int kk = 0; kk < NKB; ++kk) {
-      uint32_t h[8], md[8], l[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        int dim;
-        if (KVT == 1)
-          dim = kk * 32 + 8 * cq + i;
-        else
-          dim = 16 * (4 * (kk >> 1) + cq) + 8 * (kk & 1) + i;
-        const float v = (n < g) ? qr[dim] : 0.f;
-        uint32_t rest;
-        split_hi_lo(v, h[i], rest);
-        split_hi_lo(v - __uint_as_float(h[i] << 16), md[i], l[i]);
-      }
-      qhi[kk] = make_uint4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
-      qmd[kk] = make_uint4(pack2(md[0], md[1]), pack2(md[2], md[3]), pack2(md[4], md[5]),
-                           pack2(md[6], md[7]));
-      qlo[kk] = make_uint4(pack2(l[0], l[1]), pack2(l[2], l[3]), pack2(l[4], l[5]), pack2(l[6], l[7]));
-    }
-  }
-
+  load_query_ops<KVT, D>(a.q + ((size_t)b * nq + (size_t)j * g + (n < g ? n : 0)) * D, n < g, cq,
+                         qhi, qmd, qlo);
   const float rs = 1.0f / sqrtf((float)D);
   float m_run = -INFINITY, l_run = 0.f;
   floatx4 acc[NDB];
 #pragma unroll
   for (int nb = 0; nb < NDB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute_pair = [&](int pp, const PairRaw &r) {
+  auto compute_pair = [&](int pp, const PairRaw<D> &r) {
     const int la = min(2 * pp, np - 1), lb = 2 * pp + 1;
     const bool hasA = 2 * pp < np, hasB = lb < np;
     uint4 KA[NKB], KB[NKB];
     uint2 VA[NDB], VB[NDB];
-    if (KVT == 1) {
-#pragma unroll
-      for (int kk = 0; kk < NKB; ++kk) {
-        KA[kk] = r.k[0][kk];
-        KB[kk] = r.k[1][kk];
-      }
-#pragma unroll
-      for (int q2 = 0; q2 < NDB / 2; ++q2) {
-        VA[2 * q2] = make_uint2(r.v[0][q2].x, r.v[0][q2].y);
-        VA[2 * q2 + 1] = make_uint2(r.v[0][q2].z, r.v[0][q2].w);
-        VB[2 * q2] = make_uint2(r.v[1][q2].x, r.v[1][q2].y);
-        VB[2 * q2 + 1] = make_uint2(r.v[1][q2].z, r.v[1][q2].w);
-      }
-    } else {
-#pragma unroll
-      for (int kp = 0; kp < NKB / 2; ++kp) {
-        const uint4 ra = r.k[0][kp], rb = r.k[1][kp];
-        KA[2 * kp] = make_uint4(fp8x2_to_bf16x2<false>(ra.x), fp8x2_to_bf16x2<true>(ra.x),
-                                fp8x2_to_bf16x2<false>(ra.y), fp8x2_to_bf16x2<true>(ra.y));
-        KA[2 * kp + 1] = make_uint4(fp8x2_to_bf16x2<false>(ra.z), fp8x2_to_bf16x2<true>(ra.z),
-                                    fp8x2_to_bf16x2<false>(ra.w), fp8x2_to_bf16x2<true>(ra.w));
-        KB[2 * kp] = make_uint4(fp8x2_to_bf16x2<false>(rb.x), fp8x2_to_bf16x2<true>(rb.x),
-                                fp8x2_to_bf16x2<false>(rb.y), fp8x2_to_bf16x2<true>(rb.y));
-        KB[2 * kp + 1] = make_uint4(fp8x2_to_bf16x2<false>(rb.z), fp8x2_to_bf16x2<true>(rb.z),
-                                    fp8x2_to_bf16x2<false>(rb.w), fp8x2_to_bf16x2<true>(rb.w));
-      }
-#pragma unroll
-      for (int q4 = 0; q4 < NDB / 4; ++q4) {
-        const uint32_t wa[4] = {r.v[0][q4].x, r.v[0][q4].y, r.v[0][q4].z, r.v[0][q4].w};
-        const uint32_t wb[4] = {r.v[1][q4].x, r.v[1][q4].y, r.v[1][q4].z, r.v[1][q4].w};
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          VA[4 * q4 + jj] = make_uint2(fp8x2_to_bf16x2<false>(wa[jj]), fp8x2_to_bf16x2<true>(wa[jj]));
-          VB[4 * q4 + jj] = make_uint2(fp8x2_to_bf16x2<false>(wb[jj]), fp8x2_to_bf16x2<true>(wb[jj]));
-        }
-      }
-    }
-    // ---- scores: lane holds tokens 4cq + i of pages la and lb for head n
-    floatx4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < NKB; ++kk) {
-      sa = mfma16(KA[kk], qhi[kk], sa);
-      sa = mfma16(KA[kk], qmd[kk], sa);
-      sa = mfma16(KA[kk], qlo[kk], sa);
-      sb = mfma16(KB[kk], qhi[kk], sb);
-      sb = mfma16(KB[kk], qmd[kk], sb);
-      sb = mfma16(KB[kk], qlo[kk], sb);
-    }
-    const float sca = (KVT == 2) ? __shfl(ksc_l, la, 64) * rs : rs;
-    const float scb = (KVT == 2) ? __shfl(ksc_l, hasB ? lb : la, 64) * rs : rs;
+    unpack_pair<KVT, D>(r, KA, KB, VA, VB);
     const int ta = (p0 + la) * kPage + 4 * cq, tb = (p0 + lb) * kPage + 4 * cq;
-    float s[8];
     bool ok[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       ok[i] = hasA && (ta + i < L);
       ok[4 + i] = hasB && (tb + i < L);
-      s[i] = ok[i] ? sa[i] * sca : -INFINITY;
-      s[4 + i] = ok[4 + i] ? sb[i] * scb : -INFINITY;
     }
-    float mx = s[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) mx = fmaxf(mx, s[i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);  // finite: the first pair always has a valid token
-    const float alpha = expf(m_run - m_new);
-    m_run = m_new;
-    float pv[8], psum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      pv[i] = ok[i] ? expf(s[i] - m_new) : 0.f;
-      psum += pv[i];
-    }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int nb = 0; nb < NDB; ++nb) {
-      acc[nb][0] *= alpha;
-      acc[nb][1] *= alpha;
-      acc[nb][2] *= alpha;
-      acc[nb][3] *= alpha;
-    }
-    if (KVT == 2) {
-      const float va_s = __shfl(vsc_l, la, 64), vb_s = __shfl(vsc_l, hasB ? lb : la, 64);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        pv[i] *= va_s;
-        pv[4 + i] *= vb_s;
-      }
-    }
-    uint32_t ph[8], pl[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) split_hi_lo(pv[i], ph[i], pl[i]);
-    const uint4 Phi = make_uint4(pack2(ph[0], ph[1]), pack2(ph[2], ph[3]), pack2(ph[4], ph[5]),
-                                 pack2(ph[6], ph[7]));
-    const uint4 Plo = make_uint4(pack2(pl[0], pl[1]), pack2(pl[2], pl[3]), pack2(pl[4], pl[5]),
-                                 pack2(pl[6], pl[7]));
-    // zero V entries of masked tokens (their slots may hold NaN)
-    const uint32_t ma0 = (ok[0] ? 0xFFFFu : 0u) | (ok[1] ? 0xFFFF0000u : 0u);
-    const uint32_t ma1 = (ok[2] ? 0xFFFFu : 0u) | (ok[3] ? 0xFFFF0000u : 0u);
-    const uint32_t mb0 = (ok[4] ? 0xFFFFu : 0u) | (ok[5] ? 0xFFFF0000u : 0u);
-    const uint32_t mb1 = (ok[6] ? 0xFFFFu : 0u) | (ok[7] ? 0xFFFF0000u : 0u);
-#pragma unroll
-    for (int nb = 0; nb < NDB; ++nb) {
-      const uint4 vop = make_uint4(VA[nb].x & ma0, VA[nb].y & ma1, VB[nb].x & mb0, VB[nb].y & mb1);
-      acc[nb] = mfma16(vop, Phi, acc[nb]);
-      acc[nb] = mfma16(vop, Plo, acc[nb]);
-    }
+    const int lbc = hasB ? lb : la;
+    const float sca = (KVT == 2) ? __shfl(ksc_l, la, 64) * rs : rs;
+    const float scb = (KVT == 2) ? __shfl(ksc_l, lbc, 64) * rs : rs;
+    const float vsa = (KVT == 2) ? __shfl(vsc_l, la, 64) : 1.f;
+    const float vsb = (KVT == 2) ? __shfl(vsc_l, lbc, 64) : 1.f;
+    online_step<D>(KA, KB, VA, VB, qhi, qmd, qlo, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
   };
   // a branch-free loop over an even number of pairs: the pair past the end (if any) is fully
   // masked, and loads past the end repeat the last page (an L2 hit), so that wait counts never
@@ -645,17 +676,116 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
     load_pair(pp + 2, r0);
     compute_pair(pp + 1, r1);
   }
-  // ---- this wave's partial: lane holds acc rows d = 16 nb + 4 cq + i of head n, so each
-  // 16-byte store is contiguous with those of the 3 other lanes of the head (64 bytes)
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
-  if (n < g) {
-    float *hb = a.apart + (((size_t)b * nq + (size_t)j * g + n) * a.nch + c) * (D + 2);
-#pragma unroll
-    for (int nb = 0; nb < NDB; ++nb)
-      *(float4 *)(hb + nb * 16 + 4 * cq) = make_float4(acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3]);
-    if (cq == 0) *(float2 *)(hb + D) = make_float2(m_run, l_run);
+  if (n < g)
+    store_partial<D>(a.apart + (((size_t)b * nq + (size_t)j * g + n) * a.nch + ncp + c) * (D + 2),
+                     cq, acc, m_run, l_run);
+}
+
+// Shared-prefix attention: the members of a prefix group share the physical pages of their
+// first prefix_pages pages, which are read once for all of them. One block per (prefix chunk c,
+// kv-head j, column block) with up to 16 waves; the columns are (member, q-head of j) pairs,
+// 16 per wave (e.g. 2 members x 7 heads). The pair's K and V tiles (one head) are staged in LDS
+// once per block, double buffered, and every wave runs the online step on them with its own
+// columns. Partials go to the members' chunk slots [0, ncp).
+template <int KVT, int D>
+__global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
+  constexpr int NKB = D / 32, NDB = D / 16;
+  constexpr int EB = KVT == 1 ? 2 : 1;
+  constexpr int TILE16 = kPage * D * EB / 16;  // uint4 entries per tile
+  __shared__ uint4 stage_s[2][4][TILE16];      // [buffer][K A, K B, V A, V B]
+  const int c = blockIdx.x, j = blockIdx.y;
+  // group and column block of this block
+  int grp = 0;
+  while (grp < a.gt.n - 1 && (int)blockIdx.z >= a.gt.colblock_start[grp + 1]) ++grp;
+  const int cb = blockIdx.z - a.gt.colblock_start[grp];
+  const int m0 = a.gt.start[grp], members = a.gt.start[grp + 1] - m0;
+  const int ppages = a.gt.prefix_pages[grp];
+  const int p0 = c * kChunkPages;
+  if (p0 >= ppages) return;
+  const int np = min(ppages, p0 + kChunkPages) - p0;
+  const int npairs = (np + 1) >> 1;
+  const int nkv = a.nkv, g = a.g, nq = a.nq;
+  constexpr int nthr = 64 * kPrefixWaves;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 15, cq = lane >> 4;
+  const int col = (cb * kPrefixWaves + wave) * 16 + n;  // (member, head) column
+  const int mem = col / g, hh = col - mem * g;
+  const bool present = mem < members;
+  const int bcand = m0 + (present ? mem : 0);
+  // page ids and fp8 scales of the chunk (from the first member's table row), in lanes
+  const int ph_l = lane < np ? a.page_table[(size_t)m0 * a.max_pages + p0 + lane] : 0;
+  float ksc_l = 1.f, vsc_l = 1.f;
+  if (KVT == 2 && lane < np) {
+    ksc_l = a.ksc[(size_t)ph_l * nkv + j];
+    vsc_l = a.vsc[(size_t)ph_l * nkv + j];
   }
+  // cooperative staging: thread t copies entries t, t + nthr, ... of the pair's 4 tiles
+  constexpr int PER = (4 * TILE16 + nthr - 1) / nthr;
+  uint4 st[PER];
+  auto fetch = [&](int pp) {
+    const int pa = __shfl(ph_l, min(2 * pp, np - 1), 64);
+    const int pb = __shfl(ph_l, min(2 * pp + 1, np - 1), 64);
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = threadIdx.x + u * nthr;
+      if (e < 4 * TILE16) {
+        const int t = e / TILE16, o = e - t * TILE16;
+        const char *pool = t < 2 ? a.kp : a.vp;
+        const int pg = (t & 1) ? pb : pa;
+        st[u] = ((const uint4 *)(pool + ((size_t)pg * nkv + j) * TILE16 * 16))[o];
+      }
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = threadIdx.x + u * nthr;
+      if (e < 4 * TILE16) (&stage_s[buf][0][0])[e] = st[u];
+    }
+  };
+  fetch(0);
+  uint4 qhi[NKB], qmd[NKB], qlo[NKB];
+  load_query_ops<KVT, D>(a.q + ((size_t)bcand * nq + (size_t)j * g + hh) * D, present, cq, qhi,
+                         qmd, qlo);
+  stash(0);
+  __syncthreads();
+  const float rs = 1.0f / sqrtf((float)D);
+  float m_run = -INFINITY, l_run = 0.f;
+  floatx4 acc[NDB];
+#pragma unroll
+  for (int nb = 0; nb < NDB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int pp = 0; pp < npairs; ++pp) {
+    const int buf = pp & 1;
+    if (pp + 1 < npairs) fetch(pp + 1);
+    PairRaw<D> r;
+    load_pair_raw<KVT, D>(stage_s[buf][0], stage_s[buf][1], stage_s[buf][2], stage_s[buf][3], lane, r);
+    uint4 KA[NKB], KB[NKB];
+    uint2 VA[NDB], VB[NDB];
+    unpack_pair<KVT, D>(r, KA, KB, VA, VB);
+    const int la = 2 * pp, lb = 2 * pp + 1;
+    const bool hasB = lb < np;
+    bool ok[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ok[i] = true;  // prefix pages are full
+      ok[4 + i] = hasB;
+    }
+    const int lbc = hasB ? lb : la;
+    const float sca = (KVT == 2) ? __shfl(ksc_l, la, 64) * rs : rs;
+    const float scb = (KVT == 2) ? __shfl(ksc_l, lbc, 64) * rs : rs;
+    const float vsa = (KVT == 2) ? __shfl(vsc_l, la, 64) : 1.f;
+    const float vsb = (KVT == 2) ? __shfl(vsc_l, lbc, 64) : 1.f;
+    online_step<D>(KA, KB, VA, VB, qhi, qmd, qlo, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
+    if (pp + 1 < npairs) stash(buf ^ 1);
+    __syncthreads();
+  }
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+  if (present)
+    store_partial<D>(a.apart + (((size_t)bcand * nq + (size_t)j * g + hh) * a.nch + c) * (D + 2),
+                     cq, acc, m_run, l_run);
 }
 
 // Log-sum-exp merge of the chunk partials of one (candidate b, q-head h) with the token's own
@@ -675,7 +805,9 @@ __global__ __launch_bounds__(D) void k_merge_mx(AttnArgs a) {
   int first = 0;
   for (int gi = 0; gi < a.gt.n; ++gi)
     if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
-  const int nc = (npages - first + kChunkPages - 1) / kChunkPages;
+  // shared-prefix chunks, then private chunks
+  const int nc = (first + kChunkPages - 1) / kChunkPages +
+                 (npages - first + kChunkPages - 1) / kChunkPages;
   const float *base = a.apart + ((size_t)b * a.nq + h) * a.nch * (D + 2);
   for (int c = t; c < nc; c += D) {
     m_s[c] = base[(size_t)c * (D + 2) + D];
@@ -831,7 +963,22 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   a.op = op;
   a.NT = p.nt;
   a.Bp = p.bp;
-  dim3 grid(p.nch, p.B);
+  if (gt.n > 0) {
+    dim3 pgrid(gt.prefix_chunks, dm.nkv, gt.colblock_start[gt.n]);
+#define KVPRM_P(KVT, D) \
+  hipLaunchKernelGGL((k_prefix_mx<KVT, D>), pgrid, dim3(64 * kPrefixWaves), 0, s, a)
+    if (dm.kvdt == 1) {
+      if (dm.d == 64) KVPRM_P(1, 64);
+      else KVPRM_P(1, 128);
+    } else {
+      if (dm.d == 64) KVPRM_P(2, 64);
+      else KVPRM_P(2, 128);
+    }
+#undef KVPRM_P
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  dim3 grid(gt.private_chunks > 0 ? gt.private_chunks : p.nch - 1, p.B);
 #define KVPRM_A(KVT, D) hipLaunchKernelGGL((k_attn_mx<KVT, D>), grid, dim3(64 * dm.nkv), 0, s, a)
   if (dm.kvdt == 1) {
     if (dm.d == 64) KVPRM_A(1, 64);

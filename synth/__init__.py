@@ -18,10 +18,11 @@ SplitMix64 counter words, evaluated in Python.
 from __future__ import annotations
 
 import ctypes
+import importlib.util
 import math
 import os
 from dataclasses import dataclass, field
-from typing import List, Optional, Sequence
+from typing import Tuple, List, Optional, Sequence
 
 import numpy as np
 
@@ -112,9 +113,21 @@ def _load_host():
     return _host
 
 
+def _preload_hip_runtime():
+    """Bind the device generator to the HIP runtime torch ships with (when installed), so that a
+    process holds one runtime and torch's memory and streams are valid in the generator."""
+    spec = importlib.util.find_spec("torch")
+    for d in (spec.submodule_search_locations or []) if spec else []:
+        rt = os.path.join(d, "lib", "libamdhip64.so")
+        if os.path.exists(rt):
+            ctypes.CDLL(rt, mode=ctypes.RTLD_GLOBAL)
+            return
+
+
 def _load_dev():
     global _dev
     if _dev is None:
+        _preload_hip_runtime()
         if not os.path.exists(DEVICE_LIB):
             raise RuntimeError(f"{DEVICE_LIB} is not built; run __graft_entry__.build()")
         lib = ctypes.CDLL(DEVICE_LIB)
@@ -296,21 +309,35 @@ def global_tensors(s: ModelShape):
     ]
 
 
-def _assign_pages(seed: int, lengths: Sequence[int], ps: int, shared_prefix_pages: int = 0):
-    """Scatter logical pages over a pool 1.25x the unique page count (Fisher-Yates)."""
+def _assign_pages(seed: int, lengths: Sequence[int], ps: int,
+                  group_start: Sequence[int] = (), group_prefix_pages: Sequence[int] = ()):
+    """Scatter logical pages over a pool 1.25x the unique page count (Fisher-Yates).
+
+    Groups (candidate ranges [group_start[g], group_start[g+1])) share their first
+    group_prefix_pages[g] pages; every other page is private. Pages are dealt in order:
+    each group's prefix, then its members' private pages."""
     B = len(lengths)
-    priv = [-(-max(L - shared_prefix_pages * ps, 0) // ps) for L in lengths]
-    unique = shared_prefix_pages + sum(priv)
+    starts = list(group_start) if group_start else [0, B]
+    pref = list(group_prefix_pages) if group_start else [0]
+    first = [0] * B
+    for gi in range(len(pref)):
+        for b in range(starts[gi], starts[gi + 1]):
+            first[b] = pref[gi]
+    priv = [-(-max(L - first[b] * ps, 0) // ps) for b, L in enumerate(lengths)]
+    unique = sum(pref) + sum(priv)
     num_pages = max(1, math.ceil(1.25 * unique))
     perm = permutation(seed, stream_id(RECIPE, R_PERM), num_pages)
     rows = []
-    nxt = shared_prefix_pages
-    for b in range(B):
-        row = [perm[i] for i in range(shared_prefix_pages)]
-        for _ in range(priv[b]):
-            row.append(perm[nxt])
-            nxt += 1
-        rows.append(row)
+    nxt = 0
+    for gi in range(len(pref)):
+        shared = [perm[nxt + i] for i in range(pref[gi])]
+        nxt += pref[gi]
+        for b in range(starts[gi], starts[gi + 1]):
+            row = list(shared)
+            for _ in range(priv[b]):
+                row.append(perm[nxt])
+                nxt += 1
+            rows.append(row)
     mp = max([len(r) for r in rows] + [1])
     rows = [r + [-1] * (mp - len(r)) for r in rows]
     return rows, num_pages
@@ -323,7 +350,8 @@ LARGE_FP8 = ModelShape(64, 8192, 64, 8, 128, 28672, kv_dtype="fp8")
 
 def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional[int] = None,
                   lengths: Optional[Sequence[int]] = None, seed: Optional[int] = None,
-                  k_std: float = 1.0) -> Workload:
+                  k_std: float = 1.0,
+                  groups: Optional[Tuple[Sequence[int], Sequence[int]]] = None) -> Workload:
     """The five workloads of the benchmark plan, plus custom ones for tests.
 
     tiny_fp32    B=4, 2 layers, H=256, 4/2 heads, d_h=64, FFN 1024, fp32, L=512 each
@@ -332,7 +360,8 @@ def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional
     beam_prefix  7B shape, B=64, one shared 16384-token prefix + private U[512, 2048]
     large_fp8    B=16, 64 layers, H=8192, 64/8 heads, FFN 28672, bf16 weights,
                  e4m3 K/V with per-(layer, page, kv-head) scales, L_b ~ U[8192, 16384]
-    custom       any shape with explicit lengths (tests)
+    custom       any shape with explicit lengths (tests); ``groups`` = (group starts, prefix
+                 lengths in tokens, multiples of the page size) makes members share prefix pages
     """
     presets = {
         "tiny_fp32": (TINY, 1000),
@@ -351,7 +380,8 @@ def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional
     klen = key(seed, stream_id(RECIPE, R_LENGTHS))
     groups_start: List[int] = []
     groups_prefix: List[int] = []
-    prefix_pages = 0
+    if groups is not None:
+        groups_start, groups_prefix = [int(x) for x in groups[0]], [int(x) for x in groups[1]]
     if lengths is not None:
         lens = [int(x) for x in lengths]
     elif name == "tiny_fp32":
@@ -363,14 +393,20 @@ def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional
     elif name == "beam_prefix":
         B = batch or 64
         prefix = 16384
-        prefix_pages = prefix // ps
         lens = [prefix + uniform_int(klen, i, 512, 2048) for i in range(B)]
         groups_start, groups_prefix = [0, B], [prefix]
     elif name == "large_fp8":
         lens = [uniform_int(klen, i, 8192, 16384) for i in range(batch or 16)]
     else:
         raise ValueError(f"workload {name!r} needs explicit lengths")
-    rows, num_pages = _assign_pages(seed, lens, ps, prefix_pages)
+    if groups_start:
+        assert groups_start[0] == 0 and groups_start[-1] == len(lens)
+        assert len(groups_prefix) == len(groups_start) - 1
+        for gi, pl in enumerate(groups_prefix):
+            assert pl % ps == 0
+            assert all(lens[b] >= pl for b in range(groups_start[gi], groups_start[gi + 1]))
+    rows, num_pages = _assign_pages(seed, lens, ps, groups_start,
+                                    [pl // ps for pl in groups_prefix])
     return Workload(name, shape, seed, lens, rows, num_pages, groups_start, groups_prefix,
                     k_std=k_std)
 

@@ -100,6 +100,9 @@ def test_score_validation_errors(handle):
         (kv.make_batch(2, FAKE, 4, FAKE, [32, 40], [0, 1], [16]), {}, kv.KVPRM_E_INVALID),
         (kv.make_batch(2, FAKE, 4, FAKE, [32, 40], [0, 2], [8]), {}, kv.KVPRM_E_INVALID),
         (kv.make_batch(2, FAKE, 4, FAKE, [16, 40], [0, 2], [32]), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(2, FAKE, 4, FAKE, None, [0, 2], [16]), {}, kv.KVPRM_E_INVALID),
+        (kv.make_batch(2, FAKE, 4, FAKE, [32, 40], [0, 1, 1, 2], [16, 0, 16]), {},
+         kv.KVPRM_E_INVALID),
         (ok_batch, dict(cache=_cache(k_ptr=0)), kv.KVPRM_E_INVALID),
         (ok_batch, dict(cache=_cache(num_pages=0)), kv.KVPRM_E_INVALID),
         (ok_batch, dict(weights=_weights(null_layer=1)), kv.KVPRM_E_INVALID),

@@ -89,6 +89,68 @@ def test_attention_parity(name, lengths, k_std):
     assert err <= 2e-5 * scale
 
 
+# Shared-prefix attention: groups whose prefix ends inside a chunk, on a chunk edge, on the
+# first page; a member whose length equals the prefix; a one-member group without a prefix;
+# a group with more (member, head) columns than one shared-prefix block holds.
+def _prefix_groups(pl_pages=(40, 0, 96, 1), sizes=(5, 1, 40, 4)):
+    starts = [0]
+    for n in sizes:
+        starts.append(starts[-1] + n)
+    pl = [p * 16 for p in pl_pages]
+    lens = []
+    for gi, n in enumerate(sizes):
+        for i in range(n):
+            extra = [0, 60, 460, 1360, 1][i] if gi == 0 else (i * 37) % 900 + (i == 1)
+            lens.append(max(pl[gi] + extra, 16 if gi == 3 else 0) + (300 if gi == 1 else 0))
+    return starts, pl, lens
+
+
+def _prefix_shape(name):
+    import dataclasses
+    if name == "bf16_d128":
+        return dataclasses.replace(synth.B7, num_layers=2)
+    if name == "fp8_d128":
+        return dataclasses.replace(synth.LARGE_FP8, num_layers=2)
+    if name == "bf16_d64":
+        return synth.ModelShape(2, 1024, 16, 4, 64, 2048)
+    if name == "fp8_d64":
+        return synth.ModelShape(2, 1024, 16, 4, 64, 2048, kv_dtype="fp8")
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("name", ["bf16_d128", "fp8_d128", "bf16_d64", "fp8_d64"])
+def test_attention_shared_prefix(name):
+    shape = _prefix_shape(name)
+    starts, pl, lens = _prefix_groups()
+    _say(f"case: shared-prefix attention {name} groups={starts} prefix={pl} B={len(lens)}")
+    w = synth.make_workload("custom", shape=shape, lengths=lens, seed=4343, groups=(starts, pl))
+    dw = DeviceWorkload(w, nan_unused_pages=True, fill_weights=False)
+    q, ks, vs = host_activations(w, 0xBCD, scale=1.0)
+    layer = 1
+    o_hint = run_attention(dw, layer, q, ks, vs, with_hint=True)
+    o_none = run_attention(dw, layer, q, ks, vs, with_hint=False)
+    cache = oin.cache_from_synth(w)
+    ref = ko.attention_layer(shape, cache, layer, w.lengths, w.page_table, q.astype(np.float64),
+                             ks.astype(np.float64), vs.astype(np.float64))
+    assert np.all(np.isfinite(o_hint))
+    scale = max(1.0, float(np.max(np.abs(ref))))
+    e_hint, e_none = np.max(np.abs(o_hint - ref)), np.max(np.abs(o_none - ref))
+    _say(f"  max|do| hint {e_hint:.3e}, no hint {e_none:.3e}")
+    assert e_hint <= 2e-5 * scale and e_none <= 2e-5 * scale
+
+
+def test_score_shared_prefix_bf16():
+    import dataclasses
+    shape = dataclasses.replace(synth.B7, num_layers=2)
+    starts, pl, lens = _prefix_groups(pl_pages=(64, 0, 33), sizes=(3, 1, 20))
+    _say(f"case: shared-prefix score groups={starts} prefix={pl}")
+    w = synth.make_workload("custom", shape=shape, lengths=lens, seed=4344, groups=(starts, pl))
+    p, z = _parity(w, 2e-3, 2e-2, with_hint=True)
+    p2, z2 = run_score(DeviceWorkload(w, nan_unused_pages=True), with_hint=False)
+    _say(f"  hint vs no hint: max|dz| = {np.max(np.abs(z - z2)):.3e}")
+    assert np.max(np.abs(z - z2)) <= 1e-3
+
+
 def _parity(w, tol_p, tol_z, **kw):
     dw = DeviceWorkload(w, nan_unused_pages=True)
     p, z = run_score(dw, **kw)
