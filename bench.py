@@ -37,7 +37,8 @@ def algorithmic_bytes(w, dw):
 
 def time_attention_step(kv, dw, h, batch, ws, n, reps):
     """Average duration of the attention step (split-L partial kernel + merge kernel) of one
-    layer, measured with HIP events on the stream the kernels are launched on."""
+    layer: `reps` back-to-back calls between two HIP events recorded on the stream the kernels
+    are launched on."""
     import torch
     w = dw.w
     s = w.shape
@@ -55,15 +56,13 @@ def time_attention_step(kv, dw, h, batch, ws, n, reps):
     for l in range(s.num_layers):
         call(l)
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(reps)]
-    for i, (a, b) in enumerate(evs):
-        a.record(stream)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for i in range(reps):  # back to back, cycling through the layers' pools
         call(i % s.num_layers)
-        b.record(stream)
+    b.record(stream)
     torch.cuda.synchronize()
-    ms = [a.elapsed_time(b) for a, b in evs]
-    return sum(ms) / len(ms)
+    return a.elapsed_time(b) / reps
 
 
 def copy_bandwidth(nbytes=4 << 30, reps=10):
@@ -86,13 +85,12 @@ def copy_bandwidth(nbytes=4 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
-def cpu_baseline(w, layers_sample):
+def cpu_baseline(w, layers_sample, min_seconds=10.0):
     """The fp64 oracle, untuned, on all candidates of the workload through its first
-    `layers_sample` layers; input generation is done before the clock starts. Scaled to
-    scores/s of the full-depth model."""
+    `layers_sample` layers, repeated until at least `min_seconds` of CPU work; input generation
+    is done before the clock starts. Scaled to scores/s of the full-depth model."""
     import dataclasses
 
-    import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import inputs as oin
@@ -109,15 +107,49 @@ def cpu_baseline(w, layers_sample):
             for i in range(-(-w.lengths[b] // s.page_size)):
                 cache.tiles(l, "k", w.page_table[b][i])
                 cache.tiles(l, "v", w.page_table[b][i])
-    t0 = time.perf_counter()
-    ko.verify_pass(sub, ro, cache, w.lengths, w.page_table)
-    dt = time.perf_counter() - t0
-    per_call = dt * s.num_layers / layers_sample
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        ko.verify_pass(sub, ro, cache, w.lengths, w.page_table)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    per_call = dt / reps * s.num_layers / layers_sample
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return {"value": w.batch / per_call, "unit": "scores/s", "cores": threads, "kind": "oracle",
             "sample": (f"{w.name}: all {w.batch} candidates through the first {layers_sample} of "
-                       f"{s.num_layers} layers in {dt:.1f} s (fp64 numpy, inputs pre-generated), "
-                       f"scaled by {s.num_layers}/{layers_sample} to one full call")}
+                       f"{s.num_layers} layers, {reps} passes in {dt:.1f} s (fp64 numpy, inputs "
+                       f"pre-generated), scaled by {s.num_layers}/{layers_sample} to one full "
+                       f"call")}
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_ragged_32k_traffic.txt")
+ATTN_SOURCES = [os.path.join(ROOT, "paper_2607_09153_amd", "csrc", f)
+                for f in ("kvprm_mfma.hip", "kvprm_internal.h")]
+
+
+def attention_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per attention step from the committed FETCH_SIZE / WRITE_SIZE summary, scaled
+    by the copy-kernel calibration recorded there; None when the summary is for another
+    workload or the attention sources have changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("workload") != workload or kv.get("source_sha256") != attention_source_hash():
+        return None
+    return float(kv["traffic_bytes_per_step"])
 
 
 def main():
@@ -128,6 +160,8 @@ def main():
     ap.add_argument("--workload", default="ragged_32k")
     ap.add_argument("--cpu-layers", type=int, default=2,
                     help="layers of the oracle sample for the CPU baseline (0 = skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU work of the oracle sample (repeated passes)")
     ap.add_argument("--attn-reps", type=int, default=56)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -174,7 +208,7 @@ def main():
     ms = dt * 1e3 / args.steps
     _log(f"timed {args.steps} steps: {ms:.3f} ms/step")
 
-    attn_ms = time_attention_step(kv, dw, h, batch, ws, n, args.attn_reps)
+    attn_ms = time_attention_step(kv, dw, h, batch, ws, n, max(args.attn_reps, 1))
     kv_per_layer = kv_bytes / w.shape.num_layers
     achieved = kv_per_layer / (attn_ms * 1e-3) / 1e9
     _log(f"attention step: {attn_ms * 1e3:.1f} us/layer, {achieved:.0f} GB/s")
@@ -205,13 +239,14 @@ def main():
         "bytes_per_call": {"kv": kv_bytes, "weights": w_bytes},
         "roofline": {"kernel": "split-L paged attention step (partials + merge), one layer",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": measured_traffic(w.name),
                      "avg_us": attn_ms * 1e3, "bytes_per_launch": kv_per_layer},
         "copy_reference_gbps": copy_gbps,
     }
     if args.cpu_layers > 0:
         _log("timing the oracle on the CPU sample ...")
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
