@@ -101,13 +101,13 @@ static kvprm_status check_batch(const kvprm_handle h, const kvprm_batch *b, cons
   if (b->batch > 256) return fail(KVPRM_E_UNSUPPORTED, "%s: at most 256 candidates per call", fn);
   if (h->dm.wdt == 1 && b->batch > 64)
     return fail(KVPRM_E_UNSUPPORTED, "%s: at most 64 candidates per call with bf16 weights", fn);
-  if (h->dm.wdt == 1 && ((h->dm.H + 63) / 64) * b->batch > kMaxSS)
-    return fail(KVPRM_E_UNSUPPORTED, "%s: hidden * batch too large", fn);
   if (!b->page_table || !b->lengths) return fail(KVPRM_E_INVALID, "%s: null page_table or lengths", fn);
   if (b->max_pages < 1) return fail(KVPRM_E_INVALID, "%s: max_pages < 1", fn);
-  // chunk slots per candidate: ceil(max_pages / 32), plus one where a shared prefix splits a chunk
-  if (b->max_pages > (kMaxChunks - 1) * kChunkPages)
-    return fail(KVPRM_E_UNSUPPORTED, "%s: max_pages above %d", fn, (kMaxChunks - 1) * kChunkPages);
+  // chunk slots per candidate: one per chunk of max_pages, plus one where a shared prefix
+  // splits a chunk (the longest chunk is 64 pages, 32 on the vector-ALU path)
+  const int max_mp = (kMaxChunks - 2) * (h->dm.kvdt == 0 ? kChunkPagesValu : 64);
+  if (b->max_pages > max_mp)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: max_pages above %d", fn, max_mp);
   const int cap = b->max_pages * h->desc.page_size;
   if (b->lengths_host)
     for (int i = 0; i < b->batch; ++i)
@@ -172,7 +172,8 @@ static kvprm_status check_ws(const kvprm_handle h, const kvprm_batch *b, void *w
 // and only for up to kMaxGroups groups; otherwise it is ignored, which changes nothing but
 // speed. With lengths on the host, the chunk grid of the private pages is sized to the longest
 // private range instead of max_pages.
-static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b) {
+static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b, const Plan &p) {
+  const int CP = 1 << p.cshift;
   GroupTable gt;
   memset(&gt, 0, sizeof gt);
   const bool share = h->dm.kvdt != 0 && b->num_groups > 0 && b->num_groups <= kMaxGroups;
@@ -186,7 +187,7 @@ static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b) {
       gt.prefix_pages[i] = pp;
       const int blocks = pp > 0 ? (members * h->dm.g + cols_per_block - 1) / cols_per_block : 0;
       gt.colblock_start[i + 1] = gt.colblock_start[i] + blocks;
-      const int ch = (pp + kChunkPages - 1) / kChunkPages;
+      const int ch = (pp + CP - 1) / CP;
       if (ch > gt.prefix_chunks) gt.prefix_chunks = ch;
     }
   }
@@ -197,7 +198,7 @@ static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b) {
       for (int k = 0; k < gt.n; ++k)
         if (i >= gt.start[k] && i < gt.start[k + 1]) first = gt.prefix_pages[k];
       const int priv = (b->lengths_host[i] + kPage - 1) / kPage - first;
-      const int ch = (priv + kChunkPages - 1) / kChunkPages;
+      const int ch = (priv + CP - 1) / CP;
       if (ch > most) most = ch;
     }
     gt.private_chunks = most;
@@ -229,7 +230,7 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   hipStream_t s = (hipStream_t)stream;
   const Plan p = make_plan(dm, b->batch, b->max_pages);
   const Workspace w = carve(dm, p, workspace);
-  const GroupTable gt = group_table(h, b);
+  const GroupTable gt = group_table(h, b, p);
   const int EB = dm.kvdt == 0 ? 4 : (dm.kvdt == 1 ? 2 : 1);
   const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * EB;
   const size_t layer_scales = (size_t)cache->num_pages * dm.nkv;
@@ -319,7 +320,7 @@ kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const 
   const Workspace w = carve(dm, p, workspace);
   HIP_TRY(launch_attention(dm, p, w, layer, cache->k_pages, cache->v_pages, cache->k_scale,
                            cache->v_scale, cache->num_pages, b->page_table, b->lengths,
-                           group_table(h, b), q, k_self, v_self, o, (hipStream_t)stream),
+                           group_table(h, b, p), q, k_self, v_self, o, (hipStream_t)stream),
           "attention");
   return ok();
 }

@@ -23,14 +23,15 @@ struct GroupTable {
   int prefix_pages[kMaxGroups];        // shared pages of each group
   int colblock_start[kMaxGroups + 1];  // shared-prefix column blocks of the groups, cumulative
   int prefix_chunks;                   // chunks of the longest group prefix
-  int private_chunks;                  // chunk grid of the private pages (0 = ceil(max_pages / 32))
+  int private_chunks;                  // chunk grid of the private pages (0 = from max_pages)
 };
 
-// Attention split: each work item covers kChunkPages pages of one (candidate, kv-head).
-constexpr int kChunkPages = 32;
-constexpr int kMaxChunks = 1024;  // chunk partials one merge handles: max_pages <= 32736
-constexpr int kMaxSS = 8192;
-constexpr int kMaxKvHeadsMx = 8;  // matrix-core attention: one wave per kv-head in a block      // sums-of-squares partials staged in LDS: (H / 64) * B
+// Attention split: each work item covers one chunk of pages of one candidate (and kv-head).
+// The matrix-core kernels take the chunk length from the plan (16, 32 or 64 pages); the
+// vector-ALU kernels use kChunkPagesValu.
+constexpr int kChunkPagesValu = 32;
+constexpr int kMaxChunks = 1024;  // chunk partials one merge handles
+constexpr int kMaxKvHeadsMx = 8;  // matrix-core attention: one wave per kv-head in a block
 constexpr int kPage = 16;
 
 // Workspace carve-up (all offsets 256-byte aligned).
@@ -57,7 +58,8 @@ struct GemvPlan {
 };
 
 struct Plan {
-  int B, max_pages, nch;      // nch = chunk slots per (candidate, q-head): ceil(max_pages / 32) + 1
+  int B, max_pages, nch;      // nch = chunk slots per (candidate, q-head), see make_plan
+  int cshift;                 // matrix-core attention chunk = 1 << cshift pages
   int nss;                    // row blocks of H that carry partial sums of squares
   int rb;                     // rows per such block
   // vector-ALU path

@@ -87,8 +87,18 @@ Plan make_plan(const Dims &dm, int B, int max_pages) {
   Plan p{};
   p.B = B;
   p.max_pages = max_pages;
-  // one more slot than chunks of max_pages: a shared prefix that ends inside a chunk adds one
-  p.nch = (max_pages + kChunkPages - 1) / kChunkPages + 1;
+  // Matrix-core attention chunk: the longest of 16, 32, 64 pages that still gives at least 160
+  // work items (of 256 compute units) for a batch that fills its page table (longer chunks
+  // stream longer page runs per wave: measured faster even with some units idle), and at most
+  // kMaxChunks - 2 chunks per candidate.
+  p.cshift = 6;
+  while (p.cshift > 4 && (long long)B * max_pages < (160LL << p.cshift)) --p.cshift;
+  while (p.cshift < 6 && (max_pages >> p.cshift) + 2 > kMaxChunks) ++p.cshift;
+  // chunk slots: chunks of max_pages plus one (a shared prefix that ends inside a chunk adds
+  // one), for whichever attention path runs
+  const int n_mx = ((max_pages + (1 << p.cshift) - 1) >> p.cshift) + 1;
+  const int n_valu = (max_pages + kChunkPagesValu - 1) / kChunkPagesValu + 1;
+  p.nch = dm.kvdt == 0 ? n_valu : n_mx;
   size_t m = 0;
   if (dm.wdt == 1) {
     p.rb = 64;
@@ -329,7 +339,7 @@ __device__ __forceinline__ float kv_elem(const void *tile, int idx) {
   return e4m3_to_f32(((const uint8_t *)tile)[idx]);
 }
 
-// One block per (chunk of kChunkPages pages, kv-head j, candidate b) over the candidate's
+// One block per (chunk of kChunkPagesValu pages, kv-head j, candidate b) over the candidate's
 // private pages [first_page, npages). Writes unnormalised partials for the g q-heads of j:
 // acc = sum_t e^{s_t - m} V_t, m = max_t s_t, l = sum_t e^{s_t - m}; an empty chunk writes
 // m = -inf, l = 0.
@@ -342,14 +352,14 @@ __global__ __launch_bounds__(256) void k_attn_valu(const void *kpool, const void
                                                    float *apart, int nq) {
   constexpr int EB = KVT == 0 ? 4 : (KVT == 1 ? 2 : 1);
   constexpr int X = 16 / EB;
-  constexpr int T = kChunkPages * kPage;  // tokens per chunk
+  constexpr int T = kChunkPagesValu * kPage;  // tokens per chunk
   constexpr int NT = 256 / D;             // token groups in the PV phase
   __shared__ float q_s[16][D];
   __shared__ float s_s[16][T];
   __shared__ float acc_s[NT][16][D];
   __shared__ float ml_s[16][2];
-  __shared__ int phys_s[kChunkPages];
-  __shared__ float ksc_s[kChunkPages], vsc_s[kChunkPages];
+  __shared__ int phys_s[kChunkPagesValu];
+  __shared__ float ksc_s[kChunkPagesValu], vsc_s[kChunkPagesValu];
 
   const int c = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
   const int L = lengths[b];
@@ -357,7 +367,7 @@ __global__ __launch_bounds__(256) void k_attn_valu(const void *kpool, const void
   int first = 0;
   for (int gi = 0; gi < gt.n; ++gi)
     if (b >= gt.start[gi] && b < gt.start[gi + 1]) first = gt.prefix_pages[gi];
-  const int p0 = first + c * kChunkPages;
+  const int p0 = first + c * kChunkPagesValu;
   float *outbase = apart + (((size_t)b * nq + (size_t)j * g) * nch + c) * (D + 2);
   const size_t hstride = (size_t)nch * (D + 2);
   if (p0 >= npages) {
@@ -367,7 +377,7 @@ __global__ __launch_bounds__(256) void k_attn_valu(const void *kpool, const void
     }
     return;
   }
-  const int p1 = min(npages, p0 + kChunkPages);
+  const int p1 = min(npages, p0 + kChunkPagesValu);
   const int tok0 = p0 * kPage;
   const int ntok = min(L, p1 * kPage) - tok0;
   for (int i = threadIdx.x; i < g * D; i += 256) {
@@ -495,7 +505,7 @@ __global__ __launch_bounds__(D) void k_merge(const float *apart, int nch, GroupT
   int first = 0;
   for (int gi = 0; gi < gt.n; ++gi)
     if (b >= gt.start[gi] && b < gt.start[gi + 1]) first = gt.prefix_pages[gi];
-  const int nc = (npages - first + kChunkPages - 1) / kChunkPages;
+  const int nc = (npages - first + kChunkPagesValu - 1) / kChunkPagesValu;
   const float *pb = apart + ((size_t)b * nq + h) * nch * (D + 2);
   float mx = s_self;
   for (int c = 0; c < nc; ++c) mx = fmaxf(mx, pb[(size_t)c * (D + 2) + D]);

@@ -57,6 +57,20 @@ __device__ __forceinline__ void split_hi_lo(float x, uint32_t &hi, uint32_t &lo)
 
 __device__ __forceinline__ uint32_t pack2(uint32_t a, uint32_t b) { return a | (b << 16); }
 
+// Two fp32 values -> packed bf16 pairs hi (RNE) and lo = RNE(x - hi) (the hardware pack-convert,
+// one instruction per pair): hi + lo carries 16 significant bits of each value.
+__device__ __forceinline__ void split2(float x0, float x1, uint32_t &hi, uint32_t &lo) {
+  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+  typedef float f32x2v __attribute__((ext_vector_type(2)));
+  const f32x2v xv = {x0, x1};
+  hi = __builtin_bit_cast(uint32_t, __builtin_convertvector(xv, bf16x2v));
+  const f32x2v rv = {x0 - __uint_as_float(hi << 16), x1 - __uint_as_float(hi & 0xFFFF0000u)};
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(rv, bf16x2v));
+}
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
 __device__ __forceinline__ float ld_w(const void *p, size_t i, int wdt) {
   return wdt ? __uint_as_float((uint32_t)((const uint16_t *)p)[i] << 16) : ((const float *)p)[i];
 }
@@ -254,60 +268,78 @@ __global__ __launch_bounds__(256) void k_gemv_mx(GemvArgs a) {
   }
 }
 
-// Sum of the k-partials of output (r, b): contiguous, read with 16-byte loads, added in k order.
-__device__ __forceinline__ float ksum(const float *part, int ksp, int ksplit, int r, int B, int b) {
-  const float4 *pp = (const float4 *)(part + ((size_t)r * B + b) * ksp);
+// Sum of the k-partials of output row idx = r * B + b: contiguous, read with 16-byte loads that
+// are all issued before the first add (up to 32 partials), added in k order.
+__device__ __forceinline__ float ksum(const float *__restrict__ part, int ksp, int ksplit,
+                                      size_t idx) {
+  const float4 *pp = (const float4 *)(part + idx * ksp);
+  const int n4 = ksp >> 2;
+  float4 v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = i < n4 ? pp[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   float s = 0.f;
-  for (int k4 = 0; k4 < (ksp >> 2); ++k4) {
-    const float4 v = pp[k4];
-    const int k = 4 * k4;
-    s += v.x;
-    if (k + 1 < ksplit) s += v.y;
-    if (k + 2 < ksplit) s += v.z;
-    if (k + 3 < ksplit) s += v.w;
-  }
+  auto add4 = [&](const float4 &w, int k) {
+    if (k < ksplit) s += w.x;
+    if (k + 1 < ksplit) s += w.y;
+    if (k + 2 < ksplit) s += w.z;
+    if (k + 3 < ksplit) s += w.w;
+  };
+#pragma unroll
+  for (int i = 0; i < 8; ++i) add4(v[i], 4 * i);
+  for (int i = 8; i < n4; ++i) add4(pp[i], 4 * i);
   return s;
 }
 
-// r_b = 1 / sqrt(mean(x_b^2) + eps) from the per-row-block sums of squares, into inv_s[b].
-// The nss * B partial sums are staged in LDS (ss_s) with one round of parallel loads.
-__device__ __forceinline__ void load_inv_rms(const float *ss, int nss, int B, int H, float eps,
-                                             float *ss_s, float *inv_s) {
-  for (int i = threadIdx.x; i < nss * B; i += blockDim.x) ss_s[i] = ss[i];
-  __syncthreads();
-  for (int b = threadIdx.x; b < B; b += blockDim.x) {
-    float s = 0.f;
-    for (int i = 0; i < nss; ++i) s += ss_s[i * B + b];
-    inv_s[b] = 1.0f / sqrtf(s / (float)H + eps);
+// r_b = 1 / sqrt(mean(x_b^2) + eps) of this lane's candidate b, from the per-row-block sums of
+// squares ss[i][b], computed by the whole wave without LDS or a barrier: with Bq = B rounded up
+// to a power of two, lane l sums rows i = l / Bq, l / Bq + 64 / Bq, ... of candidate l % Bq, a
+// butterfly over the lanes of equal l % Bq completes the sums (identical in every lane and
+// block), and each lane fetches its own candidate's.
+__device__ __forceinline__ float wave_inv_rms(const float *__restrict__ ss, int nss, int B, int b,
+                                              int H, float eps) {
+  const int lane = threadIdx.x & 63;
+  int Bq = 1;
+  while (Bq < B) Bq <<= 1;
+  const int P = 64 / Bq;
+  const int bl = lane & (Bq - 1), part = lane / Bq;
+  float v = 0.f;
+  if (bl < B) {
+#pragma unroll 8
+    for (int i = part; i < nss; i += P) v += ss[(size_t)i * B + bl];
   }
-  __syncthreads();
+  for (int off = Bq; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
+  const float tot = __shfl(v, b, 64);
+  return 1.0f / sqrtf(tot / (float)H + eps);
 }
 
 // q, k_self, v_self from the QKV partials: scale by r_b (the attention RMSNorm, applied after
 // the product) and rotate q and k pairs (i, i + d/2) with the cos/sin table of position L_b.
-// One thread per (pair, candidate).
-__global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *part, int ksp, int ksplit,
-                                                    const float *ss, int nss, int H, float eps,
-                                                    int B, int nq, int nkv, int d,
-                                                    const float *rope, float *q, float *ks,
-                                                    float *vs) {
-  __shared__ float inv_s[64];
-  __shared__ float ss_s[kMaxSS];
-  load_inv_rms(ss, nss, B, H, eps, ss_s, inv_s);
+// One thread per (pair, candidate); every load is issued before the first use.
+__global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ part, int ksp,
+                                                    int ksplit, const float *__restrict__ ss,
+                                                    int nss, int H, float eps, int B, int nq,
+                                                    int nkv, int d, const float *__restrict__ rope,
+                                                    float *__restrict__ q, float *__restrict__ ks,
+                                                    float *__restrict__ vs) {
   const int hd = d / 2;
   const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= (nq + 2 * nkv) * hd * B) return;
-  const int pr = e / B, b = e - pr * B;
+  const bool act = e < (nq + 2 * nkv) * hd * B;
+  const int ec = act ? e : 0;
+  const int pr = ec / B, b = ec - pr * B;
   const int head = pr / hd, i = pr - head * hd;
   const int r = head * d + i;
-  const float inv = inv_s[b];
-  const float x1 = ksum(part, ksp, ksplit, r, B, b) * inv;
-  const float x2 = ksum(part, ksp, ksplit, r + hd, B, b) * inv;
-  float o1 = x1, o2 = x2;
-  if (head < nq + nkv) {
-    const float cs = rope[((size_t)b * hd + i) * 2], sn = rope[((size_t)b * hd + i) * 2 + 1];
-    o1 = x1 * cs - x2 * sn;
-    o2 = x2 * cs + x1 * sn;
+  const float x1 = ksum(part, ksp, ksplit, (size_t)r * B + b);
+  const float x2 = ksum(part, ksp, ksplit, (size_t)(r + hd) * B + b);
+  const bool rot = head < nq + nkv;
+  const float cs = rot ? rope[((size_t)b * hd + i) * 2] : 1.f;
+  const float sn = rot ? rope[((size_t)b * hd + i) * 2 + 1] : 0.f;
+  const float inv = wave_inv_rms(ss, nss, B, b, H, eps);
+  if (!act) return;
+  const float y1 = x1 * inv, y2 = x2 * inv;
+  float o1 = y1, o2 = y2;
+  if (rot) {
+    o1 = y1 * cs - y2 * sn;
+    o2 = y2 * cs + y1 * sn;
   }
   float *dst;
   if (head < nq)
@@ -322,18 +354,23 @@ __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *part, int ksp, 
 
 // Residual add x += sum_k partials for a block of 64 rows, the rows' sums of squares per
 // candidate (ss[block][b], fixed order), and the next GEMV's operand x * gamma_next.
-__global__ __launch_bounds__(256) void k_resid_mx(float *x, const float *part, int ksp, int ksplit,
-                                                  float *ss, int B, int H, const void *gamma_next,
-                                                  int wdt, uint16_t *op, int NT, int Bp) {
+// 512 threads: one (row, candidate) element each for B <= 8.
+__global__ __launch_bounds__(512) void k_resid_mx(float *__restrict__ x,
+                                                  const float *__restrict__ part, int ksp,
+                                                  int ksplit, float *__restrict__ ss, int B, int H,
+                                                  const void *__restrict__ gamma_next, int wdt,
+                                                  uint16_t *__restrict__ op, int NT, int Bp) {
   __shared__ float sq_s[64][65];
   const int r0 = blockIdx.x * 64;
   const int nr = min(64, H - r0);
-  for (int e = threadIdx.x; e < nr * B; e += 256) {
+  for (int e = threadIdx.x; e < nr * B; e += 512) {
     const int rl = e / B, b = e - rl * B, r = r0 + rl;
-    const float xv = x[(size_t)b * H + r] + ksum(part, ksp, ksplit, r, B, b);
+    const float xo = x[(size_t)b * H + r];
+    const float g = gamma_next ? ld_w(gamma_next, r, wdt) : 0.f;
+    const float xv = xo + ksum(part, ksp, ksplit, (size_t)r * B + b);
     x[(size_t)b * H + r] = xv;
     sq_s[rl][b] = xv * xv;
-    if (gamma_next) store_operand(op, NT, Bp, r, b, xv * ld_w(gamma_next, r, wdt));
+    if (gamma_next) store_operand(op, NT, Bp, r, b, xv * g);
   }
   __syncthreads();
   if (threadIdx.x < B) {
@@ -345,18 +382,19 @@ __global__ __launch_bounds__(256) void k_resid_mx(float *x, const float *part, i
 
 // h = silu(r_b g) * (r_b u) for gate rows f and up rows F + f (the FFN RMSNorm applied after
 // the product), written as the down projection's operand. One thread per (feature, candidate).
-__global__ __launch_bounds__(256) void k_swiglu_mx(const float *part, int ksp, int ksplit,
-                                                   const float *ss, int nss, int H, float eps,
-                                                   int B, int F, uint16_t *op, int NT, int Bp) {
-  __shared__ float inv_s[64];
-  __shared__ float ss_s[kMaxSS];
-  load_inv_rms(ss, nss, B, H, eps, ss_s, inv_s);
+__global__ __launch_bounds__(256) void k_swiglu_mx(const float *__restrict__ part, int ksp,
+                                                   int ksplit, const float *__restrict__ ss,
+                                                   int nss, int H, float eps, int B, int F,
+                                                   uint16_t *__restrict__ op, int NT, int Bp) {
   const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= F * B) return;
-  const int f = e / B, b = e - f * B;
-  const float inv = inv_s[b];
-  const float gv = ksum(part, ksp, ksplit, f, B, b) * inv;
-  const float uv = ksum(part, ksp, ksplit, F + f, B, b) * inv;
+  const bool act = e < F * B;
+  const int ec = act ? e : 0;
+  const int f = ec / B, b = ec - f * B;
+  const float g = ksum(part, ksp, ksplit, (size_t)f * B + b);
+  const float u = ksum(part, ksp, ksplit, (size_t)(F + f) * B + b);
+  const float inv = wave_inv_rms(ss, nss, B, b, H, eps);
+  if (!act) return;
+  const float gv = g * inv, uv = u * inv;
   store_operand(op, NT, Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
 }
 
@@ -486,26 +524,29 @@ __device__ __forceinline__ void load_query_ops(const float *qr, bool present, in
   }
 }
 
-// One online-softmax step over a page pair for the 16 columns of a wave: S = K Q^T (lane holds
-// tokens 4c + i of pages A and B for column lane % 16), running max / sum, then
-// O^T += V^T P^T with P split hi + lo. ok[] marks valid tokens (masked tokens get p = 0 and
-// their V entries are zeroed, since their slots may hold NaN). vsa / vsb scale P for fp8 V.
+// One online-softmax step over a page pair for the 16 columns (queries) of a wave:
+// S = K Q^T (lane holds tokens 4c + i of pages A and B for column lane % 16; q0, q1, q2 = the
+// query's hi, mid, lo bf16 terms, three MFMAs per 32-dim block), running max and sum, then
+// O^T += V^T P^T with P split hi + lo (two MFMAs per 16-dim block). Scores arrive scaled by
+// log2(e) (sca, scb include it), so the running max m_run is in log2 units and p = 2^(s - m).
+// ok[] marks valid tokens: masked tokens get p = 0 and their V entries are zeroed, since their
+// slots may hold NaN. vsa / vsb scale P for fp8 V.
 template <int D>
 __device__ __forceinline__ void online_step(const uint4 *KA, const uint4 *KB, const uint2 *VA,
-                                            const uint2 *VB, const uint4 *qhi, const uint4 *qmd,
-                                            const uint4 *qlo, const bool *ok, float sca, float scb,
+                                            const uint2 *VB, const uint4 *q0, const uint4 *q1,
+                                            const uint4 *q2, const bool *ok, float sca, float scb,
                                             float vsa, float vsb, float &m_run, float &l_run,
                                             floatx4 *acc) {
   constexpr int NKB = D / 32, NDB = D / 16;
   floatx4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int kk = 0; kk < NKB; ++kk) {
-    sa = mfma16(KA[kk], qhi[kk], sa);
-    sa = mfma16(KA[kk], qmd[kk], sa);
-    sa = mfma16(KA[kk], qlo[kk], sa);
-    sb = mfma16(KB[kk], qhi[kk], sb);
-    sb = mfma16(KB[kk], qmd[kk], sb);
-    sb = mfma16(KB[kk], qlo[kk], sb);
+    sa = mfma16(KA[kk], q0[kk], sa);
+    sa = mfma16(KA[kk], q1[kk], sa);
+    sa = mfma16(KA[kk], q2[kk], sa);
+    sb = mfma16(KB[kk], q0[kk], sb);
+    sb = mfma16(KB[kk], q1[kk], sb);
+    sb = mfma16(KB[kk], q2[kk], sb);
   }
   float sv[8];
 #pragma unroll
@@ -519,12 +560,12 @@ __device__ __forceinline__ void online_step(const uint4 *KA, const uint4 *KB, co
   mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
   const float m_new = fmaxf(m_run, mx);  // finite once any valid token has been seen
-  const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
+  const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
   m_run = m_new;
   float pv[8], psum = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    pv[i] = ok[i] ? expf(sv[i] - m_new) : 0.f;
+    pv[i] = ok[i] ? __builtin_amdgcn_exp2f(sv[i] - m_new) : 0.f;
     psum += pv[i];
   }
   l_run = l_run * alpha + psum;
@@ -540,13 +581,11 @@ __device__ __forceinline__ void online_step(const uint4 *KA, const uint4 *KB, co
     pv[i] *= vsa;
     pv[4 + i] *= vsb;
   }
-  uint32_t ph[8], pl[8];
+  uint32_t ph[4], pl[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) split_hi_lo(pv[i], ph[i], pl[i]);
-  const uint4 Phi = make_uint4(pack2(ph[0], ph[1]), pack2(ph[2], ph[3]), pack2(ph[4], ph[5]),
-                               pack2(ph[6], ph[7]));
-  const uint4 Plo = make_uint4(pack2(pl[0], pl[1]), pack2(pl[2], pl[3]), pack2(pl[4], pl[5]),
-                               pack2(pl[6], pl[7]));
+  for (int i = 0; i < 4; ++i) split2(pv[2 * i], pv[2 * i + 1], ph[i], pl[i]);
+  const uint4 Phi = make_uint4(ph[0], ph[1], ph[2], ph[3]);
+  const uint4 Plo = make_uint4(pl[0], pl[1], pl[2], pl[3]);
   const uint32_t ma0 = (ok[0] ? 0xFFFFu : 0u) | (ok[1] ? 0xFFFF0000u : 0u);
   const uint32_t ma1 = (ok[2] ? 0xFFFFu : 0u) | (ok[3] ? 0xFFFF0000u : 0u);
   const uint32_t mb0 = (ok[4] ? 0xFFFFu : 0u) | (ok[5] ? 0xFFFF0000u : 0u);
@@ -560,7 +599,7 @@ __device__ __forceinline__ void online_step(const uint4 *KA, const uint4 *KB, co
 }
 
 // Stores a wave's partial for column n (acc rows d = 16 nb + 4 cq + i; 64 bytes per head and
-// 16-dim block across the 4 lanes of the column) and its m, l.
+// 16-dim block across the 4 lanes of the column) and its m (given in log2 units), l.
 template <int D>
 __device__ __forceinline__ void store_partial(float *hb, int cq, const floatx4 *acc, float m_run,
                                               float l_run) {
@@ -568,7 +607,7 @@ __device__ __forceinline__ void store_partial(float *hb, int cq, const floatx4 *
 #pragma unroll
   for (int nb = 0; nb < NDB; ++nb)
     *(float4 *)(hb + nb * 16 + 4 * cq) = make_float4(acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3]);
-  if (cq == 0) *(float2 *)(hb + D) = make_float2(m_run, l_run);
+  if (cq == 0) *(float2 *)(hb + D) = make_float2(m_run * kLn2, l_run);  // m back to natural units
 }
 
 struct AttnArgs {
@@ -581,6 +620,7 @@ struct AttnArgs {
   GroupTable gt;
   int nch;
   const float *q, *kself, *vself;
+  int cshift;     // chunk = 1 << cshift pages
   float *apart;   // [B][nq][nch][D + 2]: per chunk the acc row, then m, then l; a candidate's
                   // shared-prefix chunks come first, its private chunks after them
   float *o;       // [B][nq][D] fp32 output (may be null)
@@ -588,7 +628,7 @@ struct AttnArgs {
   int NT, Bp;
 };
 
-// One block per (chunk of kChunkPages pages, candidate b) over the candidate's private pages,
+// One block per (chunk of pages, candidate b) over the candidate's private pages,
 // one wave per kv-head j, so the n_kv tiles of a page (contiguous in the pool) are read together.
 // Each wave walks the chunk two pages (32 tokens) at a time: S = K Q^T on the matrix cores
 // (A = the K tile, 16 tokens x 32 dims; B = the g query heads of j as columns, in three bf16
@@ -611,10 +651,11 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   int first = 0;
   for (int gi = 0; gi < a.gt.n; ++gi)
     if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
-  const int ncp = (first + kChunkPages - 1) / kChunkPages;  // this candidate's prefix chunks
-  const int p0 = first + c * kChunkPages;
+  const int CP = 1 << a.cshift;
+  const int ncp = (first + CP - 1) >> a.cshift;  // this candidate's prefix chunks
+  const int p0 = first + c * CP;
   if (p0 >= npages) return;
-  const int np = min(npages, p0 + kChunkPages) - p0;
+  const int np = min(npages, p0 + CP) - p0;
   const int lane = threadIdx.x & 63;
   const int n = lane & 15, cq = lane >> 4;
   // each wave reads the chunk's page ids itself into lane registers (lane i holds page i and,
@@ -638,10 +679,10 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   PairRaw<D> r0, r1;
   load_pair(0, r0);  // in flight while the queries are prepared
 
-  uint4 qhi[NKB], qmd[NKB], qlo[NKB];
+  uint4 q0[NKB], q1[NKB], q2[NKB];
   load_query_ops<KVT, D>(a.q + ((size_t)b * nq + (size_t)j * g + (n < g ? n : 0)) * D, n < g, cq,
-                         qhi, qmd, qlo);
-  const float rs = 1.0f / sqrtf((float)D);
+                         q0, q1, q2);
+  const float rs = kLog2e / sqrtf((float)D);  // scores in log2 units
   float m_run = -INFINITY, l_run = 0.f;
   floatx4 acc[NDB];
 #pragma unroll
@@ -665,16 +706,22 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
     const float scb = (KVT == 2) ? __shfl(ksc_l, lbc, 64) * rs : rs;
     const float vsa = (KVT == 2) ? __shfl(vsc_l, la, 64) : 1.f;
     const float vsb = (KVT == 2) ? __shfl(vsc_l, lbc, 64) : 1.f;
-    online_step<D>(KA, KB, VA, VB, qhi, qmd, qlo, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
+    online_step<D>(KA, KB, VA, VB, q0, q1, q2, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
   };
   // a branch-free loop over an even number of pairs: the pair past the end (if any) is fully
   // masked, and loads past the end repeat the last page (an L2 hit), so that wait counts never
   // cover the loads in flight for the next pair
+  // (scheduling barriers keep each pair's loads ahead of the previous pair's arithmetic, so that
+  // the waits inside a compute step cover only its own, older loads)
   for (int pp = 0; pp < npairs; pp += 2) {
     load_pair(pp + 1, r1);
+    __builtin_amdgcn_sched_barrier(0);
     compute_pair(pp, r0);
+    __builtin_amdgcn_sched_barrier(0);
     load_pair(pp + 2, r0);
+    __builtin_amdgcn_sched_barrier(0);
     compute_pair(pp + 1, r1);
+    __builtin_amdgcn_sched_barrier(0);
   }
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
@@ -702,9 +749,10 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
   const int cb = blockIdx.z - a.gt.colblock_start[grp];
   const int m0 = a.gt.start[grp], members = a.gt.start[grp + 1] - m0;
   const int ppages = a.gt.prefix_pages[grp];
-  const int p0 = c * kChunkPages;
+  const int CP = 1 << a.cshift;
+  const int p0 = c * CP;
   if (p0 >= ppages) return;
-  const int np = min(ppages, p0 + kChunkPages) - p0;
+  const int np = min(ppages, p0 + CP) - p0;
   const int npairs = (np + 1) >> 1;
   const int nkv = a.nkv, g = a.g, nq = a.nq;
   constexpr int nthr = 64 * kPrefixWaves;
@@ -751,7 +799,7 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
                          qmd, qlo);
   stash(0);
   __syncthreads();
-  const float rs = 1.0f / sqrtf((float)D);
+  const float rs = kLog2e / sqrtf((float)D);  // scores in log2 units
   float m_run = -INFINITY, l_run = 0.f;
   floatx4 acc[NDB];
 #pragma unroll
@@ -791,14 +839,20 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
 // Log-sum-exp merge of the chunk partials of one (candidate b, q-head h) with the token's own
 // key/value: m = max(s_self, m_c),
 //   o = (e^{s_self - m} v_self + sum_c e^{m_c - m} acc_c) / (e^{s_self - m} + sum_c e^{m_c - m} l_c).
-// One block of D threads per (b, h), thread d owning output dimension d: the chunk maxima and
-// sums are staged in LDS, then each chunk's acc row is read coalesced by the block. Writes o
-// (fp32) and/or the operand of the output projection.
+// One block of 512 threads per (b, h): thread (s, d) owns output dimension d for the chunks
+// c = s, s + S, ... (S = 512 / D subsets). Every load is issued at entry (the first 16 chunk
+// rows of each subset go to registers), so the merge costs about one memory round trip; the
+// subsets are added in a fixed order. Writes o (fp32) and/or the output projection's operand.
 template <int D>
-__global__ __launch_bounds__(D) void k_merge_mx(AttnArgs a) {
+__global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
+  constexpr int S = 512 / D;
+  constexpr int R = 16;
   __shared__ float m_s[kMaxChunks], f_s[kMaxChunks];
-  __shared__ float red[4];
+  __shared__ float red[3][8];
+  __shared__ float sub_s[S][D];
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
+  const int sub = t / D, dd = t - sub * D;
   const int j = h / a.g;
   const int L = a.lengths[b];
   const int npages = (L + kPage - 1) / kPage;
@@ -806,49 +860,70 @@ __global__ __launch_bounds__(D) void k_merge_mx(AttnArgs a) {
   for (int gi = 0; gi < a.gt.n; ++gi)
     if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
   // shared-prefix chunks, then private chunks
-  const int nc = (first + kChunkPages - 1) / kChunkPages +
-                 (npages - first + kChunkPages - 1) / kChunkPages;
+  const int CP = 1 << a.cshift;
+  const int nc = ((first + CP - 1) >> a.cshift) + ((npages - first + CP - 1) >> a.cshift);
   const float *base = a.apart + ((size_t)b * a.nq + h) * a.nch * (D + 2);
-  for (int c = t; c < nc; c += D) {
-    m_s[c] = base[(size_t)c * (D + 2) + D];
-    f_s[c] = base[(size_t)c * (D + 2) + D + 1];  // l_c for now
+  float rv[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int c = sub + S * i;
+    rv[i] = c < nc ? base[(size_t)c * (D + 2) + dd] : 0.f;
   }
-  // own key: s_self = q . k_self / sqrt(D)
-  float dot = wsum(a.q[((size_t)b * a.nq + h) * D + t] * a.kself[((size_t)b * a.nkv + j) * D + t]);
-  if (D > 64) {
-    if ((t & 63) == 0) red[t >> 6] = dot;
-    __syncthreads();
-    dot = red[0] + red[1];
+  float mx = -INFINITY;
+  for (int c = t; c < nc; c += 512) {
+    const float m = base[(size_t)c * (D + 2) + D];
+    m_s[c] = m;
+    f_s[c] = base[(size_t)c * (D + 2) + D + 1];  // l_c for now
+    mx = fmaxf(mx, m);
+  }
+  const float vsv = a.vself[((size_t)b * a.nkv + j) * D + dd];
+  // own key: s_self = q . k_self / sqrt(D), from the first D threads
+  float dot = t < D ? a.q[((size_t)b * a.nq + h) * D + t] * a.kself[((size_t)b * a.nkv + j) * D + t]
+                    : 0.f;
+  dot = wsum(dot);
+  mx = wmax(mx);
+  if (lane == 0) {
+    red[0][wave] = dot;
+    red[1][wave] = mx;
   }
   __syncthreads();
-  const float s_self = dot * (1.0f / sqrtf((float)D));
+  float s_self = 0.f;
+#pragma unroll
+  for (int w = 0; w < D / 64; ++w) s_self += red[0][w];
+  s_self *= 1.0f / sqrtf((float)D);
   float M = s_self;
-  for (int c = 0; c < nc; ++c) M = fmaxf(M, m_s[c]);
-  float lsum = 0.f;
-  for (int c = t; c < nc; c += D) {
+#pragma unroll
+  for (int w = 0; w < 8; ++w) M = fmaxf(M, red[1][w]);
+  float ls = 0.f;
+  for (int c = t; c < nc; c += 512) {
     const float f = expf(m_s[c] - M);
-    lsum += f * f_s[c];
+    ls += f * f_s[c];
     f_s[c] = f;
   }
-  lsum = wsum(lsum);
-  if (D > 64) {
-    __syncthreads();
-    if ((t & 63) == 0) red[2 + (t >> 6)] = lsum;
-    __syncthreads();
-    lsum = red[2] + red[3];
-  }
+  ls = wsum(ls);
+  if (lane == 0) red[2][wave] = ls;
   __syncthreads();
+  float lsum = 0.f;
+#pragma unroll
+  for (int w = 0; w < 8; ++w) lsum += red[2][w];
   float acc = 0.f;
-  const float *col = base + t;
-#pragma unroll 8
-  for (int c = 0; c < nc; ++c) acc += f_s[c] * col[(size_t)c * (D + 2)];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int c = sub + S * i;
+    if (c < nc) acc += f_s[c] * rv[i];
+  }
+  for (int c = sub + S * R; c < nc; c += S) acc += f_s[c] * base[(size_t)c * (D + 2) + dd];
+  sub_s[sub][dd] = acc;
+  __syncthreads();
+  if (sub != 0) return;
+  float tot = 0.f;
+#pragma unroll
+  for (int k = 0; k < S; ++k) tot += sub_s[k][dd];
   const float es = expf(s_self - M);
-  const float ov = (acc + es * a.vself[((size_t)b * a.nkv + j) * D + t]) / (lsum + es);
-  if (a.o) a.o[((size_t)b * a.nq + h) * D + t] = ov;
-  if (a.op) store_operand(a.op, a.NT, a.Bp, h * D + t, b, ov);
+  const float ov = (tot + es * vsv) / (lsum + es);
+  if (a.o) a.o[((size_t)b * a.nq + h) * D + dd] = ov;
+  if (a.op) store_operand(a.op, a.NT, a.Bp, h * D + dd, b, ov);
 }
-
-// ------------------------------------------------------------------------------- launchers
 
 hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *ev,
                           const void *gamma0, const int32_t *lengths, hipStream_t s) {
@@ -912,7 +987,7 @@ hipError_t launch_oproj_mx(const Dims &dm, const Plan &p, const Workspace &w, co
                            const void *gamma_ffn, hipStream_t s) {
   hipError_t e = launch_gemv_mx(p, p.g_o, wo, dm.H, nullptr, 0, nullptr, 0, w.opO, w.part, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_resid_mx, dim3(p.nss), dim3(256), 0, s, w.x, w.part, ksp_of(p.g_o),
+  hipLaunchKernelGGL(k_resid_mx, dim3(p.nss), dim3(512), 0, s, w.x, w.part, ksp_of(p.g_o),
                      p.g_o.ksplit, w.ss, p.B, dm.H, gamma_ffn, dm.wdt, w.opA, p.nt, p.bp);
   return hipGetLastError();
 }
@@ -931,7 +1006,7 @@ hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, con
                           const void *gamma_next, hipStream_t s) {
   hipError_t e = launch_gemv_mx(p, p.g_d, wd, dm.H, nullptr, 0, nullptr, 0, w.opD, w.part, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_resid_mx, dim3(p.nss), dim3(256), 0, s, w.x, w.part, ksp_of(p.g_d),
+  hipLaunchKernelGGL(k_resid_mx, dim3(p.nss), dim3(512), 0, s, w.x, w.part, ksp_of(p.g_d),
                      p.g_d.ksplit, w.ss, p.B, dm.H, gamma_next, dm.wdt, w.opA, p.nt, p.bp);
   return hipGetLastError();
 }
@@ -955,6 +1030,7 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   a.lengths = lengths;
   a.gt = gt;
   a.nch = p.nch;
+  a.cshift = p.cshift;
   a.q = q;
   a.kself = kself;
   a.vself = vself;
@@ -991,9 +1067,9 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (dm.d == 64)
-    hipLaunchKernelGGL(k_merge_mx<64>, dim3(p.B, dm.nq), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_merge_mx<64>, dim3(p.B, dm.nq), dim3(512), 0, s, a);
   else
-    hipLaunchKernelGGL(k_merge_mx<128>, dim3(p.B, dm.nq), dim3(128), 0, s, a);
+    hipLaunchKernelGGL(k_merge_mx<128>, dim3(p.B, dm.nq), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

@@ -56,6 +56,14 @@ ATTN_CASES = [
     ("b7_bf16", [4096, 0, 1, 17, 5000, 9000], 1.0),
     ("b7_bf16_spiky", [3000, 33, 16], 30.0),
     ("fp8", [2049, 0, 31, 8192], 1.0),
+    # 16 q-heads per kv-head
+    ("g16_bf16", [1000, 0, 17, 4100], 1.0),
+    ("g16_fp8", [33, 2500], 1.0),
+    # batches large enough for 32-page and 64-page attention chunks (the plan picks the chunk
+    # from batch x max_pages)
+    ("b7_bf16", [16384, 300, 17, 9000, 0, 12000], 1.0),
+    ("b7_bf16", [32768, 1, 20000, 33, 5000, 31000], 1.0),
+    ("fp8", [32768, 16, 17000, 4000, 29999, 2], 1.0),
 ]
 
 
@@ -67,6 +75,10 @@ def _shape(name):
         return dataclasses.replace(synth.B7, num_layers=2)
     if name == "fp8":
         return dataclasses.replace(synth.LARGE_FP8, num_layers=2)
+    if name == "g16_bf16":
+        return synth.ModelShape(2, 1024, 16, 1, 64, 2048)
+    if name == "g16_fp8":
+        return synth.ModelShape(2, 2048, 32, 2, 128, 2048, kv_dtype="fp8")
     raise KeyError(name)
 
 
