@@ -173,25 +173,21 @@ struct GemvArgs {
 // part[row][b][ks] = sum over k-slice ks of W[row][k] u_b[k], W in the packed tile layout
 // (1 KiB per 32-input block and 16-row tile, input block major, in A-operand lane order): one
 // load instruction reads 1 KiB, and the waves working on one k-slice sweep a contiguous region
-// together, input block by input block. The block first copies its
-// k-slice of the operand (NT column tiles) into LDS; per batch of U k-blocks the MT * U weight
-// loads are issued before the MT * NT * U MFMAs. The hi and lo halves of each candidate are
-// added before the partial is stored.
-template <int MT, int NT, int U>
-__global__ __launch_bounds__(256) void k_gemv_mx(GemvArgs a) {
+// together, input block by input block. Each wave owns MT row tiles. The weights stream in
+// batches of U input blocks, double buffered: the next batch's loads are in flight while the
+// current batch's MT * NT * U MFMAs run, and the first batch is issued before the block copies
+// its k-slice of the operand (NT column tiles) into LDS. The hi and lo halves of each candidate
+// are added before the partial is stored.
+template <int MT, int NT, int U, int WPB, bool DIRECT>
+__global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
   extern __shared__ uint4 act_s[];  // the block's k-slice of the operand: nkb * NT * 64 entries
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ks = blockIdx.y;
   const int k0 = ks * a.kslice;
   const int nkb = min(a.kslice, a.K - k0) >> 5;
-  const int tile0 = (blockIdx.x * 4 + wave) * MT;
+  const int tile0 = (blockIdx.x * WPB + wave) * MT;
   const int B = a.B;
-  {
-    const uint4 *src = a.act + (size_t)(k0 >> 5) * NT * 64;
-    for (int i = threadIdx.x; i < nkb * NT * 64; i += 256) act_s[i] = src[i];
-  }
-  __syncthreads();
-  if (tile0 * 16 >= a.rows) return;
+  const bool active = tile0 * 16 < a.rows;
   const uint4 *wt[MT];
   size_t kstride[MT];  // uint4 entries between consecutive input blocks of a tile
   bool valid[MT];
@@ -206,21 +202,20 @@ __global__ __launch_bounds__(256) void k_gemv_mx(GemvArgs a) {
     kstride[m] = ntiles * 64;
     wt[m] = (const uint4 *)a.w[seg] + ((size_t)(k0 >> 5) * ntiles + lt) * 64 + lane;
   }
+  // Rows of an absent tile read tile 0 of their segment and are never stored.
+  auto load_batch = [&](int kb, uint4 (&av)[U][MT]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) av[u][m] = wt[m][(size_t)(kb + u) * kstride[m]];
+  };
+  const uint4 *ap = (DIRECT ? a.act + (size_t)(k0 >> 5) * NT * 64 : act_s) + lane;
   floatx4 acc[MT][NT];
 #pragma unroll
   for (int m = 0; m < MT; ++m)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const uint4 *ap = act_s + lane;
-  // batches of U k-blocks: the weight loads of a batch are all issued before its MFMAs; the
-  // operand comes from LDS. Rows of an absent tile read tile 0 and are never stored.
-  int kb = 0;
-  for (; kb + U <= nkb; kb += U) {
-    uint4 av[U][MT];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int m = 0; m < MT; ++m) av[u][m] = wt[m][(size_t)(kb + u) * kstride[m]];
+  auto mma_batch = [&](int kb, const uint4 (&av)[U][MT]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       uint4 bv[NT];
@@ -231,8 +226,31 @@ __global__ __launch_bounds__(256) void k_gemv_mx(GemvArgs a) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av[u][m], bv[t], acc[m][t]);
     }
+  };
+  const int nbat = nkb / U;
+  uint4 a0[U][MT], a1[U][MT];
+  if (active && nbat > 0) load_batch(0, a0);
+  if (!DIRECT) {
+    const uint4 *src = a.act + (size_t)(k0 >> 5) * NT * 64;
+    for (int i = threadIdx.x; i < nkb * NT * 64; i += 64 * WPB) act_s[i] = src[i];
+    __syncthreads();
   }
-  for (; kb < nkb; ++kb) {
+  if (!active) return;
+  // pairs of batches; a prefetch past the last batch repeats the last one (an L2 hit) so that
+  // the loop has no conditional loads
+  int i = 0;
+  for (; i + 2 <= nbat; i += 2) {
+    load_batch((i + 1) * U, a1);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_batch(i * U, a0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_batch(min(i + 2, nbat - 1) * U, a0);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_batch((i + 1) * U, a1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (i < nbat) mma_batch(i * U, a0);
+  for (int kb = nbat * U; kb < nkb; ++kb) {
     uint4 av[MT], bv[NT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) av[m] = wt[m][(size_t)kb * kstride[m]];
@@ -268,45 +286,87 @@ __global__ __launch_bounds__(256) void k_gemv_mx(GemvArgs a) {
   }
 }
 
-// Sum of the k-partials of output row idx = r * B + b: contiguous, read with 16-byte loads that
-// are all issued before the first add (up to 32 partials), added in k order.
-__device__ __forceinline__ float ksum(const float *__restrict__ part, int ksp, int ksplit,
-                                      size_t idx) {
+// Sum of the k-partials of output row idx = r * B + b, contiguous, added in k order, in two
+// steps so that callers can issue every load of a kernel before the first add: ksum_load issues
+// the first NMAX 16-byte loads unconditionally (indices past the row's last group repeat it
+// and are not added), ksum_add adds them and loads any groups beyond NMAX itself.
+template <int NMAX>
+__device__ __forceinline__ void ksum_load(const float *__restrict__ part, int ksp, size_t idx,
+                                          float4 (&v)[NMAX]) {
   const float4 *pp = (const float4 *)(part + idx * ksp);
   const int n4 = ksp >> 2;
-  float4 v[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = i < n4 ? pp[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int i = 0; i < NMAX; ++i) v[i] = pp[min(i, n4 - 1)];
+}
+
+template <int NMAX>
+__device__ __forceinline__ float ksum_add(const float *__restrict__ part, int ksp, int ksplit,
+                                          size_t idx, const float4 (&v)[NMAX]) {
+  const int n4 = ksp >> 2;
   float s = 0.f;
   auto add4 = [&](const float4 &w, int k) {
-    if (k < ksplit) s += w.x;
-    if (k + 1 < ksplit) s += w.y;
-    if (k + 2 < ksplit) s += w.z;
-    if (k + 3 < ksplit) s += w.w;
+    s += k < ksplit ? w.x : 0.f;
+    s += k + 1 < ksplit ? w.y : 0.f;
+    s += k + 2 < ksplit ? w.z : 0.f;
+    s += k + 3 < ksplit ? w.w : 0.f;
   };
 #pragma unroll
-  for (int i = 0; i < 8; ++i) add4(v[i], 4 * i);
-  for (int i = 8; i < n4; ++i) add4(pp[i], 4 * i);
+  for (int i = 0; i < NMAX; ++i)
+    if (i < n4) add4(v[i], 4 * i);
+  const float4 *pp = (const float4 *)(part + idx * ksp);
+  for (int i = NMAX; i < n4; ++i) add4(pp[i], 4 * i);
   return s;
+}
+
+// NMAX for ksum: the number of 16-byte groups of a partial row, rounded up to 1, 2, 4 or 8.
+static int ksum_nmax(int ksp) {
+  const int n4 = ksp >> 2;
+  return n4 <= 1 ? 1 : n4 <= 2 ? 2 : n4 <= 4 ? 4 : 8;
+}
+
+__device__ __forceinline__ float ld_bf16(const void *p, size_t i) {
+  return __uint_as_float((uint32_t)((const uint16_t *)p)[i] << 16);
 }
 
 // r_b = 1 / sqrt(mean(x_b^2) + eps) of this lane's candidate b, from the per-row-block sums of
 // squares ss[i][b], computed by the whole wave without LDS or a barrier: with Bq = B rounded up
 // to a power of two, lane l sums rows i = l / Bq, l / Bq + 64 / Bq, ... of candidate l % Bq, a
 // butterfly over the lanes of equal l % Bq completes the sums (identical in every lane and
-// block), and each lane fetches its own candidate's.
-__device__ __forceinline__ float wave_inv_rms(const float *__restrict__ ss, int nss, int B, int b,
-                                              int H, float eps) {
+// block), and each lane fetches its own candidate's. inv_rms_load issues the first 8 loads of a
+// lane (zero past the end), inv_rms_finish adds any further rows and reduces.
+struct InvRmsLoads {
+  float v[8];
+};
+
+__device__ __forceinline__ void inv_rms_load(const float *__restrict__ ss, int nss, int B,
+                                             InvRmsLoads &ld) {
+  const int lane = threadIdx.x & 63;
+  int Bq = 1;
+  while (Bq < B) Bq <<= 1;
+  const int P = 64 / Bq;
+  const int bl = lane & (Bq - 1), part = lane / Bq;
+  const bool ok = bl < B;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int i = part + u * P;
+    const bool in = ok && i < nss;
+    const float t = ss[(size_t)(in ? i : 0) * B + (ok ? bl : 0)];
+    ld.v[u] = in ? t : 0.f;
+  }
+}
+
+__device__ __forceinline__ float inv_rms_finish(const float *__restrict__ ss, int nss, int B, int b,
+                                               int H, float eps, const InvRmsLoads &ld) {
   const int lane = threadIdx.x & 63;
   int Bq = 1;
   while (Bq < B) Bq <<= 1;
   const int P = 64 / Bq;
   const int bl = lane & (Bq - 1), part = lane / Bq;
   float v = 0.f;
-  if (bl < B) {
-#pragma unroll 8
-    for (int i = part; i < nss; i += P) v += ss[(size_t)i * B + bl];
-  }
+#pragma unroll
+  for (int u = 0; u < 8; ++u) v += ld.v[u];
+  if (bl < B)
+    for (int i = part + 8 * P; i < nss; i += P) v += ss[(size_t)i * B + bl];
   for (int off = Bq; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
   const float tot = __shfl(v, b, 64);
   return 1.0f / sqrtf(tot / (float)H + eps);
@@ -315,6 +375,7 @@ __device__ __forceinline__ float wave_inv_rms(const float *__restrict__ ss, int 
 // q, k_self, v_self from the QKV partials: scale by r_b (the attention RMSNorm, applied after
 // the product) and rotate q and k pairs (i, i + d/2) with the cos/sin table of position L_b.
 // One thread per (pair, candidate); every load is issued before the first use.
+template <int NMAX>
 __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ part, int ksp,
                                                     int ksplit, const float *__restrict__ ss,
                                                     int nss, int H, float eps, int B, int nq,
@@ -328,16 +389,21 @@ __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ pa
   const int pr = ec / B, b = ec - pr * B;
   const int head = pr / hd, i = pr - head * hd;
   const int r = head * d + i;
-  const float x1 = ksum(part, ksp, ksplit, (size_t)r * B + b);
-  const float x2 = ksum(part, ksp, ksplit, (size_t)(r + hd) * B + b);
-  const bool rot = head < nq + nkv;
-  const float cs = rot ? rope[((size_t)b * hd + i) * 2] : 1.f;
-  const float sn = rot ? rope[((size_t)b * hd + i) * 2 + 1] : 0.f;
-  const float inv = wave_inv_rms(ss, nss, B, b, H, eps);
+  const size_t i1 = (size_t)r * B + b, i2 = (size_t)(r + hd) * B + b;
+  float4 v1[NMAX], v2[NMAX];
+  ksum_load<NMAX>(part, ksp, i1, v1);
+  ksum_load<NMAX>(part, ksp, i2, v2);
+  const float2 csn = *(const float2 *)(rope + ((size_t)b * hd + i) * 2);
+  InvRmsLoads il;
+  inv_rms_load(ss, nss, B, il);
+  const float x1 = ksum_add<NMAX>(part, ksp, ksplit, i1, v1);
+  const float x2 = ksum_add<NMAX>(part, ksp, ksplit, i2, v2);
+  const float cs = csn.x, sn = csn.y;
+  const float inv = inv_rms_finish(ss, nss, B, b, H, eps, il);
   if (!act) return;
   const float y1 = x1 * inv, y2 = x2 * inv;
   float o1 = y1, o2 = y2;
-  if (rot) {
+  if (head < nq + nkv) {
     o1 = y1 * cs - y2 * sn;
     o2 = y2 * cs + y1 * sn;
   }
@@ -353,35 +419,40 @@ __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ pa
 }
 
 // Residual add x += sum_k partials for a block of 64 rows, the rows' sums of squares per
-// candidate (ss[block][b], fixed order), and the next GEMV's operand x * gamma_next.
-// 512 threads: one (row, candidate) element each for B <= 8.
+// candidate (ss[block][b], a fixed-order wave reduction), and the next GEMV's operand
+// x * gamma_next (bf16 gains). 512 threads: one (row, candidate) element each for B <= 8.
+template <int NMAX>
 __global__ __launch_bounds__(512) void k_resid_mx(float *__restrict__ x,
                                                   const float *__restrict__ part, int ksp,
                                                   int ksplit, float *__restrict__ ss, int B, int H,
-                                                  const void *__restrict__ gamma_next, int wdt,
+                                                  const void *__restrict__ gamma_next,
                                                   uint16_t *__restrict__ op, int NT, int Bp) {
   __shared__ float sq_s[64][65];
   const int r0 = blockIdx.x * 64;
   const int nr = min(64, H - r0);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int e = threadIdx.x; e < nr * B; e += 512) {
     const int rl = e / B, b = e - rl * B, r = r0 + rl;
+    const size_t ip = (size_t)r * B + b;
+    float4 v[NMAX];
+    ksum_load<NMAX>(part, ksp, ip, v);
     const float xo = x[(size_t)b * H + r];
-    const float g = gamma_next ? ld_w(gamma_next, r, wdt) : 0.f;
-    const float xv = xo + ksum(part, ksp, ksplit, (size_t)r * B + b);
+    const float g = ld_bf16(gamma_next ? gamma_next : (const void *)x, gamma_next ? r : 0);
+    const float xv = xo + ksum_add<NMAX>(part, ksp, ksplit, ip, v);
     x[(size_t)b * H + r] = xv;
     sq_s[rl][b] = xv * xv;
     if (gamma_next) store_operand(op, NT, Bp, r, b, xv * g);
   }
   __syncthreads();
-  if (threadIdx.x < B) {
-    float s = 0.f;
-    for (int rl = 0; rl < nr; ++rl) s += sq_s[rl][threadIdx.x];
-    ss[(size_t)blockIdx.x * B + threadIdx.x] = s;
+  for (int b = wave; b < B; b += 8) {
+    const float v = wsum(lane < nr ? sq_s[lane][b] : 0.f);
+    if (lane == 0) ss[(size_t)blockIdx.x * B + b] = v;
   }
 }
 
 // h = silu(r_b g) * (r_b u) for gate rows f and up rows F + f (the FFN RMSNorm applied after
 // the product), written as the down projection's operand. One thread per (feature, candidate).
+template <int NMAX>
 __global__ __launch_bounds__(256) void k_swiglu_mx(const float *__restrict__ part, int ksp,
                                                    int ksplit, const float *__restrict__ ss,
                                                    int nss, int H, float eps, int B, int F,
@@ -390,9 +461,15 @@ __global__ __launch_bounds__(256) void k_swiglu_mx(const float *__restrict__ par
   const bool act = e < F * B;
   const int ec = act ? e : 0;
   const int f = ec / B, b = ec - f * B;
-  const float g = ksum(part, ksp, ksplit, (size_t)f * B + b);
-  const float u = ksum(part, ksp, ksplit, (size_t)(F + f) * B + b);
-  const float inv = wave_inv_rms(ss, nss, B, b, H, eps);
+  const size_t ig = (size_t)f * B + b, iu = (size_t)(F + f) * B + b;
+  float4 vg[NMAX], vu[NMAX];
+  ksum_load<NMAX>(part, ksp, ig, vg);
+  ksum_load<NMAX>(part, ksp, iu, vu);
+  InvRmsLoads il;
+  inv_rms_load(ss, nss, B, il);
+  const float g = ksum_add<NMAX>(part, ksp, ksplit, ig, vg);
+  const float u = ksum_add<NMAX>(part, ksp, ksplit, iu, vu);
+  const float inv = inv_rms_finish(ss, nss, B, b, H, eps, il);
   if (!act) return;
   const float gv = g * inv, uv = u * inv;
   store_operand(op, NT, Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
@@ -953,10 +1030,17 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
   a.part = part;
   a.ksp = (gp.ksplit + 3) & ~3;
   const int mt = gemv_mt(p.nt);
-  dim3 grid((gp.rows / 16 + 4 * mt - 1) / (4 * mt), gp.ksplit);
-  const size_t lds = (size_t)(gp.kslice / 32) * p.nt * 64 * sizeof(uint4);
-#define KVPRM_G(MT_, NT_, U_) \
-  hipLaunchKernelGGL((k_gemv_mx<MT_, NT_, U_>), grid, dim3(256), lds, s, a)
+  // 4 waves per block; the operand k-slice is staged in LDS for one column tile and read
+  // straight from memory (L2) for more (measured faster: the staging would cap residency)
+  constexpr int WPB = 4;
+  const bool direct = p.nt >= 2;
+  dim3 grid((gp.rows / 16 + WPB * mt - 1) / (WPB * mt), gp.ksplit);
+  const size_t lds = direct ? 0 : (size_t)(gp.kslice / 32) * p.nt * 64 * sizeof(uint4);
+#define KVPRM_G(MT_, NT_, U_)                                                                  \
+  if (direct)                                                                                  \
+    hipLaunchKernelGGL((k_gemv_mx<MT_, NT_, U_, WPB, true>), grid, dim3(64 * WPB), lds, s, a); \
+  else                                                                                         \
+    hipLaunchKernelGGL((k_gemv_mx<MT_, NT_, U_, WPB, false>), grid, dim3(64 * WPB), lds, s, a)
   switch (p.nt) {
     case 1: KVPRM_G(1, 1, 4); break;
     case 2: KVPRM_G(2, 2, 4); break;
@@ -977,9 +1061,32 @@ hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, cons
                                 w.opA, w.part, s);
   if (e != hipSuccess) return e;
   const int n = (dm.nq + 2 * dm.nkv) * (dm.d / 2) * p.B;
-  hipLaunchKernelGGL(k_qkv_fin_mx, dim3((n + 255) / 256), dim3(256), 0, s, w.part, ksp_of(p.g_qkv),
-                     p.g_qkv.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.nq, dm.nkv, dm.d, w.rope,
-                     w.q, w.kself, w.vself);
+#define KVPRM_F(NM)                                                                             \
+  hipLaunchKernelGGL(k_qkv_fin_mx<NM>, dim3((n + 255) / 256), dim3(256), 0, s, w.part,          \
+                     ksp_of(p.g_qkv), p.g_qkv.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.nq,     \
+                     dm.nkv, dm.d, w.rope, w.q, w.kself, w.vself)
+  switch (ksum_nmax(ksp_of(p.g_qkv))) {
+    case 1: KVPRM_F(1); break;
+    case 2: KVPRM_F(2); break;
+    case 4: KVPRM_F(4); break;
+    default: KVPRM_F(8); break;
+  }
+#undef KVPRM_F
+  return hipGetLastError();
+}
+
+static hipError_t launch_resid_mx(const Dims &dm, const Plan &p, const Workspace &w,
+                                  const GemvPlan &g, const void *gamma_next, hipStream_t s) {
+#define KVPRM_R(NM)                                                                         \
+  hipLaunchKernelGGL(k_resid_mx<NM>, dim3(p.nss), dim3(512), 0, s, w.x, w.part, ksp_of(g), \
+                     g.ksplit, w.ss, p.B, dm.H, gamma_next, w.opA, p.nt, p.bp)
+  switch (ksum_nmax(ksp_of(g))) {
+    case 1: KVPRM_R(1); break;
+    case 2: KVPRM_R(2); break;
+    case 4: KVPRM_R(4); break;
+    default: KVPRM_R(8); break;
+  }
+#undef KVPRM_R
   return hipGetLastError();
 }
 
@@ -987,9 +1094,7 @@ hipError_t launch_oproj_mx(const Dims &dm, const Plan &p, const Workspace &w, co
                            const void *gamma_ffn, hipStream_t s) {
   hipError_t e = launch_gemv_mx(p, p.g_o, wo, dm.H, nullptr, 0, nullptr, 0, w.opO, w.part, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_resid_mx, dim3(p.nss), dim3(512), 0, s, w.x, w.part, ksp_of(p.g_o),
-                     p.g_o.ksplit, w.ss, p.B, dm.H, gamma_ffn, dm.wdt, w.opA, p.nt, p.bp);
-  return hipGetLastError();
+  return launch_resid_mx(dm, p, w, p.g_o, gamma_ffn, s);
 }
 
 hipError_t launch_gateup_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
@@ -997,8 +1102,17 @@ hipError_t launch_gateup_mx(const Dims &dm, const Plan &p, const Workspace &w, c
   hipError_t e = launch_gemv_mx(p, p.g_gu, wg, dm.F, wu, dm.F, nullptr, 0, w.opA, w.part, s);
   if (e != hipSuccess) return e;
   const int n = dm.F * p.B;
-  hipLaunchKernelGGL(k_swiglu_mx, dim3((n + 255) / 256), dim3(256), 0, s, w.part, ksp_of(p.g_gu),
-                     p.g_gu.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.F, w.opD, p.nt, p.bp);
+#define KVPRM_S(NM)                                                                             \
+  hipLaunchKernelGGL(k_swiglu_mx<NM>, dim3((n + 255) / 256), dim3(256), 0, s, w.part,           \
+                     ksp_of(p.g_gu), p.g_gu.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.F, w.opD, \
+                     p.nt, p.bp)
+  switch (ksum_nmax(ksp_of(p.g_gu))) {
+    case 1: KVPRM_S(1); break;
+    case 2: KVPRM_S(2); break;
+    case 4: KVPRM_S(4); break;
+    default: KVPRM_S(8); break;
+  }
+#undef KVPRM_S
   return hipGetLastError();
 }
 
@@ -1006,9 +1120,7 @@ hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, con
                           const void *gamma_next, hipStream_t s) {
   hipError_t e = launch_gemv_mx(p, p.g_d, wd, dm.H, nullptr, 0, nullptr, 0, w.opD, w.part, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_resid_mx, dim3(p.nss), dim3(512), 0, s, w.x, w.part, ksp_of(p.g_d),
-                     p.g_d.ksplit, w.ss, p.B, dm.H, gamma_next, dm.wdt, w.opA, p.nt, p.bp);
-  return hipGetLastError();
+  return launch_resid_mx(dm, p, w, p.g_d, gamma_next, s);
 }
 
 hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
