@@ -60,8 +60,9 @@ __device__ __forceinline__ float block_sum256(float v, float *red) {
 // ------------------------------------------------------------------------------- plan
 
 // Split-K plan of a matrix-core GEMV, in whole 32-wide input blocks: about 32 blocks per wave
-// (long contiguous weight streams), but at least ~2048 waves in all, at least 4 blocks per
-// slice, and the slice's operand (staged in LDS, 1 KiB per block and column tile) within 64 KiB.
+// (long contiguous weight streams), but at least ~2048 waves in all and at least 4 blocks per
+// slice. With one operand column tile the slice's operand is staged in LDS (1 KiB per block,
+// <= 32 KiB); with more tiles the kernel reads it from memory.
 static GemvPlan gemv_plan(int rows, int K, int B) {
   GemvPlan g;
   g.rows = rows;
@@ -75,9 +76,7 @@ static GemvPlan gemv_plan(int rows, int K, int B) {
   if (want < want_par) want = want_par;
   if (want > nkb / 4) want = nkb / 4;
   if (want < 1) want = 1;
-  int kb_per = (nkb + want - 1) / want;
-  const int kb_lds = 64 / nt;
-  if (kb_per > kb_lds) kb_per = kb_lds;
+  const int kb_per = (nkb + want - 1) / want;  // <= 32 unless the slice count is capped
   g.kslice = kb_per * 32;
   g.ksplit = (K + g.kslice - 1) / g.kslice;
   return g;

@@ -846,65 +846,76 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
     ksc_l = a.ksc[(size_t)ph_l * nkv + j];
     vsc_l = a.vsc[(size_t)ph_l * nkv + j];
   }
-  // cooperative staging: thread t copies entries t, t + nthr, ... of the pair's 4 tiles
+  // cooperative staging: thread t copies entries t, t + nthr, ... of the pair's 4 tiles. NPF
+  // pairs are in flight in registers (a ring, unrolled so that its indices are constants);
+  // the pair being computed sits in one of two LDS buffers. Fetches past the last pair repeat
+  // it (an L2 hit), so that no load is conditional.
   constexpr int PER = (4 * TILE16 + nthr - 1) / nthr;
-  uint4 st[PER];
-  auto fetch = [&](int pp) {
+  constexpr int NPF = 4;
+  uint4 st[NPF][PER];
+  auto fetch = [&](int pp, uint4(&dst)[PER]) {
+    pp = min(pp, npairs - 1);
     const int pa = __shfl(ph_l, min(2 * pp, np - 1), 64);
     const int pb = __shfl(ph_l, min(2 * pp + 1, np - 1), 64);
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      const int e = threadIdx.x + u * nthr;
-      if (e < 4 * TILE16) {
-        const int t = e / TILE16, o = e - t * TILE16;
-        const char *pool = t < 2 ? a.kp : a.vp;
-        const int pg = (t & 1) ? pb : pa;
-        st[u] = ((const uint4 *)(pool + ((size_t)pg * nkv + j) * TILE16 * 16))[o];
-      }
+      const int e = min((int)threadIdx.x + u * nthr, 4 * TILE16 - 1);
+      const int t = e / TILE16, o = e - t * TILE16;
+      const char *pool = t < 2 ? a.kp : a.vp;
+      const int pg = (t & 1) ? pb : pa;
+      dst[u] = ((const uint4 *)(pool + ((size_t)pg * nkv + j) * TILE16 * 16))[o];
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int buf, const uint4(&src)[PER]) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = threadIdx.x + u * nthr;
-      if (e < 4 * TILE16) (&stage_s[buf][0][0])[e] = st[u];
+      if (e < 4 * TILE16) (&stage_s[buf][0][0])[e] = src[u];
     }
   };
-  fetch(0);
+#pragma unroll
+  for (int k = 0; k < NPF; ++k) fetch(k, st[k]);
   uint4 qhi[NKB], qmd[NKB], qlo[NKB];
   load_query_ops<KVT, D>(a.q + ((size_t)bcand * nq + (size_t)j * g + hh) * D, present, cq, qhi,
                          qmd, qlo);
-  stash(0);
+  stash(0, st[0]);
   __syncthreads();
   const float rs = kLog2e / sqrtf((float)D);  // scores in log2 units
   float m_run = -INFINITY, l_run = 0.f;
   floatx4 acc[NDB];
 #pragma unroll
   for (int nb = 0; nb < NDB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-  for (int pp = 0; pp < npairs; ++pp) {
-    const int buf = pp & 1;
-    if (pp + 1 < npairs) fetch(pp + 1);
-    PairRaw<D> r;
-    load_pair_raw<KVT, D>(stage_s[buf][0], stage_s[buf][1], stage_s[buf][2], stage_s[buf][3], lane, r);
-    uint4 KA[NKB], KB[NKB];
-    uint2 VA[NDB], VB[NDB];
-    unpack_pair<KVT, D>(r, KA, KB, VA, VB);
-    const int la = 2 * pp, lb = 2 * pp + 1;
-    const bool hasB = lb < np;
-    bool ok[8];
+  for (int pbase = 0; pbase < npairs; pbase += NPF) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ok[i] = true;  // prefix pages are full
-      ok[4 + i] = hasB;
+    for (int k = 0; k < NPF; ++k) {
+      const int pp = pbase + k;
+      if (pp < npairs) {
+        fetch(pp + NPF, st[k]);  // pair pp left st[k] for LDS in the previous step
+        const int buf = k & 1;   // == pp & 1 (NPF is even)
+        PairRaw<D> r;
+        load_pair_raw<KVT, D>(stage_s[buf][0], stage_s[buf][1], stage_s[buf][2], stage_s[buf][3],
+                              lane, r);
+        uint4 KA[NKB], KB[NKB];
+        uint2 VA[NDB], VB[NDB];
+        unpack_pair<KVT, D>(r, KA, KB, VA, VB);
+        const int la = 2 * pp, lb = 2 * pp + 1;
+        const bool hasB = lb < np;
+        bool ok[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          ok[i] = true;  // prefix pages are full
+          ok[4 + i] = hasB;
+        }
+        const int lbc = hasB ? lb : la;
+        const float sca = (KVT == 2) ? __shfl(ksc_l, la, 64) * rs : rs;
+        const float scb = (KVT == 2) ? __shfl(ksc_l, lbc, 64) * rs : rs;
+        const float vsa = (KVT == 2) ? __shfl(vsc_l, la, 64) : 1.f;
+        const float vsb = (KVT == 2) ? __shfl(vsc_l, lbc, 64) : 1.f;
+        online_step<D>(KA, KB, VA, VB, qhi, qmd, qlo, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
+        if (pp + 1 < npairs) stash(buf ^ 1, st[(k + 1) % NPF]);
+        __syncthreads();
+      }
     }
-    const int lbc = hasB ? lb : la;
-    const float sca = (KVT == 2) ? __shfl(ksc_l, la, 64) * rs : rs;
-    const float scb = (KVT == 2) ? __shfl(ksc_l, lbc, 64) * rs : rs;
-    const float vsa = (KVT == 2) ? __shfl(vsc_l, la, 64) : 1.f;
-    const float vsb = (KVT == 2) ? __shfl(vsc_l, lbc, 64) : 1.f;
-    online_step<D>(KA, KB, VA, VB, qhi, qmd, qlo, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
-    if (pp + 1 < npairs) stash(buf ^ 1);
-    __syncthreads();
   }
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
