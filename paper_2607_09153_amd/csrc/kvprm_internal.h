@@ -104,6 +104,14 @@ hipError_t launch_gateup_mx(const Dims &dm, const Plan &p, const Workspace &w, c
                             const void *wu, hipStream_t s);
 hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
                           const void *gamma_next, hipStream_t s);
+// fused projections for one operand column tile (B <= 8): no split-K partials, the
+// element-wise step after the output, gate/up and down projections runs in the epilogue
+hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
+                              const void *gamma_ffn, hipStream_t s);
+hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
+                               const void *wu, hipStream_t s);
+hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
+                             const void *gamma_next, hipStream_t s);
 hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
                           const char *vp, const float *ksc, const float *vsc,
                           const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,

@@ -332,10 +332,11 @@ __device__ __forceinline__ float ld_bf16(const void *p, size_t i) {
 // squares ss[i][b], computed by the whole wave without LDS or a barrier: with Bq = B rounded up
 // to a power of two, lane l sums rows i = l / Bq, l / Bq + 64 / Bq, ... of candidate l % Bq, a
 // butterfly over the lanes of equal l % Bq completes the sums (identical in every lane and
-// block), and each lane fetches its own candidate's. inv_rms_load issues the first 8 loads of a
-// lane (zero past the end), inv_rms_finish adds any further rows and reduces.
+// block), and each lane fetches its own candidate's. inv_rms_load issues the first 32 loads of
+// a lane unconditionally (clamped addresses, zero past the end), inv_rms_finish adds any
+// further rows and reduces.
 struct InvRmsLoads {
-  float v[8];
+  float v[32];
 };
 
 __device__ __forceinline__ void inv_rms_load(const float *__restrict__ ss, int nss, int B,
@@ -347,7 +348,7 @@ __device__ __forceinline__ void inv_rms_load(const float *__restrict__ ss, int n
   const int bl = lane & (Bq - 1), part = lane / Bq;
   const bool ok = bl < B;
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
+  for (int u = 0; u < 32; ++u) {
     const int i = part + u * P;
     const bool in = ok && i < nss;
     const float t = ss[(size_t)(in ? i : 0) * B + (ok ? bl : 0)];
@@ -364,12 +365,167 @@ __device__ __forceinline__ float inv_rms_finish(const float *__restrict__ ss, in
   const int bl = lane & (Bq - 1), part = lane / Bq;
   float v = 0.f;
 #pragma unroll
-  for (int u = 0; u < 8; ++u) v += ld.v[u];
+  for (int u = 0; u < 32; ++u) v += ld.v[u];
   if (bl < B)
-    for (int i = part + 8 * P; i < nss; i += P) v += ss[(size_t)i * B + bl];
+    for (int i = part + 32 * P; i < nss; i += P) v += ss[(size_t)i * B + bl];
   for (int off = Bq; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
   const float tot = __shfl(v, b, 64);
   return 1.0f / sqrtf(tot / (float)H + eps);
+}
+
+// ---------------------------------------------------- GEMV with fused epilogue (B <= 8)
+
+// For one operand column tile (B <= 8: columns b and 8 + b hold the hi and lo halves of
+// candidate b) the projections and the element-wise steps that follow them run in one kernel:
+// a block owns MT row tiles over the whole input; its WPB waves split the input blocks into
+// contiguous ranges (weights double buffered in batches of U, the operand read from memory),
+// the waves' accumulators are added in LDS in a fixed order, and the block applies the
+// epilogue to complete outputs, so no split-K partials cross a kernel boundary.
+//   EPI_RESID:  one tile: x += y, the tile's sums of squares per candidate, next operand
+//               x * gamma (if gamma).
+//   EPI_SWIGLU: gate tile t and up tile t: h = silu(r g) * (r u) as the down operand.
+enum { EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+struct FusedArgs {
+  const void *w[3];  // weight segments (packed layout), stacked rows
+  int seg_rows[3];
+  int nseg;
+  int K;
+  const uint4 *act;  // operand [K / 32][64] (one column tile)
+  int B;
+  // epilogue
+  float *x;                  // residual [B][H] (RESID)
+  int H;
+  float *ss;                 // sums of squares: written per 16-row tile (RESID), read (SWIGLU)
+  int nss;
+  float eps;
+  const void *gamma;         // bf16 gain of the next RMSNorm (RESID), may be null
+  uint16_t *op;              // next operand (RESID, SWIGLU)
+  int NT, Bp;                // layout of the next operand
+  int F;
+};
+
+template <int MT, int WPB, int U, int EPI>
+__global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
+  __shared__ floatx4 red_s[WPB][MT][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int B = a.B;
+  // global row tiles of this block
+  int tile[MT];
+  if (EPI == EPI_SWIGLU) {
+    tile[0] = blockIdx.x;
+    if (MT > 1) tile[MT - 1] = blockIdx.x + a.F / 16;
+  } else {
+    tile[0] = blockIdx.x;
+  }
+  const uint4 *wt[MT];
+  size_t kstride[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    int seg = 0, base = 0;
+    while (seg < a.nseg - 1 && tile[m] * 16 >= base + a.seg_rows[seg]) base += a.seg_rows[seg++];
+    const size_t ntiles = (size_t)a.seg_rows[seg] / 16;
+    kstride[m] = ntiles * 64;
+    wt[m] = (const uint4 *)a.w[seg] + (size_t)(tile[m] - base / 16) * 64 + lane;
+  }
+  // this wave's input blocks [kb0, kb1)
+  const int nkb = a.K >> 5;
+  const int per = (nkb + WPB - 1) / WPB;
+  const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
+  const uint4 *ap = a.act + lane;
+  // the epilogue's sums of squares are fetched now and used after the product
+  InvRmsLoads il;
+  if (EPI != EPI_RESID && wave == 0) inv_rms_load(a.ss, a.nss, B, il);
+  floatx4 acc[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto load_batch = [&](int kb, uint4(&av)[U][MT], uint4(&bv)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m) av[u][m] = wt[m][(size_t)(kb + u) * kstride[m]];
+      bv[u] = ap[(size_t)(kb + u) * 64];
+    }
+  };
+  auto mma_batch = [&](const uint4(&av)[U][MT], const uint4(&bv)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m] = mfma16(av[u][m], bv[u], acc[m]);
+  };
+  const int nbat = (kb1 - kb0) / U;
+  if (nbat > 0) {
+    uint4 a0[U][MT], a1[U][MT], b0[U], b1[U];
+    load_batch(kb0, a0, b0);
+    int i = 0;
+    for (; i + 2 <= nbat; i += 2) {
+      load_batch(kb0 + (i + 1) * U, a1, b1);
+      __builtin_amdgcn_sched_barrier(0);
+      mma_batch(a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_batch(kb0 + min(i + 2, nbat - 1) * U, a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+      mma_batch(a1, b1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (i < nbat) mma_batch(a0, b0);
+  }
+  for (int kb = kb0 + nbat * U; kb < kb1; ++kb) {
+    const uint4 bv = ap[(size_t)kb * 64];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = mfma16(wt[m][(size_t)kb * kstride[m]], bv, acc[m]);
+  }
+#pragma unroll
+  for (int m = 0; m < MT; ++m) red_s[wave][m][lane] = acc[m];
+  __syncthreads();
+  if (wave != 0) return;
+  // fixed-order sum over the waves, then hi + lo of candidate n = lane % 16 (< 8)
+  const int n = lane & 15, cq = lane >> 4;
+  float y[MT][4];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    floatx4 t = red_s[0][m][lane];
+#pragma unroll
+    for (int w = 1; w < WPB; ++w) {
+      const floatx4 v = red_s[w][m][lane];
+      t[0] += v[0];
+      t[1] += v[1];
+      t[2] += v[2];
+      t[3] += v[3];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) y[m][i] = t[i] + __shfl_xor(t[i], 8, 64);
+  }
+  const bool cand_ok = n < 8 && n < B;
+  const int b = cand_ok ? n : 0;
+  if (EPI == EPI_RESID) {
+    float sq = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = tile[0] * 16 + 4 * cq + i;
+      float xv = 0.f;
+      if (cand_ok) {
+        xv = a.x[(size_t)b * a.H + r] + y[0][i];
+        a.x[(size_t)b * a.H + r] = xv;
+        if (a.gamma) store_operand(a.op, a.NT, a.Bp, r, b, xv * ld_bf16(a.gamma, r));
+      }
+      sq += xv * xv;
+    }
+    // rows of the tile: the 4 lane groups cq, in a fixed order
+    sq += __shfl_xor(sq, 16, 64);
+    sq += __shfl_xor(sq, 32, 64);
+    if (cand_ok && cq == 0) a.ss[(size_t)tile[0] * B + b] = sq;
+  } else {
+    const float inv = inv_rms_finish(a.ss, a.nss, B, b, a.H, a.eps, il);
+    {  // EPI_SWIGLU
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int f = tile[0] * 16 + 4 * cq + i;
+        const float gv = y[0][i] * inv, uv = y[MT - 1][i] * inv;
+        if (cand_ok) store_operand(a.op, a.NT, a.Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
+      }
+    }
+  }
 }
 
 // q, k_self, v_self from the QKV partials: scale by r_b (the attention RMSNorm, applied after
@@ -1132,6 +1288,62 @@ hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   hipError_t e = launch_gemv_mx(p, p.g_d, wd, dm.H, nullptr, 0, nullptr, 0, w.opD, w.part, s);
   if (e != hipSuccess) return e;
   return launch_resid_mx(dm, p, w, p.g_d, gamma_next, s);
+}
+
+// fused projections (one operand column tile, B <= 8)
+static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, int K,
+                            const uint16_t *act) {
+  FusedArgs a;
+  memset(&a, 0, sizeof a);
+  a.K = K;
+  a.act = (const uint4 *)act;
+  a.B = p.B;
+  a.x = w.x;
+  a.H = dm.H;
+  a.ss = w.ss;
+  a.nss = p.nss;
+  a.eps = dm.eps;
+  a.NT = p.nt;
+  a.Bp = p.bp;
+  a.F = dm.F;
+  return a;
+}
+
+hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
+                              const void *gamma_ffn, hipStream_t s) {
+  FusedArgs a = fused_args(dm, p, w, dm.nq * dm.d, w.opO);
+  a.w[0] = wo;
+  a.seg_rows[0] = dm.H;
+  a.nseg = 1;
+  a.gamma = gamma_ffn;
+  a.op = w.opA;
+  hipLaunchKernelGGL((k_gemv_fused<1, 16, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 16), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
+                               const void *wu, hipStream_t s) {
+  FusedArgs a = fused_args(dm, p, w, dm.H, w.opA);
+  a.w[0] = wg;
+  a.w[1] = wu;
+  a.seg_rows[0] = dm.F;
+  a.seg_rows[1] = dm.F;
+  a.nseg = 2;
+  a.op = w.opD;
+  hipLaunchKernelGGL((k_gemv_fused<2, 4, 4, EPI_SWIGLU>), dim3(dm.F / 16), dim3(64 * 4), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
+                             const void *gamma_next, hipStream_t s) {
+  FusedArgs a = fused_args(dm, p, w, dm.F, w.opD);
+  a.w[0] = wd;
+  a.seg_rows[0] = dm.H;
+  a.nseg = 1;
+  a.gamma = gamma_next;
+  a.op = w.opA;
+  hipLaunchKernelGGL((k_gemv_fused<1, 16, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 16), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
