@@ -664,6 +664,12 @@ __device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t word) {
   return (__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xFFFF0000u);
 }
 
+// Lane i's value of v, for a wave-uniform i (a scalar read of one lane: no LDS round trip).
+__device__ __forceinline__ int lane_value(int v, int i) { return __builtin_amdgcn_readlane(v, i); }
+__device__ __forceinline__ float lane_value(float v, int i) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
+}
+
 // Raw registers of one page pair of one kv-head, in tile byte order (16 bytes per lane and
 // instruction): K tiles of pages A and B, then their V tiles. bf16 uses D/32 of each, fp8 D/64.
 template <int D>
@@ -892,7 +898,7 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const int n = lane & 15, cq = lane >> 4;
   // each wave reads the chunk's page ids itself into lane registers (lane i holds page i and,
-  // for fp8, its scales) and fetches them with cross-lane reads: no LDS, no barrier
+  // for fp8, its scales) and fetches them with scalar lane reads: no LDS, no barrier
   const int ph_l = lane < np ? a.page_table[(size_t)b * a.max_pages + p0 + lane] : 0;
   float ksc_l = 0.f, vsc_l = 0.f;
   if (KVT == 2 && lane < np) {
@@ -902,8 +908,8 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   const int npairs = (np + 1) >> 1;
   auto load_pair = [&](int pp, PairRaw<D> &r) {
     // indices past the chunk are clamped to its last page: those tokens are masked anyway
-    const int pa = __shfl(ph_l, min(2 * pp, np - 1), 64);
-    const int pb = __shfl(ph_l, min(2 * pp + 1, np - 1), 64);
+    const int pa = lane_value(ph_l, min(2 * pp, np - 1));
+    const int pb = lane_value(ph_l, min(2 * pp + 1, np - 1));
     load_pair_raw<KVT, D>((const uint4 *)(a.kp + ((size_t)pa * nkv + j) * TILE),
                           (const uint4 *)(a.kp + ((size_t)pb * nkv + j) * TILE),
                           (const uint4 *)(a.vp + ((size_t)pa * nkv + j) * TILE),
@@ -935,10 +941,10 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
       ok[4 + i] = hasB && (tb + i < L);
     }
     const int lbc = hasB ? lb : la;
-    const float sca = (KVT == 2) ? __shfl(ksc_l, la, 64) * rs : rs;
-    const float scb = (KVT == 2) ? __shfl(ksc_l, lbc, 64) * rs : rs;
-    const float vsa = (KVT == 2) ? __shfl(vsc_l, la, 64) : 1.f;
-    const float vsb = (KVT == 2) ? __shfl(vsc_l, lbc, 64) : 1.f;
+    const float sca = (KVT == 2) ? lane_value(ksc_l, la) * rs : rs;
+    const float scb = (KVT == 2) ? lane_value(ksc_l, lbc) * rs : rs;
+    const float vsa = (KVT == 2) ? lane_value(vsc_l, la) : 1.f;
+    const float vsb = (KVT == 2) ? lane_value(vsc_l, lbc) : 1.f;
     online_step<D>(KA, KB, VA, VB, q0, q1, q2, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
   };
   // a branch-free loop over an even number of pairs: the pair past the end (if any) is fully
@@ -1011,8 +1017,8 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
   uint4 st[NPF][PER];
   auto fetch = [&](int pp, uint4(&dst)[PER]) {
     pp = min(pp, npairs - 1);
-    const int pa = __shfl(ph_l, min(2 * pp, np - 1), 64);
-    const int pb = __shfl(ph_l, min(2 * pp + 1, np - 1), 64);
+    const int pa = lane_value(ph_l, min(2 * pp, np - 1));
+    const int pb = lane_value(ph_l, min(2 * pp + 1, np - 1));
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = min((int)threadIdx.x + u * nthr, 4 * TILE16 - 1);
@@ -1063,10 +1069,10 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
           ok[4 + i] = hasB;
         }
         const int lbc = hasB ? lb : la;
-        const float sca = (KVT == 2) ? __shfl(ksc_l, la, 64) * rs : rs;
-        const float scb = (KVT == 2) ? __shfl(ksc_l, lbc, 64) * rs : rs;
-        const float vsa = (KVT == 2) ? __shfl(vsc_l, la, 64) : 1.f;
-        const float vsb = (KVT == 2) ? __shfl(vsc_l, lbc, 64) : 1.f;
+        const float sca = (KVT == 2) ? lane_value(ksc_l, la) * rs : rs;
+        const float scb = (KVT == 2) ? lane_value(ksc_l, lbc) * rs : rs;
+        const float vsa = (KVT == 2) ? lane_value(vsc_l, la) : 1.f;
+        const float vsb = (KVT == 2) ? lane_value(vsc_l, lbc) : 1.f;
         online_step<D>(KA, KB, VA, VB, qhi, qmd, qlo, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
         if (pp + 1 < npairs) stash(buf ^ 1, st[(k + 1) % NPF]);
         __syncthreads();
