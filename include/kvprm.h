@@ -19,8 +19,11 @@
  *     is enqueued. The returned status says what failed; kvprm_last_error() has the text.
  *   - A handle is immutable after kvprm_create. Concurrent calls on one handle are safe when
  *     they use distinct workspaces and outputs.
- *   - Out-of-range physical page ids in the page table are undefined behaviour (they are not
- *     checked on the device).
+ *   - Out-of-range physical page ids in the page table are undefined behaviour: the kernels do
+ *     not check them. With the environment variable KVPRM_DEBUG=1 set when the handle is
+ *     created, kvprm_score and kvprm_attention copy lengths and page table to the host (on
+ *     `stream`, then synchronising it) and return KVPRM_E_INVALID for any page id outside
+ *     [0, num_pages) among the pages a candidate reads, before enqueueing anything.
  *
  * Model structure (the paper names only "decoder-only transformer"; the block follows the
  * Qwen3/Llama family it evaluates): pre-norm RMSNorm -> Q/K/V projections -> rotate-half

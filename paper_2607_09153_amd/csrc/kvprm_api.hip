@@ -1,11 +1,14 @@
 // C ABI of libkvprm: argument validation, workspace carving and launch sequencing of the
-// verify-token pass. Nothing here allocates device memory or synchronises the host.
+// verify-token pass. Nothing here allocates device memory; only the debug check of the page
+// table (KVPRM_DEBUG=1 at kvprm_create) synchronises the host.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <new>
 #include <string>
+#include <vector>
 
 #include "../../include/kvprm.h"
 #include "kvprm_internal.h"
@@ -15,6 +18,7 @@ using namespace kvprm;
 struct kvprm_handle_s {
   kvprm_model_desc desc;
   Dims dm;
+  bool debug;  // KVPRM_DEBUG=1 at creation: check device page ids on the host before each call
 };
 
 static thread_local std::string g_err;
@@ -85,6 +89,8 @@ kvprm_status kvprm_create(const kvprm_model_desc *d, kvprm_handle *out) {
   m.eps = d->rms_eps;
   m.wdt = d->weight_dtype == KVPRM_BF16 ? 1 : 0;
   m.kvdt = d->kv_dtype == KVPRM_F32 ? 0 : (d->kv_dtype == KVPRM_BF16 ? 1 : 2);
+  const char *dbg = getenv("KVPRM_DEBUG");
+  h->debug = dbg && dbg[0] && strcmp(dbg, "0") != 0;
   *out = h;
   return ok();
 }
@@ -141,6 +147,31 @@ static kvprm_status check_cache(const kvprm_handle h, const kvprm_kv_cache *c, c
   if (c->num_pages < 1) return fail(KVPRM_E_INVALID, "%s: num_pages < 1", fn);
   if (h->dm.kvdt == 2 && (!c->k_scale || !c->v_scale))
     return fail(KVPRM_E_INVALID, "%s: fp8 cache needs k_scale and v_scale", fn);
+  return KVPRM_OK;
+}
+
+// Debug mode only: copy lengths and the page table to the host (on the call's stream, then
+// wait) and check every read entry against [0, num_pages) and every length against the table.
+static kvprm_status check_pages_debug(const kvprm_handle h, const kvprm_kv_cache *c,
+                                      const kvprm_batch *b, hipStream_t s, const char *fn) {
+  if (!h->debug) return KVPRM_OK;
+  std::vector<int32_t> len(b->batch), pt((size_t)b->batch * b->max_pages);
+  if (hipMemcpyAsync(len.data(), b->lengths, len.size() * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipMemcpyAsync(pt.data(), b->page_table, pt.size() * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(KVPRM_E_HIP, "%s: debug copy of the page table failed", fn);
+  const int cap = b->max_pages * h->desc.page_size;
+  for (int i = 0; i < b->batch; ++i) {
+    if (len[i] < 0 || len[i] > cap)
+      return fail(KVPRM_E_INVALID, "%s: lengths[%d] = %d outside [0, %d]", fn, i, len[i], cap);
+    const int np = (len[i] + h->desc.page_size - 1) / h->desc.page_size;
+    for (int k = 0; k < np; ++k) {
+      const int32_t id = pt[(size_t)i * b->max_pages + k];
+      if (id < 0 || id >= c->num_pages)
+        return fail(KVPRM_E_INVALID, "%s: page_table[%d][%d] = %d outside [0, %d)", fn, i, k, id,
+                    c->num_pages);
+    }
+  }
   return KVPRM_OK;
 }
 
@@ -225,6 +256,7 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   }
   if (!scores) return fail(KVPRM_E_INVALID, "%s: null scores", fn);
   if ((st = check_ws(h, b, workspace, ws_bytes, fn)) != KVPRM_OK) return st;
+  if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
 
   const Dims &dm = h->dm;
   hipStream_t s = (hipStream_t)stream;
@@ -334,6 +366,7 @@ kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const 
     return fail(KVPRM_E_INVALID, "%s: layer %d outside [0, %d)", fn, layer, h->dm.layers);
   if (!q || !k_self || !v_self || !o) return fail(KVPRM_E_INVALID, "%s: null q/k_self/v_self/o", fn);
   if ((st = check_ws(h, b, workspace, ws_bytes, fn)) != KVPRM_OK) return st;
+  if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
   const Dims &dm = h->dm;
   const Plan p = make_plan(dm, b->batch, b->max_pages);
   const Workspace w = carve(dm, p, workspace);

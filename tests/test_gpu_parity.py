@@ -240,3 +240,43 @@ def test_pack_weight_roundtrip():
     torch.cuda.synchronize()
     back = ko.unpack_tiled(dst.cpu().numpy().view(np.uint16), rows, K)
     assert np.array_equal(back, raw.reshape(rows, K))
+
+
+def test_debug_mode_rejects_out_of_range_page_ids():
+    _say("case: KVPRM_DEBUG page-table check")
+    import os
+    w = synth.make_workload("custom", shape=synth.TINY, lengths=[100, 37, 0], seed=82)
+    dw = DeviceWorkload(w)
+    m = kv()
+    old = os.environ.get("KVPRM_DEBUG")
+    os.environ["KVPRM_DEBUG"] = "1"
+    try:
+        h = m.kvprm_create(dw.desc(m))
+    finally:
+        if old is None:
+            del os.environ["KVPRM_DEBUG"]
+        else:
+            os.environ["KVPRM_DEBUG"] = old
+    try:
+        batch = dw.batch(m)
+        n = m.kvprm_workspace_size(h, batch)
+        ws = torch.empty(max(n, 256), dtype=torch.uint8, device="cuda")
+        scores = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+        st = torch.cuda.current_stream().cuda_stream
+        # valid call in debug mode: same scores as without it
+        m.kvprm_score(h, dw.cache(m), batch, dw.readout(m), ws.data_ptr(), n, scores.data_ptr(), 0,
+                      st)
+        torch.cuda.synchronize()
+        ref, _ = run_score(dw)
+        assert np.array_equal(scores.cpu().numpy().astype(np.float64), ref)
+        # the library is told the pool is one page smaller; a row naming that (allocated) page
+        # must be rejected on the host, before anything is enqueued
+        cache = m.make_cache(dw.k_pool.data_ptr(), dw.v_pool.data_ptr(), w.num_pages - 1)
+        bad = dw.page_table.clone()
+        bad[1, 0] = w.num_pages - 1
+        bb = m.make_batch(w.batch, bad.data_ptr(), w.max_pages, dw.lengths.data_ptr(), w.lengths)
+        with pytest.raises(m.KvprmError) as e:
+            m.kvprm_score(h, cache, bb, dw.readout(m), ws.data_ptr(), n, scores.data_ptr(), 0, st)
+        assert e.value.status == m.KVPRM_E_INVALID and "page_table" in m.kvprm_last_error()
+    finally:
+        m.kvprm_destroy(h)
