@@ -200,11 +200,15 @@ def main():
         step()
     torch.cuda.synchronize()
     _log(f"warmup done ({args.warmup} steps)")
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         step()
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    per_call = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
     ms = dt * 1e3 / args.steps
     _log(f"timed {args.steps} steps: {ms:.3f} ms/step")
 
@@ -242,6 +246,8 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": measured_traffic(w.name),
                      "avg_us": attn_ms * 1e3, "bytes_per_launch": kv_per_layer},
+        "per_call_ms": {"median": per_call[len(per_call) // 2], "min": per_call[0],
+                        "max": per_call[-1]},
         "copy_reference_gbps": copy_gbps,
     }
     if args.cpu_layers > 0:
