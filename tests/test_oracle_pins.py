@@ -443,3 +443,25 @@ def test_packed_weight_layout():
             l = (r % 16) + 16 * ((k % 32) // 8)
             stored[((kb * (rows // 16) + t) * 64 + l) * 8 + k % 8] = W[r, k]
     assert np.array_equal(ko.unpack_tiled(stored, rows, K), W)
+
+
+def test_split_lse_merge_equals_one_pass_softmax():
+    """Any chunking of the keys, merged by log-sum-exp with the verify token's own key as a
+    last one-element chunk, gives the one-pass attention of the oracle (the identity the
+    split-L kernels rely on)."""
+    d, n = 64, 333
+    q = RNG.normal(size=d) * 3
+    K, V = RNG.normal(size=(n + 1, d)), RNG.normal(size=(n + 1, d))
+    ref = ko.attention(q, K, V)
+    for cuts in ([0, n], [0, 16, 32, 300, n], sorted(set([0, n] + list(RNG.integers(1, n, 7))))):
+        parts = []
+        for a, b in zip(cuts[:-1], cuts[1:]):
+            s = K[a:b] @ q / np.sqrt(d)
+            m = s.max()
+            e = np.exp(s - m)
+            parts.append((m, e.sum(), e @ V[a:b]))
+        s_self = K[n] @ q / np.sqrt(d)
+        M = max([p[0] for p in parts] + [s_self])
+        num = sum(np.exp(m - M) * acc for m, _, acc in parts) + np.exp(s_self - M) * V[n]
+        den = sum(np.exp(m - M) * l for m, l, _ in parts) + np.exp(s_self - M)
+        assert np.allclose(num / den, ref, rtol=0, atol=1e-13)
