@@ -270,10 +270,10 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
     // matrix-core pipeline: five launches per layer
     HIP_TRY(launch_init_mx(dm, p, w, wts->verify_embed, wts->layers[0].attn_norm, b->lengths, s),
             "init");
-    // B <= 8: the output, gate/up and down projections run with their element-wise steps fused
-    // (no split-K partials); the QKV projection stays split-K with a separate rotary kernel,
-    // which measured faster than its fused form
-    const bool fused = p.nt == 1;
+    // B <= 16: the output, gate/up and down projections run with their element-wise steps
+    // fused (no split-K partials); the QKV projection stays split-K with a separate rotary
+    // kernel, which measured faster than its fused form
+    const bool fused = p.nt <= 2;
     for (int l = 0; l < dm.layers; ++l) {
       const kvprm_layer_weights &W = wts->layers[l];
       const void *gamma_next = l + 1 < dm.layers ? wts->layers[l + 1].attn_norm : nullptr;

@@ -104,7 +104,7 @@ hipError_t launch_gateup_mx(const Dims &dm, const Plan &p, const Workspace &w, c
                             const void *wu, hipStream_t s);
 hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
                           const void *gamma_next, hipStream_t s);
-// fused projections for one operand column tile (B <= 8): no split-K partials, the
+// fused projections for one or two operand column tiles (B <= 16): no split-K partials, the
 // element-wise step after the output, gate/up and down projections runs in the epilogue
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
                               const void *gamma_ffn, hipStream_t s);

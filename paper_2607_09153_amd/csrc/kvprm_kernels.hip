@@ -100,9 +100,9 @@ Plan make_plan(const Dims &dm, int B, int max_pages) {
   p.nch = dm.kvdt == 0 ? n_valu : n_mx;
   size_t m = 0;
   if (dm.wdt == 1) {
-    // rows per sum-of-squares block: one 16-row tile for the fused single-tile projections,
-    // 64 for the split-K path
-    p.rb = gemv_nt(B) == 1 ? 16 : 64;
+    // rows per sum-of-squares block: one 16-row tile for the fused projections (B <= 16), 64
+    // for the split-K path
+    p.rb = gemv_nt(B) <= 2 ? 16 : 64;
     p.nt = gemv_nt(B);
     p.bp = gemv_bp(B);
     p.g_qkv = gemv_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B);

@@ -328,19 +328,17 @@ __device__ __forceinline__ float ld_bf16(const void *p, size_t i) {
   return __uint_as_float((uint32_t)((const uint16_t *)p)[i] << 16);
 }
 
-// r_b = 1 / sqrt(mean(x_b^2) + eps) of this lane's candidate b, from the per-row-block sums of
-// squares ss[i][b], computed by the whole wave without LDS or a barrier: with Bq = B rounded up
-// to a power of two, lane l sums rows i = l / Bq, l / Bq + 64 / Bq, ... of candidate l % Bq, a
-// butterfly over the lanes of equal l % Bq completes the sums (identical in every lane and
-// block), and each lane fetches its own candidate's. inv_rms_load issues the first 32 loads of
-// a lane unconditionally (clamped addresses, zero past the end), inv_rms_finish adds any
-// further rows and reduces.
-struct InvRmsLoads {
+// The same for one wave (B <= 8), without LDS or barriers: with Bq = B rounded up to a power
+// of two, lane l sums rows l / Bq, l / Bq + 64 / Bq, ... of candidate l % Bq (32 loads issued by
+// wave_rms_load, any further rows in wave_rms_finish), a butterfly over the lanes of equal
+// l % Bq completes the sums (identical in every lane and block), and each lane takes its own
+// candidate's.
+struct WaveRmsLoads {
   float v[32];
 };
 
-__device__ __forceinline__ void inv_rms_load(const float *__restrict__ ss, int nss, int B,
-                                             InvRmsLoads &ld) {
+__device__ __forceinline__ void wave_rms_load(const float *__restrict__ ss, int nss, int B,
+                                              WaveRmsLoads &ld) {
   const int lane = threadIdx.x & 63;
   int Bq = 1;
   while (Bq < B) Bq <<= 1;
@@ -356,8 +354,8 @@ __device__ __forceinline__ void inv_rms_load(const float *__restrict__ ss, int n
   }
 }
 
-__device__ __forceinline__ float inv_rms_finish(const float *__restrict__ ss, int nss, int B, int b,
-                                               int H, float eps, const InvRmsLoads &ld) {
+__device__ __forceinline__ float wave_rms_finish(const float *__restrict__ ss, int nss, int B, int b,
+                                                 int H, float eps, const WaveRmsLoads &ld) {
   const int lane = threadIdx.x & 63;
   int Bq = 1;
   while (Bq < B) Bq <<= 1;
@@ -373,14 +371,68 @@ __device__ __forceinline__ float inv_rms_finish(const float *__restrict__ ss, in
   return 1.0f / sqrtf(tot / (float)H + eps);
 }
 
-// ---------------------------------------------------- GEMV with fused epilogue (B <= 8)
+// r_b = 1 / sqrt(mean(x_b^2) + eps) for every candidate, computed by a whole block of NTHR
+// threads from the per-row-block sums of squares ss[i][b] into inv_s[b]: with Bq = B rounded up
+// to a power of two, thread t sums rows t / Bq, t / Bq + NTHR / Bq, ... of candidate t % Bq,
+// and the NTHR / Bq partial sums of each candidate are added in a fixed order, so every block
+// gets identical values. rms_load issues a thread's first 16 loads (unconditional, clamped,
+// zero past the end) so that callers can start them early; rms_finish adds any further rows,
+// reduces, and contains two barriers.
+struct RmsLoads {
+  float v[16];
+};
 
-// For one operand column tile (B <= 8: columns b and 8 + b hold the hi and lo halves of
-// candidate b) the projections and the element-wise steps that follow them run in one kernel:
-// a block owns MT row tiles over the whole input; its WPB waves split the input blocks into
-// contiguous ranges (weights double buffered in batches of U, the operand read from memory),
-// the waves' accumulators are added in LDS in a fixed order, and the block applies the
-// epilogue to complete outputs, so no split-K partials cross a kernel boundary.
+template <int NTHR>
+__device__ __forceinline__ void rms_load(const float *__restrict__ ss, int nss, int B,
+                                         RmsLoads &ld) {
+  const int t = threadIdx.x;
+  int Bq = 1;
+  while (Bq < B) Bq <<= 1;
+  const int P = NTHR / Bq;
+  const int b = t & (Bq - 1), part = t / Bq;
+  const bool ok = b < B;
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int i = part + u * P;
+    const bool in = ok && i < nss;
+    const float x = ss[(size_t)(in ? i : 0) * B + (ok ? b : 0)];
+    ld.v[u] = in ? x : 0.f;
+  }
+}
+
+template <int NTHR>
+__device__ __forceinline__ void rms_finish(const float *__restrict__ ss, int nss, int B, int H,
+                                           float eps, const RmsLoads &ld, float *part_s,
+                                           float *inv_s) {
+  const int t = threadIdx.x;
+  int Bq = 1;
+  while (Bq < B) Bq <<= 1;
+  const int P = NTHR / Bq;
+  const int b = t & (Bq - 1), part = t / Bq;
+  float v = 0.f;
+#pragma unroll
+  for (int u = 0; u < 16; ++u) v += ld.v[u];
+  if (b < B)
+    for (int i = part + 16 * P; i < nss; i += P) v += ss[(size_t)i * B + b];
+  part_s[t] = v;
+  __syncthreads();
+  if (t < B) {
+    float s = 0.f;
+    for (int k = 0; k < P; ++k) s += part_s[k * Bq + t];
+    inv_s[t] = 1.0f / sqrtf(s / (float)H + eps);
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------- GEMV with fused epilogue (B <= 16)
+
+// For one or two operand column tiles (B <= 8: columns b and 8 + b of the one tile hold the hi
+// and lo halves of candidate b; B <= 16: tile 0 holds the hi halves, tile 1 the lo halves) the
+// projections and the element-wise steps that follow them run in one kernel: a block owns MT
+// row tiles over the whole input; its WPB waves split the input blocks into contiguous ranges
+// (weights double buffered in batches of U, the operand read from memory), the waves'
+// accumulators are added in LDS in a fixed order, and the block applies the epilogue to
+// complete outputs, so no split-K partials cross a kernel boundary.
 //   EPI_RESID:  one tile: x += y, the tile's sums of squares per candidate, next operand
 //               x * gamma (if gamma).
 //   EPI_SWIGLU: gate tile t and up tile t: h = silu(r g) * (r u) as the down operand.
@@ -391,7 +443,7 @@ struct FusedArgs {
   int seg_rows[3];
   int nseg;
   int K;
-  const uint4 *act;  // operand [K / 32][64] (one column tile)
+  const uint4 *act;  // operand [K / 32][NT][64]
   int B;
   // epilogue
   float *x;                  // residual [B][H] (RESID)
@@ -405,19 +457,17 @@ struct FusedArgs {
   int F;
 };
 
-template <int MT, int WPB, int U, int EPI>
+template <int MT, int NT, int WPB, int U, int EPI>
 __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
-  __shared__ floatx4 red_s[WPB][MT][64];
+  __shared__ floatx4 red_s[WPB][MT][NT][64];
+  __shared__ float part_s[64 * WPB];
+  __shared__ float inv_s[16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int B = a.B;
   // global row tiles of this block
   int tile[MT];
-  if (EPI == EPI_SWIGLU) {
-    tile[0] = blockIdx.x;
-    if (MT > 1) tile[MT - 1] = blockIdx.x + a.F / 16;
-  } else {
-    tile[0] = blockIdx.x;
-  }
+  tile[0] = blockIdx.x;
+  if (EPI == EPI_SWIGLU && MT > 1) tile[MT - 1] = blockIdx.x + a.F / 16;
   const uint4 *wt[MT];
   size_t kstride[MT];
 #pragma unroll
@@ -433,29 +483,37 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   const int per = (nkb + WPB - 1) / WPB;
   const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
   const uint4 *ap = a.act + lane;
-  // the epilogue's sums of squares are fetched now and used after the product
-  InvRmsLoads il;
-  if (EPI != EPI_RESID && wave == 0) inv_rms_load(a.ss, a.nss, B, il);
-  floatx4 acc[MT];
+  // the epilogue's sums of squares are fetched now and used after the product: by wave 0
+  // alone for one column tile (B <= 8), by the whole block for two
+  WaveRmsLoads wl;
+  RmsLoads rl;
+  if (EPI == EPI_SWIGLU && NT == 1 && wave == 0) wave_rms_load(a.ss, a.nss, B, wl);
+  if (EPI == EPI_SWIGLU && NT == 2) rms_load<64 * WPB>(a.ss, a.nss, B, rl);
+  floatx4 acc[MT][NT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
-  auto load_batch = [&](int kb, uint4(&av)[U][MT], uint4(&bv)[U]) {
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto load_batch = [&](int kb, uint4(&av)[U][MT], uint4(&bv)[U][NT]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
 #pragma unroll
       for (int m = 0; m < MT; ++m) av[u][m] = wt[m][(size_t)(kb + u) * kstride[m]];
-      bv[u] = ap[(size_t)(kb + u) * 64];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) bv[u][t] = ap[((size_t)(kb + u) * NT + t) * 64];
     }
   };
-  auto mma_batch = [&](const uint4(&av)[U][MT], const uint4(&bv)[U]) {
+  auto mma_batch = [&](const uint4(&av)[U][MT], const uint4(&bv)[U][NT]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int m = 0; m < MT; ++m) acc[m] = mfma16(av[u][m], bv[u], acc[m]);
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av[u][m], bv[u][t], acc[m][t]);
   };
   const int nbat = (kb1 - kb0) / U;
   if (nbat > 0) {
-    uint4 a0[U][MT], a1[U][MT], b0[U], b1[U];
+    uint4 a0[U][MT], a1[U][MT], b0[U][NT], b1[U][NT];
     load_batch(kb0, a0, b0);
     int i = 0;
     for (; i + 2 <= nbat; i += 2) {
@@ -471,32 +529,43 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
     if (i < nbat) mma_batch(a0, b0);
   }
   for (int kb = kb0 + nbat * U; kb < kb1; ++kb) {
-    const uint4 bv = ap[(size_t)kb * 64];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) acc[m] = mfma16(wt[m][(size_t)kb * kstride[m]], bv, acc[m]);
+    for (int t = 0; t < NT; ++t) {
+      const uint4 bv = ap[((size_t)kb * NT + t) * 64];
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m][t] = mfma16(wt[m][(size_t)kb * kstride[m]], bv, acc[m][t]);
+    }
   }
 #pragma unroll
-  for (int m = 0; m < MT; ++m) red_s[wave][m][lane] = acc[m];
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) red_s[wave][m][t][lane] = acc[m][t];
   __syncthreads();
+  if (EPI == EPI_SWIGLU && NT == 2) rms_finish<64 * WPB>(a.ss, a.nss, B, a.H, a.eps, rl, part_s, inv_s);
   if (wave != 0) return;
-  // fixed-order sum over the waves, then hi + lo of candidate n = lane % 16 (< 8)
+  // fixed-order sum over the waves, then hi + lo of candidate n = lane % 16
   const int n = lane & 15, cq = lane >> 4;
   float y[MT][4];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
-    floatx4 t = red_s[0][m][lane];
+    floatx4 tt[NT];
 #pragma unroll
-    for (int w = 1; w < WPB; ++w) {
-      const floatx4 v = red_s[w][m][lane];
-      t[0] += v[0];
-      t[1] += v[1];
-      t[2] += v[2];
-      t[3] += v[3];
+    for (int t = 0; t < NT; ++t) {
+      tt[t] = red_s[0][m][t][lane];
+#pragma unroll
+      for (int w = 1; w < WPB; ++w) {
+        const floatx4 v = red_s[w][m][t][lane];
+        tt[t][0] += v[0];
+        tt[t][1] += v[1];
+        tt[t][2] += v[2];
+        tt[t][3] += v[3];
+      }
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) y[m][i] = t[i] + __shfl_xor(t[i], 8, 64);
+    for (int i = 0; i < 4; ++i)
+      y[m][i] = NT == 1 ? tt[0][i] + __shfl_xor(tt[0][i], 8, 64) : tt[0][i] + tt[NT - 1][i];
   }
-  const bool cand_ok = n < 8 && n < B;
+  const bool cand_ok = NT == 1 ? (n < 8 && n < B) : n < B;
   const int b = cand_ok ? n : 0;
   if (EPI == EPI_RESID) {
     float sq = 0.f;
@@ -515,15 +584,13 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
     sq += __shfl_xor(sq, 16, 64);
     sq += __shfl_xor(sq, 32, 64);
     if (cand_ok && cq == 0) a.ss[(size_t)tile[0] * B + b] = sq;
-  } else {
-    const float inv = inv_rms_finish(a.ss, a.nss, B, b, a.H, a.eps, il);
-    {  // EPI_SWIGLU
+  } else {  // EPI_SWIGLU
+    const float inv = NT == 1 ? wave_rms_finish(a.ss, a.nss, B, b, a.H, a.eps, wl) : inv_s[b];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int f = tile[0] * 16 + 4 * cq + i;
-        const float gv = y[0][i] * inv, uv = y[MT - 1][i] * inv;
-        if (cand_ok) store_operand(a.op, a.NT, a.Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
-      }
+    for (int i = 0; i < 4; ++i) {
+      const int f = tile[0] * 16 + 4 * cq + i;
+      const float gv = y[0][i] * inv, uv = y[MT - 1][i] * inv;
+      if (cand_ok) store_operand(a.op, a.NT, a.Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
     }
   }
 }
@@ -550,12 +617,14 @@ __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ pa
   ksum_load<NMAX>(part, ksp, i1, v1);
   ksum_load<NMAX>(part, ksp, i2, v2);
   const float2 csn = *(const float2 *)(rope + ((size_t)b * hd + i) * 2);
-  InvRmsLoads il;
-  inv_rms_load(ss, nss, B, il);
+  RmsLoads rl;
+  rms_load<256>(ss, nss, B, rl);
+  __shared__ float part_s[256], inv_s[64];
+  rms_finish<256>(ss, nss, B, H, eps, rl, part_s, inv_s);
   const float x1 = ksum_add<NMAX>(part, ksp, ksplit, i1, v1);
   const float x2 = ksum_add<NMAX>(part, ksp, ksplit, i2, v2);
   const float cs = csn.x, sn = csn.y;
-  const float inv = inv_rms_finish(ss, nss, B, b, H, eps, il);
+  const float inv = inv_s[b];
   if (!act) return;
   const float y1 = x1 * inv, y2 = x2 * inv;
   float o1 = y1, o2 = y2;
@@ -621,11 +690,13 @@ __global__ __launch_bounds__(256) void k_swiglu_mx(const float *__restrict__ par
   float4 vg[NMAX], vu[NMAX];
   ksum_load<NMAX>(part, ksp, ig, vg);
   ksum_load<NMAX>(part, ksp, iu, vu);
-  InvRmsLoads il;
-  inv_rms_load(ss, nss, B, il);
+  RmsLoads rl;
+  rms_load<256>(ss, nss, B, rl);
+  __shared__ float part_s[256], inv_s[64];
+  rms_finish<256>(ss, nss, B, H, eps, rl, part_s, inv_s);
   const float g = ksum_add<NMAX>(part, ksp, ksplit, ig, vg);
   const float u = ksum_add<NMAX>(part, ksp, ksplit, iu, vu);
-  const float inv = inv_rms_finish(ss, nss, B, b, H, eps, il);
+  const float inv = inv_s[b];
   if (!act) return;
   const float gv = g * inv, uv = u * inv;
   store_operand(op, NT, Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
@@ -1296,7 +1367,7 @@ hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   return launch_resid_mx(dm, p, w, p.g_d, gamma_next, s);
 }
 
-// fused projections (one operand column tile, B <= 8)
+// fused projections (one or two operand column tiles, B <= 16)
 static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, int K,
                             const uint16_t *act) {
   FusedArgs a;
@@ -1323,7 +1394,10 @@ hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w,
   a.nseg = 1;
   a.gamma = gamma_ffn;
   a.op = w.opA;
-  hipLaunchKernelGGL((k_gemv_fused<1, 16, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 16), 0, s, a);
+  if (p.nt == 1)
+    hipLaunchKernelGGL((k_gemv_fused<1, 1, 16, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 16), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_gemv_fused<1, 2, 8, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 8), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1336,7 +1410,10 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
   a.seg_rows[1] = dm.F;
   a.nseg = 2;
   a.op = w.opD;
-  hipLaunchKernelGGL((k_gemv_fused<2, 4, 4, EPI_SWIGLU>), dim3(dm.F / 16), dim3(64 * 4), 0, s, a);
+  if (p.nt == 1)
+    hipLaunchKernelGGL((k_gemv_fused<2, 1, 4, 4, EPI_SWIGLU>), dim3(dm.F / 16), dim3(64 * 4), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_gemv_fused<2, 2, 4, 4, EPI_SWIGLU>), dim3(dm.F / 16), dim3(64 * 4), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1348,7 +1425,10 @@ hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, 
   a.nseg = 1;
   a.gamma = gamma_next;
   a.op = w.opA;
-  hipLaunchKernelGGL((k_gemv_fused<1, 16, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 16), 0, s, a);
+  if (p.nt == 1)
+    hipLaunchKernelGGL((k_gemv_fused<1, 1, 16, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 16), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_gemv_fused<1, 2, 8, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 8), 0, s, a);
   return hipGetLastError();
 }
 
