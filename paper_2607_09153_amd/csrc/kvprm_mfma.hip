@@ -1275,7 +1275,8 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
   a.ksp = (gp.ksplit + 3) & ~3;
   const int mt = gemv_mt(p.nt);
   // 4 waves per block; the operand k-slice is staged in LDS for one column tile and read
-  // straight from memory (L2) for more (measured faster: the staging would cap residency)
+  // straight from memory (L2) for more (measured faster than staging it: LDS would cap
+  // residency, and an LDS-streamed variant with 8 row tiles per block measured slower)
   constexpr int WPB = 4;
   const bool direct = p.nt >= 2;
   dim3 grid((gp.rows / 16 + WPB * mt - 1) / (WPB * mt), gp.ksplit);

@@ -201,6 +201,17 @@ def test_score_parity_7b_two_layers_bf16():
     _parity(w, 2e-3, 2e-2)
 
 
+@pytest.mark.parametrize("B", [9, 17, 40, 64])
+def test_score_parity_batch_sizes_bf16(B):
+    """One, two, four, six and eight operand column tiles (fused and split-K projections)."""
+    _say(f"case: score 7B shape, 2 layers, bf16, B={B}")
+    import dataclasses
+    shape = dataclasses.replace(synth.B7, num_layers=2)
+    lengths = [(37 * i * i + 11 * i) % 700 for i in range(B)]
+    w = synth.make_workload("custom", shape=shape, lengths=lengths, seed=90 + B)
+    _parity(w, 2e-3, 2e-2)
+
+
 def test_score_deterministic_and_batch_zero():
     _say("case: determinism + B=0")
     w = synth.make_workload("custom", shape=synth.TINY, lengths=[100, 513, 7], seed=80)
