@@ -1084,9 +1084,12 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
   // the pair being computed sits in one of two LDS buffers. Fetches past the last pair repeat
   // it (an L2 hit), so that no load is conditional.
   constexpr int PER = (4 * TILE16 + nthr - 1) / nthr;
-  constexpr int NPF = 4;
-  uint4 st[NPF][PER];
-  auto fetch = [&](int pp, uint4(&dst)[PER]) {
+  constexpr int NPF = KVT == 2 ? 2 : 4;  // pairs in flight (fp8 unpacking needs the registers)
+  struct Stage {
+    uint4 v[PER];
+  };
+  auto fetch = [&](int pp) __attribute__((always_inline)) {
+    Stage st;
     pp = min(pp, npairs - 1);
     const int pa = lane_value(ph_l, min(2 * pp, np - 1));
     const int pb = lane_value(ph_l, min(2 * pp + 1, np - 1));
@@ -1096,58 +1099,74 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
       const int t = e / TILE16, o = e - t * TILE16;
       const char *pool = t < 2 ? a.kp : a.vp;
       const int pg = (t & 1) ? pb : pa;
-      dst[u] = ((const uint4 *)(pool + ((size_t)pg * nkv + j) * TILE16 * 16))[o];
+      st.v[u] = ((const uint4 *)(pool + ((size_t)pg * nkv + j) * TILE16 * 16))[o];
     }
+    return st;
   };
-  auto stash = [&](int buf, const uint4(&src)[PER]) {
+  auto stash = [&](int buf, const Stage &src) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = threadIdx.x + u * nthr;
-      if (e < 4 * TILE16) (&stage_s[buf][0][0])[e] = src[u];
+      if (e < 4 * TILE16) (&stage_s[buf][0][0])[e] = src.v[u];
     }
   };
-#pragma unroll
-  for (int k = 0; k < NPF; ++k) fetch(k, st[k]);
+  // the ring of NPF register buffers is four named values, so that every index is a constant
+  Stage s0 = fetch(0), s1 = fetch(1), s2, s3;
+  if (NPF == 4) {
+    s2 = fetch(2);
+    s3 = fetch(3);
+  }
   uint4 qhi[NKB], qmd[NKB], qlo[NKB];
   load_query_ops<KVT, D>(a.q + ((size_t)bcand * nq + (size_t)j * g + hh) * D, present, cq, qhi,
                          qmd, qlo);
-  stash(0, st[0]);
+  stash(0, s0);
   __syncthreads();
   const float rs = kLog2e / sqrtf((float)D);  // scores in log2 units
   float m_run = -INFINITY, l_run = 0.f;
   floatx4 acc[NDB];
 #pragma unroll
   for (int nb = 0; nb < NDB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-  for (int pbase = 0; pbase < npairs; pbase += NPF) {
+  // step pp: refill the buffer pair pp left (with pair pp + NPF), compute pair pp from LDS, and
+  // stash pair pp + 1 (fetched NPF - 1 steps earlier) into the other LDS buffer
+  auto step = [&](int pp, Stage &mine, const Stage &next) __attribute__((always_inline)) {
+    mine = fetch(pp + NPF);
+    const int buf = pp & 1;
+    PairRaw<D> r;
+    load_pair_raw<KVT, D>(stage_s[buf][0], stage_s[buf][1], stage_s[buf][2], stage_s[buf][3], lane,
+                          r);
+    uint4 KA[NKB], KB[NKB];
+    uint2 VA[NDB], VB[NDB];
+    unpack_pair<KVT, D>(r, KA, KB, VA, VB);
+    const int la = 2 * pp, lb = 2 * pp + 1;
+    const bool hasB = lb < np;
+    bool ok[8];
 #pragma unroll
-    for (int k = 0; k < NPF; ++k) {
-      const int pp = pbase + k;
-      if (pp < npairs) {
-        fetch(pp + NPF, st[k]);  // pair pp left st[k] for LDS in the previous step
-        const int buf = k & 1;   // == pp & 1 (NPF is even)
-        PairRaw<D> r;
-        load_pair_raw<KVT, D>(stage_s[buf][0], stage_s[buf][1], stage_s[buf][2], stage_s[buf][3],
-                              lane, r);
-        uint4 KA[NKB], KB[NKB];
-        uint2 VA[NDB], VB[NDB];
-        unpack_pair<KVT, D>(r, KA, KB, VA, VB);
-        const int la = 2 * pp, lb = 2 * pp + 1;
-        const bool hasB = lb < np;
-        bool ok[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          ok[i] = true;  // prefix pages are full
-          ok[4 + i] = hasB;
-        }
-        const int lbc = hasB ? lb : la;
-        const float sca = (KVT == 2) ? lane_value(ksc_l, la) * rs : rs;
-        const float scb = (KVT == 2) ? lane_value(ksc_l, lbc) * rs : rs;
-        const float vsa = (KVT == 2) ? lane_value(vsc_l, la) : 1.f;
-        const float vsb = (KVT == 2) ? lane_value(vsc_l, lbc) : 1.f;
-        online_step<D>(KA, KB, VA, VB, qhi, qmd, qlo, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
-        if (pp + 1 < npairs) stash(buf ^ 1, st[(k + 1) % NPF]);
-        __syncthreads();
-      }
+    for (int i = 0; i < 4; ++i) {
+      ok[i] = true;  // prefix pages are full
+      ok[4 + i] = hasB;
+    }
+    const int lbc = hasB ? lb : la;
+    const float sca = (KVT == 2) ? lane_value(ksc_l, la) * rs : rs;
+    const float scb = (KVT == 2) ? lane_value(ksc_l, lbc) * rs : rs;
+    const float vsa = (KVT == 2) ? lane_value(vsc_l, la) : 1.f;
+    const float vsb = (KVT == 2) ? lane_value(vsc_l, lbc) : 1.f;
+    online_step<D>(KA, KB, VA, VB, qhi, qmd, qlo, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
+    if (pp + 1 < npairs) stash(buf ^ 1, next);
+    __syncthreads();
+  };
+  for (int pb = 0; pb < npairs; pb += NPF) {
+    if (NPF == 2) {
+      step(pb, s0, s1);
+      if (pb + 1 >= npairs) break;
+      step(pb + 1, s1, s0);
+    } else {
+      step(pb, s0, s1);
+      if (pb + 1 >= npairs) break;
+      step(pb + 1, s1, s2);
+      if (pb + 2 >= npairs) break;
+      step(pb + 2, s2, s3);
+      if (pb + 3 >= npairs) break;
+      step(pb + 3, s3, s0);
     }
   }
   l_run += __shfl_xor(l_run, 16, 64);
