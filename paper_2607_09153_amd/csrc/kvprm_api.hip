@@ -110,8 +110,8 @@ static kvprm_status check_batch(const kvprm_handle h, const kvprm_batch *b, cons
   if (!b->page_table || !b->lengths) return fail(KVPRM_E_INVALID, "%s: null page_table or lengths", fn);
   if (b->max_pages < 1) return fail(KVPRM_E_INVALID, "%s: max_pages < 1", fn);
   // chunk slots per candidate: one per chunk of max_pages, plus one where a shared prefix
-  // splits a chunk (the longest chunk is 64 pages, 32 on the vector-ALU path)
-  const int max_mp = (kMaxChunks - 2) * (h->dm.kvdt == 0 ? kChunkPagesValu : 64);
+  // splits a chunk (chunks of 16 pages at the shortest, 32 on the vector-ALU path)
+  const int max_mp = (kMaxChunks - 2) * (h->dm.kvdt == 0 ? kChunkPagesValu : 16);
   if (b->max_pages > max_mp)
     return fail(KVPRM_E_UNSUPPORTED, "%s: max_pages above %d", fn, max_mp);
   const int cap = b->max_pages * h->desc.page_size;
@@ -198,31 +198,55 @@ static kvprm_status check_ws(const kvprm_handle h, const kvprm_batch *b, void *w
   return KVPRM_OK;
 }
 
+// Longest chunk (16, 32 or 64 pages) that leaves at least 160 work items for `pages` pages.
+static int chunk_shift_for(long long pages) {
+  int sh = 6;
+  while (sh > 4 && pages < (160LL << sh)) --sh;
+  return sh;
+}
+
 // Launch table of the attention kernels. The prefix-sharing hint is used by the matrix-core
 // attention only (fp32 caches take the vector-ALU path, which reads every page per candidate)
 // and only for up to kMaxGroups groups; otherwise it is ignored, which changes nothing but
-// speed. With lengths on the host, the chunk grid of the private pages is sized to the longest
-// private range instead of max_pages.
+// speed. With lengths on the host, the chunk lengths are chosen from the pages each kernel
+// actually reads (private pages; group prefixes times their column blocks and kv-heads), and
+// the chunk grid of the private pages is sized to the longest private range; without them the
+// plan's chunk (from batch and max_pages) serves both.
 static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b, const Plan &p) {
-  const int CP = 1 << p.cshift;
   GroupTable gt;
   memset(&gt, 0, sizeof gt);
+  gt.cshift_prefix = gt.cshift_private = p.cshift;
   const bool share = h->dm.kvdt != 0 && b->num_groups > 0 && b->num_groups <= kMaxGroups;
   if (share) {
     gt.n = b->num_groups;
     for (int i = 0; i <= gt.n; ++i) gt.start[i] = b->group_start_host[i];
     const int cols_per_block = 16 * kPrefixWaves;
+    long long items = 0;  // prefix pages x column blocks (per kv-head)
     for (int i = 0; i < gt.n; ++i) {
       const int pp = b->group_prefix_len_host[i] / kPage;
       const int members = gt.start[i + 1] - gt.start[i];
       gt.prefix_pages[i] = pp;
       const int blocks = pp > 0 ? (members * h->dm.g + cols_per_block - 1) / cols_per_block : 0;
       gt.colblock_start[i + 1] = gt.colblock_start[i] + blocks;
-      const int ch = (pp + CP - 1) / CP;
+      items += (long long)pp * blocks;
+    }
+    // the hint requires host lengths (checked), so the chunks follow the actual work
+    gt.cshift_prefix = chunk_shift_for(items * h->dm.nkv);
+    for (int i = 0; i < gt.n; ++i) {
+      const int ch = (gt.prefix_pages[i] + (1 << gt.cshift_prefix) - 1) >> gt.cshift_prefix;
       if (ch > gt.prefix_chunks) gt.prefix_chunks = ch;
     }
   }
   if (b->lengths_host) {
+    long long priv_total = 0;
+    for (int i = 0; i < b->batch; ++i) {
+      int first = 0;
+      for (int k = 0; k < gt.n; ++k)
+        if (i >= gt.start[k] && i < gt.start[k + 1]) first = gt.prefix_pages[k];
+      priv_total += (b->lengths_host[i] + kPage - 1) / kPage - first;
+    }
+    gt.cshift_private = chunk_shift_for(priv_total);
+    const int CP = 1 << gt.cshift_private;
     int most = 1;
     for (int i = 0; i < b->batch; ++i) {
       int first = 0;

@@ -24,6 +24,7 @@ struct GroupTable {
   int colblock_start[kMaxGroups + 1];  // shared-prefix column blocks of the groups, cumulative
   int prefix_chunks;                   // chunks of the longest group prefix
   int private_chunks;                  // chunk grid of the private pages (0 = from max_pages)
+  int cshift_prefix, cshift_private;   // chunk lengths (1 << shift pages) of the two kernels
 };
 
 // Attention split: each work item covers one chunk of pages of one candidate (and kv-head).
@@ -59,7 +60,7 @@ struct GemvPlan {
 
 struct Plan {
   int B, max_pages, nch;      // nch = chunk slots per (candidate, q-head), see make_plan
-  int cshift;                 // matrix-core attention chunk = 1 << cshift pages
+  int cshift;                 // matrix-core attention chunk from (B, max_pages): 1 << cshift pages
   int nss;                    // row blocks of H that carry partial sums of squares
   int rb;                     // rows per such block
   // vector-ALU path

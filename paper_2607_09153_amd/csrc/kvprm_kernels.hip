@@ -92,10 +92,11 @@ Plan make_plan(const Dims &dm, int B, int max_pages) {
   // kMaxChunks - 2 chunks per candidate.
   p.cshift = 6;
   while (p.cshift > 4 && (long long)B * max_pages < (160LL << p.cshift)) --p.cshift;
-  while (p.cshift < 6 && (max_pages >> p.cshift) + 2 > kMaxChunks) ++p.cshift;
-  // chunk slots: chunks of max_pages plus one (a shared prefix that ends inside a chunk adds
-  // one), for whichever attention path runs
-  const int n_mx = ((max_pages + (1 << p.cshift) - 1) >> p.cshift) + 1;
+
+  // chunk slots: chunks of max_pages at the shortest chunk (16 pages: the call may pick shorter
+  // chunks than the plan from the host lengths) plus one (a shared prefix that ends inside a
+  // chunk adds one), for whichever attention path runs
+  const int n_mx = ((max_pages + 15) >> 4) + 1;
   const int n_valu = (max_pages + kChunkPagesValu - 1) / kChunkPagesValu + 1;
   p.nch = dm.kvdt == 0 ? n_valu : n_mx;
   size_t m = 0;

@@ -930,7 +930,6 @@ struct AttnArgs {
   GroupTable gt;
   int nch;
   const float *q, *kself, *vself;
-  int cshift;     // chunk = 1 << cshift pages
   float *apart;   // [B][nq][nch][D + 2]: per chunk the acc row, then m, then l; a candidate's
                   // shared-prefix chunks come first, its private chunks after them
   float *o;       // [B][nq][D] fp32 output (may be null)
@@ -961,8 +960,8 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   int first = 0;
   for (int gi = 0; gi < a.gt.n; ++gi)
     if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
-  const int CP = 1 << a.cshift;
-  const int ncp = (first + CP - 1) >> a.cshift;  // this candidate's prefix chunks
+  const int CP = 1 << a.gt.cshift_private;
+  const int ncp = (first + (1 << a.gt.cshift_prefix) - 1) >> a.gt.cshift_prefix;  // prefix chunks
   const int p0 = first + c * CP;
   if (p0 >= npages) return;
   const int np = min(npages, p0 + CP) - p0;
@@ -1059,7 +1058,7 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
   const int cb = blockIdx.z - a.gt.colblock_start[grp];
   const int m0 = a.gt.start[grp], members = a.gt.start[grp + 1] - m0;
   const int ppages = a.gt.prefix_pages[grp];
-  const int CP = 1 << a.cshift;
+  const int CP = 1 << a.gt.cshift_prefix;
   const int p0 = c * CP;
   if (p0 >= ppages) return;
   const int np = min(ppages, p0 + CP) - p0;
@@ -1200,8 +1199,8 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
   for (int gi = 0; gi < a.gt.n; ++gi)
     if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
   // shared-prefix chunks, then private chunks
-  const int CP = 1 << a.cshift;
-  const int nc = ((first + CP - 1) >> a.cshift) + ((npages - first + CP - 1) >> a.cshift);
+  const int sp = a.gt.cshift_prefix, sv = a.gt.cshift_private;
+  const int nc = ((first + (1 << sp) - 1) >> sp) + ((npages - first + (1 << sv) - 1) >> sv);
   const float *base = a.apart + ((size_t)b * a.nq + h) * a.nch * (D + 2);
   float rv[R];
 #pragma unroll
@@ -1471,7 +1470,6 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   a.lengths = lengths;
   a.gt = gt;
   a.nch = p.nch;
-  a.cshift = p.cshift;
   a.q = q;
   a.kself = kself;
   a.vself = vself;
