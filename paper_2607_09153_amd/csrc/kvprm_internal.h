@@ -75,7 +75,7 @@ struct Plan {
 // matrix-core helpers (kvprm_mfma.hip)
 int gemv_nt(int B);
 int gemv_bp(int B);
-int gemv_mt(int nt);
+int gemv_mt(int nt, int rows);
 hipError_t launch_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, hipStream_t s);
 
 Plan make_plan(const Dims &dm, int B, int max_pages);

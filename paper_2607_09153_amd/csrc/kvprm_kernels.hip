@@ -68,7 +68,7 @@ static GemvPlan gemv_plan(int rows, int K, int B) {
   g.rows = rows;
   g.K = K;
   const int nt = gemv_nt(B);
-  const int mt = gemv_mt(nt);
+  const int mt = gemv_mt(nt, rows);
   const int waves = (rows / 16 + mt - 1) / mt;
   const int nkb = K / 32;
   int want = (nkb + 31) / 32;

@@ -117,7 +117,9 @@ __device__ __forceinline__ float bmax(float v, float *red) {
 }
 
 int gemv_nt(int B) { return B <= 8 ? 1 : 2 * ((B + 15) / 16); }
-int gemv_mt(int nt) { return nt >= 2 ? 2 : 1; }
+// row tiles per wave of the split-K GEMV: two (sharing each operand load) for several operand
+// column tiles and many rows; one otherwise (more waves for the short projections)
+int gemv_mt(int nt, int rows) { return nt >= 2 && rows >= 8192 ? 2 : 1; }
 int gemv_bp(int B) { return B <= 8 ? 8 : 16 * ((B + 15) / 16); }
 
 // ------------------------------------------------------------------------------- init
@@ -1291,7 +1293,7 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
   a.B = p.B;
   a.part = part;
   a.ksp = (gp.ksplit + 3) & ~3;
-  const int mt = gemv_mt(p.nt);
+  const int mt = gemv_mt(p.nt, gp.rows);
   // 4 waves per block; the operand k-slice is staged in LDS for one column tile and read
   // straight from memory (L2) for more (measured faster than staging it: LDS would cap
   // residency, and an LDS-streamed variant with 8 row tiles per block measured slower)
@@ -1304,14 +1306,21 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
     hipLaunchKernelGGL((k_gemv_mx<MT_, NT_, U_, WPB, true>), grid, dim3(64 * WPB), lds, s, a); \
   else                                                                                         \
     hipLaunchKernelGGL((k_gemv_mx<MT_, NT_, U_, WPB, false>), grid, dim3(64 * WPB), lds, s, a)
+#define KVPRM_G2(NT_, U_) \
+  if (mt == 2) {          \
+    KVPRM_G(2, NT_, U_);  \
+  } else {                \
+    KVPRM_G(1, NT_, U_);  \
+  }
   switch (p.nt) {
     case 1: KVPRM_G(1, 1, 4); break;
-    case 2: KVPRM_G(2, 2, 4); break;
-    case 4: KVPRM_G(2, 4, 2); break;
-    case 6: KVPRM_G(2, 6, 2); break;
-    case 8: KVPRM_G(2, 8, 2); break;
+    case 2: KVPRM_G2(2, 4); break;
+    case 4: KVPRM_G2(4, 2); break;
+    case 6: KVPRM_G2(6, 2); break;
+    case 8: KVPRM_G2(8, 2); break;
     default: return hipErrorInvalidValue;
   }
+#undef KVPRM_G2
 #undef KVPRM_G
   return hipGetLastError();
 }
