@@ -108,14 +108,8 @@ __device__ __forceinline__ float bsum(float v, float *red) {
   return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-__device__ __forceinline__ float bmax(float v, float *red) {
-  v = wmax(v);
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-}
-
+// operand column tiles for B candidates: one (hi in columns 0..7, lo in 8..15) up to 8, else
+// hi and lo tiles of 16 candidates each
 int gemv_nt(int B) { return B <= 8 ? 1 : 2 * ((B + 15) / 16); }
 // row tiles per wave of the split-K GEMV: two (sharing each operand load) for several operand
 // column tiles and many rows; one otherwise (more waves for the short projections)
@@ -124,7 +118,7 @@ int gemv_bp(int B) { return B <= 8 ? 8 : 16 * ((B + 15) / 16); }
 
 // ------------------------------------------------------------------------------- init
 
-// x_b = e_v, the sums of squares per 64-row block, the QKV operand e_v * gamma_attn(0), and the
+// x_b = e_v, the sums of squares per RB-row block, the QKV operand e_v * gamma_attn(0), and the
 // rotary table cos/sin(L_b theta^(-2i/d)) (angles in fp64).
 __global__ __launch_bounds__(256) void k_init_mx(float *x, float *ss, int RB, const void *ev,
                                                  const void *gamma0, int wdt, int B, int H,
