@@ -7,8 +7,9 @@ L_b ~ U[16384, 32768] on 16-token pages scattered over a pool. Inputs are synthe
 generator) and resident in HBM before the timed region.
 
 Prints one JSON line: scores/s (value), the end-to-end KV-read rate, the roofline of the
-dominant kernel (the split-L attention step, timed live with HIP events on its stream) and the
-fp64 CPU oracle timed on a bounded sample of the same workload.
+dominant kernel (the split-L attention chunk kernel, timed live with HIP events on its stream;
+the whole attention step with its merge is reported beside it) and the fp64 CPU oracle timed on
+a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -35,10 +36,10 @@ def algorithmic_bytes(w, dw):
     return kv_bytes, dw.weight_bytes()
 
 
-def time_attention_step(kv, dw, h, batch, ws, n, reps):
-    """Average duration of the attention step (split-L partial kernel + merge kernel) of one
-    layer: `reps` back-to-back calls between two HIP events recorded on the stream the kernels
-    are launched on."""
+def time_attention(kv, dw, h, batch, ws, n, reps):
+    """Average durations (ms) of one layer's split-L chunk kernel alone (kvprm_attention_partials)
+    and of the whole attention step (chunk kernel + merge, kvprm_attention): `reps` back-to-back
+    calls each between two HIP events recorded on the stream the kernels are launched on."""
     import torch
     w = dw.w
     s = w.shape
@@ -49,20 +50,27 @@ def time_attention_step(kv, dw, h, batch, ws, n, reps):
     stream = torch.cuda.current_stream()
     cache = dw.cache(kv)
 
-    def call(layer):
+    def step(layer):
         kv.kvprm_attention(h, cache, batch, layer, q.data_ptr(), ks.data_ptr(), vs.data_ptr(),
                            ws.data_ptr(), n, o.data_ptr(), stream.cuda_stream)
 
-    for l in range(s.num_layers):
-        call(l)
-    torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(stream)
-    for i in range(reps):  # back to back, cycling through the layers' pools
-        call(i % s.num_layers)
-    b.record(stream)
-    torch.cuda.synchronize()
-    return a.elapsed_time(b) / reps
+    def partials(layer):
+        kv.kvprm_attention_partials(h, cache, batch, layer, q.data_ptr(), ws.data_ptr(), n,
+                                    stream.cuda_stream)
+
+    def timed(call):
+        for l in range(s.num_layers):
+            call(l)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(reps):  # back to back, cycling through the layers' pools
+            call(i % s.num_layers)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    return timed(partials), timed(step)
 
 
 def copy_bandwidth(nbytes=4 << 30, reps=10):
@@ -137,9 +145,10 @@ def attention_source_hash():
 
 
 def measured_traffic(workload):
-    """HBM bytes per attention step from the committed FETCH_SIZE / WRITE_SIZE summary, scaled
-    by the copy-kernel calibration recorded there; None when the summary is for another
-    workload or the attention sources have changed since the counters were taken."""
+    """HBM bytes per launch of the attention chunk kernel from the committed FETCH_SIZE /
+    WRITE_SIZE summary, scaled by the copy-kernel calibration recorded there; None when the
+    summary is for another workload or the attention sources have changed since the counters
+    were taken."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     kv = {}
@@ -149,7 +158,7 @@ def measured_traffic(workload):
             kv[k.strip()] = v.strip()
     if kv.get("workload") != workload or kv.get("source_sha256") != attention_source_hash():
         return None
-    return float(kv["traffic_bytes_per_step"])
+    return float(kv["traffic_bytes_per_launch"])
 
 
 def main():
@@ -212,10 +221,11 @@ def main():
     ms = dt * 1e3 / args.steps
     _log(f"timed {args.steps} steps: {ms:.3f} ms/step")
 
-    attn_ms = time_attention_step(kv, dw, h, batch, ws, n, max(args.attn_reps, 1))
+    kernel_ms, step_ms = time_attention(kv, dw, h, batch, ws, n, max(args.attn_reps, 1))
     kv_per_layer = kv_bytes / w.shape.num_layers
-    achieved = kv_per_layer / (attn_ms * 1e-3) / 1e9
-    _log(f"attention step: {attn_ms * 1e3:.1f} us/layer, {achieved:.0f} GB/s")
+    achieved = kv_per_layer / (kernel_ms * 1e-3) / 1e9
+    _log(f"attention chunk kernel: {kernel_ms * 1e3:.1f} us/layer, {achieved:.0f} GB/s; "
+         f"attention step with merge: {step_ms * 1e3:.1f} us/layer")
     kv.kvprm_destroy(h)
     copy_gbps = copy_bandwidth()
     _log(f"device copy reference: {copy_gbps:.0f} GB/s")
@@ -241,11 +251,15 @@ def main():
         "kv_read_gbps": kv_bytes / (ms * 1e-3) / 1e9,
         "end_to_end_gbps": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9,
         "bytes_per_call": {"kv": kv_bytes, "weights": w_bytes},
-        "roofline": {"kernel": "split-L paged attention step (partials + merge), one layer",
+        "roofline": {"kernel": ("k_attn_mx: split-L paged attention chunk kernel, one layer"
+                                + (" (with the shared-prefix kernel)" if w.group_start else "")),
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": measured_traffic(w.name),
-                     "avg_us": attn_ms * 1e3, "bytes_per_launch": kv_per_layer},
+                     "avg_us": kernel_ms * 1e3, "bytes_per_launch": kv_per_layer},
+        "attention_step": {"kernels": "chunk kernel + merge (kvprm_attention), one layer",
+                           "avg_us": step_ms * 1e3,
+                           "kv_gbps": kv_per_layer / (step_ms * 1e-3) / 1e9},
         "per_call_ms": {"median": per_call[len(per_call) // 2], "min": per_call[0],
                         "max": per_call[-1]},
         "copy_reference_gbps": copy_gbps,

@@ -172,6 +172,17 @@ kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const 
                              const float *v_self, void *workspace, size_t ws_bytes, float *o,
                              void *stream);
 
+/* The split-L step of kvprm_attention alone (the shared-prefix and per-candidate chunk kernels,
+ * without the merge): for every candidate, q-head and chunk of cached pages, the unnormalised
+ * softmax state of that chunk (running maximum, sum of exponentials, exponential-weighted sum of
+ * values; the split form of the appendix's softmax(qK^T/sqrt(d))V) is written to the workspace
+ * in an internal layout. The verify token's own key is not applied and nothing else is
+ * written. It exists to time and profile the chunk kernels on their own; arguments, validation
+ * and errors are as for kvprm_attention. */
+kvprm_status kvprm_attention_partials(kvprm_handle h, const kvprm_kv_cache *cache,
+                                      const kvprm_batch *batch, int32_t layer, const float *q,
+                                      void *workspace, size_t ws_bytes, void *stream);
+
 /* Repack one bf16 weight matrix W [rows][K] from row-major order into the packed tile layout
  * that kvprm_score reads for BF16 weights: blocks of 1 KiB, block kb * (rows / 16) + t holding
  * rows 16t .. 16t+15 and inputs 32kb .. 32kb+31; inside a block, 16-byte group l (0..63) holds

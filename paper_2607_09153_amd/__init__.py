@@ -21,7 +21,8 @@ KVPRM_F32, KVPRM_BF16, KVPRM_FP8_E4M3 = 0, 1, 2
 DTYPE_CODE = {"f32": KVPRM_F32, "bf16": KVPRM_BF16, "fp8": KVPRM_FP8_E4M3}
 
 EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
-            "kvprm_attention", "kvprm_pack_weight", "kvprm_last_error"]
+            "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
+            "kvprm_last_error"]
 
 
 class ModelDesc(ctypes.Structure):
@@ -91,9 +92,11 @@ def _load():
                                 ctypes.POINTER(ReadoutWeights), vp, sz, vp, vp, vp]
     lib.kvprm_attention.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
                                     ctypes.c_int32, vp, vp, vp, vp, sz, vp, vp]
+    lib.kvprm_attention_partials.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
+                                             ctypes.c_int32, vp, vp, sz, vp]
     lib.kvprm_pack_weight.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, vp]
     for f in ("kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
-              "kvprm_attention", "kvprm_pack_weight"):
+              "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kvprm_last_error.argtypes = []
     lib.kvprm_last_error.restype = ctypes.c_char_p
@@ -186,6 +189,12 @@ def kvprm_score(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeigh
 
 def kvprm_pack_weight(src_ptr: int, dst_ptr: int, rows: int, K: int, stream: int = 0) -> None:
     _check(lib.kvprm_pack_weight(src_ptr, dst_ptr, rows, K, stream or None))
+
+
+def kvprm_attention_partials(handle: int, cache: KVCache, batch: Batch, layer: int, q_ptr: int,
+                             workspace_ptr: int, ws_bytes: int, stream: int = 0) -> None:
+    _check(lib.kvprm_attention_partials(handle, ctypes.byref(cache), ctypes.byref(batch), layer,
+                                        q_ptr, workspace_ptr, ws_bytes, stream or None))
 
 
 def kvprm_attention(handle: int, cache: KVCache, batch: Batch, layer: int, q_ptr: int,

@@ -401,4 +401,29 @@ kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const 
   return ok();
 }
 
+kvprm_status kvprm_attention_partials(kvprm_handle h, const kvprm_kv_cache *cache,
+                                      const kvprm_batch *b, int32_t layer, const float *q,
+                                      void *workspace, size_t ws_bytes, void *stream) {
+  const char *fn = "kvprm_attention_partials";
+  if (!h) return fail(KVPRM_E_INVALID, "%s: null handle", fn);
+  kvprm_status st = check_batch(h, b, fn);
+  if (st != KVPRM_OK) return st;
+  if (b->batch == 0) return ok();
+  if ((st = check_cache(h, cache, fn)) != KVPRM_OK) return st;
+  if (layer < 0 || layer >= h->dm.layers)
+    return fail(KVPRM_E_INVALID, "%s: layer %d outside [0, %d)", fn, layer, h->dm.layers);
+  if (!q) return fail(KVPRM_E_INVALID, "%s: null q", fn);
+  if ((st = check_ws(h, b, workspace, ws_bytes, fn)) != KVPRM_OK) return st;
+  if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
+  const Dims &dm = h->dm;
+  const Plan p = make_plan(dm, b->batch, b->max_pages);
+  const Workspace w = carve(dm, p, workspace);
+  HIP_TRY(launch_attention(dm, p, w, layer, cache->k_pages, cache->v_pages, cache->k_scale,
+                           cache->v_scale, cache->num_pages, b->page_table, b->lengths,
+                           group_table(h, b, p), q, nullptr, nullptr, nullptr,
+                           (hipStream_t)stream, false),
+          "attention partials");
+  return ok();
+}
+
 }  // extern "C"

@@ -117,14 +117,15 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
                           const char *vp, const float *ksc, const float *vsc,
                           const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,
                           const float *q, const float *kself, const float *vself, float *o,
-                          uint16_t *op, hipStream_t s);
+                          uint16_t *op, hipStream_t s, bool merge = true);
 hipError_t launch_qkv_finish(const Dims &dm, const Plan &p, const Workspace &w,
                              const int32_t *lengths, hipStream_t s);
 hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, int layer,
                             const void *kpool, const void *vpool, const float *kscale,
                             const float *vscale, int num_pages, const int32_t *page_table,
                             const int32_t *lengths, const GroupTable &gt, const float *q,
-                            const float *kself, const float *vself, float *o, hipStream_t s);
+                            const float *kself, const float *vself, float *o, hipStream_t s,
+                            bool merge = true);
 hipError_t launch_residual(const Dims &dm, const Plan &p, const Workspace &w, int ksplit,
                            hipStream_t s);
 hipError_t launch_swiglu(const Dims &dm, const Plan &p, const Workspace &w, int ksplit,

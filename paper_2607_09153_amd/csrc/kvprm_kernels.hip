@@ -539,7 +539,8 @@ hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, i
                             const void *kpool, const void *vpool, const float *kscale,
                             const float *vscale, int num_pages, const int32_t *page_table,
                             const int32_t *lengths, const GroupTable &gt, const float *q,
-                            const float *kself, const float *vself, float *o, hipStream_t s) {
+                            const float *kself, const float *vself, float *o, hipStream_t s,
+                            bool merge) {
   const int EB = dm.kvdt == 0 ? 4 : (dm.kvdt == 1 ? 2 : 1);
   const size_t layer_elems = (size_t)num_pages * dm.nkv * kPage * dm.d;
   const char *kp = (const char *)kpool + layer_elems * EB * layer;
@@ -548,7 +549,7 @@ hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, i
   const float *vsc = vscale ? vscale + (size_t)layer * num_pages * dm.nkv : nullptr;
   if (dm.kvdt != 0)  // matrix-core kernels (bf16 and fp8 caches)
     return launch_attn_mx(dm, p, w, kp, vp, ksc, vsc, page_table, lengths, gt, q, kself, vself, o,
-                          nullptr, s);
+                          nullptr, s, merge);
   dim3 grid(p.nch, dm.nkv, p.B);
 #define KVPRM_ATT(KVT, D)                                                                     \
   hipLaunchKernelGGL((k_attn_valu<KVT, D>), grid, dim3(256), 0, s, kp, vp, ksc, vsc, dm.nkv, \
@@ -564,7 +565,7 @@ hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, i
   }
 #undef KVPRM_ATT
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !merge) return e;
   return launch_merge(dm, p, w, gt, lengths, q, kself, vself, o, s);
 }
 

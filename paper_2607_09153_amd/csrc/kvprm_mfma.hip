@@ -1458,7 +1458,7 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
                           const char *vp, const float *ksc, const float *vsc,
                           const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,
                           const float *q, const float *kself, const float *vself, float *o,
-                          uint16_t *op, hipStream_t s) {
+                          uint16_t *op, hipStream_t s, bool merge) {
   AttnArgs a;
   memset(&a, 0, sizeof a);
   a.kp = kp;
@@ -1507,7 +1507,7 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   }
 #undef KVPRM_A
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !merge) return e;
   if (dm.d == 64)
     hipLaunchKernelGGL(k_merge_mx<64>, dim3(p.B, dm.nq), dim3(512), 0, s, a);
   else

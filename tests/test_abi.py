@@ -146,6 +146,18 @@ def test_attention_validation(handle):
     assert e.value.status == kv.KVPRM_E_INVALID
 
 
+def test_attention_partials_validation(handle):
+    batch = kv.make_batch(1, FAKE, 4, FAKE)
+    cases = [dict(layer=2), dict(q=0), dict(ws=0), dict(ws_bytes=16), dict(cache=_cache(k_ptr=0))]
+    for c in cases:
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_attention_partials(handle, c.get("cache", _cache()), batch, c.get("layer", 0),
+                                        c.get("q", FAKE), c.get("ws", FAKE),
+                                        c.get("ws_bytes", 1 << 40))
+        assert e.value.status in (kv.KVPRM_E_INVALID, kv.KVPRM_E_WORKSPACE), c
+    kv.kvprm_attention_partials(handle, _cache(), kv.make_batch(0, 0, 1, 0), 0, FAKE, FAKE, 0)
+
+
 def test_pack_weight_validation():
     for args in [(0, FAKE, 16, 32), (FAKE, 0, 16, 32), (FAKE, FAKE * 4, 15, 32),
                  (FAKE, FAKE * 4, 16, 48), (FAKE, FAKE * 4, 0, 32), (FAKE, FAKE + 64, 16, 32),

@@ -101,6 +101,39 @@ def test_attention_parity(name, lengths, k_std):
     assert err <= 2e-5 * scale
 
 
+@pytest.mark.parametrize("name,lengths", [("b7_bf16", [32768, 1, 20000, 33, 5000, 31000]),
+                                          ("fp8", [9000, 0, 17000])])
+def test_attention_partials_match_the_attention_step(name, lengths):
+    """kvprm_attention_partials writes exactly what the chunk kernels of kvprm_attention write
+    into the workspace (same bytes from the same starting contents) and nothing else: bytes
+    past the workspace size and the query stay untouched."""
+    _say(f"case: attention partials {name} lengths={lengths}")
+    w = synth.make_workload("custom", shape=_shape(name), lengths=lengths, seed=4343)
+    dw = DeviceWorkload(w, nan_unused_pages=True, fill_weights=False)
+    q, ks, vs = host_activations(w, 0xABD, scale=1.0)
+    m = kv()
+    h = m.kvprm_create(dw.desc(m))
+    try:
+        batch = dw.batch(m)
+        n = m.kvprm_workspace_size(h, batch)
+        guard = 4096
+        qd, kd, vd = (torch.from_numpy(a).cuda() for a in (q, ks, vs))
+        q0 = qd.clone()
+        st = torch.cuda.current_stream().cuda_stream
+        ws1 = torch.full((n + guard,), 0x5A, dtype=torch.uint8, device="cuda")
+        ws2 = ws1.clone()
+        m.kvprm_attention_partials(h, dw.cache(m), batch, 1, qd.data_ptr(), ws1.data_ptr(), n, st)
+        o = torch.empty_like(qd)
+        m.kvprm_attention(h, dw.cache(m), batch, 1, qd.data_ptr(), kd.data_ptr(), vd.data_ptr(),
+                          ws2.data_ptr(), n, o.data_ptr(), st)
+        torch.cuda.synchronize()
+        assert torch.equal(ws1[n:], torch.full((guard,), 0x5A, dtype=torch.uint8, device="cuda"))
+        assert torch.equal(ws1, ws2)
+        assert torch.equal(qd, q0)
+    finally:
+        m.kvprm_destroy(h)
+
+
 # Shared-prefix attention: groups whose prefix ends inside a chunk, on a chunk edge, on the
 # first page; a member whose length equals the prefix; a one-member group without a prefix;
 # a group with more (member, head) columns than one shared-prefix block holds.
