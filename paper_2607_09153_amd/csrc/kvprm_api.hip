@@ -291,30 +291,14 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * EB;
   const size_t layer_scales = (size_t)cache->num_pages * dm.nkv;
   if (dm.wdt == 1) {
-    // matrix-core pipeline: five launches per layer
+    // matrix-core pipeline, seven launches per layer: QKV (split-K) and its rotary step,
+    // attention and its merge, then the output, gate/up and down projections with their
+    // element-wise steps fused (no split-K partials)
     HIP_TRY(launch_init_mx(dm, p, w, wts->verify_embed, wts->layers[0].attn_norm, b->lengths, s),
             "init");
-    // B <= 16: the output, gate/up and down projections run with their element-wise steps
-    // fused (no split-K partials); the QKV projection stays split-K with a separate rotary
-    // kernel, which measured faster than its fused form
-    const bool fused = p.nt <= 2;
     for (int l = 0; l < dm.layers; ++l) {
       const kvprm_layer_weights &W = wts->layers[l];
       const void *gamma_next = l + 1 < dm.layers ? wts->layers[l + 1].attn_norm : nullptr;
-      if (fused) {
-        HIP_TRY(launch_qkv_mx(dm, p, w, W.wq, W.wk, W.wv, s), "qkv projection");
-        HIP_TRY(launch_attn_mx(dm, p, w, (const char *)cache->k_pages + layer_bytes * l,
-                               (const char *)cache->v_pages + layer_bytes * l,
-                               cache->k_scale ? cache->k_scale + layer_scales * l : nullptr,
-                               cache->v_scale ? cache->v_scale + layer_scales * l : nullptr,
-                               b->page_table, b->lengths, gt, w.q, w.kself, w.vself, nullptr,
-                               w.opO, s),
-                "attention");
-        HIP_TRY(launch_oproj_fused(dm, p, w, W.wo, W.ffn_norm, s), "output projection");
-        HIP_TRY(launch_gateup_fused(dm, p, w, W.w_gate, W.w_up, s), "gate/up projection");
-        HIP_TRY(launch_down_fused(dm, p, w, W.w_down, gamma_next, s), "down projection");
-        continue;
-      }
       HIP_TRY(launch_qkv_mx(dm, p, w, W.wq, W.wk, W.wv, s), "qkv projection");
       HIP_TRY(launch_attn_mx(dm, p, w, (const char *)cache->k_pages + layer_bytes * l,
                              (const char *)cache->v_pages + layer_bytes * l,
@@ -323,11 +307,9 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
                              b->page_table, b->lengths, gt, w.q, w.kself, w.vself, nullptr, w.opO,
                              s),
               "attention");
-      HIP_TRY(launch_oproj_mx(dm, p, w, W.wo, W.ffn_norm, s), "output projection");
-      HIP_TRY(launch_gateup_mx(dm, p, w, W.w_gate, W.w_up, s), "gate/up projection");
-      HIP_TRY(launch_down_mx(dm, p, w, W.w_down,
-                             l + 1 < dm.layers ? wts->layers[l + 1].attn_norm : nullptr, s),
-              "down projection");
+      HIP_TRY(launch_oproj_fused(dm, p, w, W.wo, W.ffn_norm, s), "output projection");
+      HIP_TRY(launch_gateup_fused(dm, p, w, W.w_gate, W.w_up, s), "gate/up projection");
+      HIP_TRY(launch_down_fused(dm, p, w, W.w_down, gamma_next, s), "down projection");
     }
     HIP_TRY(launch_head(dm, p, w, wts->final_norm, wts->reward_w, wts->reward_b, scores, logits, s),
             "reward head");

@@ -68,7 +68,7 @@ struct Plan {
   int kslice_qkv, kslice_o, kslice_gu, kslice_d;
   // matrix-core path
   int nt, bp;                 // operand column tiles and padded batch
-  GemvPlan g_qkv, g_o, g_gu, g_d;
+  GemvPlan g_qkv;
   size_t part_elems;
 };
 
@@ -99,14 +99,8 @@ hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, con
                           const void *gamma0, const int32_t *lengths, hipStream_t s);
 hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
                          const void *wk, const void *wv, hipStream_t s);
-hipError_t launch_oproj_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
-                           const void *gamma_ffn, hipStream_t s);
-hipError_t launch_gateup_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
-                            const void *wu, hipStream_t s);
-hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
-                          const void *gamma_next, hipStream_t s);
-// fused projections for one or two operand column tiles (B <= 16): no split-K partials, the
-// element-wise step after the output, gate/up and down projections runs in the epilogue
+// fused projections: no split-K partials, the element-wise step after the output, gate/up and
+// down projections runs in the epilogue
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
                               const void *gamma_ffn, hipStream_t s);
 hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,

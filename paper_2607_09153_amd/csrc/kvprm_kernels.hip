@@ -101,20 +101,13 @@ Plan make_plan(const Dims &dm, int B, int max_pages) {
   p.nch = dm.kvdt == 0 ? n_valu : n_mx;
   size_t m = 0;
   if (dm.wdt == 1) {
-    // rows per sum-of-squares block: one 16-row tile for the fused projections (B <= 16), 64
-    // for the split-K path
-    p.rb = gemv_nt(B) <= 2 ? 16 : 64;
+    // sums of squares per 16-row tile (written by the fused projections' epilogues); split-K
+    // partials for the QKV projection only
+    p.rb = 16;
     p.nt = gemv_nt(B);
     p.bp = gemv_bp(B);
     p.g_qkv = gemv_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B);
-    p.g_o = gemv_plan(dm.H, dm.nq * dm.d, B);
-    p.g_gu = gemv_plan(2 * dm.F, dm.H, B);
-    p.g_d = gemv_plan(dm.H, dm.F, B);
-    const GemvPlan *gs[4] = {&p.g_qkv, &p.g_o, &p.g_gu, &p.g_d};
-    for (const GemvPlan *g : gs) {
-      const size_t e = (size_t)((g->ksplit + 3) & ~3) * g->rows;
-      if (e > m) m = e;
-    }
+    m = (size_t)((p.g_qkv.ksplit + 3) & ~3) * p.g_qkv.rows;
   } else {
     // vector-ALU GEMV: the activation slice of all B candidates is staged in LDS (<= 32 KiB)
     p.rb = 256;
@@ -631,23 +624,40 @@ hipError_t launch_swiglu(const Dims &dm, const Plan &p, const Workspace &w, int 
 
 // ------------------------------------------------------------------------------- reward head
 
-// z_b = w_r . (x_b / sqrt(mean(x_b^2) + eps) * gamma_f) + b_r; P(+) = sigmoid(z_b).
+// z_b = w_r . (x_b / sqrt(mean(x_b^2) + eps) * gamma_f) + b_r; P(+) = sigmoid(z_b). One pass
+// over x_b: sum(x^2) and sum(x gamma_f w_r) together (the RMS scale is a common factor of the
+// dot product), four rows per thread in flight.
 __global__ __launch_bounds__(256) void k_head(const float *x, int H, float eps, const void *gam,
                                               const void *wr, int wdt, float rb, float *scores,
                                               float *logits) {
   __shared__ float red[4];
   const int b = blockIdx.x;
   const float *xb = x + (size_t)b * H;
-  float sq = 0.f;
-  for (int r = threadIdx.x; r < H; r += 256) sq += xb[r] * xb[r];
+  float sq = 0.f, dot = 0.f;
+  int r = threadIdx.x;
+  for (; r + 3 * 256 < H; r += 4 * 256) {
+    float v[4], gw[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      v[u] = xb[r + u * 256];
+      gw[u] = load_scalar(gam, r + u * 256, wdt) * load_scalar(wr, r + u * 256, wdt);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      sq += v[u] * v[u];
+      dot += v[u] * gw[u];
+    }
+  }
+  for (; r < H; r += 256) {
+    const float v = xb[r];
+    sq += v * v;
+    dot += v * (load_scalar(gam, r, wdt) * load_scalar(wr, r, wdt));
+  }
   sq = block_sum256(sq, red);
-  const float inv = 1.0f / sqrtf(sq / (float)H + eps);
-  float dot = 0.f;
-  for (int r = threadIdx.x; r < H; r += 256)
-    dot += (xb[r] * inv * load_scalar(gam, r, wdt)) * load_scalar(wr, r, wdt);
   dot = block_sum256(dot, red);
   if (threadIdx.x == 0) {
-    const float z = dot + rb;
+    const float inv = 1.0f / sqrtf(sq / (float)H + eps);
+    const float z = dot * inv + rb;
     float pz;
     if (z >= 0.f) {
       pz = 1.0f / (1.0f + expf(-z));

@@ -324,7 +324,22 @@ __device__ __forceinline__ float ld_bf16(const void *p, size_t i) {
   return __uint_as_float((uint32_t)((const uint16_t *)p)[i] << 16);
 }
 
-// The same for one wave (B <= 8), without LDS or barriers: with Bq = B rounded up to a power
+// v += ss[i][b] for i = i0, i0 + P, ... < nss, in that order, eight loads in flight at a time.
+__device__ __forceinline__ void rms_tail(const float *__restrict__ ss, int B, int b, int i0, int P,
+                                         int nss, float &v) {
+  int i = i0;
+  for (; i + 7 * P < nss; i += 8 * P) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = ss[(size_t)(i + u * P) * B + b];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += t[u];
+  }
+  for (; i < nss; i += P) v += ss[(size_t)i * B + b];
+}
+
+// RMSNorm scales r_b = 1 / sqrt(mean(x_b^2) + eps) from the per-row-block sums of squares
+// ss[i][b], by one wave (B <= 8), without LDS or barriers: with Bq = B rounded up to a power
 // of two, lane l sums rows l / Bq, l / Bq + 64 / Bq, ... of candidate l % Bq (32 loads issued by
 // wave_rms_load, any further rows in wave_rms_finish), a butterfly over the lanes of equal
 // l % Bq completes the sums (identical in every lane and block), and each lane takes its own
@@ -360,8 +375,7 @@ __device__ __forceinline__ float wave_rms_finish(const float *__restrict__ ss, i
   float v = 0.f;
 #pragma unroll
   for (int u = 0; u < 32; ++u) v += ld.v[u];
-  if (bl < B)
-    for (int i = part + 32 * P; i < nss; i += P) v += ss[(size_t)i * B + bl];
+  if (bl < B) rms_tail(ss, B, bl, part + 32 * P, P, nss, v);
   for (int off = Bq; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
   const float tot = __shfl(v, b, 64);
   return 1.0f / sqrtf(tot / (float)H + eps);
@@ -408,8 +422,7 @@ __device__ __forceinline__ void rms_finish(const float *__restrict__ ss, int nss
   float v = 0.f;
 #pragma unroll
   for (int u = 0; u < 16; ++u) v += ld.v[u];
-  if (b < B)
-    for (int i = part + 16 * P; i < nss; i += P) v += ss[(size_t)i * B + b];
+  if (b < B) rms_tail(ss, B, b, part + 16 * P, P, nss, v);
   part_s[t] = v;
   __syncthreads();
   if (t < B) {
@@ -420,15 +433,15 @@ __device__ __forceinline__ void rms_finish(const float *__restrict__ ss, int nss
   __syncthreads();
 }
 
-// ---------------------------------------------------- GEMV with fused epilogue (B <= 16)
+// ------------------------------------------------------------- GEMV with fused epilogue
 
-// For one or two operand column tiles (B <= 8: columns b and 8 + b of the one tile hold the hi
-// and lo halves of candidate b; B <= 16: tile 0 holds the hi halves, tile 1 the lo halves) the
-// projections and the element-wise steps that follow them run in one kernel: a block owns MT
-// row tiles over the whole input; its WPB waves split the input blocks into contiguous ranges
-// (weights double buffered in batches of U, the operand read from memory), the waves'
-// accumulators are added in LDS in a fixed order, and the block applies the epilogue to
-// complete outputs, so no split-K partials cross a kernel boundary.
+// The projections and the element-wise steps that follow them run in one kernel: a block owns
+// MT row tiles over the whole input; its WPB waves split the input blocks into contiguous ranges
+// (weights double buffered in batches of U, the operand read from memory), each wave adds the
+// hi and lo halves of every candidate (B <= 8: columns b and 8 + b of the one operand tile;
+// otherwise tiles g and NT/2 + g hold the hi and lo halves of candidates 16 g .. 16 g + 15),
+// the waves' sums are added in LDS in a fixed order, and wave g applies the epilogue to the
+// complete outputs of candidate group g, so no split-K partials cross a kernel boundary.
 //   EPI_RESID:  one tile: x += y, the tile's sums of squares per candidate, next operand
 //               x * gamma (if gamma).
 //   EPI_SWIGLU: gate tile t and up tile t: h = silu(r g) * (r u) as the down operand.
@@ -455,9 +468,11 @@ struct FusedArgs {
 
 template <int MT, int NT, int WPB, int U, int EPI>
 __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
-  __shared__ floatx4 red_s[WPB][MT][NT][64];
+  constexpr int NG = NT == 1 ? 1 : NT / 2;  // candidate groups
+  static_assert(NG <= WPB, "one wave per candidate group in the epilogue");
+  __shared__ floatx4 red_s[WPB][MT][NG][64];
   __shared__ float part_s[64 * WPB];
-  __shared__ float inv_s[16];
+  __shared__ float inv_s[64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int B = a.B;
   // global row tiles of this block
@@ -484,7 +499,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   WaveRmsLoads wl;
   RmsLoads rl;
   if (EPI == EPI_SWIGLU && NT == 1 && wave == 0) wave_rms_load(a.ss, a.nss, B, wl);
-  if (EPI == EPI_SWIGLU && NT == 2) rms_load<64 * WPB>(a.ss, a.nss, B, rl);
+  if (EPI == EPI_SWIGLU && NT >= 2) rms_load<64 * WPB>(a.ss, a.nss, B, rl);
   floatx4 acc[MT][NT];
 #pragma unroll
   for (int m = 0; m < MT; ++m)
@@ -532,37 +547,43 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
       for (int m = 0; m < MT; ++m) acc[m][t] = mfma16(wt[m][(size_t)kb * kstride[m]], bv, acc[m][t]);
     }
   }
+  // hi + lo, then the waves' sums in LDS
 #pragma unroll
   for (int m = 0; m < MT; ++m)
 #pragma unroll
-    for (int t = 0; t < NT; ++t) red_s[wave][m][t][lane] = acc[m][t];
+    for (int gi = 0; gi < NG; ++gi) {
+      floatx4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        v[i] = NT == 1 ? acc[m][0][i] + __shfl_xor(acc[m][0][i], 8, 64)
+                       : acc[m][gi][i] + acc[m][gi + NG][i];
+      red_s[wave][m][gi][lane] = v;
+    }
   __syncthreads();
-  if (EPI == EPI_SWIGLU && NT == 2) rms_finish<64 * WPB>(a.ss, a.nss, B, a.H, a.eps, rl, part_s, inv_s);
-  if (wave != 0) return;
-  // fixed-order sum over the waves, then hi + lo of candidate n = lane % 16
+  if (EPI == EPI_SWIGLU && NT >= 2) rms_finish<64 * WPB>(a.ss, a.nss, B, a.H, a.eps, rl, part_s, inv_s);
+  if (wave >= NG) return;
+  const int gi = wave;
+  // fixed-order sum over the waves; lane (n, cq) holds rows 4 cq .. 4 cq + 3 of candidate n of
+  // group gi
   const int n = lane & 15, cq = lane >> 4;
   float y[MT][4];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
-    floatx4 tt[NT];
+    floatx4 tt = red_s[0][m][gi][lane];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      tt[t] = red_s[0][m][t][lane];
-#pragma unroll
-      for (int w = 1; w < WPB; ++w) {
-        const floatx4 v = red_s[w][m][t][lane];
-        tt[t][0] += v[0];
-        tt[t][1] += v[1];
-        tt[t][2] += v[2];
-        tt[t][3] += v[3];
-      }
+    for (int w = 1; w < WPB; ++w) {
+      const floatx4 v = red_s[w][m][gi][lane];
+      tt[0] += v[0];
+      tt[1] += v[1];
+      tt[2] += v[2];
+      tt[3] += v[3];
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      y[m][i] = NT == 1 ? tt[0][i] + __shfl_xor(tt[0][i], 8, 64) : tt[0][i] + tt[NT - 1][i];
+    for (int i = 0; i < 4; ++i) y[m][i] = tt[i];
   }
-  const bool cand_ok = NT == 1 ? (n < 8 && n < B) : n < B;
-  const int b = cand_ok ? n : 0;
+  const int cand = NT == 1 ? n : 16 * gi + n;
+  const bool cand_ok = NT == 1 ? (n < 8 && n < B) : cand < B;
+  const int b = cand_ok ? cand : 0;
   if (EPI == EPI_RESID) {
     float sq = 0.f;
 #pragma unroll
@@ -639,67 +660,6 @@ __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ pa
   dst[i + hd] = o2;
 }
 
-// Residual add x += sum_k partials for a block of 64 rows, the rows' sums of squares per
-// candidate (ss[block][b], a fixed-order wave reduction), and the next GEMV's operand
-// x * gamma_next (bf16 gains). 512 threads: one (row, candidate) element each for B <= 8.
-template <int NMAX>
-__global__ __launch_bounds__(512) void k_resid_mx(float *__restrict__ x,
-                                                  const float *__restrict__ part, int ksp,
-                                                  int ksplit, float *__restrict__ ss, int B, int H,
-                                                  const void *__restrict__ gamma_next,
-                                                  uint16_t *__restrict__ op, int NT, int Bp) {
-  __shared__ float sq_s[64][65];
-  const int r0 = blockIdx.x * 64;
-  const int nr = min(64, H - r0);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int e = threadIdx.x; e < nr * B; e += 512) {
-    const int rl = e / B, b = e - rl * B, r = r0 + rl;
-    const size_t ip = (size_t)r * B + b;
-    float4 v[NMAX];
-    ksum_load<NMAX>(part, ksp, ip, v);
-    const float xo = x[(size_t)b * H + r];
-    const float g = ld_bf16(gamma_next ? gamma_next : (const void *)x, gamma_next ? r : 0);
-    const float xv = xo + ksum_add<NMAX>(part, ksp, ksplit, ip, v);
-    x[(size_t)b * H + r] = xv;
-    sq_s[rl][b] = xv * xv;
-    if (gamma_next) store_operand(op, NT, Bp, r, b, xv * g);
-  }
-  __syncthreads();
-  for (int b = wave; b < B; b += 8) {
-    const float v = wsum(lane < nr ? sq_s[lane][b] : 0.f);
-    if (lane == 0) ss[(size_t)blockIdx.x * B + b] = v;
-  }
-}
-
-// h = silu(r_b g) * (r_b u) for gate rows f and up rows F + f (the FFN RMSNorm applied after
-// the product), written as the down projection's operand. One thread per (feature, candidate).
-template <int NMAX>
-__global__ __launch_bounds__(256) void k_swiglu_mx(const float *__restrict__ part, int ksp,
-                                                   int ksplit, const float *__restrict__ ss,
-                                                   int nss, int H, float eps, int B, int F,
-                                                   uint16_t *__restrict__ op, int NT, int Bp) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  const bool act = e < F * B;
-  const int ec = act ? e : 0;
-  const int f = ec / B, b = ec - f * B;
-  const size_t ig = (size_t)f * B + b, iu = (size_t)(F + f) * B + b;
-  float4 vg[NMAX], vu[NMAX];
-  ksum_load<NMAX>(part, ksp, ig, vg);
-  ksum_load<NMAX>(part, ksp, iu, vu);
-  RmsLoads rl;
-  rms_load<256>(ss, nss, B, rl);
-  __shared__ float part_s[256], inv_s[64];
-  rms_finish<256>(ss, nss, B, H, eps, rl, part_s, inv_s);
-  const float g = ksum_add<NMAX>(part, ksp, ksplit, ig, vg);
-  const float u = ksum_add<NMAX>(part, ksp, ksplit, iu, vu);
-  const float inv = inv_s[b];
-  if (!act) return;
-  const float gv = g * inv, uv = u * inv;
-  store_operand(op, NT, Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
-}
-
-// Row-major [rows][K] -> packed tile layout: 16-byte group l of block kb * (rows/16) + t holds
-// W[16 t + l % 16][32 kb + 8 (l / 16) + i], i = 0..7. One thread per group.
 __global__ __launch_bounds__(256) void k_pack_weight(const uint4 *src, uint4 *dst, int64_t rows,
                                                      int64_t K) {
   const int64_t ngroups = rows * K / 8;
@@ -1341,55 +1301,20 @@ hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, cons
   return hipGetLastError();
 }
 
-static hipError_t launch_resid_mx(const Dims &dm, const Plan &p, const Workspace &w,
-                                  const GemvPlan &g, const void *gamma_next, hipStream_t s) {
-#define KVPRM_R(NM)                                                                         \
-  hipLaunchKernelGGL(k_resid_mx<NM>, dim3(p.nss), dim3(512), 0, s, w.x, w.part, ksp_of(g), \
-                     g.ksplit, w.ss, p.B, dm.H, gamma_next, w.opA, p.nt, p.bp)
-  switch (ksum_nmax(ksp_of(g))) {
-    case 1: KVPRM_R(1); break;
-    case 2: KVPRM_R(2); break;
-    case 4: KVPRM_R(4); break;
-    default: KVPRM_R(8); break;
+// fused projections
+static hipError_t launch_resid_fused(const Plan &p, const FusedArgs &a, int tiles, hipStream_t s) {
+  const dim3 grid(tiles);
+  switch (p.nt) {
+    case 1: hipLaunchKernelGGL((k_gemv_fused<1, 1, 16, 4, EPI_RESID>), grid, dim3(64 * 16), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_gemv_fused<1, 2, 8, 4, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_gemv_fused<1, 4, 8, 2, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
+    case 6: hipLaunchKernelGGL((k_gemv_fused<1, 6, 8, 1, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_gemv_fused<1, 8, 8, 1, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
+    default: return hipErrorInvalidValue;
   }
-#undef KVPRM_R
   return hipGetLastError();
 }
 
-hipError_t launch_oproj_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
-                           const void *gamma_ffn, hipStream_t s) {
-  hipError_t e = launch_gemv_mx(p, p.g_o, wo, dm.H, nullptr, 0, nullptr, 0, w.opO, w.part, s);
-  if (e != hipSuccess) return e;
-  return launch_resid_mx(dm, p, w, p.g_o, gamma_ffn, s);
-}
-
-hipError_t launch_gateup_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
-                            const void *wu, hipStream_t s) {
-  hipError_t e = launch_gemv_mx(p, p.g_gu, wg, dm.F, wu, dm.F, nullptr, 0, w.opA, w.part, s);
-  if (e != hipSuccess) return e;
-  const int n = dm.F * p.B;
-#define KVPRM_S(NM)                                                                             \
-  hipLaunchKernelGGL(k_swiglu_mx<NM>, dim3((n + 255) / 256), dim3(256), 0, s, w.part,           \
-                     ksp_of(p.g_gu), p.g_gu.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.F, w.opD, \
-                     p.nt, p.bp)
-  switch (ksum_nmax(ksp_of(p.g_gu))) {
-    case 1: KVPRM_S(1); break;
-    case 2: KVPRM_S(2); break;
-    case 4: KVPRM_S(4); break;
-    default: KVPRM_S(8); break;
-  }
-#undef KVPRM_S
-  return hipGetLastError();
-}
-
-hipError_t launch_down_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
-                          const void *gamma_next, hipStream_t s) {
-  hipError_t e = launch_gemv_mx(p, p.g_d, wd, dm.H, nullptr, 0, nullptr, 0, w.opD, w.part, s);
-  if (e != hipSuccess) return e;
-  return launch_resid_mx(dm, p, w, p.g_d, gamma_next, s);
-}
-
-// fused projections (one or two operand column tiles, B <= 16)
 static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, int K,
                             const uint16_t *act) {
   FusedArgs a;
@@ -1416,11 +1341,7 @@ hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w,
   a.nseg = 1;
   a.gamma = gamma_ffn;
   a.op = w.opA;
-  if (p.nt == 1)
-    hipLaunchKernelGGL((k_gemv_fused<1, 1, 16, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 16), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_gemv_fused<1, 2, 8, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 8), 0, s, a);
-  return hipGetLastError();
+  return launch_resid_fused(p, a, dm.H / 16, s);
 }
 
 hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
@@ -1432,10 +1353,15 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
   a.seg_rows[1] = dm.F;
   a.nseg = 2;
   a.op = w.opD;
-  if (p.nt == 1)
-    hipLaunchKernelGGL((k_gemv_fused<2, 1, 4, 4, EPI_SWIGLU>), dim3(dm.F / 16), dim3(64 * 4), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_gemv_fused<2, 2, 4, 4, EPI_SWIGLU>), dim3(dm.F / 16), dim3(64 * 4), 0, s, a);
+  const dim3 grid(dm.F / 16);
+  switch (p.nt) {
+    case 1: hipLaunchKernelGGL((k_gemv_fused<2, 1, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_gemv_fused<2, 2, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_gemv_fused<2, 4, 4, 2, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
+    case 6: hipLaunchKernelGGL((k_gemv_fused<2, 6, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_gemv_fused<2, 8, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
@@ -1447,11 +1373,7 @@ hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, 
   a.nseg = 1;
   a.gamma = gamma_next;
   a.op = w.opA;
-  if (p.nt == 1)
-    hipLaunchKernelGGL((k_gemv_fused<1, 1, 16, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 16), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_gemv_fused<1, 2, 8, 4, EPI_RESID>), dim3(dm.H / 16), dim3(64 * 8), 0, s, a);
-  return hipGetLastError();
+  return launch_resid_fused(p, a, dm.H / 16, s);
 }
 
 hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
