@@ -47,6 +47,21 @@ def readout_from_synth(shape: synth.ModelShape, seed: int, layer_cache: int = 2)
     return ko.Readout(layer, g["verify_embed"], g["final_norm"], g["reward_w"], 0.0)
 
 
+def lora_from_synth(shape: synth.ModelShape, seed: int, rank: int,
+                    targets=synth.LORA_PROJECTIONS, layer_cache: int = 2):
+    """Adapter factors of a synthetic model: layer -> {projection: (A, B)} in float64, stored
+    like the base matrices (packed when bf16)."""
+    wdt = shape.weight_dtype
+
+    @lru_cache(maxsize=layer_cache)
+    def factors(l: int):
+        t = {name: _gen_tensor(name, kind, dims, seed, l, wdt, shape)
+             for name, kind, dims in synth.lora_tensors(shape, rank, targets)}
+        return {p: (t[f"lora_a_{p}"], t[f"lora_b_{p}"]) for p in targets}
+
+    return factors
+
+
 def cache_from_synth(w: synth.Workload, nan_pages=(), page_cache: int = 4096) -> ko.PagedCache:
     """Paged pools of a workload, one physical page per call, decoded to float64."""
     s = w.shape
@@ -76,10 +91,16 @@ def cache_from_synth(w: synth.Workload, nan_pages=(), page_cache: int = 4096) ->
     return ko.PagedCache(tiles)
 
 
-def score_workload(w: synth.Workload, candidates=None, return_hidden: bool = False):
-    """Oracle scores (z, P(+)) of the listed candidates (default: all) of a workload."""
+def score_workload(w: synth.Workload, candidates=None, return_hidden: bool = False,
+                   lora_rank: int = 0, lora_targets=synth.LORA_PROJECTIONS):
+    """Oracle scores (z, P(+)) of the listed candidates (default: all) of a workload; with
+    lora_rank > 0 the verify token runs the base weights with the synthetic adapter of that
+    rank on lora_targets (scale alpha / rank)."""
     cand = list(range(w.batch)) if candidates is None else list(candidates)
     ro = readout_from_synth(w.shape, w.seed)
+    if lora_rank > 0:
+        ro = ko.readout_with_adapter(ro, lora_from_synth(w.shape, w.seed, lora_rank, lora_targets),
+                                     synth.lora_scale(lora_rank))
     cache = cache_from_synth(w)
     lens = [w.lengths[b] for b in cand]
     pt = [w.page_table[b] for b in cand]

@@ -194,7 +194,8 @@ class LayerWeights:
 
 class Readout:
     """Everything the verify pass needs besides the cache: per-layer weights (theta + dtheta,
-    already merged), the verify-token embedding, the final norm gain, and the reward vector
+    merged; readout_with_adapter forms them from a base readout and adapter factors), the
+    verify-token embedding, the final norm gain, and the reward vector
     w_r = W_out[+] - W_out[-] with bias b_r = b[+] - b[-]."""
 
     def __init__(self, layer: Callable[[int], LayerWeights], verify_embed, final_norm, reward_w,
@@ -204,6 +205,35 @@ class Readout:
         self.final_norm = final_norm
         self.reward_w = reward_w
         self.reward_b = reward_b
+
+
+# Low-rank adapter (section 4.1, Eq. (score): the verify token runs f_{theta + dtheta}, where
+# dtheta is a LoRA adapter of the base model, Hu et al. 2022). A projection W [out, in] with
+# factors A [r, in] and B [out, r] and scale alpha / r acts as W + scale * B A on the verify
+# token; the cached positions were produced by the base weights alone.
+
+LORA_FIELDS = {"q": "wq", "k": "wk", "v": "wv", "o": "wo", "gate": "w_gate", "up": "w_up",
+               "down": "w_down"}
+_LAYER_FIELDS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+
+
+def lora_adapted(W: LayerWeights, factors: Dict[str, Tuple[np.ndarray, np.ndarray]],
+                 scale: float) -> LayerWeights:
+    """The layer's weights with scale * B @ A added to each projection listed in factors
+    (projection name -> (A, B))."""
+    mats = {f: getattr(W, f) for f in _LAYER_FIELDS}
+    for proj, (A, B) in factors.items():
+        f = LORA_FIELDS[proj]
+        assert A.shape[1] == mats[f].shape[1] and B.shape[0] == mats[f].shape[0]
+        assert A.shape[0] == B.shape[1]
+        mats[f] = mats[f] + scale * (B @ A)
+    return LayerWeights(**mats)
+
+
+def readout_with_adapter(base: "Readout", layer_factors: Callable[[int], Dict], scale: float):
+    """The readout of f_{theta + dtheta}: base weights with each layer's adapter applied."""
+    return Readout(lambda l: lora_adapted(base.layer(l), layer_factors(l), scale),
+                   base.verify_embed, base.final_norm, base.reward_w, base.reward_b)
 
 
 class PagedCache:

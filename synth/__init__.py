@@ -38,6 +38,9 @@ DT_F32, DT_BF16, DT_F64 = 0, 1, 2
 
 # stream ids: per-layer tensors are (layer << 8) | kind
 K_ATTN_NORM, K_WQ, K_WK, K_WV, K_WO, K_FFN_NORM, K_WGATE, K_WUP, K_WDOWN, K_KPOOL, K_VPOOL = range(11)
+# low-rank adapter factors of projection p (LORA_PROJECTIONS order): A at K_LORA + 2p, B at
+# K_LORA + 2p + 1
+K_LORA = 16
 GLOBAL = 0xFFFF
 G_VERIFY_EMBED, G_FINAL_NORM, G_REWARD_W, G_EMBED_TABLE = range(4)
 RECIPE = 0xFFFE
@@ -298,6 +301,32 @@ def tensor_mean_std(name: str, dims) -> tuple:
     if name == "reward_w":
         return 0.0, 1.0 / math.sqrt(dims[0])
     return 0.0, 1.0 / math.sqrt(dims[1])
+
+
+# projections that can carry a low-rank adapter, in the order of their stream kinds
+LORA_PROJECTIONS = ("q", "k", "v", "o", "gate", "up", "down")
+LORA_ALPHA = 32.0  # the adapter's alpha (with rank 256 as in the paper: scale alpha / r = 0.125)
+
+
+def lora_tensors(s: ModelShape, rank: int, targets: Sequence[str] = LORA_PROJECTIONS):
+    """Factors of the low-rank adapters of one layer: for projection p with base matrix
+    [out, in], A_p [rank, in] and B_p [out, rank], as (name, kind, dims) like layer_tensors.
+    Both factors are N(0, 1/sqrt(fan_in)) (the matrix rule of tensor_mean_std), so the update
+    scale * B A has entries of about scale times the base matrix's."""
+    H, d, nq, nkv, F = s.hidden, s.head_dim, s.num_q_heads, s.num_kv_heads, s.ffn_dim
+    dims = {"q": (nq * d, H), "k": (nkv * d, H), "v": (nkv * d, H), "o": (H, nq * d),
+            "gate": (F, H), "up": (F, H), "down": (H, F)}
+    out = []
+    for i, p in enumerate(LORA_PROJECTIONS):
+        if p in targets:
+            o_, in_ = dims[p]
+            out.append((f"lora_a_{p}", K_LORA + 2 * i, (rank, in_)))
+            out.append((f"lora_b_{p}", K_LORA + 2 * i + 1, (o_, rank)))
+    return out
+
+
+def lora_scale(rank: int) -> float:
+    return LORA_ALPHA / rank
 
 
 def global_tensors(s: ModelShape):

@@ -465,3 +465,102 @@ def test_split_lse_merge_equals_one_pass_softmax():
         num = sum(np.exp(m - M) * acc for m, _, acc in parts) + np.exp(s_self - M) * V[n]
         den = sum(np.exp(m - M) * l for m, l, _ in parts) + np.exp(s_self - M)
         assert np.allclose(num / den, ref, rtol=0, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------------------------
+# low-rank adapter of the verify token (Eq. (score): f_{theta + dtheta})
+
+
+def _adapter(shape, seed, rank, targets=synth.LORA_PROJECTIONS):
+    return inputs.lora_from_synth(shape, seed, rank, targets, layer_cache=64)
+
+
+def _random_cache(shape, lengths, seed):
+    """Paged cache of random K/V for the listed lengths (NaN past each length)."""
+    rng = np.random.default_rng(seed)
+    Ks = [rng.normal(size=(shape.num_layers, shape.num_kv_heads, n, shape.head_dim)) for n in lengths]
+    Vs = [rng.normal(size=(shape.num_layers, shape.num_kv_heads, n, shape.head_dim)) for n in lengths]
+    return _dense_cache(Ks, Vs, shape.page_size)
+
+
+def test_adapter_with_zero_b_is_the_base_readout():
+    """B = 0 leaves every projection unchanged: the adapted pass equals the base pass exactly."""
+    shape = _tiny_small()
+    base = _readout(shape, 31)
+    fac = _adapter(shape, 31, 32)
+    zero_b = lambda l: {p: (A, np.zeros_like(B)) for p, (A, B) in fac(l).items()}
+    ro = ko.readout_with_adapter(base, zero_b, synth.lora_scale(32))
+    cache, pt = _random_cache(shape, [37, 0, 16], 3)
+    z0, _ = ko.verify_pass(shape, base, cache, [37, 0, 16], pt)
+    z1, _ = ko.verify_pass(shape, ro, cache, [37, 0, 16], pt)
+    assert np.array_equal(z0, z1)
+
+
+@pytest.mark.parametrize("proj", synth.LORA_PROJECTIONS)
+def test_rank_one_adapter_moves_one_weight(proj):
+    """A = e_i^T (a row selector), B = c e_j: the update scale * B A is scale * c at entry
+    (j, i) of the projection alone, so the adapted pass equals the base pass with that one
+    weight changed (pins the product order B A, its orientation and the scale)."""
+    shape = _tiny_small()
+    base = _readout(shape, 41)
+    W0 = base.layer(1)
+    f = ko.LORA_FIELDS[proj]
+    out, inn = getattr(W0, f).shape
+    i, j, c, scale = inn - 3, out // 2 + 1, 0.75, 0.125
+    A = np.zeros((1, inn))
+    A[0, i] = 1.0
+    B = np.zeros((out, 1))
+    B[j, 0] = c
+    ro = ko.readout_with_adapter(base, lambda l: {proj: (A, B)} if l == 1 else {}, scale)
+    edited = {k: getattr(W0, k) for k in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm",
+                                           "w_gate", "w_up", "w_down")}
+    M = edited[f].copy()
+    M[j, i] += scale * c
+    edited[f] = M
+    W1 = ko.LayerWeights(**edited)
+    ref = ko.Readout(lambda l: W1 if l == 1 else base.layer(l), base.verify_embed,
+                     base.final_norm, base.reward_w)
+    cache, pt = _random_cache(shape, [29, 5], 4)
+    z_ad, _ = ko.verify_pass(shape, ro, cache, [29, 5], pt)
+    z_ref, _ = ko.verify_pass(shape, ref, cache, [29, 5], pt)
+    z_base, _ = ko.verify_pass(shape, base, cache, [29, 5], pt)
+    assert np.allclose(z_ad, z_ref, rtol=0, atol=1e-14)
+    assert np.max(np.abs(z_ad - z_base)) > 1e-6  # the edited weight matters
+
+
+def test_adapter_rank_split_is_additive():
+    """An adapter of rank r equals its two halves applied one after the other
+    (B A = B_1 A_1 + B_2 A_2 for A = [A_1; A_2], B = [B_1 B_2])."""
+    shape = _tiny_small(layers=1)
+    base = _readout(shape, 51)
+    fac = _adapter(shape, 51, 64)(0)
+    h1 = {p: (A[:32], B[:, :32]) for p, (A, B) in fac.items()}
+    h2 = {p: (A[32:], B[:, 32:]) for p, (A, B) in fac.items()}
+    W = base.layer(0)
+    full = ko.lora_adapted(W, fac, 0.5)
+    two = ko.lora_adapted(ko.lora_adapted(W, h1, 0.5), h2, 0.5)
+    for f in ko.LORA_FIELDS.values():
+        assert np.allclose(getattr(full, f), getattr(two, f), rtol=0, atol=1e-14)
+
+
+@pytest.mark.parametrize("targets", [synth.LORA_PROJECTIONS, ("q", "v", "down")])
+def test_adapter_on_the_verify_token_only_equals_reencode(targets):
+    """The cache comes from the base model (adapter disabled during generation) and only the
+    verify token runs theta + dtheta: the verify pass with the adapter equals a causal
+    re-encode whose last position alone uses the adapted weights."""
+    shape = _tiny_small()
+    seed = 61
+    base = _readout(shape, seed)
+    ro = ko.readout_with_adapter(base, _adapter(shape, seed, 32, targets), synth.lora_scale(32))
+    E = _embed(shape, seed)
+    Ks, Vs, zs, lens = [], [], [], []
+    for b, n in enumerate([33, 16, 0]):
+        toks = synth.token_ids(seed + b, n)
+        z, p, h, K, V = ko.reencode(shape, base.layer, ro.layer, E, toks, ro.verify_embed,
+                                    ro.final_norm, ro.reward_w)
+        Ks.append(K), Vs.append(V), zs.append(z), lens.append(n)
+    cache, pt = _dense_cache(Ks, Vs, shape.page_size)
+    z2, _ = ko.verify_pass(shape, ro, cache, lens, pt)
+    assert np.allclose(z2, zs, rtol=0, atol=1e-12)
+    z_base, _ = ko.verify_pass(shape, base, cache, lens, pt)
+    assert np.max(np.abs(z2 - z_base)) > 1e-3  # the adapter changes the score
