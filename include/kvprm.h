@@ -72,9 +72,10 @@ typedef struct {
   int32_t page_size; /* tokens per cache page; must be 16 */
 } kvprm_model_desc;
 
-/* One decoder layer of the readout weights theta + dtheta (the LoRA update is merged into the
- * base weights by the caller: W' = W + (alpha / r) B A; section 4.1 and the hyperparameter
- * table). Element type weight_dtype. Matrices are [out, in]: row-major for F32 weights; for BF16
+/* One decoder layer of the readout weights theta + dtheta (for kvprm_score the LoRA update is
+ * merged into the base weights by the caller: W' = W + (alpha / r) B A; section 4.1 and the
+ * hyperparameter table; kvprm_score_lora takes the base weights and the factors instead).
+ * Element type weight_dtype. Matrices are [out, in]: row-major for F32 weights; for BF16
  * weights in the packed tile layout written by kvprm_pack_weight (so that the matrix cores
  * stream them contiguously). Gains are plain vectors. */
 typedef struct {
@@ -182,6 +183,44 @@ kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const 
 kvprm_status kvprm_attention_partials(kvprm_handle h, const kvprm_kv_cache *cache,
                                       const kvprm_batch *batch, int32_t layer, const float *q,
                                       void *workspace, size_t ws_bytes, void *stream);
+
+/* Low-rank adapter of the readout, unmerged (section 4.1, Eq. (score): the verify token runs
+ * f_{theta + dtheta}, the base model with a LoRA adapter dtheta; the paper trains rank 256,
+ * alpha 32). For a projection with base matrix W [out][in], the factors are A [r][in] and
+ * B [out][r]; the verify token applies W u + scale * B (A u), with scale = alpha / r, which
+ * equals merging W' = W + scale * B A without holding a second copy of the weights (the cache
+ * positions were produced by the base weights, adapter off). Factors are bf16 in the packed tile
+ * layout of kvprm_pack_weight (A: rows = r, K = in; B: rows = out, K = r). A projection without
+ * an adapter has a == b == NULL; a and b are both set or both NULL. */
+typedef struct {
+  const void *a; /* [r][in] */
+  const void *b; /* [out][r] */
+} kvprm_lora_factors;
+
+typedef struct {
+  kvprm_lora_factors q, k, v, o, gate, up, down; /* in = H (q, k, v, gate, up), n_q d_h (o), F (down) */
+} kvprm_layer_lora;
+
+typedef struct {
+  const kvprm_layer_lora *layers; /* HOST array [num_layers] of device pointers */
+  int32_t rank;                   /* r: a multiple of 32 in [32, 512] */
+  float scale;                    /* alpha / r */
+} kvprm_lora;
+
+/* Workspace bytes of kvprm_score_lora for this batch and adapter rank (>= the bytes of
+ * kvprm_workspace_size). KVPRM_E_UNSUPPORTED for fp32 weights. */
+kvprm_status kvprm_workspace_size_lora(kvprm_handle h, const kvprm_batch *batch, int32_t rank,
+                                       size_t *bytes);
+
+/* kvprm_score with the base weights and an unmerged adapter: every adapted projection of the
+ * verify token is W u + scale * B (A u); the rest of the pass, the outputs and the conventions
+ * are those of kvprm_score. Requires BF16 weights (KVPRM_E_UNSUPPORTED otherwise); rank outside
+ * [32, 512] or not a multiple of 32, or a factor pair with one pointer NULL, is
+ * KVPRM_E_INVALID. The workspace must hold kvprm_workspace_size_lora(batch, rank) bytes. */
+kvprm_status kvprm_score_lora(kvprm_handle h, const kvprm_kv_cache *cache,
+                              const kvprm_batch *batch, const kvprm_readout_weights *base,
+                              const kvprm_lora *lora, void *workspace, size_t ws_bytes,
+                              float *scores, float *logits, void *stream);
 
 /* Repack one bf16 weight matrix W [rows][K] from row-major order into the packed tile layout
  * that kvprm_score reads for BF16 weights: blocks of 1 KiB, block kb * (rows / 16) + t holding

@@ -22,7 +22,8 @@ DTYPE_CODE = {"f32": KVPRM_F32, "bf16": KVPRM_BF16, "fp8": KVPRM_FP8_E4M3}
 
 EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
             "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
-            "kvprm_last_error"]
+            "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_last_error"]
+LORA_PROJECTIONS = ("q", "k", "v", "o", "gate", "up", "down")
 
 
 class ModelDesc(ctypes.Structure):
@@ -43,6 +44,19 @@ class ReadoutWeights(ctypes.Structure):
     _fields_ = [("layers", ctypes.POINTER(LayerWeights)), ("verify_embed", ctypes.c_void_p),
                 ("final_norm", ctypes.c_void_p), ("reward_w", ctypes.c_void_p),
                 ("reward_b", ctypes.c_float)]
+
+
+class LoraFactors(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_void_p), ("b", ctypes.c_void_p)]
+
+
+class LayerLora(ctypes.Structure):
+    _fields_ = [(n, LoraFactors) for n in LORA_PROJECTIONS]
+
+
+class Lora(ctypes.Structure):
+    _fields_ = [("layers", ctypes.POINTER(LayerLora)), ("rank", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
 
 
 class KVCache(ctypes.Structure):
@@ -95,8 +109,14 @@ def _load():
     lib.kvprm_attention_partials.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
                                              ctypes.c_int32, vp, vp, sz, vp]
     lib.kvprm_pack_weight.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, vp]
+    lib.kvprm_workspace_size_lora.argtypes = [vp, ctypes.POINTER(Batch), ctypes.c_int32,
+                                              ctypes.POINTER(sz)]
+    lib.kvprm_score_lora.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
+                                     ctypes.POINTER(ReadoutWeights), ctypes.POINTER(Lora), vp, sz,
+                                     vp, vp, vp]
     for f in ("kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
-              "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight"):
+              "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
+              "kvprm_workspace_size_lora", "kvprm_score_lora"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kvprm_last_error.argtypes = []
     lib.kvprm_last_error.restype = ctypes.c_char_p
@@ -172,6 +192,33 @@ def make_readout(layers: Sequence[dict], verify_embed: int, final_norm: int, rew
                        reward_w, reward_b)
     r._keep = arr
     return r
+
+
+def make_lora(layers: Sequence[dict], rank: int, scale: float) -> Lora:
+    """layers: per layer a dict projection -> (a_ptr, b_ptr) of device pointers; projections
+    missing from the dict have no adapter."""
+    arr = (LayerLora * len(layers))()
+    for i, d in enumerate(layers):
+        for p in LORA_PROJECTIONS:
+            a, b = d.get(p, (None, None))
+            setattr(arr[i], p, LoraFactors(a or None, b or None))
+    r = Lora(ctypes.cast(arr, ctypes.POINTER(LayerLora)), rank, scale)
+    r._keep = arr
+    return r
+
+
+def kvprm_workspace_size_lora(handle: int, batch: Batch, rank: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.kvprm_workspace_size_lora(handle, ctypes.byref(batch), rank, ctypes.byref(n)))
+    return n.value
+
+
+def kvprm_score_lora(handle: int, cache: KVCache, batch: Batch, base: ReadoutWeights,
+                     lora: Lora, workspace_ptr: int, ws_bytes: int, scores_ptr: int,
+                     logits_ptr: int = 0, stream: int = 0) -> None:
+    _check(lib.kvprm_score_lora(handle, ctypes.byref(cache), ctypes.byref(batch),
+                                ctypes.byref(base), ctypes.byref(lora), workspace_ptr, ws_bytes,
+                                scores_ptr, logits_ptr or None, stream or None))
 
 
 def kvprm_workspace_size(handle: int, batch: Batch) -> int:

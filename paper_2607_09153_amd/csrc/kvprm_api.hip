@@ -261,6 +261,108 @@ static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b, const 
   return gt;
 }
 
+static kvprm_status check_readout(const kvprm_handle h, const kvprm_readout_weights *wts,
+                                  const char *fn) {
+  if (!wts || !wts->layers || !wts->verify_embed || !wts->final_norm || !wts->reward_w)
+    return fail(KVPRM_E_INVALID, "%s: null readout weights", fn);
+  for (int l = 0; l < h->dm.layers; ++l) {
+    const kvprm_layer_weights &W = wts->layers[l];
+    if (!W.attn_norm || !W.wq || !W.wk || !W.wv || !W.wo || !W.ffn_norm || !W.w_gate ||
+        !W.w_up || !W.w_down)
+      return fail(KVPRM_E_INVALID, "%s: null weight in layer %d", fn, l);
+  }
+  return KVPRM_OK;
+}
+
+static kvprm_status check_lora_rank(const kvprm_handle h, int32_t rank, const char *fn) {
+  if (h->dm.wdt != 1)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: unmerged adapters need bf16 weights", fn);
+  if (rank < 32 || rank > 512 || rank % 32 != 0)
+    return fail(KVPRM_E_INVALID, "%s: adapter rank %d is not a multiple of 32 in [32, 512]", fn,
+                rank);
+  return KVPRM_OK;
+}
+
+static kvprm_status check_lora(const kvprm_handle h, const kvprm_lora *lora, const char *fn) {
+  if (!lora || !lora->layers) return fail(KVPRM_E_INVALID, "%s: null adapter", fn);
+  kvprm_status st = check_lora_rank(h, lora->rank, fn);
+  if (st != KVPRM_OK) return st;
+  if (!(lora->scale == lora->scale)) return fail(KVPRM_E_INVALID, "%s: adapter scale is NaN", fn);
+  static const char *names[7] = {"q", "k", "v", "o", "gate", "up", "down"};
+  for (int l = 0; l < h->dm.layers; ++l) {
+    const kvprm_layer_lora &L = lora->layers[l];
+    const kvprm_lora_factors f[7] = {L.q, L.k, L.v, L.o, L.gate, L.up, L.down};
+    for (int i = 0; i < 7; ++i)
+      if ((f[i].a == nullptr) != (f[i].b == nullptr))
+        return fail(KVPRM_E_INVALID, "%s: layer %d adapter %s has one factor null", fn, l,
+                    names[i]);
+  }
+  return KVPRM_OK;
+}
+
+// The matrix-core pipeline (bf16 weights): seven launches per layer, QKV (split-K) and its
+// rotary step, attention and its merge, then the output, gate/up and down projections with
+// their element-wise steps fused (no split-K partials). With an adapter, each projection group
+// that has one first computes scale * A u (a split-K GEMV and its finish) and the projection
+// adds B (scale * A u) as a tail of its input range.
+static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
+                             const kvprm_batch *b, const kvprm_readout_weights *wts,
+                             const kvprm_lora *lora, const Plan &p, const Workspace &w,
+                             const GroupTable &gt, float *scores, float *logits, hipStream_t s) {
+  const Dims &dm = h->dm;
+  const int EB = dm.kvdt == 0 ? 4 : (dm.kvdt == 1 ? 2 : 1);
+  const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * EB;
+  const size_t layer_scales = (size_t)cache->num_pages * dm.nkv;
+  const int tkb = lora ? lora->rank / 32 : 0;
+  const LoraTail none{{nullptr, nullptr, nullptr}, 0};
+  auto tail_of = [&](const void *b0, const void *b1, const void *b2) {
+    LoraTail t{{b0, b1, b2}, (b0 || b1 || b2) ? tkb : 0};
+    return t;
+  };
+  HIP_TRY(launch_init_mx(dm, p, w, wts->verify_embed, wts->layers[0].attn_norm, b->lengths, s),
+          "init");
+  for (int l = 0; l < dm.layers; ++l) {
+    const kvprm_layer_weights &W = wts->layers[l];
+    const void *gamma_next = l + 1 < dm.layers ? wts->layers[l + 1].attn_norm : nullptr;
+    LoraTail t_qkv = none, t_o = none, t_gu = none, t_d = none;
+    if (lora) {
+      const kvprm_layer_lora &A = lora->layers[l];
+      t_qkv = tail_of(A.q.b, A.k.b, A.v.b);
+      t_o = tail_of(A.o.b, nullptr, nullptr);
+      t_gu = tail_of(A.gate.b, A.up.b, nullptr);
+      t_d = tail_of(A.down.b, nullptr, nullptr);
+      const void *a_qkv[3] = {A.q.a, A.k.a, A.v.a};
+      HIP_TRY(launch_lora_a(dm, p, w, LORA_QKV, a_qkv, lora->scale, w.opA, s), "q/k/v adapter");
+    }
+    HIP_TRY(launch_qkv_mx(dm, p, w, W.wq, W.wk, W.wv, t_qkv, s), "qkv projection");
+    HIP_TRY(launch_attn_mx(dm, p, w, (const char *)cache->k_pages + layer_bytes * l,
+                           (const char *)cache->v_pages + layer_bytes * l,
+                           cache->k_scale ? cache->k_scale + layer_scales * l : nullptr,
+                           cache->v_scale ? cache->v_scale + layer_scales * l : nullptr,
+                           b->page_table, b->lengths, gt, w.q, w.kself, w.vself, nullptr, w.opO,
+                           s),
+            "attention");
+    if (lora && t_o.tkb) {
+      const void *a_o[3] = {lora->layers[l].o.a, nullptr, nullptr};
+      HIP_TRY(launch_lora_a(dm, p, w, LORA_O, a_o, lora->scale, w.opO, s), "output adapter");
+    }
+    HIP_TRY(launch_oproj_fused(dm, p, w, W.wo, W.ffn_norm, t_o, s), "output projection");
+    if (lora && t_gu.tkb) {
+      const void *a_gu[3] = {lora->layers[l].gate.a, lora->layers[l].up.a, nullptr};
+      HIP_TRY(launch_lora_a(dm, p, w, LORA_GU, a_gu, lora->scale, w.opA, s), "gate/up adapter");
+    }
+    HIP_TRY(launch_gateup_fused(dm, p, w, W.w_gate, W.w_up, t_gu, s), "gate/up projection");
+    if (lora && t_d.tkb) {
+      const void *a_d[3] = {lora->layers[l].down.a, nullptr, nullptr};
+      HIP_TRY(launch_lora_a(dm, p, w, LORA_DOWN, a_d, lora->scale, w.opD, s), "down adapter");
+    }
+    HIP_TRY(launch_down_fused(dm, p, w, W.w_down, gamma_next, t_d, s), "down projection");
+  }
+  HIP_TRY(launch_head(dm, p, w, wts->final_norm, wts->reward_w, wts->reward_b, scores, logits, s),
+          "reward head");
+  return KVPRM_OK;
+}
+
 kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
                          const kvprm_readout_weights *wts, void *workspace, size_t ws_bytes,
                          float *scores, float *logits, void *stream) {
@@ -270,14 +372,7 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   if (st != KVPRM_OK) return st;
   if (b->batch == 0) return ok();
   if ((st = check_cache(h, cache, fn)) != KVPRM_OK) return st;
-  if (!wts || !wts->layers || !wts->verify_embed || !wts->final_norm || !wts->reward_w)
-    return fail(KVPRM_E_INVALID, "%s: null readout weights", fn);
-  for (int l = 0; l < h->dm.layers; ++l) {
-    const kvprm_layer_weights &W = wts->layers[l];
-    if (!W.attn_norm || !W.wq || !W.wk || !W.wv || !W.wo || !W.ffn_norm || !W.w_gate ||
-        !W.w_up || !W.w_down)
-      return fail(KVPRM_E_INVALID, "%s: null weight in layer %d", fn, l);
-  }
+  if ((st = check_readout(h, wts, fn)) != KVPRM_OK) return st;
   if (!scores) return fail(KVPRM_E_INVALID, "%s: null scores", fn);
   if ((st = check_ws(h, b, workspace, ws_bytes, fn)) != KVPRM_OK) return st;
   if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
@@ -287,32 +382,9 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   const Plan p = make_plan(dm, b->batch, b->max_pages);
   const Workspace w = carve(dm, p, workspace);
   const GroupTable gt = group_table(h, b, p);
-  const int EB = dm.kvdt == 0 ? 4 : (dm.kvdt == 1 ? 2 : 1);
-  const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * EB;
-  const size_t layer_scales = (size_t)cache->num_pages * dm.nkv;
   if (dm.wdt == 1) {
-    // matrix-core pipeline, seven launches per layer: QKV (split-K) and its rotary step,
-    // attention and its merge, then the output, gate/up and down projections with their
-    // element-wise steps fused (no split-K partials)
-    HIP_TRY(launch_init_mx(dm, p, w, wts->verify_embed, wts->layers[0].attn_norm, b->lengths, s),
-            "init");
-    for (int l = 0; l < dm.layers; ++l) {
-      const kvprm_layer_weights &W = wts->layers[l];
-      const void *gamma_next = l + 1 < dm.layers ? wts->layers[l + 1].attn_norm : nullptr;
-      HIP_TRY(launch_qkv_mx(dm, p, w, W.wq, W.wk, W.wv, s), "qkv projection");
-      HIP_TRY(launch_attn_mx(dm, p, w, (const char *)cache->k_pages + layer_bytes * l,
-                             (const char *)cache->v_pages + layer_bytes * l,
-                             cache->k_scale ? cache->k_scale + layer_scales * l : nullptr,
-                             cache->v_scale ? cache->v_scale + layer_scales * l : nullptr,
-                             b->page_table, b->lengths, gt, w.q, w.kself, w.vself, nullptr, w.opO,
-                             s),
-              "attention");
-      HIP_TRY(launch_oproj_fused(dm, p, w, W.wo, W.ffn_norm, s), "output projection");
-      HIP_TRY(launch_gateup_fused(dm, p, w, W.w_gate, W.w_up, s), "gate/up projection");
-      HIP_TRY(launch_down_fused(dm, p, w, W.w_down, gamma_next, s), "down projection");
-    }
-    HIP_TRY(launch_head(dm, p, w, wts->final_norm, wts->reward_w, wts->reward_b, scores, logits, s),
-            "reward head");
+    if ((st = score_mx(h, cache, b, wts, nullptr, p, w, gt, scores, logits, s)) != KVPRM_OK)
+      return st;
     return ok();
   }
   // vector-ALU pipeline (fp32 weights)
@@ -342,6 +414,50 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   }
   HIP_TRY(launch_head(dm, p, w, wts->final_norm, wts->reward_w, wts->reward_b, scores, logits, s),
           "reward head");
+  return ok();
+}
+
+kvprm_status kvprm_workspace_size_lora(kvprm_handle h, const kvprm_batch *b, int32_t rank,
+                                       size_t *bytes) {
+  const char *fn = "kvprm_workspace_size_lora";
+  if (!h || !bytes) return fail(KVPRM_E_INVALID, "%s: null argument", fn);
+  kvprm_status st = check_lora_rank(h, rank, fn);
+  if (st != KVPRM_OK) return st;
+  if ((st = check_batch(h, b, fn)) != KVPRM_OK) return st;
+  if (b->batch == 0) {
+    *bytes = 0;
+    return ok();
+  }
+  const Plan p = make_plan(h->dm, b->batch, b->max_pages, rank);
+  *bytes = carve(h->dm, p, nullptr).bytes;
+  return ok();
+}
+
+kvprm_status kvprm_score_lora(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                              const kvprm_readout_weights *base, const kvprm_lora *lora,
+                              void *workspace, size_t ws_bytes, float *scores, float *logits,
+                              void *stream) {
+  const char *fn = "kvprm_score_lora";
+  if (!h) return fail(KVPRM_E_INVALID, "%s: null handle", fn);
+  kvprm_status st = check_lora(h, lora, fn);
+  if (st != KVPRM_OK) return st;
+  if ((st = check_batch(h, b, fn)) != KVPRM_OK) return st;
+  if (b->batch == 0) return ok();
+  if ((st = check_cache(h, cache, fn)) != KVPRM_OK) return st;
+  if ((st = check_readout(h, base, fn)) != KVPRM_OK) return st;
+  if (!scores) return fail(KVPRM_E_INVALID, "%s: null scores", fn);
+  const Plan p = make_plan(h->dm, b->batch, b->max_pages, lora->rank);
+  const Workspace w = carve(h->dm, p, workspace);
+  if (!workspace || ws_bytes < w.bytes)
+    return fail(KVPRM_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, w.bytes,
+                workspace ? ws_bytes : (size_t)0);
+  if (((uintptr_t)workspace & 255) != 0)
+    return fail(KVPRM_E_WORKSPACE, "%s: workspace not 256-byte aligned", fn);
+  if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
+  const GroupTable gt = group_table(h, b, p);
+  if ((st = score_mx(h, cache, b, base, lora, p, w, gt, scores, logits, (hipStream_t)stream)) !=
+      KVPRM_OK)
+    return st;
   return ok();
 }
 

@@ -46,6 +46,7 @@ struct Workspace {
   float *apart;    // attention partials [B][nq][nch][d + 2] (acc..., m, l)
   float *o;        // [B][nq * d]
   float *hffn;     // [B][F] (vector-ALU path)
+  uint16_t *topd;  // adapter operand slots [3][rank / 32][NT][64][8] bf16 (scale * A u)
   // matrix-core path
   float *rope;       // [B][d/2][2] cos, sin of the verify position
   uint16_t *opA;     // GEMV operands (bf16 hi/lo): QKV and gate/up input (K = H)
@@ -56,6 +57,13 @@ struct Workspace {
 
 struct GemvPlan {
   int rows, K, kslice, ksplit;
+  int ktail;  // 1: one more k-slice for an adapter tail
+};
+
+// Adapter of one projection group (q/k/v, o, gate/up or down) of one layer.
+struct LoraTail {
+  const void *b[3];  // B factor of each segment (packed [rows_i][rank]); null = no adapter
+  int tkb;           // rank / 32; 0 = no tail
 };
 
 struct Plan {
@@ -69,8 +77,14 @@ struct Plan {
   // matrix-core path
   int nt, bp;                 // operand column tiles and padded batch
   GemvPlan g_qkv;
+  // low-rank adapter (0 = none): the split-K plans of the A-factor products of the q/k/v,
+  // output, gate/up and down groups
+  int lora_rank;
+  GemvPlan g_la[4];
   size_t part_elems;
 };
+
+enum { LORA_QKV = 0, LORA_O = 1, LORA_GU = 2, LORA_DOWN = 3 };
 
 // matrix-core helpers (kvprm_mfma.hip)
 int gemv_nt(int B);
@@ -78,7 +92,7 @@ int gemv_bp(int B);
 int gemv_mt(int nt, int rows);
 hipError_t launch_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, hipStream_t s);
 
-Plan make_plan(const Dims &dm, int B, int max_pages);
+Plan make_plan(const Dims &dm, int B, int max_pages, int lora_rank = 0);
 Workspace carve(const Dims &dm, const Plan &p, void *base);
 
 // Kernel launchers (return hipGetLastError()).
@@ -98,15 +112,19 @@ hipError_t launch_gemv(const Dims &dm, const Plan &p, const GemvSegs &segs, int 
 hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *ev,
                           const void *gamma0, const int32_t *lengths, hipStream_t s);
 hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
-                         const void *wk, const void *wv, hipStream_t s);
+                         const void *wk, const void *wv, const LoraTail &tail, hipStream_t s);
+// scale * A u of one projection group's adapters into the operand slots w.topd (slot i =
+// segment i; a[i] null = segment without adapter): a split-K GEMV and a finish kernel
+hipError_t launch_lora_a(const Dims &dm, const Plan &p, const Workspace &w, int group,
+                         const void *const a[3], float scale, const uint16_t *act, hipStream_t s);
 // fused projections: no split-K partials, the element-wise step after the output, gate/up and
 // down projections runs in the epilogue
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
-                              const void *gamma_ffn, hipStream_t s);
+                              const void *gamma_ffn, const LoraTail &tail, hipStream_t s);
 hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
-                               const void *wu, hipStream_t s);
+                               const void *wu, const LoraTail &tail, hipStream_t s);
 hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
-                             const void *gamma_next, hipStream_t s);
+                             const void *gamma_next, const LoraTail &tail, hipStream_t s);
 hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
                           const char *vp, const float *ksc, const float *vsc,
                           const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,

@@ -79,13 +79,19 @@ static GemvPlan gemv_plan(int rows, int K, int B) {
   const int kb_per = (nkb + want - 1) / want;  // <= 32 unless the slice count is capped
   g.kslice = kb_per * 32;
   g.ksplit = (K + g.kslice - 1) / g.kslice;
+  g.ktail = 0;
   return g;
 }
 
-Plan make_plan(const Dims &dm, int B, int max_pages) {
+static size_t partial_elems(const GemvPlan &g) {
+  return (size_t)((g.ksplit + g.ktail + 3) & ~3) * g.rows;
+}
+
+Plan make_plan(const Dims &dm, int B, int max_pages, int lora_rank) {
   Plan p{};
   p.B = B;
   p.max_pages = max_pages;
+  p.lora_rank = lora_rank;
   // Matrix-core attention chunk: the longest of 16, 32, 64 pages that still gives at least 160
   // work items (of 256 compute units) for a batch that fills its page table (longer chunks
   // stream longer page runs per wave: measured faster even with some units idle), and at most
@@ -107,7 +113,16 @@ Plan make_plan(const Dims &dm, int B, int max_pages) {
     p.nt = gemv_nt(B);
     p.bp = gemv_bp(B);
     p.g_qkv = gemv_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B);
-    m = (size_t)((p.g_qkv.ksplit + 3) & ~3) * p.g_qkv.rows;
+    p.g_qkv.ktail = lora_rank > 0 ? 1 : 0;
+    m = partial_elems(p.g_qkv);
+    if (lora_rank > 0) {
+      // A-factor products: rows = adapter rank per segment, input = the group's input width
+      p.g_la[LORA_QKV] = gemv_plan(3 * lora_rank, dm.H, B);
+      p.g_la[LORA_O] = gemv_plan(lora_rank, dm.nq * dm.d, B);
+      p.g_la[LORA_GU] = gemv_plan(2 * lora_rank, dm.H, B);
+      p.g_la[LORA_DOWN] = gemv_plan(lora_rank, dm.F, B);
+      for (const GemvPlan &g : p.g_la) m = partial_elems(g) > m ? partial_elems(g) : m;
+    }
   } else {
     // vector-ALU GEMV: the activation slice of all B candidates is staged in LDS (<= 32 KiB)
     p.rb = 256;
@@ -161,6 +176,7 @@ Workspace carve(const Dims &dm, const Plan &p, void *base) {
     w.opA = (uint16_t *)take((per_k * dm.H + 1) / 2);
     w.opO = (uint16_t *)take((per_k * dm.nq * dm.d + 1) / 2);
     w.opD = (uint16_t *)take((per_k * dm.F + 1) / 2);
+    if (p.lora_rank > 0) w.topd = (uint16_t *)take((per_k * 3 * p.lora_rank + 1) / 2);
   }
   w.bytes = off;
   return w;

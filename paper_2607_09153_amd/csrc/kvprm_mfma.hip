@@ -172,8 +172,14 @@ struct GemvArgs {
   int rows, K, kslice, ksplit;
   const uint4 *act;  // operand buffer of the input
   int B;
-  float *part;  // [rows][B][ksp] k-partials, ksp = ksplit rounded up to 4
+  float *part;  // [rows][B][ksp] k-partials, ksp = ksplit (+ 1 with a tail) rounded up to 4
   int ksp;
+  // adapter tail (tkb > 0): one more k-slice, index ksplit, over the tkb input blocks of the
+  // segments' B factors (packed [rows_i][32 tkb], null = no adapter: the slice stores zeros)
+  // with operand slot i of tact (tstride uint4 entries apart) as input
+  const void *tw[3];
+  const uint4 *tact;
+  int tkb, tstride;
 };
 
 // part[row][b][ks] = sum over k-slice ks of W[row][k] u_b[k], W in the packed tile layout
@@ -189,14 +195,16 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
   extern __shared__ uint4 act_s[];  // the block's k-slice of the operand: nkb * NT * 64 entries
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ks = blockIdx.y;
-  const int k0 = ks * a.kslice;
-  const int nkb = min(a.kslice, a.K - k0) >> 5;
+  const bool tail = ks == a.ksplit;  // the adapter slice (only launched with a tail)
+  const int k0 = tail ? 0 : ks * a.kslice;
+  const int nkb = tail ? 0 : min(a.kslice, a.K - k0) >> 5;
   const int tile0 = (blockIdx.x * WPB + wave) * MT;
   const int B = a.B;
   const bool active = tile0 * 16 < a.rows;
   const uint4 *wt[MT];
   size_t kstride[MT];  // uint4 entries between consecutive input blocks of a tile
   bool valid[MT];
+  int segm[MT], ltm[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     const int tile = tile0 + m;
@@ -207,6 +215,8 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
     const size_t ntiles = (size_t)a.seg_rows[seg] / 16;
     kstride[m] = ntiles * 64;
     wt[m] = (const uint4 *)a.w[seg] + ((size_t)(k0 >> 5) * ntiles + lt) * 64 + lane;
+    segm[m] = seg;
+    ltm[m] = lt;
   }
   // Rows of an absent tile read tile 0 of their segment and are never stored.
   auto load_batch = [&](int kb, uint4 (&av)[U][MT]) {
@@ -266,6 +276,22 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av[m], bv[t], acc[m][t]);
+  }
+  if (tail) {
+    // B_seg (scale * A_seg u): the segment's B factor tiles over the adapter rank, the
+    // segment's operand slot as input (tiles of a segment without an adapter stay zero)
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const uint4 *bw = (const uint4 *)a.tw[segm[m]];
+      if (!bw) continue;
+      bw += (size_t)ltm[m] * 64 + lane;
+      const uint4 *tp = a.tact + (size_t)segm[m] * a.tstride + lane;
+      for (int kb = 0; kb < a.tkb; ++kb) {
+        const uint4 av = ld_stream(&bw[(size_t)kb * kstride[m]]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av, tp[(kb * NT + t) * 64], acc[m][t]);
+      }
+    }
   }
   const int n = lane & 15, c4 = (lane >> 4) * 4;
 #pragma unroll
@@ -474,6 +500,11 @@ struct FusedArgs {
   uint16_t *op;              // next operand (RESID, SWIGLU)
   int NT, Bp;                // layout of the next operand
   int F;
+  // adapter tail (tkb > 0): tkb more input blocks from the segments' B factors (packed
+  // [rows_i][32 tkb], null = no adapter) with operand slot i of tact as input
+  const void *tw[3];
+  const uint4 *tact;
+  int tkb, tstride;
 };
 
 template <int MT, int NT, int WPB, int U, int EPI>
@@ -491,6 +522,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   if (EPI == EPI_SWIGLU && MT > 1) tile[MT - 1] = blockIdx.x + a.F / 16;
   const uint4 *wt[MT];
   size_t kstride[MT];
+  int segm[MT], ltm[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     int seg = 0, base = 0;
@@ -498,6 +530,8 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
     const size_t ntiles = (size_t)a.seg_rows[seg] / 16;
     kstride[m] = ntiles * 64;
     wt[m] = (const uint4 *)a.w[seg] + (size_t)(tile[m] - base / 16) * 64 + lane;
+    segm[m] = seg;
+    ltm[m] = tile[m] - base / 16;
   }
   // this wave's input blocks [kb0, kb1)
   const int nkb = a.K >> 5;
@@ -556,6 +590,22 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
 #pragma unroll
       for (int m = 0; m < MT; ++m)
         acc[m][t] = mfma16(ld_stream(&wt[m][(size_t)kb * kstride[m]]), bv, acc[m][t]);
+    }
+  }
+  // adapter tail: B_seg (scale * A_seg u), its tkb input blocks spread over the waves
+  if (a.tkb > 0) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const uint4 *bw = (const uint4 *)a.tw[segm[m]];
+      if (!bw) continue;
+      bw += (size_t)ltm[m] * 64 + lane;
+      const uint4 *tp = a.tact + (size_t)segm[m] * a.tstride + lane;
+      for (int kb = wave; kb < a.tkb; kb += WPB) {
+        const uint4 av = ld_stream(&bw[(size_t)kb * kstride[m]]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          acc[m][t] = mfma16(av, tp[((size_t)kb * NT + t) * 64], acc[m][t]);
+      }
     }
   }
   // hi + lo, then the waves' sums in LDS
@@ -1247,9 +1297,15 @@ hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, con
 
 static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *w0, int r0,
                                  const void *w1, int r1, const void *w2, int r2,
-                                 const uint16_t *act, float *part, hipStream_t s) {
+                                 const uint16_t *act, float *part, const LoraTail &tail,
+                                 const uint16_t *tact, hipStream_t s) {
   GemvArgs a;
   memset(&a, 0, sizeof a);
+  const bool has_tail = gp.ktail > 0 && tail.tkb > 0;
+  for (int i = 0; i < 3; ++i) a.tw[i] = tail.b[i];
+  a.tact = (const uint4 *)tact;
+  a.tkb = has_tail ? tail.tkb : 0;
+  a.tstride = tail.tkb * p.nt * 64;
   a.w[0] = w0;
   a.w[1] = w1;
   a.w[2] = w2;
@@ -1264,14 +1320,14 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
   a.act = (const uint4 *)act;
   a.B = p.B;
   a.part = part;
-  a.ksp = (gp.ksplit + 3) & ~3;
+  a.ksp = (gp.ksplit + gp.ktail + 3) & ~3;
   const int mt = gemv_mt(p.nt, gp.rows);
   // 4 waves per block; the operand k-slice is staged in LDS for one column tile and read
   // straight from memory (L2) for more (measured faster than staging it: LDS would cap
   // residency, and an LDS-streamed variant with 8 row tiles per block measured slower)
   constexpr int WPB = 4;
   const bool direct = p.nt >= 2;
-  dim3 grid((gp.rows / 16 + WPB * mt - 1) / (WPB * mt), gp.ksplit);
+  dim3 grid((gp.rows / 16 + WPB * mt - 1) / (WPB * mt), gp.ksplit + (has_tail ? 1 : 0));
   const size_t lds = direct ? 0 : (size_t)(gp.kslice / 32) * p.nt * 64 * sizeof(uint4);
 #define KVPRM_G(MT_, NT_, U_)                                                                  \
   if (direct)                                                                                  \
@@ -1297,18 +1353,22 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
   return hipGetLastError();
 }
 
-static int ksp_of(const GemvPlan &g) { return (g.ksplit + 3) & ~3; }
+static int ksp_of(const GemvPlan &g) { return (g.ksplit + g.ktail + 3) & ~3; }
 
 hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
-                         const void *wk, const void *wv, hipStream_t s) {
+                         const void *wk, const void *wv, const LoraTail &tail, hipStream_t s) {
+  // with an adapter plan the tail slice always runs (it stores zeros for segments without an
+  // adapter), since the finish adds ksplit + 1 partials
+  LoraTail t = tail;
+  if (p.g_qkv.ktail > 0) t.tkb = p.lora_rank / 32;
   hipError_t e = launch_gemv_mx(p, p.g_qkv, wq, dm.nq * dm.d, wk, dm.nkv * dm.d, wv, dm.nkv * dm.d,
-                                w.opA, w.part, s);
+                                w.opA, w.part, t, w.topd, s);
   if (e != hipSuccess) return e;
   const int n = (dm.nq + 2 * dm.nkv) * (dm.d / 2) * p.B;
 #define KVPRM_F(NM)                                                                             \
   hipLaunchKernelGGL(k_qkv_fin_mx<NM>, dim3((n + 255) / 256), dim3(256), 0, s, w.part,          \
-                     ksp_of(p.g_qkv), p.g_qkv.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.nq,     \
-                     dm.nkv, dm.d, w.rope, w.q, w.kself, w.vself)
+                     ksp_of(p.g_qkv), p.g_qkv.ksplit + p.g_qkv.ktail, w.ss, p.nss, dm.H, dm.eps, \
+                     p.B, dm.nq, dm.nkv, dm.d, w.rope, w.q, w.kself, w.vself)
   switch (ksum_nmax(ksp_of(p.g_qkv))) {
     case 1: KVPRM_F(1); break;
     case 2: KVPRM_F(2); break;
@@ -1317,6 +1377,66 @@ hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, cons
   }
 #undef KVPRM_F
   return hipGetLastError();
+}
+
+// scale * (sum of the k-partials) of adapter row r (segment r / rank, index r % rank) for
+// candidate b, stored into operand slot slot[segment] of topd. One thread per (row, candidate).
+template <int NMAX>
+__global__ __launch_bounds__(256) void k_lora_fin(const float *__restrict__ part, int ksp,
+                                                  int ksplit, int rows, int B, int rank, int3 slot,
+                                                  float scale, uint16_t *topd, int NT, int Bp,
+                                                  size_t slot_elems) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= rows * B) return;
+  float4 v[NMAX];
+  ksum_load<NMAX>(part, ksp, (size_t)e, v);
+  const float sum = ksum_add<NMAX>(part, ksp, ksplit, (size_t)e, v);
+  const int r = e / B, b = e - r * B;
+  const int seg = r / rank, k = r - seg * rank;
+  const int sl = seg == 0 ? slot.x : (seg == 1 ? slot.y : slot.z);
+  store_operand(topd + (size_t)sl * slot_elems, NT, Bp, k, b, scale * sum);
+}
+
+hipError_t launch_lora_a(const Dims &dm, const Plan &p, const Workspace &w, int group,
+                         const void *const a[3], float scale, const uint16_t *act, hipStream_t s) {
+  (void)dm;
+  const void *seg[3] = {nullptr, nullptr, nullptr};
+  int slot[3] = {0, 0, 0}, n = 0;
+  for (int i = 0; i < 3; ++i)
+    if (a[i]) {
+      seg[n] = a[i];
+      slot[n++] = i;
+    }
+  if (n == 0) return hipSuccess;
+  const int r = p.lora_rank;
+  GemvPlan g = p.g_la[group];
+  g.rows = n * r;
+  const LoraTail none{{nullptr, nullptr, nullptr}, 0};
+  hipError_t e = launch_gemv_mx(p, g, seg[0], r, seg[1], n > 1 ? r : 0, seg[2], n > 2 ? r : 0,
+                                act, w.part, none, nullptr, s);
+  if (e != hipSuccess) return e;
+  const int cnt = g.rows * p.B;
+  const size_t slot_elems = (size_t)(r / 32) * p.nt * 64 * 8;
+  const int3 sl = make_int3(slot[0], slot[1], slot[2]);
+#define KVPRM_L(NM)                                                                            \
+  hipLaunchKernelGGL(k_lora_fin<NM>, dim3((cnt + 255) / 256), dim3(256), 0, s, w.part,         \
+                     ksp_of(g), g.ksplit, g.rows, p.B, r, sl, scale, w.topd, p.nt, p.bp,       \
+                     slot_elems)
+  switch (ksum_nmax(ksp_of(g))) {
+    case 1: KVPRM_L(1); break;
+    case 2: KVPRM_L(2); break;
+    case 4: KVPRM_L(4); break;
+    default: KVPRM_L(8); break;
+  }
+#undef KVPRM_L
+  return hipGetLastError();
+}
+
+static void set_tail(FusedArgs &a, const Plan &p, const Workspace &w, const LoraTail &tail) {
+  for (int i = 0; i < 3; ++i) a.tw[i] = tail.b[i];
+  a.tact = (const uint4 *)w.topd;
+  a.tkb = tail.tkb;
+  a.tstride = tail.tkb * p.nt * 64;
 }
 
 // fused projections
@@ -1352,8 +1472,9 @@ static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, i
 }
 
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
-                              const void *gamma_ffn, hipStream_t s) {
+                              const void *gamma_ffn, const LoraTail &tail, hipStream_t s) {
   FusedArgs a = fused_args(dm, p, w, dm.nq * dm.d, w.opO);
+  set_tail(a, p, w, tail);
   a.w[0] = wo;
   a.seg_rows[0] = dm.H;
   a.nseg = 1;
@@ -1363,8 +1484,9 @@ hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w,
 }
 
 hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
-                               const void *wu, hipStream_t s) {
+                               const void *wu, const LoraTail &tail, hipStream_t s) {
   FusedArgs a = fused_args(dm, p, w, dm.H, w.opA);
+  set_tail(a, p, w, tail);
   a.w[0] = wg;
   a.w[1] = wu;
   a.seg_rows[0] = dm.F;
@@ -1384,8 +1506,9 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
 }
 
 hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
-                             const void *gamma_next, hipStream_t s) {
+                             const void *gamma_next, const LoraTail &tail, hipStream_t s) {
   FusedArgs a = fused_args(dm, p, w, dm.F, w.opD);
+  set_tail(a, p, w, tail);
   a.w[0] = wd;
   a.seg_rows[0] = dm.H;
   a.nseg = 1;

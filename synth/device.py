@@ -83,6 +83,32 @@ class DeviceWorkload:
             else:
                 v[:, unused] = float("nan")
 
+    def add_lora(self, rank: int, targets=synth.LORA_PROJECTIONS):
+        """Adapter factors of every layer (bf16, packed storage like the base matrices; the
+        same values the host generator gives the oracle)."""
+        s = self.w.shape
+        stream = torch.cuda.current_stream().cuda_stream
+        self.lora_rank = rank
+        self.lora_targets = tuple(targets)
+        self.lora_layers: List[Dict[str, torch.Tensor]] = []
+        for l in range(s.num_layers):
+            d = {}
+            for name, kind, dims in synth.lora_tensors(s, rank, targets):
+                t = torch.empty(dims, dtype=_TORCH_W[s.weight_dtype], device=self.device)
+                mean, std = synth.tensor_mean_std(name, dims)
+                synth.device_normal(t.data_ptr(), t.numel(), self.w.seed, synth.stream_id(l, kind),
+                                    0, mean, std, _DT[s.weight_dtype], stream)
+                d[name] = t
+            self.lora_layers.append(d)
+
+    def lora_bytes(self) -> int:
+        return sum(t.numel() * t.element_size() for d in self.lora_layers for t in d.values())
+
+    def lora(self, kv):
+        layers = [{p: (d[f"lora_a_{p}"].data_ptr(), d[f"lora_b_{p}"].data_ptr())
+                   for p in self.lora_targets} for d in self.lora_layers]
+        return kv.make_lora(layers, self.lora_rank, synth.lora_scale(self.lora_rank))
+
     def weight_bytes(self) -> int:
         n = sum(t.numel() * t.element_size() for d in self.layers for t in d.values())
         return n + sum(t.numel() * t.element_size() for t in self.globals.values())

@@ -64,3 +64,23 @@ def run_attention(dw: DeviceWorkload, layer, q, ks, vs, with_hint=True):
         return o.cpu().numpy().astype(np.float64)
     finally:
         m.kvprm_destroy(h)
+
+
+def run_score_lora(dw: DeviceWorkload, stream=None):
+    """kvprm_score_lora with the workload's base weights and its adapter (dw.add_lora)."""
+    m = kv()
+    h = m.kvprm_create(dw.desc(m))
+    try:
+        batch = dw.batch(m)
+        n = m.kvprm_workspace_size_lora(h, batch, dw.lora_rank)
+        ws = torch.empty(max(n, 256), dtype=torch.uint8, device="cuda")
+        B = dw.w.batch
+        scores = torch.full((B,), float("nan"), dtype=torch.float32, device="cuda")
+        logits = torch.full((B,), float("nan"), dtype=torch.float32, device="cuda")
+        st = stream or torch.cuda.current_stream()
+        m.kvprm_score_lora(h, dw.cache(m), batch, dw.readout(m), dw.lora(m), ws.data_ptr(), n,
+                           scores.data_ptr(), logits.data_ptr(), st.cuda_stream)
+        st.synchronize()
+        return scores.cpu().numpy().astype(np.float64), logits.cpu().numpy().astype(np.float64)
+    finally:
+        m.kvprm_destroy(h)

@@ -165,3 +165,57 @@ def test_pack_weight_validation():
         with pytest.raises(kv.KvprmError) as e:
             kv.kvprm_pack_weight(*args)
         assert e.value.status == kv.KVPRM_E_INVALID
+
+
+def _lora(nl=2, rank=32, scale=1.0, drop=None, half=None):
+    layers = []
+    for l in range(nl):
+        d = {p: (FAKE, FAKE) for p in kv.LORA_PROJECTIONS}
+        if drop:
+            del d[drop]
+        if half and l == 1:
+            d[half] = (FAKE, 0)
+        layers.append(d)
+    return kv.make_lora(layers, rank, scale)
+
+
+def test_score_lora_validation():
+    """Adapters need bf16 weights; the rank must be a multiple of 32 in [32, 512]; a factor
+    pair is both set or both null; the workspace covers the adapter slots."""
+    hf = kv.kvprm_create(_desc())
+    try:
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_workspace_size_lora(hf, kv.make_batch(1, FAKE, 4, FAKE), 32)
+        assert e.value.status == kv.KVPRM_E_UNSUPPORTED
+    finally:
+        kv.kvprm_destroy(hf)
+    h = kv.kvprm_create(_desc(weight_dtype="bf16", kv_dtype="bf16"))
+    try:
+        batch = kv.make_batch(2, FAKE, 4, FAKE, [10, 64])
+        base = kv.kvprm_workspace_size(h, batch)
+        n = kv.kvprm_workspace_size_lora(h, batch, 64)
+        assert n > base
+        assert kv.kvprm_workspace_size_lora(h, batch, 512) > n
+        assert kv.kvprm_workspace_size_lora(h, kv.make_batch(0, FAKE, 4, FAKE), 64) == 0
+        cases = [
+            (dict(lora=_lora(rank=48)), kv.KVPRM_E_INVALID),
+            (dict(lora=_lora(rank=0)), kv.KVPRM_E_INVALID),
+            (dict(lora=_lora(rank=544)), kv.KVPRM_E_INVALID),
+            (dict(lora=_lora(half="up")), kv.KVPRM_E_INVALID),
+            (dict(lora=_lora(scale=float("nan"))), kv.KVPRM_E_INVALID),
+            (dict(ws_bytes=base), kv.KVPRM_E_WORKSPACE),
+            (dict(weights=_weights(null_layer=0)), kv.KVPRM_E_INVALID),
+            (dict(scores=0), kv.KVPRM_E_INVALID),
+        ]
+        for kw, status in cases:
+            args = dict(lora=_lora(rank=64), ws_bytes=n, weights=_weights(), scores=FAKE)
+            args.update(kw)
+            with pytest.raises(kv.KvprmError) as e:
+                kv.kvprm_score_lora(h, _cache(), batch, args["weights"], args["lora"], FAKE,
+                                    args["ws_bytes"], args["scores"])
+            assert e.value.status == status, (kw, kv.kvprm_last_error())
+        # B = 0: nothing to check or enqueue
+        kv.kvprm_score_lora(h, _cache(), kv.make_batch(0, FAKE, 4, FAKE), _weights(),
+                            _lora(drop="q"), 0, 0, FAKE)
+    finally:
+        kv.kvprm_destroy(h)
