@@ -8,8 +8,9 @@ generator) and resident in HBM before the timed region.
 
 Prints one JSON line: scores/s (value), the end-to-end KV-read rate, the roofline of the
 dominant kernel (the split-L attention chunk kernel, timed live with HIP events on its stream;
-the whole attention step with its merge is reported beside it) and the fp64 CPU oracle timed on
-a bounded sample of the same workload.
+the whole attention step with its merge is reported beside it), the same workload scored with
+the base weights and an unmerged rank-256 adapter on every projection (kvprm_score_lora,
+`lora_readout`), and the fp64 CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -71,6 +72,36 @@ def time_attention(kv, dw, h, batch, ws, n, reps):
         return a.elapsed_time(b) / reps
 
     return timed(partials), timed(step)
+
+
+def time_lora(kv, dw, h, batch, rank, steps, warmup):
+    """Whole scoring calls with the base weights and an unmerged adapter of this rank on every
+    projection (kvprm_score_lora): the same workload, K calls between two synchronisations."""
+    import torch
+    import synth
+    w = dw.w
+    dw.add_lora(rank)
+    n = kv.kvprm_workspace_size_lora(h, batch, rank)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    scores = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    cache, base, lora = dw.cache(kv), dw.readout(kv), dw.lora(kv)
+
+    def call():
+        kv.kvprm_score_lora(h, cache, batch, base, lora, ws.data_ptr(), n, scores.data_ptr(), 0,
+                            stream.cuda_stream)
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        call()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    return {"rank": rank, "scale": synth.lora_scale(rank),
+            "targets": list(synth.LORA_PROJECTIONS), "ms_per_call": ms,
+            "scores_per_s": w.batch / (ms * 1e-3), "adapter_bytes_per_call": dw.lora_bytes()}
 
 
 def copy_bandwidth(nbytes=4 << 30, reps=10):
@@ -172,9 +203,11 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU work of the oracle sample (repeated passes)")
     ap.add_argument("--attn-reps", type=int, default=56)
+    ap.add_argument("--lora-rank", type=int, default=256,
+                    help="rank of the unmerged adapter of the second timed line (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+        print(f"bench.py measures one GPU only: the library has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
 
@@ -221,6 +254,12 @@ def main():
     ms = dt * 1e3 / args.steps
     _log(f"timed {args.steps} steps: {ms:.3f} ms/step")
 
+    lora = None
+    if args.lora_rank > 0:
+        lora = time_lora(kv, dw, h, batch, args.lora_rank, args.steps, args.warmup)
+        _log(f"unmerged rank-{args.lora_rank} adapter: {lora['ms_per_call']:.3f} ms/call")
+        lora["end_to_end_gbps"] = (kv_bytes + w_bytes + lora["adapter_bytes_per_call"]) / (
+            lora["ms_per_call"] * 1e-3) / 1e9
     kernel_ms, step_ms = time_attention(kv, dw, h, batch, ws, n, max(args.attn_reps, 1))
     kv_per_layer = kv_bytes / w.shape.num_layers
     achieved = kv_per_layer / (kernel_ms * 1e-3) / 1e9
@@ -264,6 +303,8 @@ def main():
                         "max": per_call[-1]},
         "copy_reference_gbps": copy_gbps,
     }
+    if lora is not None:
+        out["lora_readout"] = lora
     if args.cpu_layers > 0:
         _log("timing the oracle on the CPU sample ...")
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers, args.cpu_seconds)

@@ -28,11 +28,22 @@ SAMPLES = {
 }
 
 
-def make(name):
+# workloads scored with the unmerged adapter of this rank on every projection (the verify
+# token runs theta + scale * B A; kvprm_score_lora on the GPU): file <workload>_lora<rank>.json
+LORA_SAMPLES = {
+    "ragged_32k": ([0, 5], 256),
+}
+
+
+def make(name, lora_rank=0):
     w = synth.make_workload(name)
-    cand = SAMPLES[name]
+    cand = LORA_SAMPLES[name][0] if lora_rank else SAMPLES[name]
     t0 = time.time()
     ro = oin.readout_from_synth(w.shape, w.seed, layer_cache=1)
+    if lora_rank:
+        ro = ko.readout_with_adapter(ro, oin.lora_from_synth(w.shape, w.seed, lora_rank,
+                                                             layer_cache=1),
+                                     synth.lora_scale(lora_rank))
     cache = oin.cache_from_synth(w, page_cache=64)
     z, p = ko.verify_pass(w.shape, ro, cache, [w.lengths[b] for b in cand],
                           [w.page_table[b] for b in cand])
@@ -47,12 +58,21 @@ def make(name):
         "source": "fp64 oracle (oracle/kvprm_oracle.py verify_pass), Eq. (score) of section 4.1",
         "oracle_seconds": round(time.time() - t0, 1),
     }
-    path = os.path.join(HERE, f"{name}.json")
+    if lora_rank:
+        out["lora_rank"] = lora_rank
+        out["lora_targets"] = list(synth.LORA_PROJECTIONS)
+        out["source"] += "; adapter theta + scale * B A on the verify token (readout_with_adapter)"
+    path = os.path.join(HERE, f"{name}_lora{lora_rank}.json" if lora_rank else f"{name}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
     print(f"{name}: z={out['z']} in {out['oracle_seconds']} s -> {path}", flush=True)
 
 
 if __name__ == "__main__":
-    for name in (sys.argv[1:] or list(SAMPLES)):
-        make(name)
+    # names: a workload (stored values of the base readout) or <workload>_lora (with the adapter)
+    for name in (sys.argv[1:] or list(SAMPLES) + [f"{n}_lora" for n in LORA_SAMPLES]):
+        if name.endswith("_lora"):
+            base = name[: -len("_lora")]
+            make(base, LORA_SAMPLES[base][1])
+        else:
+            make(name)

@@ -45,3 +45,32 @@ def test_full_size_against_stored_oracle(name):
     print(f"  max|dP| = {dp:.3e}  max|dz| = {dz:.3e}", flush=True)
     assert dp <= 2e-3
     assert dz <= 2e-2
+
+
+def test_full_size_adapter_against_stored_oracle():
+    """The ragged 32k batch with the unmerged rank-256 adapter on every projection
+    (kvprm_score_lora, as the benchmark's adapter line runs it), sampled candidates against
+    stored fp64 oracle values."""
+    from gpu_common import run_score_lora
+    path = os.path.join(GOLDEN, "ragged_32k_lora256.json")
+    if not os.path.exists(path):
+        pytest.skip("no stored oracle values (run tests/golden/make_golden.py ragged_32k_lora)")
+    ref = json.load(open(path))
+    w = synth.make_workload(ref["workload"])
+    assert w.seed == ref["seed"] and w.batch == ref["batch"]
+    assert [w.lengths[b] for b in ref["candidates"]] == ref["lengths"]
+    print(f"case: full size {ref['workload']} with a rank-{ref['lora_rank']} adapter", flush=True)
+    dw = DeviceWorkload(w, nan_unused_pages=True)
+    dw.add_lora(ref["lora_rank"], tuple(ref["lora_targets"]))
+    try:
+        p, z = run_score_lora(dw)
+    finally:
+        del dw
+        torch.cuda.empty_cache()
+    cand = ref["candidates"]
+    dp = np.max(np.abs(p[cand] - np.array(ref["p"])))
+    dz = np.max(np.abs(z[cand] - np.array(ref["z"])))
+    print(f"  max|dP| = {dp:.3e}  max|dz| = {dz:.3e}", flush=True)
+    assert np.all(np.isfinite(p)) and np.all((p >= 0) & (p <= 1))
+    assert dp <= 2e-3
+    assert dz <= 2e-2
