@@ -92,10 +92,11 @@ def cache_from_synth(w: synth.Workload, nan_pages=(), page_cache: int = 4096) ->
 
 
 def score_workload(w: synth.Workload, candidates=None, return_hidden: bool = False,
-                   lora_rank: int = 0, lora_targets=synth.LORA_PROJECTIONS):
+                   lora_rank: int = 0, lora_targets=synth.LORA_PROJECTIONS, depth: int = 1):
     """Oracle scores (z, P(+)) of the listed candidates (default: all) of a workload; with
     lora_rank > 0 the verify token runs the base weights with the synthetic adapter of that
-    rank on lora_targets (scale alpha / rank)."""
+    rank on lora_targets (scale alpha / rank); depth > 1 scores with that many verify tokens
+    (the depth-k readout)."""
     cand = list(range(w.batch)) if candidates is None else list(candidates)
     ro = readout_from_synth(w.shape, w.seed)
     if lora_rank > 0:
@@ -104,4 +105,7 @@ def score_workload(w: synth.Workload, candidates=None, return_hidden: bool = Fal
     cache = cache_from_synth(w)
     lens = [w.lengths[b] for b in cand]
     pt = [w.page_table[b] for b in cand]
+    if depth > 1:
+        return ko.verify_pass_depth(w.shape, ro, cache, lens, pt, depth,
+                                    return_hidden=return_hidden)
     return ko.verify_pass(w.shape, ro, cache, lens, pt, return_hidden=return_hidden)

@@ -305,6 +305,50 @@ def verify_pass(shape, readout: Readout, cache: PagedCache, lengths: Sequence[in
     return z, p
 
 
+def verify_pass_depth(shape, readout: Readout, cache: PagedCache, lengths: Sequence[int],
+                      page_table, depth: int, return_hidden: bool = False):
+    """Depth-k readout (section 3, definition of the depth-k readout; the k > 1 experiment of
+    section 5): `depth` verify tokens are appended after the L_b cached tokens, at positions
+    L_b .. L_b + depth - 1, and pass through the readout layers together, token i attending to
+    the cached keys and to verify tokens 0..i (causal, as decoding an appended suffix). The
+    score is read from the last verify token. depth = 1 is verify_pass."""
+    B = len(lengths)
+    H, nq, nkv, d = shape.hidden, shape.num_q_heads, shape.num_kv_heads, shape.head_dim
+    g = nq // nkv
+    eps, theta, ps = shape.rms_eps, shape.rope_theta, shape.page_size
+    k = int(depth)
+    x = np.tile(np.asarray(readout.verify_embed, dtype=np.float64), (B, k, 1))  # [B, k, H]
+    for l in range(shape.num_layers):
+        W = readout.layer(l)
+        o = np.empty((B, k, nq, d))
+        for b in range(B):
+            L = int(lengths[b])
+            u = rms_norm(x[b], W.attn_norm, eps)  # [k, H]
+            q = np.stack([rope((W.wq @ u[i]).reshape(nq, d), L + i, theta) for i in range(k)])
+            ks = np.stack([rope((W.wk @ u[i]).reshape(nkv, d), L + i, theta) for i in range(k)])
+            vs = np.stack([(W.wv @ u[i]).reshape(nkv, d) for i in range(k)])
+            Kc = cache.sequence(l, "k", page_table[b], L, ps)
+            Vc = cache.sequence(l, "v", page_table[b], L, ps)
+            for i in range(k):
+                for h in range(nq):
+                    j = h // g
+                    Ks, Vs = ks[: i + 1, j], vs[: i + 1, j]
+                    K = Ks if Kc is None else np.concatenate([Kc[j], Ks], axis=0)
+                    V = Vs if Vc is None else np.concatenate([Vc[j], Vs], axis=0)
+                    o[b, i, h] = attention(q[i, h], K, V)
+        x = x + np.einsum("oi,bki->bko", W.wo, o.reshape(B, k, nq * d))
+        u2 = rms_norm(x, W.ffn_norm, eps)
+        a = np.einsum("fi,bki->bkf", W.w_gate, u2)
+        c = np.einsum("fi,bki->bkf", W.w_up, u2)
+        x = x + np.einsum("of,bkf->bko", W.w_down, silu(a) * c)
+    h_fin = rms_norm(x[:, k - 1], readout.final_norm, eps)
+    z = h_fin @ readout.reward_w + readout.reward_b
+    p = sigmoid(z)
+    if return_hidden:
+        return z, p, h_fin
+    return z, p
+
+
 def attention_layer(shape, cache: PagedCache, layer: int, lengths, page_table, q, k_self, v_self):
     """Attention step alone for one layer: q [B][n_q][d] (already rotated), k_self/v_self
     [B][n_kv][d]. Returns o [B][n_q][d]."""
@@ -334,31 +378,35 @@ def attention_layer(shape, cache: PagedCache, layer: int, lengths, page_table, q
 def reencode(shape, layer_base: Callable[[int], LayerWeights],
              layer_verify: Callable[[int], LayerWeights], embed: np.ndarray,
              tokens: Sequence[int], verify_embed: np.ndarray, final_norm, reward_w,
-             reward_b: float = 0.0):
-    """Causal forward over n prefix tokens and the verify token at position n.
+             reward_b: float = 0.0, n_verify: int = 1):
+    """Causal forward over n prefix tokens and n_verify verify tokens at positions n ..
 
     Positions t < n use the base weights (adapter off, as during generation);
-    position n uses `layer_verify` (adapter on). With both equal this is the
-    Text-PRM computation on [x; v]. Attention at position t sees keys 0..t.
+    positions >= n use `layer_verify` (adapter on). With both equal and one verify
+    token this is the Text-PRM computation on [x; v]. Attention at position t sees
+    keys 0..t. The score is read at the last position.
 
     Returns (z, P(+), h_final, K, V) where K, V are [N_L][n_kv][n][d] float64:
     the cache the generator would have written (keys after rotation).
     """
     n = len(tokens)
+    nv = int(n_verify)
     H, nq, nkv, d = shape.hidden, shape.num_q_heads, shape.num_kv_heads, shape.head_dim
     g = nq // nkv
     eps, theta = shape.rms_eps, shape.rope_theta
-    X = np.concatenate([embed[np.asarray(tokens, dtype=np.int64)],
-                        np.asarray(verify_embed, dtype=np.float64)[None, :]], axis=0)  # [n+1, H]
+    X = np.concatenate([embed[np.asarray(tokens, dtype=np.int64)].reshape(n, embed.shape[1]),
+                        np.tile(np.asarray(verify_embed, dtype=np.float64), (nv, 1))],
+                       axis=0)  # [n + nv, H]
+    T = n + nv
     Kcache = np.empty((shape.num_layers, nkv, n, d))
     Vcache = np.empty((shape.num_layers, nkv, n, d))
     for l in range(shape.num_layers):
         Wb, Wv = layer_base(l), layer_verify(l)
         Xn = np.empty_like(X)
-        Q = np.empty((n + 1, nq, d))
-        K = np.empty((n + 1, nkv, d))
-        V = np.empty((n + 1, nkv, d))
-        for t in range(n + 1):
+        Q = np.empty((T, nq, d))
+        K = np.empty((T, nkv, d))
+        V = np.empty((T, nkv, d))
+        for t in range(T):
             W = Wb if t < n else Wv
             u = rms_norm(X[t], W.attn_norm, eps)
             Q[t] = rope((W.wq @ u).reshape(nq, d), t, theta)
@@ -366,7 +414,7 @@ def reencode(shape, layer_base: Callable[[int], LayerWeights],
             V[t] = (W.wv @ u).reshape(nkv, d)
         Kcache[l] = K[:n].transpose(1, 0, 2)
         Vcache[l] = V[:n].transpose(1, 0, 2)
-        for t in range(n + 1):
+        for t in range(T):
             W = Wb if t < n else Wv
             o = np.empty((nq, d))
             for h in range(nq):
@@ -376,6 +424,6 @@ def reencode(shape, layer_base: Callable[[int], LayerWeights],
             u2 = rms_norm(xt, W.ffn_norm, eps)
             Xn[t] = xt + swiglu_ffn(u2, W.w_gate, W.w_up, W.w_down)
         X = Xn
-    h_fin = rms_norm(X[n], final_norm, eps)
+    h_fin = rms_norm(X[T - 1], final_norm, eps)
     z = float(h_fin @ reward_w + reward_b)
     return z, float(sigmoid(np.array([z]))[0]), h_fin, Kcache, Vcache

@@ -564,3 +564,65 @@ def test_adapter_on_the_verify_token_only_equals_reencode(targets):
     assert np.allclose(z2, zs, rtol=0, atol=1e-12)
     z_base, _ = ko.verify_pass(shape, base, cache, lens, pt)
     assert np.max(np.abs(z2 - z_base)) > 1e-3  # the adapter changes the score
+
+
+# ---------------------------------------------------------------------------------------------
+# depth-k readout (k verify tokens, causal among themselves, score at the last one)
+
+
+def test_depth_one_is_the_verify_pass():
+    shape = _tiny_small()
+    ro = _readout(shape, 71)
+    cache, pt = _random_cache(shape, [40, 0, 17], 5)
+    z1, _ = ko.verify_pass(shape, ro, cache, [40, 0, 17], pt)
+    zk, _ = ko.verify_pass_depth(shape, ro, cache, [40, 0, 17], pt, 1)
+    assert np.allclose(z1, zk, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("depth,mixed", [(2, False), (3, True), (5, True)])
+def test_depth_k_equals_causal_reencode(depth, mixed):
+    """The depth-k pass over the cache a causal forward wrote equals that forward continued
+    over k verify tokens (the verify tokens using the adapted weights when mixed), read at the
+    last position."""
+    shape = _tiny_small()
+    seed = 81
+    base = _readout(shape, seed)
+    ver = (ko.readout_with_adapter(base, _adapter(shape, seed, 32), synth.lora_scale(32))
+           if mixed else base)
+    E = _embed(shape, seed)
+    Ks, Vs, zs, lens = [], [], [], []
+    for b, n in enumerate([21, 16, 0]):
+        toks = synth.token_ids(seed + b, n)
+        z, p, h, K, V = ko.reencode(shape, base.layer, ver.layer, E, toks, ver.verify_embed,
+                                    ver.final_norm, ver.reward_w, n_verify=depth)
+        Ks.append(K), Vs.append(V), zs.append(z), lens.append(n)
+    cache, pt = _dense_cache(Ks, Vs, shape.page_size)
+    zk, _ = ko.verify_pass_depth(shape, ver, cache, lens, pt, depth)
+    assert np.allclose(zk, zs, rtol=0, atol=1e-12)
+    z1, _ = ko.verify_pass(shape, ver, cache, lens, pt)
+    assert np.max(np.abs(zk - z1)) > 1e-3  # more verify tokens change the score
+
+
+def test_depth_k_against_transformers_llama_with_kv_cache():
+    """transformers' Llama decoder encodes the trajectory, then runs k verify tokens at once
+    against its own cache (causal among themselves); the oracle's depth-k pass over that cache
+    agrees at the last position."""
+    shape = synth.ModelShape(2, 256, 4, 2, 64, 1024, weight_dtype="f32", kv_dtype="f32")
+    seed = 1000
+    ro = _readout(shape, seed)
+    E = _embed(shape, seed).copy()
+    vid = 999
+    E[vid] = ro.verify_embed
+    m = _hf_model(shape, ro, E)
+    n, depth = 40, 3
+    toks = torch.tensor([synth.token_ids(seed, n)])
+    with torch.no_grad():
+        out = m(input_ids=toks, use_cache=True)
+        pkv = out.past_key_values
+        Ks = np.stack([pkv.layers[l].keys[0, :, :n].numpy() for l in range(shape.num_layers)])
+        Vs = np.stack([pkv.layers[l].values[0, :, :n].numpy() for l in range(shape.num_layers)])
+        out2 = m(input_ids=torch.tensor([[vid] * depth]), past_key_values=pkv, use_cache=True)
+    z_ref = out2.logits[0, -1, 1].item() - out2.logits[0, -1, 0].item()
+    cache, pt = _dense_cache([Ks], [Vs], shape.page_size)
+    z, _ = ko.verify_pass_depth(shape, ro, cache, [n], pt, depth)
+    assert abs(z[0] - z_ref) < 1e-5
