@@ -222,6 +222,32 @@ kvprm_status kvprm_score_lora(kvprm_handle h, const kvprm_kv_cache *cache,
                               const kvprm_lora *lora, void *workspace, size_t ws_bytes,
                               float *scores, float *logits, void *stream);
 
+/* Options of kvprm_score_ex. */
+typedef struct {
+  /* Unmerged adapter (as kvprm_score_lora), or NULL when the weights are theta + dtheta
+   * merged (as kvprm_score). */
+  const kvprm_lora *lora;
+  /* Depth-k readout (section 3, definition of the depth-k readout; the k > 1 experiment of
+   * section 5): depth = k verify tokens are appended to each candidate at positions
+   * L_b .. L_b + k - 1 and pass through the readout together, token i attending to the L_b
+   * cached keys and to verify tokens 0..i (causal), the adapter active on all of them; the
+   * score and logit are read from the last one. depth = 1 is Eq. (score). depth > 1 requires
+   * BF16 weights, depth * (num_q_heads / num_kv_heads) <= 16 and batch * depth <= 64
+   * (KVPRM_E_UNSUPPORTED otherwise). */
+  int32_t depth;
+} kvprm_score_options;
+
+/* Workspace bytes of kvprm_score_ex for this batch and these options. */
+kvprm_status kvprm_workspace_size_ex(kvprm_handle h, const kvprm_batch *batch,
+                                     const kvprm_score_options *options, size_t *bytes);
+
+/* kvprm_score with options (unmerged adapter, depth-k readout); outputs and conventions are
+ * those of kvprm_score, one score per candidate. options NULL is kvprm_score. */
+kvprm_status kvprm_score_ex(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *batch,
+                            const kvprm_readout_weights *weights,
+                            const kvprm_score_options *options, void *workspace, size_t ws_bytes,
+                            float *scores, float *logits, void *stream);
+
 /* Repack one bf16 weight matrix W [rows][K] from row-major order into the packed tile layout
  * that kvprm_score reads for BF16 weights: blocks of 1 KiB, block kb * (rows / 16) + t holding
  * rows 16t .. 16t+15 and inputs 32kb .. 32kb+31; inside a block, 16-byte group l (0..63) holds

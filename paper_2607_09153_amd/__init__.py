@@ -22,7 +22,8 @@ DTYPE_CODE = {"f32": KVPRM_F32, "bf16": KVPRM_BF16, "fp8": KVPRM_FP8_E4M3}
 
 EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
             "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
-            "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_last_error"]
+            "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
+            "kvprm_score_ex", "kvprm_last_error"]
 LORA_PROJECTIONS = ("q", "k", "v", "o", "gate", "up", "down")
 
 
@@ -57,6 +58,10 @@ class LayerLora(ctypes.Structure):
 class Lora(ctypes.Structure):
     _fields_ = [("layers", ctypes.POINTER(LayerLora)), ("rank", ctypes.c_int32),
                 ("scale", ctypes.c_float)]
+
+
+class ScoreOptions(ctypes.Structure):
+    _fields_ = [("lora", ctypes.POINTER(Lora)), ("depth", ctypes.c_int32)]
 
 
 class KVCache(ctypes.Structure):
@@ -114,9 +119,15 @@ def _load():
     lib.kvprm_score_lora.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
                                      ctypes.POINTER(ReadoutWeights), ctypes.POINTER(Lora), vp, sz,
                                      vp, vp, vp]
+    lib.kvprm_workspace_size_ex.argtypes = [vp, ctypes.POINTER(Batch), ctypes.POINTER(ScoreOptions),
+                                            ctypes.POINTER(sz)]
+    lib.kvprm_score_ex.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
+                                   ctypes.POINTER(ReadoutWeights), ctypes.POINTER(ScoreOptions),
+                                   vp, sz, vp, vp, vp]
     for f in ("kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
               "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
-              "kvprm_workspace_size_lora", "kvprm_score_lora"):
+              "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
+              "kvprm_score_ex"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kvprm_last_error.argtypes = []
     lib.kvprm_last_error.restype = ctypes.c_char_p
@@ -219,6 +230,30 @@ def kvprm_score_lora(handle: int, cache: KVCache, batch: Batch, base: ReadoutWei
     _check(lib.kvprm_score_lora(handle, ctypes.byref(cache), ctypes.byref(batch),
                                 ctypes.byref(base), ctypes.byref(lora), workspace_ptr, ws_bytes,
                                 scores_ptr, logits_ptr or None, stream or None))
+
+
+def make_options(lora: Optional[Lora] = None, depth: int = 1) -> ScoreOptions:
+    o = ScoreOptions(ctypes.pointer(lora) if lora is not None else None, depth)
+    o._keep = lora
+    return o
+
+
+def kvprm_workspace_size_ex(handle: int, batch: Batch, options: Optional[ScoreOptions]) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.kvprm_workspace_size_ex(handle, ctypes.byref(batch),
+                                       ctypes.byref(options) if options is not None else None,
+                                       ctypes.byref(n)))
+    return n.value
+
+
+def kvprm_score_ex(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeights,
+                   options: Optional[ScoreOptions], workspace_ptr: int, ws_bytes: int,
+                   scores_ptr: int, logits_ptr: int = 0, stream: int = 0) -> None:
+    _check(lib.kvprm_score_ex(handle, ctypes.byref(cache), ctypes.byref(batch),
+                              ctypes.byref(weights),
+                              ctypes.byref(options) if options is not None else None,
+                              workspace_ptr, ws_bytes, scores_ptr, logits_ptr or None,
+                              stream or None))
 
 
 def kvprm_workspace_size(handle: int, batch: Batch) -> int:

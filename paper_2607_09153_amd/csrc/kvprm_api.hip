@@ -217,9 +217,10 @@ static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b, const 
   memset(&gt, 0, sizeof gt);
   gt.cshift_prefix = gt.cshift_private = p.cshift;
   const bool share = h->dm.kvdt != 0 && b->num_groups > 0 && b->num_groups <= kMaxGroups;
+  const int kq = p.kq;  // group ranges are kept in rows (candidates x verify tokens)
   if (share) {
     gt.n = b->num_groups;
-    for (int i = 0; i <= gt.n; ++i) gt.start[i] = b->group_start_host[i];
+    for (int i = 0; i <= gt.n; ++i) gt.start[i] = b->group_start_host[i] * kq;
     const int cols_per_block = 16 * kPrefixWaves;
     long long items = 0;  // prefix pages x column blocks (per kv-head)
     for (int i = 0; i < gt.n; ++i) {
@@ -242,7 +243,7 @@ static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b, const 
     for (int i = 0; i < b->batch; ++i) {
       int first = 0;
       for (int k = 0; k < gt.n; ++k)
-        if (i >= gt.start[k] && i < gt.start[k + 1]) first = gt.prefix_pages[k];
+        if (i * kq >= gt.start[k] && i * kq < gt.start[k + 1]) first = gt.prefix_pages[k];
       priv_total += (b->lengths_host[i] + kPage - 1) / kPage - first;
     }
     gt.cshift_private = chunk_shift_for(priv_total);
@@ -251,7 +252,7 @@ static GroupTable group_table(const kvprm_handle h, const kvprm_batch *b, const 
     for (int i = 0; i < b->batch; ++i) {
       int first = 0;
       for (int k = 0; k < gt.n; ++k)
-        if (i >= gt.start[k] && i < gt.start[k + 1]) first = gt.prefix_pages[k];
+        if (i * kq >= gt.start[k] && i * kq < gt.start[k + 1]) first = gt.prefix_pages[k];
       const int priv = (b->lengths_host[i] + kPage - 1) / kPage - first;
       const int ch = (priv + CP - 1) / CP;
       if (ch > most) most = ch;
@@ -363,27 +364,58 @@ static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
   return KVPRM_OK;
 }
 
-kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
-                         const kvprm_readout_weights *wts, void *workspace, size_t ws_bytes,
-                         float *scores, float *logits, void *stream) {
-  const char *fn = "kvprm_score";
+static kvprm_status check_options(const kvprm_handle h, const kvprm_batch *b, const kvprm_lora *lora,
+                                  int32_t depth, const char *fn) {
+  if (depth < 1) return fail(KVPRM_E_INVALID, "%s: depth %d < 1", fn, depth);
+  if (depth > 1) {
+    if (h->dm.wdt != 1)
+      return fail(KVPRM_E_UNSUPPORTED, "%s: a depth-k readout needs bf16 weights", fn);
+    if (depth * h->dm.g > 16)
+      return fail(KVPRM_E_UNSUPPORTED, "%s: depth %d x %d query heads per kv-head exceeds 16", fn,
+                  depth, h->dm.g);
+    if (b && (long long)b->batch * depth > 64)
+      return fail(KVPRM_E_UNSUPPORTED, "%s: batch %d x depth %d exceeds 64 rows", fn, b->batch,
+                  depth);
+  }
+  if (lora) return check_lora(h, lora, fn);
+  return KVPRM_OK;
+}
+
+static size_t ws_bytes_ex(const kvprm_handle h, const kvprm_batch *b, const kvprm_lora *lora,
+                          int32_t depth) {
+  const Plan p = make_plan(h->dm, b->batch, b->max_pages, lora ? lora->rank : 0, depth);
+  return carve(h->dm, p, nullptr).bytes;
+}
+
+// Every scoring entry point: validation, then the matrix-core pipeline (bf16 weights) or the
+// vector-ALU one (fp32 weights; no adapter, depth 1).
+static kvprm_status score_impl(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                               const kvprm_readout_weights *wts, const kvprm_lora *lora,
+                               int32_t depth, void *workspace, size_t ws_bytes, float *scores,
+                               float *logits, void *stream, const char *fn) {
   if (!h) return fail(KVPRM_E_INVALID, "%s: null handle", fn);
   kvprm_status st = check_batch(h, b, fn);
   if (st != KVPRM_OK) return st;
+  if ((st = check_options(h, b, lora, depth, fn)) != KVPRM_OK) return st;
   if (b->batch == 0) return ok();
   if ((st = check_cache(h, cache, fn)) != KVPRM_OK) return st;
   if ((st = check_readout(h, wts, fn)) != KVPRM_OK) return st;
   if (!scores) return fail(KVPRM_E_INVALID, "%s: null scores", fn);
-  if ((st = check_ws(h, b, workspace, ws_bytes, fn)) != KVPRM_OK) return st;
+  const size_t need = ws_bytes_ex(h, b, lora, depth);
+  if (!workspace || ws_bytes < need)
+    return fail(KVPRM_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                workspace ? ws_bytes : (size_t)0);
+  if (((uintptr_t)workspace & 255) != 0)
+    return fail(KVPRM_E_WORKSPACE, "%s: workspace not 256-byte aligned", fn);
   if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
 
   const Dims &dm = h->dm;
   hipStream_t s = (hipStream_t)stream;
-  const Plan p = make_plan(dm, b->batch, b->max_pages);
+  const Plan p = make_plan(dm, b->batch, b->max_pages, lora ? lora->rank : 0, depth);
   const Workspace w = carve(dm, p, workspace);
   const GroupTable gt = group_table(h, b, p);
   if (dm.wdt == 1) {
-    if ((st = score_mx(h, cache, b, wts, nullptr, p, w, gt, scores, logits, s)) != KVPRM_OK)
+    if ((st = score_mx(h, cache, b, wts, lora, p, w, gt, scores, logits, s)) != KVPRM_OK)
       return st;
     return ok();
   }
@@ -417,6 +449,13 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
   return ok();
 }
 
+kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                         const kvprm_readout_weights *wts, void *workspace, size_t ws_bytes,
+                         float *scores, float *logits, void *stream) {
+  return score_impl(h, cache, b, wts, nullptr, 1, workspace, ws_bytes, scores, logits, stream,
+                    "kvprm_score");
+}
+
 kvprm_status kvprm_workspace_size_lora(kvprm_handle h, const kvprm_batch *b, int32_t rank,
                                        size_t *bytes) {
   const char *fn = "kvprm_workspace_size_lora";
@@ -439,26 +478,29 @@ kvprm_status kvprm_score_lora(kvprm_handle h, const kvprm_kv_cache *cache, const
                               void *stream) {
   const char *fn = "kvprm_score_lora";
   if (!h) return fail(KVPRM_E_INVALID, "%s: null handle", fn);
-  kvprm_status st = check_lora(h, lora, fn);
+  if (!lora) return fail(KVPRM_E_INVALID, "%s: null adapter", fn);
+  return score_impl(h, cache, b, base, lora, 1, workspace, ws_bytes, scores, logits, stream, fn);
+}
+
+kvprm_status kvprm_workspace_size_ex(kvprm_handle h, const kvprm_batch *b,
+                                     const kvprm_score_options *opt, size_t *bytes) {
+  const char *fn = "kvprm_workspace_size_ex";
+  if (!h || !bytes) return fail(KVPRM_E_INVALID, "%s: null argument", fn);
+  kvprm_status st = check_batch(h, b, fn);
   if (st != KVPRM_OK) return st;
-  if ((st = check_batch(h, b, fn)) != KVPRM_OK) return st;
-  if (b->batch == 0) return ok();
-  if ((st = check_cache(h, cache, fn)) != KVPRM_OK) return st;
-  if ((st = check_readout(h, base, fn)) != KVPRM_OK) return st;
-  if (!scores) return fail(KVPRM_E_INVALID, "%s: null scores", fn);
-  const Plan p = make_plan(h->dm, b->batch, b->max_pages, lora->rank);
-  const Workspace w = carve(h->dm, p, workspace);
-  if (!workspace || ws_bytes < w.bytes)
-    return fail(KVPRM_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, w.bytes,
-                workspace ? ws_bytes : (size_t)0);
-  if (((uintptr_t)workspace & 255) != 0)
-    return fail(KVPRM_E_WORKSPACE, "%s: workspace not 256-byte aligned", fn);
-  if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
-  const GroupTable gt = group_table(h, b, p);
-  if ((st = score_mx(h, cache, b, base, lora, p, w, gt, scores, logits, (hipStream_t)stream)) !=
-      KVPRM_OK)
-    return st;
+  const kvprm_lora *lora = opt ? opt->lora : nullptr;
+  const int32_t depth = opt ? opt->depth : 1;
+  if ((st = check_options(h, b, lora, depth, fn)) != KVPRM_OK) return st;
+  *bytes = b->batch == 0 ? 0 : ws_bytes_ex(h, b, lora, depth);
   return ok();
+}
+
+kvprm_status kvprm_score_ex(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                            const kvprm_readout_weights *wts, const kvprm_score_options *opt,
+                            void *workspace, size_t ws_bytes, float *scores, float *logits,
+                            void *stream) {
+  return score_impl(h, cache, b, wts, opt ? opt->lora : nullptr, opt ? opt->depth : 1, workspace,
+                    ws_bytes, scores, logits, stream, "kvprm_score_ex");
 }
 
 kvprm_status kvprm_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, void *stream) {

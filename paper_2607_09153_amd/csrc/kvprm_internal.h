@@ -67,7 +67,10 @@ struct LoraTail {
 };
 
 struct Plan {
-  int B, max_pages, nch;      // nch = chunk slots per (candidate, q-head), see make_plan
+  // B = rows of the pass: candidates x verify tokens per candidate (kq, the depth-k readout);
+  // row v is verify token v % kq of candidate v / kq. Breal = candidates.
+  int B, max_pages, nch;      // nch = chunk slots per (row, q-head), see make_plan
+  int kq, Breal;
   int cshift;                 // matrix-core attention chunk from (B, max_pages): 1 << cshift pages
   int nss;                    // row blocks of H that carry partial sums of squares
   int rb;                     // rows per such block
@@ -92,7 +95,7 @@ int gemv_bp(int B);
 int gemv_mt(int nt, int rows);
 hipError_t launch_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, hipStream_t s);
 
-Plan make_plan(const Dims &dm, int B, int max_pages, int lora_rank = 0);
+Plan make_plan(const Dims &dm, int B, int max_pages, int lora_rank = 0, int depth = 1);
 Workspace carve(const Dims &dm, const Plan &p, void *base);
 
 // Kernel launchers (return hipGetLastError()).

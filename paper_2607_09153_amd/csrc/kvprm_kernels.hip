@@ -87,9 +87,12 @@ static size_t partial_elems(const GemvPlan &g) {
   return (size_t)((g.ksplit + g.ktail + 3) & ~3) * g.rows;
 }
 
-Plan make_plan(const Dims &dm, int B, int max_pages, int lora_rank) {
+Plan make_plan(const Dims &dm, int Breal, int max_pages, int lora_rank, int depth) {
   Plan p{};
+  const int B = Breal * depth;  // rows of the pass (verify tokens of all candidates)
   p.B = B;
+  p.Breal = Breal;
+  p.kq = depth;
   p.max_pages = max_pages;
   p.lora_rank = lora_rank;
   // Matrix-core attention chunk: the longest of 16, 32, 64 pages that still gives at least 160
@@ -97,7 +100,7 @@ Plan make_plan(const Dims &dm, int B, int max_pages, int lora_rank) {
   // stream longer page runs per wave: measured faster even with some units idle), and at most
   // kMaxChunks - 2 chunks per candidate.
   p.cshift = 6;
-  while (p.cshift > 4 && (long long)B * max_pages < (160LL << p.cshift)) --p.cshift;
+  while (p.cshift > 4 && (long long)Breal * max_pages < (160LL << p.cshift)) --p.cshift;
 
   // chunk slots: chunks of max_pages at the shortest chunk (16 pages: the call may pick shorter
   // chunks than the plan from the host lengths) plus one (a shared prefix that ends inside a
@@ -645,10 +648,10 @@ hipError_t launch_swiglu(const Dims &dm, const Plan &p, const Workspace &w, int 
 // dot product), four rows per thread in flight.
 __global__ __launch_bounds__(256) void k_head(const float *x, int H, float eps, const void *gam,
                                               const void *wr, int wdt, float rb, float *scores,
-                                              float *logits) {
+                                              float *logits, int kq) {
   __shared__ float red[4];
   const int b = blockIdx.x;
-  const float *xb = x + (size_t)b * H;
+  const float *xb = x + ((size_t)b * kq + kq - 1) * H;  // the candidate's last verify token
   float sq = 0.f, dot = 0.f;
   int r = threadIdx.x;
   for (; r + 3 * 256 < H; r += 4 * 256) {
@@ -689,8 +692,8 @@ __global__ __launch_bounds__(256) void k_head(const float *x, int H, float eps, 
 hipError_t launch_head(const Dims &dm, const Plan &p, const Workspace &w, const void *final_norm,
                        const void *reward_w, float reward_b, float *scores, float *logits,
                        hipStream_t s) {
-  hipLaunchKernelGGL(k_head, dim3(p.B), dim3(256), 0, s, w.x, dm.H, dm.eps, final_norm, reward_w,
-                     dm.wdt, reward_b, scores, logits);
+  hipLaunchKernelGGL(k_head, dim3(p.Breal), dim3(256), 0, s, w.x, dm.H, dm.eps, final_norm,
+                     reward_w, dm.wdt, reward_b, scores, logits, p.kq);
   return hipGetLastError();
 }
 

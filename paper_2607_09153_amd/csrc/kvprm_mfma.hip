@@ -133,8 +133,8 @@ int gemv_bp(int B) { return B <= 8 ? 8 : 16 * ((B + 15) / 16); }
 __global__ __launch_bounds__(256) void k_init_mx(float *x, float *ss, int RB, const void *ev,
                                                  const void *gamma0, int wdt, int B, int H,
                                                  uint16_t *opA, int NT, int Bp,
-                                                 const int32_t *lengths, float theta, int d,
-                                                 float *rope) {
+                                                 const int32_t *lengths, int kq, float theta,
+                                                 int d, float *rope) {
   __shared__ float red[4];
   const int r0 = blockIdx.x * RB;
   const int nr = min(RB, H - r0);
@@ -153,10 +153,11 @@ __global__ __launch_bounds__(256) void k_init_mx(float *x, float *ss, int RB, co
   if (threadIdx.x < B) ss[(size_t)blockIdx.x * B + threadIdx.x] = sq;
   if (blockIdx.x == 0) {
     for (int e = threadIdx.x; e < B * (d / 2); e += 256) {
+      // row b is verify token b % kq of candidate b / kq, at position L + b % kq
       const int b = e / (d / 2), i = e - b * (d / 2);
       const double inv = pow((double)theta, (-2.0 * (double)i) / (double)d);
       double sn, cs;
-      sincos((double)lengths[b] * inv, &sn, &cs);
+      sincos((double)(lengths[b / kq] + b % kq) * inv, &sn, &cs);
       rope[2 * e] = (float)cs;
       rope[2 * e + 1] = (float)sn;
     }
@@ -959,6 +960,9 @@ struct AttnArgs {
   float *o;       // [B][nq][D] fp32 output (may be null)
   uint16_t *op;   // operand buffer of the output projection (may be null)
   int NT, Bp;
+  int kq;         // verify tokens per candidate: row v = token v % kq of candidate v / kq; q,
+                  // k_self, v_self, partials and o are per row, lengths and page table per
+                  // candidate, group ranges in rows
 };
 
 // One block per (chunk of pages, candidate b) over the candidate's private pages,
@@ -976,14 +980,14 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   constexpr int NDB = D / 16;  // 16-dim blocks of the output
   constexpr int EB = KVT == 1 ? 2 : 1;
   constexpr size_t TILE = (size_t)kPage * D * EB;
-  const int c = blockIdx.x, b = blockIdx.y;
+  const int c = blockIdx.x, b = blockIdx.y;  // chunk, candidate
   const int j = threadIdx.x >> 6;
-  const int nkv = a.nkv, g = a.g, nq = a.nq;
+  const int nkv = a.nkv, g = a.g, nq = a.nq, kq = a.kq;
   const int L = a.lengths[b];
   const int npages = (L + kPage - 1) / kPage;
   int first = 0;
   for (int gi = 0; gi < a.gt.n; ++gi)
-    if (b >= a.gt.start[gi] && b < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
+    if (b * kq >= a.gt.start[gi] && b * kq < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
   const int CP = 1 << a.gt.cshift_private;
   const int ncp = (first + (1 << a.gt.cshift_prefix) - 1) >> a.gt.cshift_prefix;  // prefix chunks
   const int p0 = first + c * CP;
@@ -1012,9 +1016,12 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   PairRaw<D> r0, r1;
   load_pair(0, r0);  // in flight while the queries are prepared
 
+  // column n: verify token n / g of this candidate, q-head j g + n % g (kq g <= 16 columns)
+  const bool colv = n < kq * g;
+  const int ti = colv ? n / g : 0, hh = colv ? n - (n / g) * g : 0;
+  const size_t row = (size_t)b * kq + ti;
   uint4 q0[NKB], q1[NKB], q2[NKB];
-  load_query_ops<KVT, D>(a.q + ((size_t)b * nq + (size_t)j * g + (n < g ? n : 0)) * D, n < g, cq,
-                         q0, q1, q2);
+  load_query_ops<KVT, D>(a.q + (row * nq + (size_t)j * g + hh) * D, colv, cq, q0, q1, q2);
   const float rs = kLog2e / sqrtf((float)D);  // scores in log2 units
   float m_run = -INFINITY, l_run = 0.f;
   floatx4 acc[NDB];
@@ -1058,9 +1065,9 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   }
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
-  if (n < g)
-    store_partial<D>(a.apart + (((size_t)b * nq + (size_t)j * g + n) * a.nch + ncp + c) * (D + 2),
-                     cq, acc, m_run, l_run);
+  if (colv)
+    store_partial<D>(a.apart + ((row * nq + (size_t)j * g + hh) * a.nch + ncp + c) * (D + 2), cq,
+                     acc, m_run, l_run);
 }
 
 // Shared-prefix attention: the members of a prefix group share the physical pages of their
@@ -1096,7 +1103,7 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
   const bool present = mem < members;
   const int bcand = m0 + (present ? mem : 0);
   // page ids and fp8 scales of the chunk (from the first member's table row), in lanes
-  const int ph_l = lane < np ? a.page_table[(size_t)m0 * a.max_pages + p0 + lane] : 0;
+  const int ph_l = lane < np ? a.page_table[(size_t)(m0 / a.kq) * a.max_pages + p0 + lane] : 0;
   float ksc_l = 1.f, vsc_l = 1.f;
   if (KVT == 2 && lane < np) {
     ksc_l = a.ksc[(size_t)ph_l * nkv + j];
@@ -1213,11 +1220,13 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
   __shared__ float m_s[kMaxChunks], f_s[kMaxChunks];
   __shared__ float red[3][8];
   __shared__ float sub_s[S][D];
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+  __shared__ float sself_s[16];
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;  // row (candidate, verify token)
   const int lane = t & 63, wave = t >> 6;
   const int sub = t / D, dd = t - sub * D;
   const int j = h / a.g;
-  const int L = a.lengths[b];
+  const int kq = a.kq, cand = b / kq, tok = b - cand * kq;
+  const int L = a.lengths[cand];
   const int npages = (L + kPage - 1) / kPage;
   int first = 0;
   for (int gi = 0; gi < a.gt.n; ++gi)
@@ -1239,22 +1248,23 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
     f_s[c] = base[(size_t)c * (D + 2) + D + 1];  // l_c for now
     mx = fmaxf(mx, m);
   }
-  const float vsv = a.vself[((size_t)b * a.nkv + j) * D + dd];
-  // own key: s_self = q . k_self / sqrt(D), from the first D threads
-  float dot = t < D ? a.q[((size_t)b * a.nq + h) * D + t] * a.kself[((size_t)b * a.nkv + j) * D + t]
-                    : 0.f;
-  dot = wsum(dot);
-  mx = wmax(mx);
-  if (lane == 0) {
-    red[0][wave] = dot;
-    red[1][wave] = mx;
-  }
-  __syncthreads();
-  float s_self = 0.f;
+  // the verify tokens' own keys: this row's token attends to tokens 0..tok of its candidate
+  // (rows cand kq + i); s_i = q . k_self_i / sqrt(D), one wave per key
+  const size_t row0 = (size_t)cand * kq;
+  const float *qr = a.q + ((size_t)b * a.nq + h) * D;
+  for (int i = wave; i <= tok; i += 8) {
+    const float *kr = a.kself + ((row0 + i) * a.nkv + j) * D;
+    float dot = 0.f;
 #pragma unroll
-  for (int w = 0; w < D / 64; ++w) s_self += red[0][w];
-  s_self *= 1.0f / sqrtf((float)D);
-  float M = s_self;
+    for (int u = 0; u < D / 64; ++u) dot += qr[lane + 64 * u] * kr[lane + 64 * u];
+    dot = wsum(dot);
+    if (lane == 0) sself_s[i] = dot * (1.0f / sqrtf((float)D));
+  }
+  mx = wmax(mx);
+  if (lane == 0) red[1][wave] = mx;
+  __syncthreads();
+  float M = -INFINITY;
+  for (int i = 0; i <= tok; ++i) M = fmaxf(M, sself_s[i]);
 #pragma unroll
   for (int w = 0; w < 8; ++w) M = fmaxf(M, red[1][w]);
   float ls = 0.f;
@@ -1282,8 +1292,13 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
   float tot = 0.f;
 #pragma unroll
   for (int k = 0; k < S; ++k) tot += sub_s[k][dd];
-  const float es = expf(s_self - M);
-  const float ov = (tot + es * vsv) / (lsum + es);
+  float es_sum = 0.f;
+  for (int i = 0; i <= tok; ++i) {
+    const float es = expf(sself_s[i] - M);
+    es_sum += es;
+    tot += es * a.vself[((row0 + i) * a.nkv + j) * D + dd];
+  }
+  const float ov = tot / (lsum + es_sum);
   if (a.o) a.o[((size_t)b * a.nq + h) * D + dd] = ov;
   if (a.op) store_operand(a.op, a.NT, a.Bp, h * D + dd, b, ov);
 }
@@ -1291,7 +1306,7 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
 hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *ev,
                           const void *gamma0, const int32_t *lengths, hipStream_t s) {
   hipLaunchKernelGGL(k_init_mx, dim3(p.nss), dim3(256), 0, s, w.x, w.ss, p.rb, ev, gamma0, dm.wdt,
-                     p.B, dm.H, w.opA, p.nt, p.bp, lengths, dm.theta, dm.d, w.rope);
+                     p.B, dm.H, w.opA, p.nt, p.bp, lengths, p.kq, dm.theta, dm.d, w.rope);
   return hipGetLastError();
 }
 
@@ -1544,6 +1559,7 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
   a.op = op;
   a.NT = p.nt;
   a.Bp = p.bp;
+  a.kq = p.kq;
   if (gt.n > 0) {
     dim3 pgrid(gt.prefix_chunks, dm.nkv, gt.colblock_start[gt.n]);
 #define KVPRM_P(KVT, D) \
@@ -1559,7 +1575,7 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  dim3 grid(gt.private_chunks > 0 ? gt.private_chunks : p.nch - 1, p.B);
+  dim3 grid(gt.private_chunks > 0 ? gt.private_chunks : p.nch - 1, p.Breal);
 #define KVPRM_A(KVT, D) hipLaunchKernelGGL((k_attn_mx<KVT, D>), grid, dim3(64 * dm.nkv), 0, s, a)
   if (dm.kvdt == 1) {
     if (dm.d == 64) KVPRM_A(1, 64);

@@ -84,3 +84,25 @@ def run_score_lora(dw: DeviceWorkload, stream=None):
         return scores.cpu().numpy().astype(np.float64), logits.cpu().numpy().astype(np.float64)
     finally:
         m.kvprm_destroy(h)
+
+
+def run_score_ex(dw: DeviceWorkload, depth: int = 1, lora: bool = False, with_hint: bool = True,
+                 stream=None):
+    """kvprm_score_ex with a depth-k readout (and the workload's adapter when lora)."""
+    m = kv()
+    h = m.kvprm_create(dw.desc(m))
+    try:
+        batch = dw.batch(m, with_hint=with_hint)
+        opt = m.make_options(dw.lora(m) if lora else None, depth)
+        n = m.kvprm_workspace_size_ex(h, batch, opt)
+        ws = torch.empty(max(n, 256), dtype=torch.uint8, device="cuda")
+        B = dw.w.batch
+        scores = torch.full((B,), float("nan"), dtype=torch.float32, device="cuda")
+        logits = torch.full((B,), float("nan"), dtype=torch.float32, device="cuda")
+        st = stream or torch.cuda.current_stream()
+        m.kvprm_score_ex(h, dw.cache(m), batch, dw.readout(m), opt, ws.data_ptr(), n,
+                         scores.data_ptr(), logits.data_ptr(), st.cuda_stream)
+        st.synchronize()
+        return scores.cpu().numpy().astype(np.float64), logits.cpu().numpy().astype(np.float64)
+    finally:
+        m.kvprm_destroy(h)

@@ -219,3 +219,42 @@ def test_score_lora_validation():
                             _lora(drop="q"), 0, 0, FAKE)
     finally:
         kv.kvprm_destroy(h)
+
+
+def test_score_ex_validation():
+    """Depth-k readout: depth >= 1; depth > 1 needs bf16 weights, depth x g <= 16 and
+    batch x depth <= 64; the workspace grows with the rows; options NULL is kvprm_score."""
+    hf = kv.kvprm_create(_desc())  # fp32 weights, g = 2
+    try:
+        batch = kv.make_batch(2, FAKE, 4, FAKE, [10, 64])
+        assert (kv.kvprm_workspace_size_ex(hf, batch, None) ==
+                kv.kvprm_workspace_size(hf, batch))
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_workspace_size_ex(hf, batch, kv.make_options(depth=2))
+        assert e.value.status == kv.KVPRM_E_UNSUPPORTED
+    finally:
+        kv.kvprm_destroy(hf)
+    h = kv.kvprm_create(_desc(weight_dtype="bf16", kv_dtype="bf16"))  # g = 2
+    try:
+        batch = kv.make_batch(2, FAKE, 4, FAKE, [10, 64])
+        n1 = kv.kvprm_workspace_size_ex(h, batch, kv.make_options(depth=1))
+        n8 = kv.kvprm_workspace_size_ex(h, batch, kv.make_options(depth=8))
+        assert n8 > n1 == kv.kvprm_workspace_size(h, batch)
+        nl = kv.kvprm_workspace_size_ex(h, batch, kv.make_options(_lora(rank=64), depth=4))
+        assert nl > kv.kvprm_workspace_size_ex(h, batch, kv.make_options(depth=4))
+        cases = [
+            (kv.make_options(depth=0), batch, kv.KVPRM_E_INVALID),
+            (kv.make_options(depth=9), batch, kv.KVPRM_E_UNSUPPORTED),  # 9 x 2 > 16 columns
+            (kv.make_options(depth=8), kv.make_batch(9, FAKE, 4, FAKE), kv.KVPRM_E_UNSUPPORTED),
+            (kv.make_options(_lora(rank=40), depth=2), batch, kv.KVPRM_E_INVALID),
+        ]
+        for opt, bt, status in cases:
+            with pytest.raises(kv.KvprmError) as e:
+                kv.kvprm_score_ex(h, _cache(), bt, _weights(), opt, FAKE, 1 << 40, FAKE)
+            assert e.value.status == status, kv.kvprm_last_error()
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_score_ex(h, _cache(), batch, _weights(), kv.make_options(depth=8), FAKE, n1,
+                              FAKE)
+        assert e.value.status == kv.KVPRM_E_WORKSPACE
+    finally:
+        kv.kvprm_destroy(h)
