@@ -10,7 +10,8 @@ Prints one JSON line: scores/s (value), the end-to-end KV-read rate, the rooflin
 dominant kernel (the split-L attention chunk kernel, timed live with HIP events on its stream;
 the whole attention step with its merge is reported beside it), the same workload scored with
 the base weights and an unmerged rank-256 adapter on every projection (kvprm_score_lora,
-`lora_readout`), and the fp64 CPU oracle timed on a bounded sample of the same workload.
+`lora_readout`) and with two verify tokens per candidate (the depth-k readout, kvprm_score_ex,
+`depth_readout`), and the fp64 CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -102,6 +103,34 @@ def time_lora(kv, dw, h, batch, rank, steps, warmup):
     return {"rank": rank, "scale": synth.lora_scale(rank),
             "targets": list(synth.LORA_PROJECTIONS), "ms_per_call": ms,
             "scores_per_s": w.batch / (ms * 1e-3), "adapter_bytes_per_call": dw.lora_bytes()}
+
+
+def time_depth(kv, dw, h, batch, depth, steps, warmup):
+    """Whole scoring calls of the depth-k readout (kvprm_score_ex, `depth` verify tokens per
+    candidate, merged weights) on the same workload, K calls between two synchronisations."""
+    import torch
+    w = dw.w
+    opt = kv.make_options(None, depth)
+    n = kv.kvprm_workspace_size_ex(h, batch, opt)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    scores = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    cache, ro = dw.cache(kv), dw.readout(kv)
+
+    def call():
+        kv.kvprm_score_ex(h, cache, batch, ro, opt, ws.data_ptr(), n, scores.data_ptr(), 0,
+                          stream.cuda_stream)
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        call()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    return {"depth": depth, "ms_per_call": ms, "scores_per_s": w.batch / (ms * 1e-3),
+            "verify_tokens_per_s": w.batch * depth / (ms * 1e-3)}
 
 
 def copy_bandwidth(nbytes=4 << 30, reps=10):
@@ -205,6 +234,8 @@ def main():
     ap.add_argument("--attn-reps", type=int, default=56)
     ap.add_argument("--lora-rank", type=int, default=256,
                     help="rank of the unmerged adapter of the second timed line (0 = skip)")
+    ap.add_argument("--depth", type=int, default=2,
+                    help="verify tokens per candidate of the depth-k timed line (1 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the library has no multi-GPU path "
@@ -260,6 +291,11 @@ def main():
         _log(f"unmerged rank-{args.lora_rank} adapter: {lora['ms_per_call']:.3f} ms/call")
         lora["end_to_end_gbps"] = (kv_bytes + w_bytes + lora["adapter_bytes_per_call"]) / (
             lora["ms_per_call"] * 1e-3) / 1e9
+    depth = None
+    if args.depth > 1:
+        depth = time_depth(kv, dw, h, batch, args.depth, args.steps, args.warmup)
+        _log(f"depth-{args.depth} readout: {depth['ms_per_call']:.3f} ms/call")
+        depth["end_to_end_gbps"] = (kv_bytes + w_bytes) / (depth["ms_per_call"] * 1e-3) / 1e9
     kernel_ms, step_ms = time_attention(kv, dw, h, batch, ws, n, max(args.attn_reps, 1))
     kv_per_layer = kv_bytes / w.shape.num_layers
     achieved = kv_per_layer / (kernel_ms * 1e-3) / 1e9
@@ -305,6 +341,8 @@ def main():
     }
     if lora is not None:
         out["lora_readout"] = lora
+    if depth is not None:
+        out["depth_readout"] = depth
     if args.cpu_layers > 0:
         _log("timing the oracle on the CPU sample ...")
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers, args.cpu_seconds)
