@@ -626,3 +626,75 @@ def test_depth_k_against_transformers_llama_with_kv_cache():
     cache, pt = _dense_cache([Ks], [Vs], shape.page_size)
     z, _ = ko.verify_pass_depth(shape, ro, cache, [n], pt, depth)
     assert abs(z[0] - z_ref) < 1e-5
+
+
+# ---------------------------------------------------------------------------------------------
+# KV steering: the gradient of -log P(+) with respect to the cache (appendix algorithm)
+
+from oracle import kv_steering as ks  # noqa: E402
+
+
+def _dense_random(shape, lengths, seed):
+    rng = np.random.default_rng(seed)
+    K = [rng.normal(size=(shape.num_layers, shape.num_kv_heads, n, shape.head_dim)) for n in lengths]
+    V = [rng.normal(size=(shape.num_layers, shape.num_kv_heads, n, shape.head_dim)) for n in lengths]
+    return K, V
+
+
+def test_steering_forward_equals_the_verify_pass():
+    """The torch float64 forward that is differentiated is the oracle's verify pass."""
+    shape = _tiny_small()
+    ro = _readout(shape, 91)
+    lengths = [37, 0, 16]
+    K, V = _dense_random(shape, lengths, 7)
+    cache, pt = _dense_cache(K, V, shape.page_size)
+    z_ref, _ = ko.verify_pass(shape, ro, cache, lengths, pt)
+    res = ks.loss_and_grads(shape, ro, K, V, lengths)
+    for b in range(len(lengths)):
+        assert abs(res[b][1] - z_ref[b]) < 1e-12
+        assert abs(res[b][0] - (-math.log(ko.sigmoid(np.array([z_ref[b]]))[0]))) < 1e-12
+
+
+def test_steering_gradient_matches_finite_differences():
+    """d(-log P(+))/d(K, V) at sampled cache entries (every layer, keys and values, first and
+    last positions) against central differences of the loss."""
+    shape = _tiny_small()
+    ro = _readout(shape, 92)
+    lengths = [29]
+    K, V = _dense_random(shape, lengths, 8)
+    (_, _, dK, dV), = ks.loss_and_grads(shape, ro, K, V, lengths)
+    rng = np.random.default_rng(3)
+    hstep = 1e-6
+    for which, G in (("k", dK), ("v", dV)):
+        for _ in range(12):
+            l = int(rng.integers(shape.num_layers))
+            j = int(rng.integers(shape.num_kv_heads))
+            t = int(rng.choice([0, lengths[0] - 1, int(rng.integers(lengths[0]))]))
+            m = int(rng.integers(shape.head_dim))
+            vals = []
+            for sgn in (1.0, -1.0):
+                Kp = [torch.tensor(K[0][i]) for i in range(shape.num_layers)]
+                Vp = [torch.tensor(V[0][i]) for i in range(shape.num_layers)]
+                T = Kp if which == "k" else Vp
+                T[l] = T[l].clone()
+                T[l][j, t, m] += sgn * hstep
+                vals.append(float(ks.candidate_loss(shape, ro, Kp, Vp, lengths[0])[0]))
+            fd = (vals[0] - vals[1]) / (2 * hstep)
+            assert abs(fd - G[l, j, t, m]) <= 1e-7 + 1e-5 * abs(G[l, j, t, m]), (which, l, j, t, m)
+
+
+def test_steering_steps_lower_the_loss_and_round_to_storage():
+    shape = _tiny_small()
+    ro = _readout(shape, 93)
+    lengths = [40, 17]
+    K, V = _dense_random(shape, lengths, 9)
+    K = [ks.round_to_storage(k, "bf16") for k in K]
+    V = [ks.round_to_storage(v, "bf16") for v in V]
+    K2, V2, losses = ks.steer(shape, ro, K, V, lengths, eta=0.5, steps=3, store_dtype="bf16")
+    for b in range(len(lengths)):
+        assert losses[-1][b] < losses[0][b]
+    # stored values stay bf16: rounding them again changes nothing, and equals torch's bf16
+    assert np.array_equal(ks.round_to_storage(K2[0], "bf16"), K2[0])
+    x = np.random.default_rng(4).normal(size=10000) * 3
+    ref = torch.tensor(x, dtype=torch.float64).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(ks.round_to_storage(x, "bf16"), ref)
