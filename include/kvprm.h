@@ -10,8 +10,8 @@
  *
  * Conventions for every entry point
  *   - All tensor pointers are DEVICE pointers unless the name ends in _host. The caller owns
- *     every buffer; the library never frees, never writes the cache, the page table or the
- *     weights, and never allocates device memory inside kvprm_score / kvprm_attention (the
+ *     every buffer; the library never frees, never writes the cache (except kvprm_steer, which
+ *     exists to update it), the page table or the weights, and never allocates device memory inside kvprm_score / kvprm_attention (the
  *     caller passes a workspace sized by kvprm_workspace_size).
  *   - Calls only enqueue work on `stream` (a hipStream_t; NULL = the null stream) and never
  *     synchronise the host. Outputs are valid once the stream reaches that point.
@@ -247,6 +247,38 @@ kvprm_status kvprm_score_ex(kvprm_handle h, const kvprm_kv_cache *cache, const k
                             const kvprm_readout_weights *weights,
                             const kvprm_score_options *options, void *workspace, size_t ws_bytes,
                             float *scores, float *logits, void *stream);
+
+/* Gradients of the score with respect to the cache (appendix, KV Steering: the score is a
+ * differentiable function of the cached keys and values). For every candidate b the loss is
+ * -log P(+)_b, and the derivative with respect to every cached key and value the candidate
+ * reads (every layer, positions 0..L_b-1) is produced by a backward pass through the readout:
+ * reward head, final RMSNorm, and per layer (last to first) the FFN, the output projection,
+ * the attention over the cache and the token's own key (softmax recomputed from the forward's
+ * log-sum-exp), the rotary embedding, the q/k/v projections and the RMSNorms. Requires BF16
+ * weights and a BF16 cache, batch <= 8, and candidates that do not share cache pages (no
+ * prefix-sharing hint; a page read by two candidates would get one of the two gradients):
+ * KVPRM_E_UNSUPPORTED / KVPRM_E_INVALID otherwise. The workspace is
+ * kvprm_workspace_size_grad bytes (activations of every layer are kept). */
+kvprm_status kvprm_workspace_size_grad(kvprm_handle h, const kvprm_batch *batch, size_t *bytes);
+
+/* scores[b] = P(+) as kvprm_score; grad_k, grad_v: device fp32 arrays with the element order of
+ * the pools ([num_layers][num_pages][num_kv_heads][tile], element i is the derivative with
+ * respect to pool element i). Elements of the pages a candidate reads are written (zero for
+ * slots at or beyond L_b); elements of other pages are left as they are. */
+kvprm_status kvprm_score_grad(kvprm_handle h, const kvprm_kv_cache *cache,
+                              const kvprm_batch *batch, const kvprm_readout_weights *weights,
+                              void *workspace, size_t ws_bytes, float *scores, float *grad_k,
+                              float *grad_v, void *stream);
+
+/* KV Steering (appendix algorithm): `steps` times, every cached key and value the candidates
+ * read (slots 0..L_b-1) becomes round_bf16(kv - eta * d(-log P(+))/d kv), the gradient taken at
+ * the cache as it is at that step. The pools of `cache` are WRITTEN in place (the only entry
+ * point that writes the cache). scores_before[b] = P(+) before the first step, scores_after[b]
+ * = P(+) after the last (device fp32 [B]). Requirements as for kvprm_score_grad; steps >= 1. */
+kvprm_status kvprm_steer(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *batch,
+                         const kvprm_readout_weights *weights, float eta, int32_t steps,
+                         void *workspace, size_t ws_bytes, float *scores_before,
+                         float *scores_after, void *stream);
 
 /* Repack one bf16 weight matrix W [rows][K] from row-major order into the packed tile layout
  * that kvprm_score reads for BF16 weights: blocks of 1 KiB, block kb * (rows / 16) + t holding

@@ -23,7 +23,8 @@ DTYPE_CODE = {"f32": KVPRM_F32, "bf16": KVPRM_BF16, "fp8": KVPRM_FP8_E4M3}
 EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
             "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
             "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
-            "kvprm_score_ex", "kvprm_last_error"]
+            "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer",
+            "kvprm_last_error"]
 LORA_PROJECTIONS = ("q", "k", "v", "o", "gate", "up", "down")
 
 
@@ -124,10 +125,16 @@ def _load():
     lib.kvprm_score_ex.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
                                    ctypes.POINTER(ReadoutWeights), ctypes.POINTER(ScoreOptions),
                                    vp, sz, vp, vp, vp]
+    lib.kvprm_workspace_size_grad.argtypes = [vp, ctypes.POINTER(Batch), ctypes.POINTER(sz)]
+    lib.kvprm_score_grad.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
+                                     ctypes.POINTER(ReadoutWeights), vp, sz, vp, vp, vp, vp]
+    lib.kvprm_steer.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
+                                ctypes.POINTER(ReadoutWeights), ctypes.c_float, ctypes.c_int32, vp,
+                                sz, vp, vp, vp]
     for f in ("kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
               "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
               "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
-              "kvprm_score_ex"):
+              "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kvprm_last_error.argtypes = []
     lib.kvprm_last_error.restype = ctypes.c_char_p
@@ -254,6 +261,28 @@ def kvprm_score_ex(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWe
                               ctypes.byref(options) if options is not None else None,
                               workspace_ptr, ws_bytes, scores_ptr, logits_ptr or None,
                               stream or None))
+
+
+def kvprm_workspace_size_grad(handle: int, batch: Batch) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.kvprm_workspace_size_grad(handle, ctypes.byref(batch), ctypes.byref(n)))
+    return n.value
+
+
+def kvprm_score_grad(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeights,
+                     workspace_ptr: int, ws_bytes: int, scores_ptr: int, grad_k_ptr: int,
+                     grad_v_ptr: int, stream: int = 0) -> None:
+    _check(lib.kvprm_score_grad(handle, ctypes.byref(cache), ctypes.byref(batch),
+                                ctypes.byref(weights), workspace_ptr, ws_bytes, scores_ptr,
+                                grad_k_ptr, grad_v_ptr, stream or None))
+
+
+def kvprm_steer(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeights, eta: float,
+                steps: int, workspace_ptr: int, ws_bytes: int, scores_before_ptr: int,
+                scores_after_ptr: int, stream: int = 0) -> None:
+    _check(lib.kvprm_steer(handle, ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(weights),
+                           eta, steps, workspace_ptr, ws_bytes, scores_before_ptr,
+                           scores_after_ptr, stream or None))
 
 
 def kvprm_workspace_size(handle: int, batch: Batch) -> int:

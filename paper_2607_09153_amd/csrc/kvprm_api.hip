@@ -306,10 +306,12 @@ static kvprm_status check_lora(const kvprm_handle h, const kvprm_lora *lora, con
 // their element-wise steps fused (no split-K partials). With an adapter, each projection group
 // that has one first computes scale * A u (a split-K GEMV and its finish) and the projection
 // adds B (scale * A u) as a tail of its input range.
+// With sv, the activations the backward pass needs are kept per layer (GradSave).
 static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
                              const kvprm_batch *b, const kvprm_readout_weights *wts,
                              const kvprm_lora *lora, const Plan &p, const Workspace &w,
-                             const GroupTable &gt, float *scores, float *logits, hipStream_t s) {
+                             const GroupTable &gt, float *scores, float *logits, hipStream_t s,
+                             const GradSave *sv = nullptr) {
   const Dims &dm = h->dm;
   const int EB = dm.kvdt == 0 ? 4 : (dm.kvdt == 1 ? 2 : 1);
   const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * EB;
@@ -322,9 +324,24 @@ static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
   };
   HIP_TRY(launch_init_mx(dm, p, w, wts->verify_embed, wts->layers[0].attn_norm, b->lengths, s),
           "init");
+  const size_t xb = (size_t)p.B * dm.H * sizeof(float);
+  const size_t qd = (size_t)p.B * dm.nq * dm.d, kd = (size_t)p.B * dm.nkv * dm.d;
   for (int l = 0; l < dm.layers; ++l) {
     const kvprm_layer_weights &W = wts->layers[l];
     const void *gamma_next = l + 1 < dm.layers ? wts->layers[l + 1].attn_norm : nullptr;
+    Workspace wl = w;  // with sv: q, k_self, v_self written to the layer's saved copies
+    float *o_save = nullptr, *lse_save = nullptr, *gu_save = nullptr;
+    if (sv) {
+      HIP_TRY(hipMemcpyAsync(sv->x_in + (size_t)l * p.B * dm.H, w.x, xb, hipMemcpyDeviceToDevice,
+                             s),
+              "save");
+      wl.q = sv->q + l * qd;
+      wl.kself = sv->ks + l * kd;
+      wl.vself = sv->vs + l * kd;
+      o_save = sv->o + l * qd;
+      lse_save = sv->lse + (size_t)l * p.B * dm.nq;
+      gu_save = sv->gu + (size_t)l * p.B * 2 * dm.F;
+    }
     LoraTail t_qkv = none, t_o = none, t_gu = none, t_d = none;
     if (lora) {
       const kvprm_layer_lora &A = lora->layers[l];
@@ -335,24 +352,29 @@ static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
       const void *a_qkv[3] = {A.q.a, A.k.a, A.v.a};
       HIP_TRY(launch_lora_a(dm, p, w, LORA_QKV, a_qkv, lora->scale, w.opA, s), "q/k/v adapter");
     }
-    HIP_TRY(launch_qkv_mx(dm, p, w, W.wq, W.wk, W.wv, t_qkv, s), "qkv projection");
+    HIP_TRY(launch_qkv_mx(dm, p, wl, W.wq, W.wk, W.wv, t_qkv, s), "qkv projection");
     HIP_TRY(launch_attn_mx(dm, p, w, (const char *)cache->k_pages + layer_bytes * l,
                            (const char *)cache->v_pages + layer_bytes * l,
                            cache->k_scale ? cache->k_scale + layer_scales * l : nullptr,
                            cache->v_scale ? cache->v_scale + layer_scales * l : nullptr,
-                           b->page_table, b->lengths, gt, w.q, w.kself, w.vself, nullptr, w.opO,
-                           s),
+                           b->page_table, b->lengths, gt, wl.q, wl.kself, wl.vself, o_save,
+                           w.opO, s, true, lse_save),
             "attention");
     if (lora && t_o.tkb) {
       const void *a_o[3] = {lora->layers[l].o.a, nullptr, nullptr};
       HIP_TRY(launch_lora_a(dm, p, w, LORA_O, a_o, lora->scale, w.opO, s), "output adapter");
     }
     HIP_TRY(launch_oproj_fused(dm, p, w, W.wo, W.ffn_norm, t_o, s), "output projection");
+    if (sv)
+      HIP_TRY(hipMemcpyAsync(sv->x_mid + (size_t)l * p.B * dm.H, w.x, xb,
+                             hipMemcpyDeviceToDevice, s),
+              "save");
     if (lora && t_gu.tkb) {
       const void *a_gu[3] = {lora->layers[l].gate.a, lora->layers[l].up.a, nullptr};
       HIP_TRY(launch_lora_a(dm, p, w, LORA_GU, a_gu, lora->scale, w.opA, s), "gate/up adapter");
     }
-    HIP_TRY(launch_gateup_fused(dm, p, w, W.w_gate, W.w_up, t_gu, s), "gate/up projection");
+    HIP_TRY(launch_gateup_fused(dm, p, w, W.w_gate, W.w_up, t_gu, s, gu_save),
+            "gate/up projection");
     if (lora && t_d.tkb) {
       const void *a_d[3] = {lora->layers[l].down.a, nullptr, nullptr};
       HIP_TRY(launch_lora_a(dm, p, w, LORA_DOWN, a_d, lora->scale, w.opD, s), "down adapter");
@@ -501,6 +523,106 @@ kvprm_status kvprm_score_ex(kvprm_handle h, const kvprm_kv_cache *cache, const k
                             void *stream) {
   return score_impl(h, cache, b, wts, opt ? opt->lora : nullptr, opt ? opt->depth : 1, workspace,
                     ws_bytes, scores, logits, stream, "kvprm_score_ex");
+}
+
+// ------------------------------------------------------------------ gradients and steering
+
+static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static kvprm_status check_grad(const kvprm_handle h, const kvprm_batch *b, const char *fn) {
+  if (h->dm.wdt != 1 || h->dm.kvdt != 1)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: cache gradients need bf16 weights and a bf16 cache", fn);
+  if (b->batch > 8) return fail(KVPRM_E_UNSUPPORTED, "%s: at most 8 candidates", fn);
+  if (b->num_groups != 0)
+    return fail(KVPRM_E_INVALID, "%s: candidates must not share cache pages (no prefix hint)", fn);
+  return KVPRM_OK;
+}
+
+static size_t grad_ws_bytes(const kvprm_handle h, const kvprm_batch *b) {
+  const Plan p = make_plan(h->dm, b->batch, b->max_pages);
+  return align_up(carve(h->dm, p, nullptr).bytes) + carve_grad(h->dm, p, nullptr).bytes;
+}
+
+kvprm_status kvprm_workspace_size_grad(kvprm_handle h, const kvprm_batch *b, size_t *bytes) {
+  const char *fn = "kvprm_workspace_size_grad";
+  if (!h || !bytes) return fail(KVPRM_E_INVALID, "%s: null argument", fn);
+  kvprm_status st = check_batch(h, b, fn);
+  if (st != KVPRM_OK) return st;
+  if (b->batch == 0) {
+    *bytes = 0;
+    return ok();
+  }
+  if ((st = check_grad(h, b, fn)) != KVPRM_OK) return st;
+  *bytes = grad_ws_bytes(h, b);
+  return ok();
+}
+
+// `steps` rounds of forward (activations saved) and backward; with grad_k / grad_v the
+// backward writes the gradient (one round), otherwise it steps the cache in place by -eta.
+static kvprm_status grad_impl(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                              const kvprm_readout_weights *wts, void *workspace, size_t ws_bytes,
+                              float *scores, float *grad_k, float *grad_v, float eta,
+                              int32_t steps, float *scores_after, void *stream, const char *fn) {
+  if (!h) return fail(KVPRM_E_INVALID, "%s: null handle", fn);
+  kvprm_status st = check_batch(h, b, fn);
+  if (st != KVPRM_OK) return st;
+  if (b->batch == 0) return ok();
+  if ((st = check_grad(h, b, fn)) != KVPRM_OK) return st;
+  if ((st = check_cache(h, cache, fn)) != KVPRM_OK) return st;
+  if ((st = check_readout(h, wts, fn)) != KVPRM_OK) return st;
+  const size_t need = grad_ws_bytes(h, b);
+  if (!workspace || ws_bytes < need)
+    return fail(KVPRM_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                workspace ? ws_bytes : (size_t)0);
+  if (((uintptr_t)workspace & 255) != 0)
+    return fail(KVPRM_E_WORKSPACE, "%s: workspace not 256-byte aligned", fn);
+  if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
+  const Dims &dm = h->dm;
+  hipStream_t s = (hipStream_t)stream;
+  const Plan p = make_plan(dm, b->batch, b->max_pages);
+  const Workspace w = carve(dm, p, workspace);
+  const GradSave sv = carve_grad(dm, p, (char *)workspace + align_up(w.bytes));
+  const GroupTable gt = group_table(h, b, p);
+  const int CP = 1 << gt.cshift_private;
+  const int chunks = gt.private_chunks > 0 ? gt.private_chunks : p.nch - 1;
+  const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * 2;
+  for (int t = 0; t < steps; ++t) {
+    // scores of the cache as it enters each step; the caller's array holds the first
+    if ((st = score_mx(h, cache, b, wts, nullptr, p, w, gt, t == 0 ? scores : sv.Dh, nullptr, s,
+                       &sv)) != KVPRM_OK)
+      return st;
+    HIP_TRY(launch_backward(dm, p, w, sv, wts->layers, wts->final_norm, wts->reward_w,
+                            wts->reward_b, (char *)cache->k_pages, (char *)cache->v_pages,
+                            layer_bytes, b->page_table, b->lengths, CP, chunks, grad_k, grad_v,
+                            eta, s),
+            "backward");
+  }
+  if (scores_after)
+    if ((st = score_mx(h, cache, b, wts, nullptr, p, w, gt, scores_after, nullptr, s)) != KVPRM_OK)
+      return st;
+  return ok();
+}
+
+kvprm_status kvprm_score_grad(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                              const kvprm_readout_weights *weights, void *workspace,
+                              size_t ws_bytes, float *scores, float *grad_k, float *grad_v,
+                              void *stream) {
+  const char *fn = "kvprm_score_grad";
+  if (!scores || !grad_k || !grad_v) return fail(KVPRM_E_INVALID, "%s: null output", fn);
+  return grad_impl(h, cache, b, weights, workspace, ws_bytes, scores, grad_k, grad_v, 0.f, 1,
+                   nullptr, stream, fn);
+}
+
+kvprm_status kvprm_steer(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                         const kvprm_readout_weights *weights, float eta, int32_t steps,
+                         void *workspace, size_t ws_bytes, float *scores_before,
+                         float *scores_after, void *stream) {
+  const char *fn = "kvprm_steer";
+  if (!scores_before || !scores_after) return fail(KVPRM_E_INVALID, "%s: null output", fn);
+  if (steps < 1) return fail(KVPRM_E_INVALID, "%s: steps %d < 1", fn, steps);
+  if (!(eta == eta)) return fail(KVPRM_E_INVALID, "%s: eta is NaN", fn);
+  return grad_impl(h, cache, b, weights, workspace, ws_bytes, scores_before, nullptr, nullptr,
+                   eta, steps, scores_after, stream, fn);
 }
 
 kvprm_status kvprm_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, void *stream) {

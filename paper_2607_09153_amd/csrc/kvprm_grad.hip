@@ -1,0 +1,591 @@
+// Backward pass of the verify-token readout with respect to the key/value cache (gfx950), for
+// KV Steering (appendix: gradient steps on the cache that lower -log P(+)).
+//
+// The forward pass (the matrix-core pipeline) saves, per layer, the residual stream entering
+// the layer and after the attention block, q / k_self / v_self of the verify token, the
+// attention output o and the log-sum-exp of every head's softmax (the token's own key
+// included), and the gate / up pre-activations. Then, from the reward head back to layer 0:
+//
+//   head:       dz = sigmoid(z) - 1, through the final RMSNorm            -> dx
+//   FFN:        dh = W_down^T dx; SwiGLU derivative -> (d gate, d up);
+//               du2 = [W_gate; W_up]^T (d gate, d up); RMSNorm backward    -> dx_mid
+//   attention:  do = W_o^T dx_mid; per cached token t and head h of kv-head j:
+//               p = exp(q.K_t / sqrt(d) - lse_h), ds = p (do_h.V_t - do_h.o_h),
+//               dK_t = sum_h ds q_h / sqrt(d), dV_t = sum_h p do_h, dq_h += ds K_t / sqrt(d);
+//               the same for the token's own key; rotary backward;
+//               du1 = [W_q; W_k; W_v]^T (dq, dk, dv); RMSNorm backward  -> dx_in
+//
+// The transposed products read the packed bf16 weight tiles and multiply on the vector ALUs
+// (a handful of candidates: two flops per weight byte per candidate, far below the rate the
+// ALUs sustain while the tiles stream from HBM). All reductions have a fixed order.
+#include <math.h>
+#include <string.h>
+
+#include "kvprm_internal.h"
+
+namespace kvprm {
+
+namespace {
+
+__device__ __forceinline__ float bf(uint32_t h) { return __uint_as_float(h << 16); }
+
+__device__ __forceinline__ float ldw(const void *p, size_t i) {
+  return bf(((const uint16_t *)p)[i]);
+}
+
+__device__ __forceinline__ uint16_t bf16_round(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// sum over the N lanes of an aligned N-lane group (N a power of two <= 64)
+template <int N>
+__device__ __forceinline__ float sum_lanes(float v) {
+#pragma unroll
+  for (int off = N / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sum over a block of NTHR threads (multiple of 64); every thread gets the result.
+template <int NTHR>
+__device__ __forceinline__ float block_sum(float v, float *red) {
+  v = wave_sum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float s = 0.f;
+#pragma unroll
+  for (int w = 0; w < NTHR / 64; ++w) s += red[w];
+  return s;
+}
+
+__device__ __forceinline__ uint4 ld_nt(const uint4 *p) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------- head, norms
+
+// Reward head backward for one candidate per block: z = w_r . (x r gamma) + b_r with
+// r = 1/sqrt(mean(x^2) + eps); the loss -log sigmoid(z) has dz = sigmoid(z) - 1, and
+// dx = dz (r gamma w_r - (r^3 / H) x sum_i gamma_i w_r,i x_i).
+__global__ __launch_bounds__(256) void k_head_bwd(const float *x, const void *gam, const void *wr,
+                                                  float rb, int H, float eps, float *dx,
+                                                  float *dxT, int B) {
+  __shared__ float red[4];
+  const int b = blockIdx.x;
+  const float *xb = x + (size_t)b * H;
+  float sq = 0.f, dot = 0.f;
+  for (int i = threadIdx.x; i < H; i += 256) {
+    const float v = xb[i];
+    sq += v * v;
+    dot += v * ldw(gam, i) * ldw(wr, i);
+  }
+  sq = block_sum<256>(sq, red);
+  dot = block_sum<256>(dot, red);
+  const float r = 1.0f / sqrtf(sq / (float)H + eps);
+  const float z = dot * r + rb;
+  const float dz = 1.0f / (1.0f + expf(-z)) - 1.0f;
+  const float c = r * r * r / (float)H * dot;
+  for (int i = threadIdx.x; i < H; i += 256) {
+    const float v = dz * (r * ldw(gam, i) * ldw(wr, i) - c * xb[i]);
+    dx[(size_t)b * H + i] = v;
+    dxT[(size_t)i * B + b] = v;
+  }
+}
+
+// RMSNorm backward plus the residual path, one candidate per block:
+// out = res + r (gamma dy) - (r^3 / H) x sum_i gamma_i dy_i x_i (out may be res), also written
+// transposed to outT [H][B].
+__global__ __launch_bounds__(256) void k_rms_bwd(const float *x, const void *gam, const float *dy,
+                                                 const float *res, float *out, float *outT, int B,
+                                                 int H, float eps) {
+  __shared__ float red[4];
+  const int b = blockIdx.x;
+  const size_t o = (size_t)b * H;
+  float sq = 0.f, dot = 0.f;
+  for (int i = threadIdx.x; i < H; i += 256) {
+    const float v = x[o + i];
+    sq += v * v;
+    dot += ldw(gam, i) * dy[o + i] * v;
+  }
+  sq = block_sum<256>(sq, red);
+  dot = block_sum<256>(dot, red);
+  const float r = 1.0f / sqrtf(sq / (float)H + eps);
+  const float c = r * r * r / (float)H * dot;
+  for (int i = threadIdx.x; i < H; i += 256) {
+    const float v = res[o + i] + r * ldw(gam, i) * dy[o + i] - c * x[o + i];
+    out[o + i] = v;
+    outT[(size_t)i * B + b] = v;
+  }
+}
+
+// ------------------------------------------------------------------------------- W^T d
+
+// y[b][k] = sum over the stacked rows r of W[r][k] d[r][b] for packed bf16 matrices (1 KiB
+// blocks, block kb * (rows_i / 16) + t, lane l holding W[16 t + l % 16][32 kb + 8 (l / 16) + i]).
+// One wave per (32-input block kb, row split): it streams the contiguous blocks of its row
+// tiles, each lane multiplying its 8 weights by the d values of its row, then the 16 lanes of
+// an input group add their sums. Partials: part[split][b][k].
+struct TgemvArgs {
+  const void *w[3];
+  int seg_tiles[3];  // row tiles of each segment
+  int nseg;
+  int K;             // inputs (columns) of every segment
+  const float *d;    // [stacked rows][B]
+  int B;
+  int tiles, tps, nsplit;  // stacked row tiles, tiles per split, splits
+  float *part;       // [nsplit][B][K]
+};
+
+template <int BMAX>
+__global__ __launch_bounds__(256) void k_tgemv(TgemvArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wg = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nkb = a.K >> 5;
+  const int kb = wg % nkb, split = wg / nkb;
+  if (split >= a.nsplit) return;
+  const int n = lane & 15, c = lane >> 4;
+  const int t0 = split * a.tps, t1 = min(a.tiles, t0 + a.tps);
+  float acc[BMAX][8];
+#pragma unroll
+  for (int b = 0; b < BMAX; ++b)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[b][i] = 0.f;
+  int seg = 0, base = 0;
+  for (int t = t0; t < t1; ++t) {
+    while (seg < a.nseg - 1 && t >= base + a.seg_tiles[seg]) base += a.seg_tiles[seg++];
+    const uint4 wv = ld_nt((const uint4 *)a.w[seg] + ((size_t)kb * a.seg_tiles[seg] + (t - base)) * 64 + lane);
+    const float w8[8] = {bf(wv.x & 0xFFFFu), bf(wv.x >> 16), bf(wv.y & 0xFFFFu), bf(wv.y >> 16),
+                         bf(wv.z & 0xFFFFu), bf(wv.z >> 16), bf(wv.w & 0xFFFFu), bf(wv.w >> 16)};
+    const float *dr = a.d + (size_t)(t * 16 + n) * a.B;
+#pragma unroll
+    for (int b = 0; b < BMAX; ++b) {
+      if (b < a.B) {
+        const float dv = dr[b];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[b][i] += w8[i] * dv;
+      }
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < BMAX; ++b)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[b][i] = sum_lanes<16>(acc[b][i]);
+  if (n == 0) {
+#pragma unroll
+    for (int b = 0; b < BMAX; ++b) {
+      if (b < a.B) {
+        float *dst = a.part + ((size_t)split * a.B + b) * a.K + kb * 32 + c * 8;
+        *(float4 *)dst = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
+        *(float4 *)(dst + 4) = make_float4(acc[b][4], acc[b][5], acc[b][6], acc[b][7]);
+      }
+    }
+  }
+}
+
+// Sum of the splits, in split order: y[b][k] = sum_s part[s][b][k]. With SWIGLU the sum is the
+// gradient dh of the SwiGLU output h = silu(a) c (a, c the saved gate / up pre-activations,
+// gu[b][0..F) and gu[b][F..2F)), and the kernel writes the stacked d vector of the gate/up
+// products: out[f][b] = dh c silu'(a), out[F + f][b] = dh silu(a).
+template <bool SWIGLU>
+__global__ __launch_bounds__(256) void k_tgemv_sum(const float *part, int nsplit, int B, int K,
+                                                   const float *gu, float *out) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= B * K) return;
+  float s = 0.f;
+  for (int i = 0; i < nsplit; ++i) s += part[(size_t)i * B * K + e];
+  if (!SWIGLU) {
+    out[e] = s;
+    return;
+  }
+  const int b = e / K, f = e - b * K;
+  const float av = gu[(size_t)b * 2 * K + f], cv = gu[(size_t)b * 2 * K + K + f];
+  const float sg = 1.0f / (1.0f + expf(-av));
+  const float silu = av * sg;
+  const float dsilu = sg * (1.0f + av * (1.0f - sg));
+  out[(size_t)f * B + b] = s * cv * dsilu;
+  out[(size_t)(K + f) * B + b] = s * silu;
+}
+
+// ------------------------------------------------------------------------------- attention
+
+// The verify token's own key, per (candidate, kv-head j): for the g heads h of j,
+// Dh = do_h . o_h, p = exp(q_h . k_self / sqrt(d) - lse_h), ds = p (do_h . v_self - Dh);
+// dk_self = sum_h ds q_h / sqrt(d), dv_self = sum_h p do_h, dq_h = ds k_self / sqrt(d).
+// One thread per dimension.
+template <int D>
+__global__ __launch_bounds__(D) void k_attn_bwd_self(const float *q, const float *ks,
+                                                     const float *vs, const float *o,
+                                                     const float *lse, const float *dout, int nq,
+                                                     int nkv, float *Dh, float *dq_self,
+                                                     float *dk_self, float *dv_self) {
+  __shared__ float red[D / 64];
+  const int b = blockIdx.x, j = blockIdx.y, m = threadIdx.x;
+  const int g = nq / nkv;
+  const float sc = 1.0f / sqrtf((float)D);
+  const float kv = ks[((size_t)b * nkv + j) * D + m], vv = vs[((size_t)b * nkv + j) * D + m];
+  float dk = 0.f, dv = 0.f;
+  for (int hh = 0; hh < g; ++hh) {
+    const int h = j * g + hh;
+    const size_t r = ((size_t)b * nq + h) * D + m;
+    const float qv = q[r], dov = dout[r];
+    const float Dv = block_sum<D>(dov * o[r], red);
+    const float s = block_sum<D>(qv * kv, red) * sc;
+    const float dp = block_sum<D>(dov * vv, red);
+    const float p = expf(s - lse[(size_t)b * nq + h]);
+    const float ds = p * (dp - Dv);
+    dk += ds * qv * sc;
+    dv += p * dov;
+    dq_self[r] = ds * kv * sc;
+    if (m == 0) Dh[(size_t)b * nq + h] = Dv;
+  }
+  dk_self[((size_t)b * nkv + j) * D + m] = dk;
+  dv_self[((size_t)b * nkv + j) * D + m] = dv;
+}
+
+struct AttnBwdArgs {
+  char *kp, *vp;               // this layer's pools (bf16), updated in place when steering
+  float *gk, *gv;              // this layer's gradient pools (fp32, pool element order) or null
+  float eta;                   // steering step (in place) when gk is null
+  const int32_t *page_table;
+  int max_pages;
+  const int32_t *lengths;
+  int nkv, nq, CP, nch;        // chunk length in pages, chunk slots per (candidate, head)
+  const float *q, *dout, *lse, *Dh;  // [B][nq][D], [B][nq][D], [B][nq], [B][nq]
+  float *dq_part;              // [B][nq][nch][D]
+};
+
+// Attention backward over one chunk of one candidate's pages for one kv-head (bf16 cache):
+// thread (token s, dims 8 c .. 8 c + 7) of each page. The page's V tile is re-laid in LDS as
+// [token][dim] (its storage interleaves slots), the scores and the dot products with do are
+// added across the 16 lanes of a token, and each thread keeps its dq sums over the chunk's
+// pages for every head; those are added over the 16 tokens at the end. Slots at or beyond L
+// get zero gradient (and are left untouched by a steering step).
+template <int D>
+__global__ __launch_bounds__(16 * (D / 8)) void k_attn_bwd(AttnBwdArgs a) {
+  constexpr int NS = D / 8;      // dim slices
+  constexpr int NT = 16 * NS;    // threads
+  constexpr int GMAX = 16;
+  constexpr int TILE = kPage * D;  // elements of a tile
+  __shared__ float q_s[GMAX][D], do_s[GMAX][D];
+  __shared__ uint16_t v_s[TILE];
+  __shared__ float dv_s[TILE];
+  __shared__ float dq_red[16][D];
+  const int c = blockIdx.x, b = blockIdx.y, j = blockIdx.z;
+  const int t = threadIdx.x;
+  const int s = t / NS, sl = t - s * NS;  // token, dim slice
+  const int m0 = sl * 8;
+  const int g = a.nq / a.nkv;
+  const int L = a.lengths[b];
+  const int npages = (L + kPage - 1) / kPage;
+  const int p0 = c * a.CP;
+  if (p0 >= npages) return;
+  const int np = min(npages, p0 + a.CP) - p0;
+  const float sc = 1.0f / sqrtf((float)D);
+  for (int e = t; e < g * D; e += NT) {
+    const int hh = e / D, m = e - hh * D;
+    const size_t r = ((size_t)b * a.nq + j * g + hh) * D + m;
+    q_s[hh][m] = a.q[r];
+    do_s[hh][m] = a.dout[r];
+  }
+  float lse_h[GMAX], Dh_h[GMAX];
+#pragma unroll
+  for (int hh = 0; hh < GMAX; ++hh) {
+    lse_h[hh] = hh < g ? a.lse[(size_t)b * a.nq + j * g + hh] : 0.f;
+    Dh_h[hh] = hh < g ? a.Dh[(size_t)b * a.nq + j * g + hh] : 0.f;
+  }
+  float dq[GMAX][8];
+#pragma unroll
+  for (int hh = 0; hh < GMAX; ++hh)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) dq[hh][i] = 0.f;
+  __syncthreads();
+  // element (slot s, dim m) of a V tile (bf16: x = 8, r = 2)
+  auto v_index = [](int ss, int m) {
+    return ((((m >> 5) * 4 + (ss >> 2)) * 16 + (m & 15)) * 2 + ((m >> 4) & 1)) * 4 + (ss & 3);
+  };
+  for (int pi = 0; pi < np; ++pi) {
+    const int pg = a.page_table[(size_t)b * a.max_pages + p0 + pi];
+    const size_t toff = ((size_t)pg * a.nkv + j) * TILE;
+    uint16_t *kt = (uint16_t *)a.kp + toff;
+    uint16_t *vt = (uint16_t *)a.vp + toff;
+    // V tile -> LDS (coalesced 16-byte loads), K slice -> registers
+    for (int e = t; e < TILE / 8; e += NT) ((uint4 *)v_s)[e] = ((const uint4 *)vt)[e];
+    const bool valid = (p0 + pi) * kPage + s < L;
+    const int kidx = ((m0 >> 3) * 16 + s) * 8;  // K tile: ((m / 8) * 16 + s) * 8 + m % 8
+    const uint4 kraw = *(const uint4 *)(kt + kidx);
+    float kv[8];
+    kv[0] = bf(kraw.x & 0xFFFFu); kv[1] = bf(kraw.x >> 16);
+    kv[2] = bf(kraw.y & 0xFFFFu); kv[3] = bf(kraw.y >> 16);
+    kv[4] = bf(kraw.z & 0xFFFFu); kv[5] = bf(kraw.z >> 16);
+    kv[6] = bf(kraw.w & 0xFFFFu); kv[7] = bf(kraw.w >> 16);
+    __syncthreads();
+    float vv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) vv[i] = bf(v_s[v_index(s, m0 + i)]);
+    if (!valid) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) kv[i] = vv[i] = 0.f;  // the slot may hold anything
+    }
+    float dk[8], dvv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) dk[i] = dvv[i] = 0.f;
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) {
+      if (hh < g) {
+        float sp = 0.f, dp = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          sp += q_s[hh][m0 + i] * kv[i];
+          dp += do_s[hh][m0 + i] * vv[i];
+        }
+        sp = sum_lanes<NS>(sp);  // the NS lanes of a token hold its NS dim slices
+        dp = sum_lanes<NS>(dp);
+        const float p = valid ? expf(sp * sc - lse_h[hh]) : 0.f;
+        const float ds = p * (dp - Dh_h[hh]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          dk[i] += ds * q_s[hh][m0 + i] * sc;
+          dvv[i] += p * do_s[hh][m0 + i];
+          dq[hh][i] += ds * kv[i] * sc;
+        }
+      }
+    }
+    // dV through LDS into the V layout, then out with the K gradient
+#pragma unroll
+    for (int i = 0; i < 8; ++i) dv_s[v_index(s, m0 + i)] = dvv[i];
+    __syncthreads();
+    if (a.gk) {
+      float *gk = a.gk + toff + kidx;
+      *(float4 *)gk = make_float4(dk[0], dk[1], dk[2], dk[3]);
+      *(float4 *)(gk + 4) = make_float4(dk[4], dk[5], dk[6], dk[7]);
+      for (int e = t; e < TILE / 4; e += NT) ((float4 *)(a.gv + toff))[e] = ((const float4 *)dv_s)[e];
+    } else {
+      if (valid) {
+        uint32_t w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          w[i] = (uint32_t)bf16_round(kv[2 * i] - a.eta * dk[2 * i]) |
+                 ((uint32_t)bf16_round(kv[2 * i + 1] - a.eta * dk[2 * i + 1]) << 16);
+        *(uint4 *)(kt + kidx) = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+      // V: element e of the tile holds slot ((e >> 7) & 3) * 4 + (e & 3) (inverse of v_index)
+      for (int e = t; e < TILE; e += NT) {
+        const int ss = ((e >> 7) & 3) * 4 + (e & 3);
+        if ((p0 + pi) * kPage + ss < L) vt[e] = bf16_round(bf(v_s[e]) - a.eta * dv_s[e]);
+      }
+    }
+    __syncthreads();
+  }
+  // dq partial of this chunk: add the 16 tokens' sums per (head, dim)
+#pragma unroll
+  for (int hh = 0; hh < GMAX; ++hh) {
+    if (hh < g) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) dq_red[s][m0 + i] = dq[hh][i];
+      __syncthreads();
+      for (int m = t; m < D; m += NT) {
+        float acc = 0.f;
+        for (int ss = 0; ss < 16; ++ss) acc += dq_red[ss][m];
+        a.dq_part[(((size_t)b * a.nq + j * g + hh) * a.nch + c) * D + m] = acc;
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// dq of every head (chunk partials in order, then the own-key term), the rotary backward of
+// dq and dk_self (the transposed rotation by the same angles), and the stacked d vector of the
+// q/k/v products: rows [0, nq d) dq, then n_kv d of dk, then n_kv d of dv; layout [row][B].
+template <int D>
+__global__ __launch_bounds__(D / 2) void k_attn_bwd_merge(const float *dq_part, int nch,
+                                                          const int32_t *lengths, int CP,
+                                                          const float *dq_self,
+                                                          const float *dk_self,
+                                                          const float *dv_self, const float *rope,
+                                                          int nq, int nkv, int B, float *dqkv) {
+  const int b = blockIdx.x, h = blockIdx.y, i = threadIdx.x;  // h < nq: q-head; else kv-head
+  constexpr int HD = D / 2;
+  const float cs = rope[((size_t)b * HD + i) * 2], sn = rope[((size_t)b * HD + i) * 2 + 1];
+  float y1, y2;
+  size_t row;
+  if (h < nq) {
+    const int L = lengths[b];
+    const int nc = ((L + kPage - 1) / kPage + CP - 1) / CP;
+    y1 = dq_self[((size_t)b * nq + h) * D + i];
+    y2 = dq_self[((size_t)b * nq + h) * D + i + HD];
+    for (int c = 0; c < nc; ++c) {
+      const float *pp = dq_part + (((size_t)b * nq + h) * nch + c) * D;
+      y1 += pp[i];
+      y2 += pp[i + HD];
+    }
+    row = (size_t)h * D;
+  } else if (h < nq + nkv) {
+    const int j = h - nq;
+    y1 = dk_self[((size_t)b * nkv + j) * D + i];
+    y2 = dk_self[((size_t)b * nkv + j) * D + i + HD];
+    row = (size_t)nq * D + (size_t)j * D;
+  } else {
+    const int j = h - nq - nkv;
+    dqkv[((size_t)(nq + nkv) * D + (size_t)j * D + i) * B + b] = dv_self[((size_t)b * nkv + j) * D + i];
+    dqkv[((size_t)(nq + nkv) * D + (size_t)j * D + i + HD) * B + b] =
+        dv_self[((size_t)b * nkv + j) * D + i + HD];
+    return;
+  }
+  // forward: (a, c) -> (a cos - c sin, c cos + a sin); backward is the transpose
+  dqkv[(row + i) * B + b] = y1 * cs + y2 * sn;
+  dqkv[(row + i + HD) * B + b] = y2 * cs - y1 * sn;
+}
+
+// ------------------------------------------------------------------------------- sequencing
+
+int grad_tgemv_splits(int K, int tiles) {
+  const int nkb = K / 32;
+  int nsplit = (2048 + nkb - 1) / nkb;
+  if (nsplit > tiles) nsplit = tiles;
+  if (nsplit > kGradMaxSplits) nsplit = kGradMaxSplits;
+  const int tps = (tiles + nsplit - 1) / nsplit;
+  return (tiles + tps - 1) / tps;
+}
+
+// out = W^T d over stacked segments (rows[i] rows each, packed, K inputs): the split partials
+// and their sum; with swiglu the sum is turned into the gate/up d vector (see k_tgemv_sum).
+static hipError_t tgemv(const Plan &p, const void *const w[3], const int rows[3], int nseg, int K,
+                        const float *d, float *part, float *out, const float *gu, bool swiglu,
+                        hipStream_t s) {
+  TgemvArgs a;
+  memset(&a, 0, sizeof a);
+  int tiles = 0;
+  for (int i = 0; i < nseg; ++i) {
+    a.w[i] = w[i];
+    a.seg_tiles[i] = rows[i] / 16;
+    tiles += rows[i] / 16;
+  }
+  a.nseg = nseg;
+  a.K = K;
+  a.d = d;
+  a.B = p.B;
+  a.tiles = tiles;
+  a.nsplit = grad_tgemv_splits(K, tiles);
+  a.tps = (tiles + a.nsplit - 1) / a.nsplit;
+  a.part = part;
+  const int waves = (K / 32) * a.nsplit;
+  hipLaunchKernelGGL(k_tgemv<8>, dim3((waves + 3) / 4), dim3(256), 0, s, a);
+  const int n = p.B * K;
+  if (swiglu)
+    hipLaunchKernelGGL(k_tgemv_sum<true>, dim3((n + 255) / 256), dim3(256), 0, s, part, a.nsplit,
+                       p.B, K, gu, out);
+  else
+    hipLaunchKernelGGL(k_tgemv_sum<false>, dim3((n + 255) / 256), dim3(256), 0, s, part, a.nsplit,
+                       p.B, K, gu, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_backward(const Dims &dm, const Plan &p, const Workspace &w, const GradSave &sv,
+                           const kvprm_layer_weights *layers, const void *final_norm,
+                           const void *reward_w, float reward_b, char *kpool, char *vpool,
+                           size_t layer_bytes, const int32_t *page_table, const int32_t *lengths,
+                           int CP, int chunks, float *grad_k, float *grad_v, float eta,
+                           hipStream_t s) {
+  const int B = p.B, H = dm.H, F = dm.F, D = dm.d, nq = dm.nq, nkv = dm.nkv;
+  hipError_t e;
+#define KVPRM_CHECK()                       \
+  do {                                      \
+    if ((e = hipGetLastError()) != hipSuccess) return e; \
+  } while (0)
+  hipLaunchKernelGGL(k_head_bwd, dim3(B), dim3(256), 0, s, w.x, final_norm, reward_w, reward_b, H,
+                     dm.eps, sv.dx, sv.dxT, B);
+  KVPRM_CHECK();
+  const size_t qd = (size_t)B * nq * D, kd = (size_t)B * nkv * D;
+  const size_t elems = layer_bytes / 2;  // bf16 elements of one layer's pool
+  for (int l = dm.layers - 1; l >= 0; --l) {
+    const kvprm_layer_weights &W = layers[l];
+    const float *x_in = sv.x_in + (size_t)l * B * H, *x_mid = sv.x_mid + (size_t)l * B * H;
+    const float *q = sv.q + l * qd, *ks = sv.ks + l * kd, *vs = sv.vs + l * kd;
+    const float *o = sv.o + l * qd, *lse = sv.lse + (size_t)l * B * nq;
+    const float *gu = sv.gu + (size_t)l * B * 2 * F;
+    // FFN: dh = W_down^T dx -> (d gate, d up) -> du2 = [W_gate; W_up]^T (.) -> dx_mid
+    {
+      const void *wd[3] = {W.w_down, nullptr, nullptr};
+      const int rd[3] = {H, 0, 0};
+      if ((e = tgemv(p, wd, rd, 1, F, sv.dxT, sv.part, sv.dgu, gu, true, s)) != hipSuccess) return e;
+      const void *wgu[3] = {W.w_gate, W.w_up, nullptr};
+      const int rgu[3] = {F, F, 0};
+      if ((e = tgemv(p, wgu, rgu, 2, H, sv.dgu, sv.part, sv.du, nullptr, false, s)) != hipSuccess)
+        return e;
+      hipLaunchKernelGGL(k_rms_bwd, dim3(B), dim3(256), 0, s, x_mid, W.ffn_norm, sv.du, sv.dx,
+                         sv.dxm, sv.dxmT, B, H, dm.eps);
+      KVPRM_CHECK();
+    }
+    // attention: do = W_o^T dx_mid; the own key; the cached keys and values; dq -> du1 -> dx
+    {
+      const void *wo[3] = {W.wo, nullptr, nullptr};
+      const int ro[3] = {H, 0, 0};
+      if ((e = tgemv(p, wo, ro, 1, nq * D, sv.dxmT, sv.part, sv.dout, nullptr, false, s)) !=
+          hipSuccess)
+        return e;
+      if (D == 64)
+        hipLaunchKernelGGL(k_attn_bwd_self<64>, dim3(B, nkv), dim3(64), 0, s, q, ks, vs, o, lse,
+                           sv.dout, nq, nkv, sv.Dh, sv.dq_self, sv.dk_self, sv.dv_self);
+      else
+        hipLaunchKernelGGL(k_attn_bwd_self<128>, dim3(B, nkv), dim3(128), 0, s, q, ks, vs, o, lse,
+                           sv.dout, nq, nkv, sv.Dh, sv.dq_self, sv.dk_self, sv.dv_self);
+      KVPRM_CHECK();
+      AttnBwdArgs a;
+      memset(&a, 0, sizeof a);
+      a.kp = kpool + layer_bytes * l;
+      a.vp = vpool + layer_bytes * l;
+      a.gk = grad_k ? grad_k + elems * l : nullptr;
+      a.gv = grad_v ? grad_v + elems * l : nullptr;
+      a.eta = eta;
+      a.page_table = page_table;
+      a.max_pages = p.max_pages;
+      a.lengths = lengths;
+      a.nkv = nkv;
+      a.nq = nq;
+      a.CP = CP;
+      a.nch = p.nch;
+      a.q = q;
+      a.dout = sv.dout;
+      a.lse = lse;
+      a.Dh = sv.Dh;
+      a.dq_part = sv.dq_part;
+      if (D == 64)
+        hipLaunchKernelGGL(k_attn_bwd<64>, dim3(chunks, B, nkv), dim3(16 * 8), 0, s, a);
+      else
+        hipLaunchKernelGGL(k_attn_bwd<128>, dim3(chunks, B, nkv), dim3(16 * 16), 0, s, a);
+      KVPRM_CHECK();
+      if (D == 64)
+        hipLaunchKernelGGL(k_attn_bwd_merge<64>, dim3(B, nq + 2 * nkv), dim3(32), 0, s,
+                           sv.dq_part, p.nch, lengths, CP, sv.dq_self, sv.dk_self, sv.dv_self,
+                           w.rope, nq, nkv, B, sv.dqkv);
+      else
+        hipLaunchKernelGGL(k_attn_bwd_merge<128>, dim3(B, nq + 2 * nkv), dim3(64), 0, s,
+                           sv.dq_part, p.nch, lengths, CP, sv.dq_self, sv.dk_self, sv.dv_self,
+                           w.rope, nq, nkv, B, sv.dqkv);
+      KVPRM_CHECK();
+      const void *wqkv[3] = {W.wq, W.wk, W.wv};
+      const int rqkv[3] = {nq * D, nkv * D, nkv * D};
+      if ((e = tgemv(p, wqkv, rqkv, 3, H, sv.dqkv, sv.part, sv.du, nullptr, false, s)) != hipSuccess)
+        return e;
+      hipLaunchKernelGGL(k_rms_bwd, dim3(B), dim3(256), 0, s, x_in, W.attn_norm, sv.du, sv.dxm,
+                         sv.dx, sv.dxT, B, H, dm.eps);
+      KVPRM_CHECK();
+    }
+  }
+#undef KVPRM_CHECK
+  return hipSuccess;
+}
+
+}  // namespace kvprm

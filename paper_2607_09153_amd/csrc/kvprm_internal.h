@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/kvprm.h"
+
 namespace kvprm {
 
 // Shape of the model as the kernels see it.
@@ -89,6 +91,36 @@ struct Plan {
 
 enum { LORA_QKV = 0, LORA_O = 1, LORA_GU = 2, LORA_DOWN = 3 };
 
+// Backward pass for KV steering (kvprm_grad.hip): activations the forward pass saves per layer
+// (B rows each) and the backward scratch. Vectors that enter a transposed product are
+// [row][B]; the others [B][width].
+constexpr int kGradMaxSplits = 64;  // row splits of a transposed product
+struct GradSave {
+  float *x_in, *x_mid;           // [N_L][B][H] residual stream entering the layer / after attention
+  float *q, *ks, *vs, *o;        // [N_L][B][n_q | n_kv][d] (q, k_self after rotary)
+  float *lse;                    // [N_L][B][n_q] log-sum-exp of each head's softmax (own key incl.)
+  float *gu;                     // [N_L][B][2F] gate / up pre-activations
+  float *dx, *dxT, *dxm, *dxmT;  // [B][H] and [H][B]: residual gradient after / inside the layer
+  float *du;                     // [B][H]
+  float *dgu;                    // [2F][B]
+  float *dout;                   // [B][n_q d]
+  float *Dh;                     // [B][n_q]
+  float *dq_self;                // [B][n_q][d]
+  float *dk_self, *dv_self;      // [B][n_kv][d]
+  float *dqkv;                   // [(n_q + 2 n_kv) d][B]
+  float *dq_part;                // [B][n_q][nch][d]
+  float *part;                   // transposed-product split partials
+  size_t bytes;
+};
+int grad_tgemv_splits(int K, int tiles);
+GradSave carve_grad(const Dims &dm, const Plan &p, void *base);
+hipError_t launch_backward(const Dims &dm, const Plan &p, const Workspace &w, const GradSave &sv,
+                           const kvprm_layer_weights *layers, const void *final_norm,
+                           const void *reward_w, float reward_b, char *kpool, char *vpool,
+                           size_t layer_bytes, const int32_t *page_table, const int32_t *lengths,
+                           int CP, int chunks, float *grad_k, float *grad_v, float eta,
+                           hipStream_t s);
+
 // matrix-core helpers (kvprm_mfma.hip)
 int gemv_nt(int B);
 int gemv_bp(int B);
@@ -125,14 +157,15 @@ hipError_t launch_lora_a(const Dims &dm, const Plan &p, const Workspace &w, int 
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
                               const void *gamma_ffn, const LoraTail &tail, hipStream_t s);
 hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
-                               const void *wu, const LoraTail &tail, hipStream_t s);
+                               const void *wu, const LoraTail &tail, hipStream_t s,
+                               float *save_gu = nullptr);
 hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
                              const void *gamma_next, const LoraTail &tail, hipStream_t s);
 hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
                           const char *vp, const float *ksc, const float *vsc,
                           const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,
                           const float *q, const float *kself, const float *vself, float *o,
-                          uint16_t *op, hipStream_t s, bool merge = true);
+                          uint16_t *op, hipStream_t s, bool merge = true, float *lse = nullptr);
 hipError_t launch_qkv_finish(const Dims &dm, const Plan &p, const Workspace &w,
                              const int32_t *lengths, hipStream_t s);
 hipError_t launch_attention(const Dims &dm, const Plan &p, const Workspace &w, int layer,

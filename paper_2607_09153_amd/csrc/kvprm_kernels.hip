@@ -185,6 +185,52 @@ Workspace carve(const Dims &dm, const Plan &p, void *base) {
   return w;
 }
 
+// Workspace of the backward pass, after the forward's (see GradSave).
+GradSave carve_grad(const Dims &dm, const Plan &p, void *base) {
+  GradSave g{};
+  char *c = (char *)base;
+  size_t off = 0;
+  auto take = [&](size_t elems) {
+    float *r = base ? (float *)(c + off) : nullptr;
+    off += align256(elems * sizeof(float));
+    return r;
+  };
+  const size_t B = (size_t)p.B, NL = (size_t)dm.layers, H = dm.H, F = dm.F, d = dm.d;
+  const size_t nq = dm.nq, nkv = dm.nkv;
+  g.x_in = take(NL * B * H);
+  g.x_mid = take(NL * B * H);
+  g.q = take(NL * B * nq * d);
+  g.ks = take(NL * B * nkv * d);
+  g.vs = take(NL * B * nkv * d);
+  g.o = take(NL * B * nq * d);
+  g.lse = take(NL * B * nq);
+  g.gu = take(NL * B * 2 * F);
+  g.dx = take(B * H);
+  g.dxT = take(B * H);
+  g.dxm = take(B * H);
+  g.dxmT = take(B * H);
+  g.du = take(B * H);
+  g.dgu = take(2 * F * B);
+  g.dout = take(B * nq * d);
+  g.Dh = take(B * nq);
+  g.dq_self = take(B * nq * d);
+  g.dk_self = take(B * nkv * d);
+  g.dv_self = take(B * nkv * d);
+  g.dqkv = take((nq + 2 * nkv) * d * B);
+  g.dq_part = take(B * nq * (size_t)p.nch * d);
+  // split partials of the four transposed products
+  size_t part = 0;
+  const size_t cand[4][2] = {{F, H / 16}, {H, 2 * F / 16}, {nq * d, H / 16},
+                             {H, (nq + 2 * nkv) * d / 16}};
+  for (const auto &kt : cand) {
+    const size_t n = (size_t)grad_tgemv_splits((int)kt[0], (int)kt[1]) * B * kt[0];
+    part = n > part ? n : part;
+  }
+  g.part = take(part);
+  g.bytes = off;
+  return g;
+}
+
 // ------------------------------------------------------------------------------- init
 
 // x[b] = e_v for every candidate (the verify token's embedding); ss = its sum of squares per

@@ -506,6 +506,7 @@ struct FusedArgs {
   const void *tw[3];
   const uint4 *tact;
   int tkb, tstride;
+  float *save;  // SWIGLU: gate / up pre-activations [B][2F] (may be null)
 };
 
 template <int MT, int NT, int WPB, int U, int EPI>
@@ -670,6 +671,10 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
       const int f = tile[0] * 16 + 4 * cq + i;
       const float gv = y[0][i] * inv, uv = y[MT - 1][i] * inv;
       if (cand_ok) store_operand(a.op, a.NT, a.Bp, f, b, gv / (1.0f + expf(-gv)) * uv);
+      if (cand_ok && a.save) {
+        a.save[(size_t)b * 2 * a.F + f] = gv;
+        a.save[(size_t)b * 2 * a.F + a.F + f] = uv;
+      }
     }
   }
 }
@@ -960,6 +965,7 @@ struct AttnArgs {
   float *o;       // [B][nq][D] fp32 output (may be null)
   uint16_t *op;   // operand buffer of the output projection (may be null)
   int NT, Bp;
+  float *lse;     // [B][nq] log-sum-exp of each softmax, own keys included (may be null)
   int kq;         // verify tokens per candidate: row v = token v % kq of candidate v / kq; q,
                   // k_self, v_self, partials and o are per row, lengths and page table per
                   // candidate, group ranges in rows
@@ -1299,6 +1305,7 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
     tot += es * a.vself[((row0 + i) * a.nkv + j) * D + dd];
   }
   const float ov = tot / (lsum + es_sum);
+  if (a.lse && dd == 0) a.lse[(size_t)b * a.nq + h] = M + logf(lsum + es_sum);
   if (a.o) a.o[((size_t)b * a.nq + h) * D + dd] = ov;
   if (a.op) store_operand(a.op, a.NT, a.Bp, h * D + dd, b, ov);
 }
@@ -1499,9 +1506,11 @@ hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w,
 }
 
 hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
-                               const void *wu, const LoraTail &tail, hipStream_t s) {
+                               const void *wu, const LoraTail &tail, hipStream_t s,
+                               float *save_gu) {
   FusedArgs a = fused_args(dm, p, w, dm.H, w.opA);
   set_tail(a, p, w, tail);
+  a.save = save_gu;
   a.w[0] = wg;
   a.w[1] = wu;
   a.seg_rows[0] = dm.F;
@@ -1536,9 +1545,10 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
                           const char *vp, const float *ksc, const float *vsc,
                           const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,
                           const float *q, const float *kself, const float *vself, float *o,
-                          uint16_t *op, hipStream_t s, bool merge) {
+                          uint16_t *op, hipStream_t s, bool merge, float *lse) {
   AttnArgs a;
   memset(&a, 0, sizeof a);
+  a.lse = lse;
   a.kp = kp;
   a.vp = vp;
   a.ksc = ksc;

@@ -258,3 +258,43 @@ def test_score_ex_validation():
         assert e.value.status == kv.KVPRM_E_WORKSPACE
     finally:
         kv.kvprm_destroy(h)
+
+
+def test_grad_and_steer_validation():
+    """Cache gradients need bf16 weights and cache, at most 8 candidates and no shared pages."""
+    hf = kv.kvprm_create(_desc())
+    try:
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_workspace_size_grad(hf, kv.make_batch(1, FAKE, 4, FAKE))
+        assert e.value.status == kv.KVPRM_E_UNSUPPORTED
+    finally:
+        kv.kvprm_destroy(hf)
+    h8 = kv.kvprm_create(_desc(weight_dtype="bf16", kv_dtype="fp8"))
+    try:
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_workspace_size_grad(h8, kv.make_batch(1, FAKE, 4, FAKE))
+        assert e.value.status == kv.KVPRM_E_UNSUPPORTED
+    finally:
+        kv.kvprm_destroy(h8)
+    h = kv.kvprm_create(_desc(weight_dtype="bf16", kv_dtype="bf16"))
+    try:
+        batch = kv.make_batch(2, FAKE, 4, FAKE, [10, 64])
+        n = kv.kvprm_workspace_size_grad(h, batch)
+        assert n > kv.kvprm_workspace_size(h, batch)
+        cases = [
+            (kv.make_batch(9, FAKE, 4, FAKE), {}, kv.KVPRM_E_UNSUPPORTED),
+            (kv.make_batch(2, FAKE, 4, FAKE, [32, 40], [0, 2], [16]), {}, kv.KVPRM_E_INVALID),
+            (batch, dict(ws_bytes=n - 1), kv.KVPRM_E_WORKSPACE),
+            (batch, dict(steps=0), kv.KVPRM_E_INVALID),
+            (batch, dict(after=0), kv.KVPRM_E_INVALID),
+        ]
+        for bt, kw, status in cases:
+            with pytest.raises(kv.KvprmError) as e:
+                kv.kvprm_steer(h, _cache(), bt, _weights(), 0.1, kw.get("steps", 2), FAKE,
+                               kw.get("ws_bytes", n), FAKE, kw.get("after", FAKE))
+            assert e.value.status == status, kv.kvprm_last_error()
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_score_grad(h, _cache(), batch, _weights(), FAKE, n, FAKE, 0, FAKE)
+        assert e.value.status == kv.KVPRM_E_INVALID
+    finally:
+        kv.kvprm_destroy(h)
