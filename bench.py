@@ -11,7 +11,8 @@ dominant kernel (the split-L attention chunk kernel, timed live with HIP events 
 the whole attention step with its merge is reported beside it), the same workload scored with
 the base weights and an unmerged rank-256 adapter on every projection (kvprm_score_lora,
 `lora_readout`) and with two verify tokens per candidate (the depth-k readout, kvprm_score_ex,
-`depth_readout`), and the fp64 CPU oracle timed on a bounded sample of the same workload.
+`depth_readout`), KV steering steps on its cache (kvprm_steer, `kv_steering`), and the fp64
+CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -133,6 +134,39 @@ def time_depth(kv, dw, h, batch, depth, steps, warmup):
             "verify_tokens_per_s": w.batch * depth / (ms * 1e-3)}
 
 
+def time_steer(kv, dw, h, batch, steps):
+    """KV Steering on the workload's cache (kvprm_steer, eta = 0.1): one call of one step and
+    one call of 1 + steps steps, each between two synchronisations; a step (forward with the
+    activations kept, backward through every layer, in-place update of every cached key and
+    value) costs the difference divided by steps. The cache is rewritten."""
+    import torch
+    w = dw.w
+    n = kv.kvprm_workspace_size_grad(h, batch)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    before = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+    after = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    cache, ro = dw.cache(kv), dw.readout(kv)
+
+    def call(k):
+        kv.kvprm_steer(h, cache, batch, ro, 0.1, k, ws.data_ptr(), n, before.data_ptr(),
+                       after.data_ptr(), stream.cuda_stream)
+
+    call(1)  # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    call(1)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    call(1 + steps)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    one, many = (t1 - t0) * 1e3, (t2 - t1) * 1e3
+    return {"eta": 0.1, "ms_one_step_call": one, "ms_per_step": (many - one) / steps,
+            "p_before": before.cpu().tolist(), "p_after": after.cpu().tolist(),
+            "workspace_bytes": n}
+
+
 def copy_bandwidth(nbytes=4 << 30, reps=10):
     """Streaming reference on this GPU: a device-to-device copy of nbytes (read + write bytes
     counted), timed with events; context for the HBM fraction, not a kernel of the path."""
@@ -236,6 +270,9 @@ def main():
                     help="rank of the unmerged adapter of the second timed line (0 = skip)")
     ap.add_argument("--depth", type=int, default=2,
                     help="verify tokens per candidate of the depth-k timed line (1 = skip)")
+    ap.add_argument("--steer-steps", type=int, default=2,
+                    help="KV steering steps of the last timed line (0 = skip; it rewrites the "
+                         "cache, so it runs after every other measurement)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the library has no multi-GPU path "
@@ -301,6 +338,10 @@ def main():
     achieved = kv_per_layer / (kernel_ms * 1e-3) / 1e9
     _log(f"attention chunk kernel: {kernel_ms * 1e3:.1f} us/layer, {achieved:.0f} GB/s; "
          f"attention step with merge: {step_ms * 1e3:.1f} us/layer")
+    steer = None
+    if args.steer_steps > 0:
+        steer = time_steer(kv, dw, h, batch, args.steer_steps)
+        _log(f"KV steering: {steer['ms_per_step']:.3f} ms per step")
     kv.kvprm_destroy(h)
     copy_gbps = copy_bandwidth()
     _log(f"device copy reference: {copy_gbps:.0f} GB/s")
@@ -343,6 +384,8 @@ def main():
         out["lora_readout"] = lora
     if depth is not None:
         out["depth_readout"] = depth
+    if steer is not None:
+        out["kv_steering"] = steer
     if args.cpu_layers > 0:
         _log("timing the oracle on the CPU sample ...")
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers, args.cpu_seconds)

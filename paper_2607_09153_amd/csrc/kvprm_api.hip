@@ -583,8 +583,9 @@ static kvprm_status grad_impl(kvprm_handle h, const kvprm_kv_cache *cache, const
   const Workspace w = carve(dm, p, workspace);
   const GradSave sv = carve_grad(dm, p, (char *)workspace + align_up(w.bytes));
   const GroupTable gt = group_table(h, b, p);
-  const int CP = 1 << gt.cshift_private;
-  const int chunks = gt.private_chunks > 0 ? gt.private_chunks : p.nch - 1;
+  // the backward attention walks 16-page chunks (partial slots of the plan are sized for them)
+  const int CP = 16;
+  const int chunks = p.nch - 1;
   const size_t layer_bytes = (size_t)cache->num_pages * dm.nkv * kPage * dm.d * 2;
   for (int t = 0; t < steps; ++t) {
     // scores of the cache as it enters each step; the caller's array holds the first

@@ -100,13 +100,13 @@ __global__ __launch_bounds__(256) void k_head_bwd(const float *x, const void *ga
   for (int i = threadIdx.x; i < H; i += 256) {
     const float v = dz * (r * ldw(gam, i) * ldw(wr, i) - c * xb[i]);
     dx[(size_t)b * H + i] = v;
-    dxT[(size_t)i * B + b] = v;
+    dxT[(size_t)i * kDPad + b] = v;
   }
 }
 
 // RMSNorm backward plus the residual path, one candidate per block:
 // out = res + r (gamma dy) - (r^3 / H) x sum_i gamma_i dy_i x_i (out may be res), also written
-// transposed to outT [H][B].
+// transposed to outT [H][kDPad].
 __global__ __launch_bounds__(256) void k_rms_bwd(const float *x, const void *gam, const float *dy,
                                                  const float *res, float *out, float *outT, int B,
                                                  int H, float eps) {
@@ -126,7 +126,7 @@ __global__ __launch_bounds__(256) void k_rms_bwd(const float *x, const void *gam
   for (int i = threadIdx.x; i < H; i += 256) {
     const float v = res[o + i] + r * ldw(gam, i) * dy[o + i] - c * x[o + i];
     out[o + i] = v;
-    outT[(size_t)i * B + b] = v;
+    outT[(size_t)i * kDPad + b] = v;
   }
 }
 
@@ -142,7 +142,7 @@ struct TgemvArgs {
   int seg_tiles[3];  // row tiles of each segment
   int nseg;
   int K;             // inputs (columns) of every segment
-  const float *d;    // [stacked rows][B]
+  const float *d;    // [stacked rows][kDPad] (columns >= B ignored)
   int B;
   int tiles, tps, nsplit;  // stacked row tiles, tiles per split, splits
   float *part;       // [nsplit][B][K]
@@ -150,6 +150,7 @@ struct TgemvArgs {
 
 template <int BMAX>
 __global__ __launch_bounds__(256) void k_tgemv(TgemvArgs a) {
+  constexpr int U = 8;  // tiles whose loads are in flight together
   const int lane = threadIdx.x & 63;
   const int wg = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int nkb = a.K >> 5;
@@ -157,25 +158,39 @@ __global__ __launch_bounds__(256) void k_tgemv(TgemvArgs a) {
   if (split >= a.nsplit) return;
   const int n = lane & 15, c = lane >> 4;
   const int t0 = split * a.tps, t1 = min(a.tiles, t0 + a.tps);
+  // first stacked tile of segments 1 and 2 (past the end when absent)
+  const int cum1 = a.nseg > 1 ? a.seg_tiles[0] : a.tiles;
+  const int cum2 = a.nseg > 2 ? a.seg_tiles[0] + a.seg_tiles[1] : a.tiles;
   float acc[BMAX][8];
 #pragma unroll
   for (int b = 0; b < BMAX; ++b)
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[b][i] = 0.f;
-  int seg = 0, base = 0;
-  for (int t = t0; t < t1; ++t) {
-    while (seg < a.nseg - 1 && t >= base + a.seg_tiles[seg]) base += a.seg_tiles[seg++];
-    const uint4 wv = ld_nt((const uint4 *)a.w[seg] + ((size_t)kb * a.seg_tiles[seg] + (t - base)) * 64 + lane);
-    const float w8[8] = {bf(wv.x & 0xFFFFu), bf(wv.x >> 16), bf(wv.y & 0xFFFFu), bf(wv.y >> 16),
-                         bf(wv.z & 0xFFFFu), bf(wv.z >> 16), bf(wv.w & 0xFFFFu), bf(wv.w >> 16)};
-    const float *dr = a.d + (size_t)(t * 16 + n) * a.B;
+  for (int t = t0; t < t1; t += U) {
+    uint4 wv[U];
+    float dv[U][BMAX];
 #pragma unroll
-    for (int b = 0; b < BMAX; ++b) {
-      if (b < a.B) {
-        const float dv = dr[b];
+    for (int u = 0; u < U; ++u) {
+      const bool in = t + u < t1;
+      const int tt = in ? t + u : t1 - 1;  // past the end: repeat the last tile, weight 0
+      const int sg = tt >= cum2 ? 2 : (tt >= cum1 ? 1 : 0);
+      const int base = sg == 0 ? 0 : (sg == 1 ? cum1 : cum2);
+      wv[u] = ld_nt((const uint4 *)a.w[sg] + ((size_t)kb * a.seg_tiles[sg] + (tt - base)) * 64 + lane);
+      const float4 *dr = (const float4 *)(a.d + (size_t)(tt * 16 + n) * kDPad);
+      const float4 d0 = dr[0], d1 = dr[1];
+      const float dd[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc[b][i] += w8[i] * dv;
-      }
+      for (int b = 0; b < BMAX; ++b) dv[u][b] = in ? dd[b] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float w8[8] = {bf(wv[u].x & 0xFFFFu), bf(wv[u].x >> 16), bf(wv[u].y & 0xFFFFu),
+                           bf(wv[u].y >> 16),     bf(wv[u].z & 0xFFFFu), bf(wv[u].z >> 16),
+                           bf(wv[u].w & 0xFFFFu), bf(wv[u].w >> 16)};
+#pragma unroll
+      for (int b = 0; b < BMAX; ++b)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[b][i] += w8[i] * dv[u][b];
     }
   }
 #pragma unroll
@@ -197,7 +212,7 @@ __global__ __launch_bounds__(256) void k_tgemv(TgemvArgs a) {
 // Sum of the splits, in split order: y[b][k] = sum_s part[s][b][k]. With SWIGLU the sum is the
 // gradient dh of the SwiGLU output h = silu(a) c (a, c the saved gate / up pre-activations,
 // gu[b][0..F) and gu[b][F..2F)), and the kernel writes the stacked d vector of the gate/up
-// products: out[f][b] = dh c silu'(a), out[F + f][b] = dh silu(a).
+// products: out[f][b] = dh c silu'(a), out[F + f][b] = dh silu(a) (rows of kDPad columns).
 template <bool SWIGLU>
 __global__ __launch_bounds__(256) void k_tgemv_sum(const float *part, int nsplit, int B, int K,
                                                    const float *gu, float *out) {
@@ -214,8 +229,8 @@ __global__ __launch_bounds__(256) void k_tgemv_sum(const float *part, int nsplit
   const float sg = 1.0f / (1.0f + expf(-av));
   const float silu = av * sg;
   const float dsilu = sg * (1.0f + av * (1.0f - sg));
-  out[(size_t)f * B + b] = s * cv * dsilu;
-  out[(size_t)(K + f) * B + b] = s * silu;
+  out[(size_t)f * kDPad + b] = s * cv * dsilu;
+  out[(size_t)(K + f) * kDPad + b] = s * silu;
 }
 
 // ------------------------------------------------------------------------------- attention
@@ -278,6 +293,7 @@ __global__ __launch_bounds__(16 * (D / 8)) void k_attn_bwd(AttnBwdArgs a) {
   constexpr int NT = 16 * NS;    // threads
   constexpr int GMAX = 16;
   constexpr int TILE = kPage * D;  // elements of a tile
+  static_assert(TILE / 8 == NT, "one 16-byte piece of the V tile per thread");
   __shared__ float q_s[GMAX][D], do_s[GMAX][D];
   __shared__ uint16_t v_s[TILE];
   __shared__ float dv_s[TILE];
@@ -315,16 +331,28 @@ __global__ __launch_bounds__(16 * (D / 8)) void k_attn_bwd(AttnBwdArgs a) {
   auto v_index = [](int ss, int m) {
     return ((((m >> 5) * 4 + (ss >> 2)) * 16 + (m & 15)) * 2 + ((m >> 4) & 1)) * 4 + (ss & 3);
   };
-  for (int pi = 0; pi < np; ++pi) {
+  const int kidx = ((m0 >> 3) * 16 + s) * 8;  // K tile: ((m / 8) * 16 + s) * 8 + m % 8
+  // thread t holds 16 bytes of a page's V tile (TILE / 8 == NT entries) and its own K slice;
+  // the next page's are loaded while the current one is computed
+  auto tile_off = [&](int pi) {
     const int pg = a.page_table[(size_t)b * a.max_pages + p0 + pi];
-    const size_t toff = ((size_t)pg * a.nkv + j) * TILE;
+    return ((size_t)pg * a.nkv + j) * TILE;
+  };
+  size_t toff_next = tile_off(0);
+  uint4 knext = *(const uint4 *)((const uint16_t *)a.kp + toff_next + kidx);
+  uint4 vnext = ((const uint4 *)((const uint16_t *)a.vp + toff_next))[t];
+  for (int pi = 0; pi < np; ++pi) {
+    const size_t toff = toff_next;
     uint16_t *kt = (uint16_t *)a.kp + toff;
     uint16_t *vt = (uint16_t *)a.vp + toff;
-    // V tile -> LDS (coalesced 16-byte loads), K slice -> registers
-    for (int e = t; e < TILE / 8; e += NT) ((uint4 *)v_s)[e] = ((const uint4 *)vt)[e];
+    const uint4 kraw = knext;
+    ((uint4 *)v_s)[t] = vnext;  // V tile -> LDS, read below in [token][dim] order
+    if (pi + 1 < np) {
+      toff_next = tile_off(pi + 1);
+      knext = *(const uint4 *)((const uint16_t *)a.kp + toff_next + kidx);
+      vnext = ((const uint4 *)((const uint16_t *)a.vp + toff_next))[t];
+    }
     const bool valid = (p0 + pi) * kPage + s < L;
-    const int kidx = ((m0 >> 3) * 16 + s) * 8;  // K tile: ((m / 8) * 16 + s) * 8 + m % 8
-    const uint4 kraw = *(const uint4 *)(kt + kidx);
     float kv[8];
     kv[0] = bf(kraw.x & 0xFFFFu); kv[1] = bf(kraw.x >> 16);
     kv[2] = bf(kraw.y & 0xFFFFu); kv[3] = bf(kraw.y >> 16);
@@ -380,10 +408,28 @@ __global__ __launch_bounds__(16 * (D / 8)) void k_attn_bwd(AttnBwdArgs a) {
                  ((uint32_t)bf16_round(kv[2 * i + 1] - a.eta * dk[2 * i + 1]) << 16);
         *(uint4 *)(kt + kidx) = make_uint4(w[0], w[1], w[2], w[3]);
       }
-      // V: element e of the tile holds slot ((e >> 7) & 3) * 4 + (e & 3) (inverse of v_index)
-      for (int e = t; e < TILE; e += NT) {
-        const int ss = ((e >> 7) & 3) * 4 + (e & 3);
-        if ((p0 + pi) * kPage + ss < L) vt[e] = bf16_round(bf(v_s[e]) - a.eta * dv_s[e]);
+      // V: thread t rewrites elements 8 t .. 8 t + 7 of the tile; element e holds slot
+      // ((e >> 7) & 3) * 4 + (e & 3) (inverse of v_index); slots past L keep their bits
+      {
+        const uint4 vo = ((const uint4 *)v_s)[t];
+        const uint32_t vw[4] = {vo.x, vo.y, vo.z, vo.w};
+        uint32_t nw[4];
+#pragma unroll
+        for (int q2 = 0; q2 < 4; ++q2) {
+          uint32_t out = 0;
+#pragma unroll
+          for (int hb = 0; hb < 2; ++hb) {
+            const int e = 8 * t + 2 * q2 + hb;
+            const int ss = ((e >> 7) & 3) * 4 + (e & 3);
+            const uint32_t old16 = (vw[q2] >> (16 * hb)) & 0xFFFFu;
+            const uint32_t new16 = (p0 + pi) * kPage + ss < L
+                                       ? bf16_round(bf(old16) - a.eta * dv_s[e])
+                                       : old16;
+            out |= new16 << (16 * hb);
+          }
+          nw[q2] = out;
+        }
+        ((uint4 *)vt)[t] = make_uint4(nw[0], nw[1], nw[2], nw[3]);
       }
     }
     __syncthreads();
@@ -407,7 +453,8 @@ __global__ __launch_bounds__(16 * (D / 8)) void k_attn_bwd(AttnBwdArgs a) {
 
 // dq of every head (chunk partials in order, then the own-key term), the rotary backward of
 // dq and dk_self (the transposed rotation by the same angles), and the stacked d vector of the
-// q/k/v products: rows [0, nq d) dq, then n_kv d of dk, then n_kv d of dv; layout [row][B].
+// q/k/v products: rows [0, nq d) dq, then n_kv d of dk, then n_kv d of dv; layout
+// [row][kDPad].
 template <int D>
 __global__ __launch_bounds__(D / 2) void k_attn_bwd_merge(const float *dq_part, int nch,
                                                           const int32_t *lengths, int CP,
@@ -438,14 +485,15 @@ __global__ __launch_bounds__(D / 2) void k_attn_bwd_merge(const float *dq_part, 
     row = (size_t)nq * D + (size_t)j * D;
   } else {
     const int j = h - nq - nkv;
-    dqkv[((size_t)(nq + nkv) * D + (size_t)j * D + i) * B + b] = dv_self[((size_t)b * nkv + j) * D + i];
-    dqkv[((size_t)(nq + nkv) * D + (size_t)j * D + i + HD) * B + b] =
+    dqkv[((size_t)(nq + nkv) * D + (size_t)j * D + i) * kDPad + b] =
+        dv_self[((size_t)b * nkv + j) * D + i];
+    dqkv[((size_t)(nq + nkv) * D + (size_t)j * D + i + HD) * kDPad + b] =
         dv_self[((size_t)b * nkv + j) * D + i + HD];
     return;
   }
   // forward: (a, c) -> (a cos - c sin, c cos + a sin); backward is the transpose
-  dqkv[(row + i) * B + b] = y1 * cs + y2 * sn;
-  dqkv[(row + i + HD) * B + b] = y2 * cs - y1 * sn;
+  dqkv[(row + i) * kDPad + b] = y1 * cs + y2 * sn;
+  dqkv[(row + i + HD) * kDPad + b] = y2 * cs - y1 * sn;
 }
 
 // ------------------------------------------------------------------------------- sequencing

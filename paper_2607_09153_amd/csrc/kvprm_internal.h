@@ -93,21 +93,22 @@ enum { LORA_QKV = 0, LORA_O = 1, LORA_GU = 2, LORA_DOWN = 3 };
 
 // Backward pass for KV steering (kvprm_grad.hip): activations the forward pass saves per layer
 // (B rows each) and the backward scratch. Vectors that enter a transposed product are
-// [row][B]; the others [B][width].
+// [row][kDPad]; the others [B][width].
 constexpr int kGradMaxSplits = 64;  // row splits of a transposed product
+constexpr int kDPad = 8;            // columns of a transposed product's d rows (batch <= 8)
 struct GradSave {
   float *x_in, *x_mid;           // [N_L][B][H] residual stream entering the layer / after attention
   float *q, *ks, *vs, *o;        // [N_L][B][n_q | n_kv][d] (q, k_self after rotary)
   float *lse;                    // [N_L][B][n_q] log-sum-exp of each head's softmax (own key incl.)
   float *gu;                     // [N_L][B][2F] gate / up pre-activations
-  float *dx, *dxT, *dxm, *dxmT;  // [B][H] and [H][B]: residual gradient after / inside the layer
+  float *dx, *dxT, *dxm, *dxmT;  // [B][H] and [H][kDPad]: residual gradient after / inside
   float *du;                     // [B][H]
-  float *dgu;                    // [2F][B]
+  float *dgu;                    // [2F][kDPad]
   float *dout;                   // [B][n_q d]
   float *Dh;                     // [B][n_q]
   float *dq_self;                // [B][n_q][d]
   float *dk_self, *dv_self;      // [B][n_kv][d]
-  float *dqkv;                   // [(n_q + 2 n_kv) d][B]
+  float *dqkv;                   // [(n_q + 2 n_kv) d][kDPad]
   float *dq_part;                // [B][n_q][nch][d]
   float *part;                   // transposed-product split partials
   size_t bytes;

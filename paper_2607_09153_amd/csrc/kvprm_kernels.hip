@@ -206,17 +206,17 @@ GradSave carve_grad(const Dims &dm, const Plan &p, void *base) {
   g.lse = take(NL * B * nq);
   g.gu = take(NL * B * 2 * F);
   g.dx = take(B * H);
-  g.dxT = take(B * H);
+  g.dxT = take(kDPad * H);
   g.dxm = take(B * H);
-  g.dxmT = take(B * H);
+  g.dxmT = take(kDPad * H);
   g.du = take(B * H);
-  g.dgu = take(2 * F * B);
+  g.dgu = take(2 * F * kDPad);
   g.dout = take(B * nq * d);
   g.Dh = take(B * nq);
   g.dq_self = take(B * nq * d);
   g.dk_self = take(B * nkv * d);
   g.dv_self = take(B * nkv * d);
-  g.dqkv = take((nq + 2 * nkv) * d * B);
+  g.dqkv = take((nq + 2 * nkv) * d * kDPad);
   g.dq_part = take(B * nq * (size_t)p.nch * d);
   // split partials of the four transposed products
   size_t part = 0;
