@@ -59,7 +59,6 @@ struct Workspace {
 
 struct GemvPlan {
   int rows, K, kslice, ksplit;
-  int ktail;  // 1: one more k-slice for an adapter tail
 };
 
 // Adapter of one projection group (q/k/v, o, gate/up or down) of one layer.
@@ -81,7 +80,6 @@ struct Plan {
   int kslice_qkv, kslice_o, kslice_gu, kslice_d;
   // matrix-core path
   int nt, bp;                 // operand column tiles and padded batch
-  GemvPlan g_qkv;
   // low-rank adapter (0 = none): the split-K plans of the A-factor products of the q/k/v,
   // output, gate/up and down groups
   int lora_rank;

@@ -79,12 +79,11 @@ static GemvPlan gemv_plan(int rows, int K, int B) {
   const int kb_per = (nkb + want - 1) / want;  // <= 32 unless the slice count is capped
   g.kslice = kb_per * 32;
   g.ksplit = (K + g.kslice - 1) / g.kslice;
-  g.ktail = 0;
   return g;
 }
 
 static size_t partial_elems(const GemvPlan &g) {
-  return (size_t)((g.ksplit + g.ktail + 3) & ~3) * g.rows;
+  return (size_t)((g.ksplit + 3) & ~3) * g.rows;
 }
 
 Plan make_plan(const Dims &dm, int Breal, int max_pages, int lora_rank, int depth) {
@@ -111,13 +110,10 @@ Plan make_plan(const Dims &dm, int Breal, int max_pages, int lora_rank, int dept
   size_t m = 0;
   if (dm.wdt == 1) {
     // sums of squares per 16-row tile (written by the fused projections' epilogues); split-K
-    // partials for the QKV projection only
+    // partials only for the adapter's A-factor products
     p.rb = 16;
     p.nt = gemv_nt(B);
     p.bp = gemv_bp(B);
-    p.g_qkv = gemv_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B);
-    p.g_qkv.ktail = lora_rank > 0 ? 1 : 0;
-    m = partial_elems(p.g_qkv);
     if (lora_rank > 0) {
       // A-factor products: rows = adapter rank per segment, input = the group's input width
       p.g_la[LORA_QKV] = gemv_plan(3 * lora_rank, dm.H, B);

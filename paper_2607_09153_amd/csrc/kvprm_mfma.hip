@@ -1,15 +1,17 @@
 // Matrix-core (MFMA, v_mfma_f32_16x16x32_bf16) pipeline of the verify-token pass for gfx950,
 // used with bf16 weights and bf16 or fp8 (OCP e4m3) caches. Per layer:
 //
-//   QKV GEMV -> finish (RMSNorm scale + rotary -> q, k_self, v_self)
+//   q/k/v projection, RMSNorm scale and rotary in its epilogue      -> q, k_self, v_self
 //   attention (split-L paged partials) -> merge with the token's own key (-> o, as operand)
-//   O GEMV -> residual (x += .., sums of squares, operand x * gamma_ffn)
-//   gate/up GEMV -> SwiGLU (RMSNorm scale, silu(g) * u, operand of the down projection)
-//   down GEMV -> residual (x += .., sums of squares, operand x * gamma_attn of the next layer)
+//   output projection + residual (x += .., sums of squares, operand x * gamma_ffn)
+//   gate/up projection + SwiGLU (RMSNorm scale, silu(g) * u, operand of the down projection)
+//   down projection + residual (x += .., sums of squares, operand x * gamma_attn of the next layer)
 //
-// GEMVs split K over blocks and store k-partials; the following small kernel sums them in a
-// fixed order, so results are bitwise reproducible. RMSNorm is applied as a per-candidate
-// scale after the product: W (x * gamma * r) = r * (W (x * gamma)), r = 1/sqrt(mean(x^2) + eps).
+// Each projection block owns whole output rows: its waves split the input range and add their
+// sums in a fixed order, so results are bitwise reproducible. RMSNorm is applied as a
+// per-candidate scale after the product: W (x * gamma * r) = r * (W (x * gamma)),
+// r = 1/sqrt(mean(x^2) + eps). The split-K GEMV (k-partials, then a finish kernel) serves the
+// A factors of unmerged adapters.
 //
 // Precision: weights and cache values enter the matrix cores exactly (bf16, or e4m3 widened to
 // bf16, which is exact). The fp32 operands on the other side are split into bf16 terms,
@@ -173,14 +175,8 @@ struct GemvArgs {
   int rows, K, kslice, ksplit;
   const uint4 *act;  // operand buffer of the input
   int B;
-  float *part;  // [rows][B][ksp] k-partials, ksp = ksplit (+ 1 with a tail) rounded up to 4
+  float *part;  // [rows][B][ksp] k-partials, ksp = ksplit rounded up to 4
   int ksp;
-  // adapter tail (tkb > 0): one more k-slice, index ksplit, over the tkb input blocks of the
-  // segments' B factors (packed [rows_i][32 tkb], null = no adapter: the slice stores zeros)
-  // with operand slot i of tact (tstride uint4 entries apart) as input
-  const void *tw[3];
-  const uint4 *tact;
-  int tkb, tstride;
 };
 
 // part[row][b][ks] = sum over k-slice ks of W[row][k] u_b[k], W in the packed tile layout
@@ -196,16 +192,14 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
   extern __shared__ uint4 act_s[];  // the block's k-slice of the operand: nkb * NT * 64 entries
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ks = blockIdx.y;
-  const bool tail = ks == a.ksplit;  // the adapter slice (only launched with a tail)
-  const int k0 = tail ? 0 : ks * a.kslice;
-  const int nkb = tail ? 0 : min(a.kslice, a.K - k0) >> 5;
+  const int k0 = ks * a.kslice;
+  const int nkb = min(a.kslice, a.K - k0) >> 5;
   const int tile0 = (blockIdx.x * WPB + wave) * MT;
   const int B = a.B;
   const bool active = tile0 * 16 < a.rows;
   const uint4 *wt[MT];
   size_t kstride[MT];  // uint4 entries between consecutive input blocks of a tile
   bool valid[MT];
-  int segm[MT], ltm[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
     const int tile = tile0 + m;
@@ -216,8 +210,6 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
     const size_t ntiles = (size_t)a.seg_rows[seg] / 16;
     kstride[m] = ntiles * 64;
     wt[m] = (const uint4 *)a.w[seg] + ((size_t)(k0 >> 5) * ntiles + lt) * 64 + lane;
-    segm[m] = seg;
-    ltm[m] = lt;
   }
   // Rows of an absent tile read tile 0 of their segment and are never stored.
   auto load_batch = [&](int kb, uint4 (&av)[U][MT]) {
@@ -277,22 +269,6 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_mx(GemvArgs a) {
     for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av[m], bv[t], acc[m][t]);
-  }
-  if (tail) {
-    // B_seg (scale * A_seg u): the segment's B factor tiles over the adapter rank, the
-    // segment's operand slot as input (tiles of a segment without an adapter stay zero)
-#pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      const uint4 *bw = (const uint4 *)a.tw[segm[m]];
-      if (!bw) continue;
-      bw += (size_t)ltm[m] * 64 + lane;
-      const uint4 *tp = a.tact + (size_t)segm[m] * a.tstride + lane;
-      for (int kb = 0; kb < a.tkb; ++kb) {
-        const uint4 av = ld_stream(&bw[(size_t)kb * kstride[m]]);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av, tp[(kb * NT + t) * 64], acc[m][t]);
-      }
-    }
   }
   const int n = lane & 15, c4 = (lane >> 4) * 4;
 #pragma unroll
@@ -482,7 +458,9 @@ __device__ __forceinline__ void rms_finish(const float *__restrict__ ss, int nss
 //   EPI_RESID:  one tile: x += y, the tile's sums of squares per candidate, next operand
 //               x * gamma (if gamma).
 //   EPI_SWIGLU: gate tile t and up tile t: h = silu(r g) * (r u) as the down operand.
-enum { EPI_RESID = 1, EPI_SWIGLU = 2 };
+//   EPI_ROPE:   tile t and tile t + d/32 of one q/k/v head (the two halves of its rotary
+//               pairs): q, k_self, v_self = rotary(r y) written as fp32 (no rotation for v).
+enum { EPI_RESID = 1, EPI_SWIGLU = 2, EPI_ROPE = 3 };
 
 struct FusedArgs {
   const void *w[3];  // weight segments (packed layout), stacked rows
@@ -507,6 +485,10 @@ struct FusedArgs {
   const uint4 *tact;
   int tkb, tstride;
   float *save;  // SWIGLU: gate / up pre-activations [B][2F] (may be null)
+  // ROPE: outputs [B][nq | nkv][d] and the rotary table [B][d/2][cos, sin]
+  float *q, *ks, *vs;
+  const float *rope;
+  int nq, nkv, d;
 };
 
 template <int MT, int NT, int WPB, int U, int EPI>
@@ -522,6 +504,11 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   int tile[MT];
   tile[0] = blockIdx.x;
   if (EPI == EPI_SWIGLU && MT > 1) tile[MT - 1] = blockIdx.x + a.F / 16;
+  if (EPI == EPI_ROPE) {  // block = (head, tile of the head's first half)
+    const int half = a.d / 32;
+    tile[0] = (blockIdx.x / half) * (a.d / 16) + blockIdx.x % half;
+    tile[MT - 1] = tile[0] + half;
+  }
   const uint4 *wt[MT];
   size_t kstride[MT];
   int segm[MT], ltm[MT];
@@ -544,8 +531,9 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   // alone for one column tile (B <= 8), by the whole block for two
   WaveRmsLoads wl;
   RmsLoads rl;
-  if (EPI == EPI_SWIGLU && NT == 1 && wave == 0) wave_rms_load(a.ss, a.nss, B, wl);
-  if (EPI == EPI_SWIGLU && NT >= 2) rms_load<64 * WPB>(a.ss, a.nss, B, rl);
+  constexpr bool RMS = EPI == EPI_SWIGLU || EPI == EPI_ROPE;  // RMSNorm scale in the epilogue
+  if (RMS && NT == 1 && wave == 0) wave_rms_load(a.ss, a.nss, B, wl);
+  if (RMS && NT >= 2) rms_load<64 * WPB>(a.ss, a.nss, B, rl);
   floatx4 acc[MT][NT];
 #pragma unroll
   for (int m = 0; m < MT; ++m)
@@ -623,7 +611,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
       red_s[wave][m][gi][lane] = v;
     }
   __syncthreads();
-  if (EPI == EPI_SWIGLU && NT >= 2) rms_finish<64 * WPB>(a.ss, a.nss, B, a.H, a.eps, rl, part_s, inv_s);
+  if (RMS && NT >= 2) rms_finish<64 * WPB>(a.ss, a.nss, B, a.H, a.eps, rl, part_s, inv_s);
   if (wave >= NG) return;
   const int gi = wave;
   // fixed-order sum over the waves; lane (n, cq) holds rows 4 cq .. 4 cq + 3 of candidate n of
@@ -664,6 +652,24 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
     sq += __shfl_xor(sq, 16, 64);
     sq += __shfl_xor(sq, 32, 64);
     if (cand_ok && cq == 0) a.ss[(size_t)tile[0] * B + b] = sq;
+  } else if (EPI == EPI_ROPE) {
+    const float inv = NT == 1 ? wave_rms_finish(a.ss, a.nss, B, b, a.H, a.eps, wl) : inv_s[b];
+    const int d = a.d, hd = d / 2;
+    const int head = tile[0] / (d / 16);
+    const bool rot = head < a.nq + a.nkv;  // q and k heads rotate, v heads do not
+    float *dst = head < a.nq ? a.q + ((size_t)b * a.nq + head) * d
+                 : head < a.nq + a.nkv ? a.ks + ((size_t)b * a.nkv + head - a.nq) * d
+                                       : a.vs + ((size_t)b * a.nkv + head - a.nq - a.nkv) * d;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int di = tile[0] * 16 + 4 * cq + i - head * d;  // dimension in the first half
+      const float y1 = y[0][i] * inv, y2 = y[MT - 1][i] * inv;
+      const float2 csn = *(const float2 *)(a.rope + ((size_t)b * hd + di) * 2);
+      if (cand_ok) {
+        dst[di] = rot ? y1 * csn.x - y2 * csn.y : y1;
+        dst[di + hd] = rot ? y2 * csn.x + y1 * csn.y : y2;
+      }
+    }
   } else {  // EPI_SWIGLU
     const float inv = NT == 1 ? wave_rms_finish(a.ss, a.nss, B, b, a.H, a.eps, wl) : inv_s[b];
 #pragma unroll
@@ -677,54 +683,6 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
       }
     }
   }
-}
-
-// q, k_self, v_self from the QKV partials: scale by r_b (the attention RMSNorm, applied after
-// the product) and rotate q and k pairs (i, i + d/2) with the cos/sin table of position L_b.
-// One thread per (pair, candidate); every load is issued before the first use.
-template <int NMAX>
-__global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ part, int ksp,
-                                                    int ksplit, const float *__restrict__ ss,
-                                                    int nss, int H, float eps, int B, int nq,
-                                                    int nkv, int d, const float *__restrict__ rope,
-                                                    float *__restrict__ q, float *__restrict__ ks,
-                                                    float *__restrict__ vs) {
-  const int hd = d / 2;
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  const bool act = e < (nq + 2 * nkv) * hd * B;
-  const int ec = act ? e : 0;
-  const int pr = ec / B, b = ec - pr * B;
-  const int head = pr / hd, i = pr - head * hd;
-  const int r = head * d + i;
-  const size_t i1 = (size_t)r * B + b, i2 = (size_t)(r + hd) * B + b;
-  float4 v1[NMAX], v2[NMAX];
-  ksum_load<NMAX>(part, ksp, i1, v1);
-  ksum_load<NMAX>(part, ksp, i2, v2);
-  const float2 csn = *(const float2 *)(rope + ((size_t)b * hd + i) * 2);
-  RmsLoads rl;
-  rms_load<256>(ss, nss, B, rl);
-  __shared__ float part_s[256], inv_s[64];
-  rms_finish<256>(ss, nss, B, H, eps, rl, part_s, inv_s);
-  const float x1 = ksum_add<NMAX>(part, ksp, ksplit, i1, v1);
-  const float x2 = ksum_add<NMAX>(part, ksp, ksplit, i2, v2);
-  const float cs = csn.x, sn = csn.y;
-  const float inv = inv_s[b];
-  if (!act) return;
-  const float y1 = x1 * inv, y2 = x2 * inv;
-  float o1 = y1, o2 = y2;
-  if (head < nq + nkv) {
-    o1 = y1 * cs - y2 * sn;
-    o2 = y2 * cs + y1 * sn;
-  }
-  float *dst;
-  if (head < nq)
-    dst = q + ((size_t)b * nq + head) * d;
-  else if (head < nq + nkv)
-    dst = ks + ((size_t)b * nkv + (head - nq)) * d;
-  else
-    dst = vs + ((size_t)b * nkv + (head - nq - nkv)) * d;
-  dst[i] = o1;
-  dst[i + hd] = o2;
 }
 
 __global__ __launch_bounds__(256) void k_pack_weight(const uint4 *src, uint4 *dst, int64_t rows,
@@ -1319,15 +1277,9 @@ hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, con
 
 static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *w0, int r0,
                                  const void *w1, int r1, const void *w2, int r2,
-                                 const uint16_t *act, float *part, const LoraTail &tail,
-                                 const uint16_t *tact, hipStream_t s) {
+                                 const uint16_t *act, float *part, hipStream_t s) {
   GemvArgs a;
   memset(&a, 0, sizeof a);
-  const bool has_tail = gp.ktail > 0 && tail.tkb > 0;
-  for (int i = 0; i < 3; ++i) a.tw[i] = tail.b[i];
-  a.tact = (const uint4 *)tact;
-  a.tkb = has_tail ? tail.tkb : 0;
-  a.tstride = tail.tkb * p.nt * 64;
   a.w[0] = w0;
   a.w[1] = w1;
   a.w[2] = w2;
@@ -1342,14 +1294,14 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
   a.act = (const uint4 *)act;
   a.B = p.B;
   a.part = part;
-  a.ksp = (gp.ksplit + gp.ktail + 3) & ~3;
+  a.ksp = (gp.ksplit + 3) & ~3;
   const int mt = gemv_mt(p.nt, gp.rows);
   // 4 waves per block; the operand k-slice is staged in LDS for one column tile and read
   // straight from memory (L2) for more (measured faster than staging it: LDS would cap
   // residency, and an LDS-streamed variant with 8 row tiles per block measured slower)
   constexpr int WPB = 4;
   const bool direct = p.nt >= 2;
-  dim3 grid((gp.rows / 16 + WPB * mt - 1) / (WPB * mt), gp.ksplit + (has_tail ? 1 : 0));
+  dim3 grid((gp.rows / 16 + WPB * mt - 1) / (WPB * mt), gp.ksplit);
   const size_t lds = direct ? 0 : (size_t)(gp.kslice / 32) * p.nt * 64 * sizeof(uint4);
 #define KVPRM_G(MT_, NT_, U_)                                                                  \
   if (direct)                                                                                  \
@@ -1375,30 +1327,48 @@ static hipError_t launch_gemv_mx(const Plan &p, const GemvPlan &gp, const void *
   return hipGetLastError();
 }
 
-static int ksp_of(const GemvPlan &g) { return (g.ksplit + g.ktail + 3) & ~3; }
+static int ksp_of(const GemvPlan &g) { return (g.ksplit + 3) & ~3; }
+
+static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, int K,
+                            const uint16_t *act);
+static void set_tail(FusedArgs &a, const Plan &p, const Workspace &w, const LoraTail &tail);
+
+// q, k_self, v_self in one launch: a block owns both halves of the rotary pairs of one head
+// (tiles t and t + d/32) over the whole input and rotates them in its epilogue.
+static hipError_t launch_qkv_rope_fused(const Dims &dm, const Plan &p, const Workspace &w,
+                                        const void *wq, const void *wk, const void *wv,
+                                        const LoraTail &tail, hipStream_t s) {
+  FusedArgs a = fused_args(dm, p, w, dm.H, w.opA);
+  set_tail(a, p, w, tail);
+  a.w[0] = wq;
+  a.w[1] = wk;
+  a.w[2] = wv;
+  a.seg_rows[0] = dm.nq * dm.d;
+  a.seg_rows[1] = dm.nkv * dm.d;
+  a.seg_rows[2] = dm.nkv * dm.d;
+  a.nseg = 3;
+  a.q = w.q;
+  a.ks = w.kself;
+  a.vs = w.vself;
+  a.rope = w.rope;
+  a.nq = dm.nq;
+  a.nkv = dm.nkv;
+  a.d = dm.d;
+  const dim3 grid((dm.nq + 2 * dm.nkv) * (dm.d / 32));
+  switch (p.nt) {
+    case 1: hipLaunchKernelGGL((k_gemv_fused<2, 1, 8, 4, EPI_ROPE>), grid, dim3(64 * 8), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_gemv_fused<2, 2, 8, 4, EPI_ROPE>), grid, dim3(64 * 8), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_gemv_fused<2, 4, 8, 2, EPI_ROPE>), grid, dim3(64 * 8), 0, s, a); break;
+    case 6: hipLaunchKernelGGL((k_gemv_fused<2, 6, 8, 1, EPI_ROPE>), grid, dim3(64 * 8), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_gemv_fused<2, 8, 8, 1, EPI_ROPE>), grid, dim3(64 * 8), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
                          const void *wk, const void *wv, const LoraTail &tail, hipStream_t s) {
-  // with an adapter plan the tail slice always runs (it stores zeros for segments without an
-  // adapter), since the finish adds ksplit + 1 partials
-  LoraTail t = tail;
-  if (p.g_qkv.ktail > 0) t.tkb = p.lora_rank / 32;
-  hipError_t e = launch_gemv_mx(p, p.g_qkv, wq, dm.nq * dm.d, wk, dm.nkv * dm.d, wv, dm.nkv * dm.d,
-                                w.opA, w.part, t, w.topd, s);
-  if (e != hipSuccess) return e;
-  const int n = (dm.nq + 2 * dm.nkv) * (dm.d / 2) * p.B;
-#define KVPRM_F(NM)                                                                             \
-  hipLaunchKernelGGL(k_qkv_fin_mx<NM>, dim3((n + 255) / 256), dim3(256), 0, s, w.part,          \
-                     ksp_of(p.g_qkv), p.g_qkv.ksplit + p.g_qkv.ktail, w.ss, p.nss, dm.H, dm.eps, \
-                     p.B, dm.nq, dm.nkv, dm.d, w.rope, w.q, w.kself, w.vself)
-  switch (ksum_nmax(ksp_of(p.g_qkv))) {
-    case 1: KVPRM_F(1); break;
-    case 2: KVPRM_F(2); break;
-    case 4: KVPRM_F(4); break;
-    default: KVPRM_F(8); break;
-  }
-#undef KVPRM_F
-  return hipGetLastError();
+  return launch_qkv_rope_fused(dm, p, w, wq, wk, wv, tail, s);
 }
 
 // scale * (sum of the k-partials) of adapter row r (segment r / rank, index r % rank) for
@@ -1433,9 +1403,8 @@ hipError_t launch_lora_a(const Dims &dm, const Plan &p, const Workspace &w, int 
   const int r = p.lora_rank;
   GemvPlan g = p.g_la[group];
   g.rows = n * r;
-  const LoraTail none{{nullptr, nullptr, nullptr}, 0};
   hipError_t e = launch_gemv_mx(p, g, seg[0], r, seg[1], n > 1 ? r : 0, seg[2], n > 2 ? r : 0,
-                                act, w.part, none, nullptr, s);
+                                act, w.part, s);
   if (e != hipSuccess) return e;
   const int cnt = g.rows * p.B;
   const size_t slot_elems = (size_t)(r / 32) * p.nt * 64 * 8;
