@@ -166,3 +166,169 @@ def test_kv_steering_matches_the_oracle():
         for pg in range(w.num_pages):
             if pg not in used:
                 assert torch.equal(a[:, pg], o[:, pg])
+
+
+# ---------------------------------------------------------------------------------------------
+# Full size (the ragged 32k batch: 28 layers of the 7B shape, 8 candidates, 216k cached tokens).
+# The fp64 oracle cannot differentiate this size in memory, so the gradient is checked against
+# what holds at any size: central differences of the scores themselves (kvprm_score, whose
+# full-size values are checked against the stored oracle values elsewhere), and the steering
+# step against the gradient it is built from.
+
+def _bf16_spacing(x: torch.Tensor) -> torch.Tensor:
+    """Spacing of bf16 numbers in the binade of |x| (x holds bf16 values, float32): x +- it are
+    both bf16 numbers (just below a power of two the spacing halves, so the step down stays
+    representable). Zero where x is zero."""
+    _, e = torch.frexp(x)  # x = m 2^e, 0.5 <= |m| < 1: 8 significant bits -> spacing 2^(e-8)
+    sp = torch.pow(2.0, (e - 8).to(torch.float32))
+    return torch.where(x == 0, torch.zeros_like(x), sp)
+
+
+def _page_owner(w) -> torch.Tensor:
+    owner = np.full(w.num_pages, -1, dtype=np.int64)
+    for b, L in enumerate(w.lengths):
+        for i in range(-(-L // w.shape.page_size)):
+            owner[w.page_table[b][i]] = b
+    return torch.from_numpy(owner).cuda()
+
+
+def _softplus_neg(z: np.ndarray) -> np.ndarray:
+    return np.logaddexp(0.0, -np.asarray(z, dtype=np.float64))  # -log sigmoid(z)
+
+
+@pytest.fixture(scope="module")
+def full_size():
+    _say("setup: ragged 32k workload on the device, cache gradient by kvprm_score_grad")
+    w = synth.make_workload("ragged_32k")
+    dw = DeviceWorkload(w)
+    m = kv()
+    h = m.kvprm_create(dw.desc(m))
+    batch = dw.batch(m)
+    n = m.kvprm_workspace_size_grad(h, batch)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    scores = torch.full((w.batch,), float("nan"), device="cuda")
+    gk = torch.zeros(dw.k_pool.shape, dtype=torch.float32, device="cuda")
+    gv = torch.zeros(dw.v_pool.shape, dtype=torch.float32, device="cuda")
+    m.kvprm_score_grad(h, dw.cache(m), batch, dw.readout(m), ws.data_ptr(), n, scores.data_ptr(),
+                       gk.data_ptr(), gv.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    state = dict(w=w, dw=dw, m=m, h=h, batch=batch, ws=ws, n=n, gk=gk, gv=gv,
+                 p=scores.cpu().numpy().astype(np.float64), owner=_page_owner(w))
+    yield state
+    m.kvprm_destroy(h)
+
+
+def _logits(st) -> np.ndarray:
+    m, dw, w = st["m"], st["dw"], st["w"]
+    nbytes = m.kvprm_workspace_size(st["h"], st["batch"])
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+    scores = torch.full((w.batch,), float("nan"), device="cuda")
+    logits = torch.full((w.batch,), float("nan"), device="cuda")
+    m.kvprm_score(st["h"], dw.cache(m), st["batch"], dw.readout(m), ws.data_ptr(), nbytes,
+                  scores.data_ptr(), logits.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    return logits.cpu().numpy().astype(np.float64)
+
+
+def test_full_size_gradient_matches_central_differences(full_size):
+    """For each candidate, a perturbation d of one bf16 spacing against the gradient's sign on a
+    seeded random subset of its cached elements (sized so that g.d is about -0.02): the central
+    difference (loss(kv + d) - loss(kv - d)) / 2 of the scoring pass equals g.d within 2%.
+    A wrong sign, a missing term or a misplaced element anywhere in the 28 layers' backward
+    moves g.d away from the scores' own change."""
+    st = full_size
+    w, dw, owner = st["w"], st["dw"], st["owner"]
+    s = w.shape
+    B, P = w.batch, w.num_pages
+    _say("case: full-size gradient vs central differences of kvprm_score (ragged 32k)")
+    z0 = _logits(st)
+    assert np.allclose(1.0 / (1.0 + np.exp(-z0)), st["p"], atol=1e-6)
+    # first pass: sum over each candidate's elements of |g| * spacing
+    mass = torch.zeros(B, dtype=torch.float64, device="cuda")
+    valid = owner >= 0
+    oidx = owner.clamp(min=0)
+    for pool, grad in ((dw.k_pool, st["gk"]), (dw.v_pool, st["gv"])):
+        for l in range(s.num_layers):
+            x = pool[l].view(P, -1).float()
+            g = grad[l].view(P, -1)
+            per_page = (g.abs() * _bf16_spacing(x)).sum(dim=1, dtype=torch.float64)
+            mass.index_add_(0, oidx[valid], per_page[valid])
+    target = 0.02
+    frac = torch.clamp(target / mass, max=1.0)
+    frac_page = torch.where(valid, frac[oidx], torch.zeros_like(frac[oidx])).float()
+    gen = torch.Generator(device="cuda").manual_seed(20260)
+    pred = torch.zeros(B, dtype=torch.float64, device="cuda")
+    plus, minus = [], []
+    for pool, grad in ((dw.k_pool, st["gk"]), (dw.v_pool, st["gv"])):
+        pp, mm = torch.empty_like(pool), torch.empty_like(pool)
+        for l in range(s.num_layers):
+            x = pool[l].view(P, -1).float()
+            g = grad[l].view(P, -1)
+            pick = torch.rand(x.shape, generator=gen, device="cuda") < frac_page[:, None]
+            d = torch.where(pick & (g != 0), -torch.sign(g) * _bf16_spacing(x),
+                            torch.zeros_like(x))
+            pred.index_add_(0, oidx[valid], (g.double() * d.double()).sum(dim=1)[valid])
+            xp, xm = x + d, x - d
+            pp[l].view(P, -1).copy_(xp.to(torch.bfloat16))
+            mm[l].view(P, -1).copy_(xm.to(torch.bfloat16))
+            assert torch.equal(pp[l].view(P, -1).float(), xp)  # exactly representable
+            assert torch.equal(mm[l].view(P, -1).float(), xm)
+        plus.append(pp), minus.append(mm)
+    k0, v0 = dw.k_pool.clone(), dw.v_pool.clone()
+    try:
+        dw.k_pool.copy_(plus[0]), dw.v_pool.copy_(plus[1])
+        zp = _logits(st)
+        dw.k_pool.copy_(minus[0]), dw.v_pool.copy_(minus[1])
+        zm = _logits(st)
+    finally:
+        dw.k_pool.copy_(k0), dw.v_pool.copy_(v0)
+    cd = (_softplus_neg(zp) - _softplus_neg(zm)) / 2
+    pr = pred.cpu().numpy()
+    for b in range(B):
+        _say(f"  candidate {b}: L={w.lengths[b]} g.d {pr[b]:+.6e} central difference {cd[b]:+.6e}"
+             f" (rel {abs(cd[b] - pr[b]) / abs(pr[b]):.2e})")
+    assert np.all(pr < -0.01)
+    assert np.all(np.abs(cd - pr) <= 0.02 * np.abs(pr) + 2e-5)
+
+
+def test_full_size_steering_step(full_size):
+    """kvprm_steer at full size, one step: every stored key and value of every candidate equals
+    round_bf16(kv - eta g) with g from kvprm_score_grad (within one bf16 spacing: the kernel may
+    fuse the multiply-add), pages no candidate reads are untouched bit for bit, and P(+) rises
+    for every candidate. Runs last on the module's workload: it rewrites the cache."""
+    st = full_size
+    w, dw, m, owner = st["w"], st["dw"], st["m"], st["owner"]
+    s = w.shape
+    P = w.num_pages
+    _say("case: full-size steering step (ragged 32k)")
+    gn2 = torch.zeros(w.batch, dtype=torch.float64, device="cuda")
+    valid = owner >= 0
+    for grad in (st["gk"], st["gv"]):
+        for l in range(s.num_layers):
+            gn2.index_add_(0, owner[valid],
+                           (grad[l].view(P, -1).double() ** 2).sum(dim=1)[valid])
+    eta = float(0.05 / gn2.max().item())  # a first-order decrease of up to 0.05 in the loss
+    k0, v0 = dw.k_pool.clone(), dw.v_pool.clone()
+    before = torch.full((w.batch,), float("nan"), device="cuda")
+    after = torch.full((w.batch,), float("nan"), device="cuda")
+    m.kvprm_steer(st["h"], dw.cache(m), st["batch"], dw.readout(m), eta, 1, st["ws"].data_ptr(),
+                  st["n"], before.data_ptr(), after.data_ptr(),
+                  torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    pb, pa = before.cpu().numpy(), after.cpu().numpy()
+    _say(f"  eta {eta:.4e}; P before {pb}; after {pa}")
+    assert np.allclose(pb, st["p"], atol=1e-6)
+    assert np.all(pa > pb)
+    moved_total = 0
+    for pool, orig, grad in ((dw.k_pool, k0, st["gk"]), (dw.v_pool, v0, st["gv"])):
+        for l in range(s.num_layers):
+            x = orig[l].view(P, -1).float()
+            got = pool[l].view(P, -1).float()
+            want = (x - eta * grad[l].view(P, -1)).to(torch.bfloat16).float()
+            off = (got - want).abs()
+            assert bool((off <= _bf16_spacing(want) + 1e-30).all()), f"layer {l}"
+            assert float((off > 0).float().mean()) < 1e-3
+            assert torch.equal(pool[l].view(P, -1)[~valid], orig[l].view(P, -1)[~valid])
+            moved_total += int((got != x).sum())
+    _say(f"  elements changed: {moved_total}")
+    assert moved_total > 0
