@@ -533,6 +533,8 @@ static kvprm_status check_grad(const kvprm_handle h, const kvprm_batch *b, const
   if (h->dm.wdt != 1 || h->dm.kvdt != 1)
     return fail(KVPRM_E_UNSUPPORTED, "%s: cache gradients need bf16 weights and a bf16 cache", fn);
   if (b->batch > 8) return fail(KVPRM_E_UNSUPPORTED, "%s: at most 8 candidates", fn);
+  if (h->dm.H > kGradMaxHidden)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: hidden size above %d", fn, kGradMaxHidden);
   if (b->num_groups != 0)
     return fail(KVPRM_E_INVALID, "%s: candidates must not share cache pages (no prefix hint)", fn);
   return KVPRM_OK;

@@ -72,6 +72,32 @@ __device__ __forceinline__ uint4 ld_nt(const uint4 *p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+
+// Matrix-core products (lane l, c = l / 16, n = l % 16; D = accumulator):
+//   16x16x32: A lane holds row n, reduction slots 8c .. 8c+7; B lane holds column n, the same
+//             slots; D lane holds rows 4c .. 4c+3 of column n
+//   16x16x16: as above with reduction slots 4c .. 4c+3
+// Any assignment of the contracted index to slots works if A and B use the same one.
+__device__ __forceinline__ floatx4 mma32(const uint4 &a, const uint4 &b, const floatx4 &c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 mma16(const uint2 &a, const uint2 &b, const floatx4 &c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(shortx4, a),
+                                                   __builtin_bit_cast(shortx4, b), c, 0, 0, 0);
+}
+
+// x = hi + lo with hi, lo bf16 (nearest-even each): hi * y + lo * y keeps ~16 bits of x
+__device__ __forceinline__ void split_bf16(float x, uint32_t &hi, uint32_t &lo) {
+  hi = bf16_round(x);
+  lo = bf16_round(x - bf(hi));
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------------------- head, norms
@@ -106,27 +132,40 @@ __global__ __launch_bounds__(256) void k_head_bwd(const float *x, const void *ga
 
 // RMSNorm backward plus the residual path, one candidate per block:
 // out = res + r (gamma dy) - (r^3 / H) x sum_i gamma_i dy_i x_i (out may be res), also written
-// transposed to outT [H][kDPad].
-__global__ __launch_bounds__(256) void k_rms_bwd(const float *x, const void *gam, const float *dy,
-                                                 const float *res, float *out, float *outT, int B,
-                                                 int H, float eps) {
-  __shared__ float red[4];
+// transposed to outT [H][kDPad]. Each thread keeps its inputs in registers between the two
+// passes (H <= kGradMaxHidden).
+constexpr int kRmsPer = kGradMaxHidden / 1024;
+__global__ __launch_bounds__(1024) void k_rms_bwd(const float *x, const void *gam, const float *dy,
+                                                  const float *res, float *out, float *outT, int B,
+                                                  int H, float eps) {
+  __shared__ float red[16];
   const int b = blockIdx.x;
   const size_t o = (size_t)b * H;
+  float xv[kRmsPer], gd[kRmsPer];
   float sq = 0.f, dot = 0.f;
-  for (int i = threadIdx.x; i < H; i += 256) {
-    const float v = x[o + i];
-    sq += v * v;
-    dot += ldw(gam, i) * dy[o + i] * v;
+#pragma unroll
+  for (int k = 0; k < kRmsPer; ++k) {
+    const int i = threadIdx.x + k * 1024;
+    xv[k] = i < H ? x[o + i] : 0.f;
+    gd[k] = i < H ? ldw(gam, i) * dy[o + i] : 0.f;
   }
-  sq = block_sum<256>(sq, red);
-  dot = block_sum<256>(dot, red);
+#pragma unroll
+  for (int k = 0; k < kRmsPer; ++k) {
+    sq += xv[k] * xv[k];
+    dot += gd[k] * xv[k];
+  }
+  sq = block_sum<1024>(sq, red);
+  dot = block_sum<1024>(dot, red);
   const float r = 1.0f / sqrtf(sq / (float)H + eps);
   const float c = r * r * r / (float)H * dot;
-  for (int i = threadIdx.x; i < H; i += 256) {
-    const float v = res[o + i] + r * ldw(gam, i) * dy[o + i] - c * x[o + i];
-    out[o + i] = v;
-    outT[(size_t)i * kDPad + b] = v;
+#pragma unroll
+  for (int k = 0; k < kRmsPer; ++k) {
+    const int i = threadIdx.x + k * 1024;
+    if (i < H) {
+      const float v = res[o + i] + r * gd[k] - c * xv[k];
+      out[o + i] = v;
+      outT[(size_t)i * kDPad + b] = v;
+    }
   }
 }
 
@@ -451,6 +490,260 @@ __global__ __launch_bounds__(16 * (D / 8)) void k_attn_bwd(AttnBwdArgs a) {
   }
 }
 
+// The same on the matrix cores. Block = W waves of one (candidate b, kv-head j); wave w walks
+// the CP pages of chunk W x + w of b. Per page of 16 cached tokens, with the g q-heads of j as
+// the other side of every product (padded to 16):
+//   S^T = Q K^T              16x16x32 over the dims (A = q in three bf16 terms, B = the K tile
+//                            as loaded)
+//   dP^T = dO V^T            over the dims (B = the V tile read back from LDS token-major)
+//   P = exp(S / sqrt(d) - lse), dS = P (dP - D)      lane = token, its 4 heads in registers
+//   dV = P dO                16x16x16 over the heads: a lane ends with 4 consecutive slots of
+//                            two dims, i.e. its own 16 bytes of the V tile
+//   dK^T = (q / sqrt(d))^T dS^T   over the heads: 4 consecutive dims of one token per lane
+//   dQ += dS^T K             over the tokens (dS transposed and K read dims-major through LDS)
+// fp32 operands enter as bf16 hi + lo. The q / dO operands with the heads as the reduction index
+// are built once per block in LDS. Slots at or beyond L get zero gradient (their stored values
+// may be anything, NaN included, and are masked before every product that mixes tokens).
+template <int D, int W>
+__global__ __launch_bounds__(64 * W) void k_attn_bwd_mx(AttnBwdArgs a) {
+  constexpr int NKB = D / 32, NDB = D / 16;
+  constexpr int TILE = kPage * D;  // elements of a tile
+  constexpr int TL = TILE / 512;   // 16-byte pieces of a tile per lane (= NKB)
+  constexpr int DST = 20;          // row stride (elements) of the dS transpose
+  static_assert(TL == NKB, "tile pieces per lane");
+  __shared__ uint4 qT_s[NDB][64];            // lane (dim 16 nb + n, c): heads 4c.. of q / sqrt(d), hi.xy lo.zw
+  __shared__ uint4 dO_s[NDB][64];            // the same for dO
+  __shared__ uint4 qa_s[3][NKB][64];         // lane (head n, c): dims 32 kk + 8c .. of q, three terms
+  __shared__ uint4 oa_s[2][NKB][64];         // the same for dO, two terms
+  __shared__ uint4 kt_s[W][TL * 64];         // the page's K tile as stored
+  __shared__ uint4 vt_s[W][TL * 64];         // the page's V tile as stored
+  __shared__ uint16_t ds_s[W][2][16 * DST];  // dS^T hi, lo: [head][token]
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n = lane & 15, c = lane >> 4;
+  const int b = blockIdx.y, j = blockIdx.z;
+  const int nq = a.nq, g = nq / a.nkv;
+  const int L = a.lengths[b];
+  const int npages = (L + kPage - 1) / kPage;
+  if ((int)blockIdx.x * W * a.CP >= npages) return;  // the whole block
+  const float sc = 1.0f / sqrtf((float)D);
+  const size_t hb = (size_t)b * nq + (size_t)j * g;  // row of the first q-head of kv-head j
+  for (int e = threadIdx.x; e < NDB * 64; e += 64 * W) {
+    const int nb = e >> 6, ln = e & 63;
+    const int m = 16 * nb + (ln & 15), c4 = 4 * (ln >> 4);
+    uint32_t qh[4], ql[4], oh[4], ol[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool hv = c4 + i < g;
+      const size_t r = (hb + (hv ? c4 + i : 0)) * D + m;
+      split_bf16(hv ? a.q[r] * sc : 0.f, qh[i], ql[i]);
+      split_bf16(hv ? a.dout[r] : 0.f, oh[i], ol[i]);
+    }
+    qT_s[nb][ln] = make_uint4(qh[0] | qh[1] << 16, qh[2] | qh[3] << 16, ql[0] | ql[1] << 16,
+                              ql[2] | ql[3] << 16);
+    dO_s[nb][ln] = make_uint4(oh[0] | oh[1] << 16, oh[2] | oh[3] << 16, ol[0] | ol[1] << 16,
+                              ol[2] | ol[3] << 16);
+  }
+  // q (three terms) and dO (two) with the dims as reduction index, lane = head n
+  for (int e = threadIdx.x; e < NKB * 64; e += 64 * W) {
+    const int kk = e >> 6, ln = e & 63, hn = ln & 15, c8 = 8 * (ln >> 4);
+    const bool hv = hn < g;
+    const float *qr = a.q + (hb + (hv ? hn : 0)) * D + 32 * kk + c8;
+    const float *orow = a.dout + (hb + (hv ? hn : 0)) * D + 32 * kk + c8;
+    uint32_t h[8], md[8], lo[8], oh[8], ol[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float qv = hv ? qr[i] : 0.f;
+      uint32_t rest;
+      split_bf16(qv, h[i], rest);
+      split_bf16(qv - bf(h[i]), md[i], lo[i]);
+      split_bf16(hv ? orow[i] : 0.f, oh[i], ol[i]);
+    }
+    qa_s[0][kk][ln] = make_uint4(h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16);
+    qa_s[1][kk][ln] = make_uint4(md[0] | md[1] << 16, md[2] | md[3] << 16, md[4] | md[5] << 16,
+                                 md[6] | md[7] << 16);
+    qa_s[2][kk][ln] = make_uint4(lo[0] | lo[1] << 16, lo[2] | lo[3] << 16, lo[4] | lo[5] << 16,
+                                 lo[6] | lo[7] << 16);
+    oa_s[0][kk][ln] = make_uint4(oh[0] | oh[1] << 16, oh[2] | oh[3] << 16, oh[4] | oh[5] << 16,
+                                 oh[6] | oh[7] << 16);
+    oa_s[1][kk][ln] = make_uint4(ol[0] | ol[1] << 16, ol[2] | ol[3] << 16, ol[4] | ol[5] << 16,
+                                 ol[6] | ol[7] << 16);
+  }
+  float lse2[4], Dh4[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int h = 4 * c + i;
+    lse2[i] = h < g ? a.lse[hb + h] * kLog2e : 0.f;
+    Dh4[i] = h < g ? a.Dh[hb + h] : 0.f;
+  }
+  floatx4 dq[NDB];
+#pragma unroll
+  for (int nb = 0; nb < NDB; ++nb) dq[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();  // block operands ready; no other barrier below (every LDS region after this
+                    // is private to one wave, whose LDS accesses execute in program order)
+  const int chunk = blockIdx.x * W + wv;
+  const int pw0 = chunk * a.CP, pw1 = min(npages, pw0 + a.CP);
+  if (pw0 >= pw1) return;
+  uint4 *ks = kt_s[wv], *vs = vt_s[wv];
+  const uint16_t *ks16 = (const uint16_t *)ks, *vs16 = (const uint16_t *)vs;
+  uint16_t *dsh = ds_s[wv][0], *dsl = ds_s[wv][1];
+  const float rs2 = kLog2e * sc;
+  const int32_t *prow = a.page_table + (size_t)b * a.max_pages;
+  const uint4 *kp4 = (const uint4 *)a.kp, *vp4 = (const uint4 *)a.vp;
+  size_t toff = ((size_t)prow[pw0] * a.nkv + j) * TILE;  // element offset of the next tile
+  uint4 kn[TL], vn[TL];
+#pragma unroll
+  for (int t = 0; t < TL; ++t) {
+    kn[t] = ld_nt(kp4 + toff / 8 + t * 64 + lane);
+    vn[t] = ld_nt(vp4 + toff / 8 + t * 64 + lane);
+  }
+  for (int pi = pw0; pi < pw1; ++pi) {
+    const size_t tcur = toff;
+    uint4 kr[TL], vr[TL];
+#pragma unroll
+    for (int t = 0; t < TL; ++t) {
+      kr[t] = kn[t];
+      vr[t] = vn[t];
+    }
+    if (pi + 1 < pw1) {  // the next page's tiles are in flight while this one is computed
+      toff = ((size_t)prow[pi + 1] * a.nkv + j) * TILE;
+#pragma unroll
+      for (int t = 0; t < TL; ++t) {
+        kn[t] = ld_nt(kp4 + toff / 8 + t * 64 + lane);
+        vn[t] = ld_nt(vp4 + toff / 8 + t * 64 + lane);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < TL; ++t) {
+      ks[t * 64 + lane] = kr[t];
+      vs[t * 64 + lane] = vr[t];
+    }
+    // S^T and dP^T: lane = token n of the page, rows = heads 4c .. 4c+3
+    floatx4 st = {0.f, 0.f, 0.f, 0.f}, dpt = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < NKB; ++kk) {
+      st = mma32(qa_s[0][kk][lane], kr[kk], st);
+      st = mma32(qa_s[1][kk][lane], kr[kk], st);
+      st = mma32(qa_s[2][kk][lane], kr[kk], st);
+    }
+#pragma unroll
+    for (int kk = 0; kk < NKB; ++kk) {
+      // V element (slot n, dim m) of the stored tile (bf16: x = 8, r = 2)
+      uint32_t e[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int m = 32 * kk + 8 * c + i;
+        e[i] = vs16[((((m >> 5) * 4 + (n >> 2)) * 16 + (m & 15)) * 2 + ((m >> 4) & 1)) * 4 + (n & 3)];
+      }
+      const uint4 vb = make_uint4(e[0] | e[1] << 16, e[2] | e[3] << 16, e[4] | e[5] << 16,
+                                  e[6] | e[7] << 16);
+      dpt = mma32(oa_s[0][kk][lane], vb, dpt);
+      dpt = mma32(oa_s[1][kk][lane], vb, dpt);
+    }
+    const int t0 = pi * kPage;
+    const bool tv = t0 + n < L;
+    uint32_t ph[4], pl[4], sh[4], sl[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool ok = tv && 4 * c + i < g;
+      const float p = ok ? __builtin_amdgcn_exp2f(st[i] * rs2 - lse2[i]) : 0.f;
+      const float ds = ok ? p * (dpt[i] - Dh4[i]) : 0.f;
+      split_bf16(p, ph[i], pl[i]);
+      split_bf16(ds, sh[i], sl[i]);
+      dsh[(4 * c + i) * DST + n] = (uint16_t)sh[i];
+      dsl[(4 * c + i) * DST + n] = (uint16_t)sl[i];
+    }
+    const uint2 Ph = make_uint2(ph[0] | ph[1] << 16, ph[2] | ph[3] << 16);
+    const uint2 Pl = make_uint2(pl[0] | pl[1] << 16, pl[2] | pl[3] << 16);
+    const uint2 Sh = make_uint2(sh[0] | sh[1] << 16, sh[2] | sh[3] << 16);
+    const uint2 Sl = make_uint2(sl[0] | sl[1] << 16, sl[2] | sl[3] << 16);
+    // dV, two 16-dim blocks at a time: lane = dim 16 nb + n, rows = slots 4c .. 4c+3, which is
+    // the lane's own 16-byte piece t of the V tile
+#pragma unroll
+    for (int t = 0; t < TL; ++t) {
+      floatx4 dv[2];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const uint4 ob = dO_s[2 * t + r][lane];
+        const uint2 oh = make_uint2(ob.x, ob.y), ol = make_uint2(ob.z, ob.w);
+        floatx4 v = {0.f, 0.f, 0.f, 0.f};
+        v = mma16(Ph, oh, v);
+        v = mma16(Ph, ol, v);
+        v = mma16(Pl, oh, v);
+        dv[r] = v;
+      }
+      if (a.gk) {
+        float *gv = a.gv + tcur + (size_t)(t * 64 + lane) * 8;
+        *(float4 *)gv = make_float4(dv[0][0], dv[0][1], dv[0][2], dv[0][3]);
+        *(float4 *)(gv + 4) = make_float4(dv[1][0], dv[1][1], dv[1][2], dv[1][3]);
+      } else {
+        const uint32_t w[4] = {vr[t].x, vr[t].y, vr[t].z, vr[t].w};
+        uint32_t nw[4];
+#pragma unroll
+        for (int q2 = 0; q2 < 4; ++q2) {
+          uint32_t out = 0;
+#pragma unroll
+          for (int hb2 = 0; hb2 < 2; ++hb2) {
+            const int i = (q2 & 1) * 2 + hb2;  // slot 4c + i, dim block r = q2 / 2
+            const uint32_t old16 = (w[q2] >> (16 * hb2)) & 0xFFFFu;
+            const uint32_t new16 =
+                t0 + 4 * c + i < L ? bf16_round(bf(old16) - a.eta * dv[q2 >> 1][i]) : old16;
+            out |= new16 << (16 * hb2);
+          }
+          nw[q2] = out;
+        }
+        ((uint4 *)((uint16_t *)a.vp + tcur))[t * 64 + lane] = make_uint4(nw[0], nw[1], nw[2], nw[3]);
+      }
+    }
+    // dK^T: lane = token n, rows = dims 16 nb + 4c .. +3 (half of a 16-byte group of the K tile)
+#pragma unroll
+    for (int nb = 0; nb < NDB; ++nb) {
+      const uint4 qb = qT_s[nb][lane];
+      const uint2 qh = make_uint2(qb.x, qb.y), ql = make_uint2(qb.z, qb.w);
+      floatx4 k = {0.f, 0.f, 0.f, 0.f};
+      k = mma16(qh, Sh, k);
+      k = mma16(qh, Sl, k);
+      k = mma16(ql, Sh, k);
+      const int m = 16 * nb + 4 * c;
+      const int idx = ((m >> 3) * 16 + n) * 8 + (m & 7);
+      if (a.gk) {
+        *(float4 *)(a.gk + tcur + idx) = make_float4(k[0], k[1], k[2], k[3]);
+      } else if (tv) {
+        const uint2 old = *(const uint2 *)(ks16 + idx);
+        const uint32_t o4[4] = {old.x & 0xFFFFu, old.x >> 16, old.y & 0xFFFFu, old.y >> 16};
+        uint32_t nv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) nv[i] = bf16_round(bf(o4[i]) - a.eta * k[i]);
+        *(uint2 *)((uint16_t *)a.kp + tcur + idx) = make_uint2(nv[0] | nv[1] << 16, nv[2] | nv[3] << 16);
+      }
+    }
+    // dQ += dS^T K: A = dS^T (lane = head n, slots = tokens 4c .. 4c+3), B = K (lane = dim
+    // 16 nb + n, the same tokens; slots past L zeroed)
+    const uint2 Ah = *(const uint2 *)(dsh + n * DST + 4 * c);
+    const uint2 Al = *(const uint2 *)(dsl + n * DST + 4 * c);
+#pragma unroll
+    for (int nb = 0; nb < NDB; ++nb) {
+      const int m = 16 * nb + n;
+      uint32_t kv4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int s2 = 4 * c + i;
+        const uint32_t v = ks16[((m >> 3) * 16 + s2) * 8 + (m & 7)];
+        kv4[i] = t0 + s2 < L ? v : 0u;
+      }
+      const uint2 kb = make_uint2(kv4[0] | kv4[1] << 16, kv4[2] | kv4[3] << 16);
+      dq[nb] = mma16(Ah, kb, dq[nb]);
+      dq[nb] = mma16(Al, kb, dq[nb]);
+    }
+  }
+  // this chunk's dq partial: lane = dim 16 nb + n, rows = heads 4c .. 4c+3
+#pragma unroll
+  for (int nb = 0; nb < NDB; ++nb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (4 * c + i < g)
+        a.dq_part[((hb + 4 * c + i) * a.nch + chunk) * D + 16 * nb + n] = dq[nb][i] * sc;
+}
+
 // dq of every head (chunk partials in order, then the own-key term), the rotary backward of
 // dq and dk_self (the transposed rotation by the same angles), and the stacked d vector of the
 // q/k/v products: rows [0, nq d) dq, then n_kv d of dk, then n_kv d of dv; layout
@@ -472,10 +765,24 @@ __global__ __launch_bounds__(D / 2) void k_attn_bwd_merge(const float *dq_part, 
     const int nc = ((L + kPage - 1) / kPage + CP - 1) / CP;
     y1 = dq_self[((size_t)b * nq + h) * D + i];
     y2 = dq_self[((size_t)b * nq + h) * D + i + HD];
-    for (int c = 0; c < nc; ++c) {
-      const float *pp = dq_part + (((size_t)b * nq + h) * nch + c) * D;
-      y1 += pp[i];
-      y2 += pp[i + HD];
+    const float *pp = dq_part + ((size_t)b * nq + h) * nch * D;
+    int c = 0;
+    for (; c + 8 <= nc; c += 8) {  // eight partials in flight, added in chunk order
+      float u1[8], u2[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        u1[k] = pp[(size_t)(c + k) * D + i];
+        u2[k] = pp[(size_t)(c + k) * D + i + HD];
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        y1 += u1[k];
+        y2 += u2[k];
+      }
+    }
+    for (; c < nc; ++c) {
+      y1 += pp[(size_t)c * D + i];
+      y2 += pp[(size_t)c * D + i + HD];
     }
     row = (size_t)h * D;
   } else if (h < nq + nkv) {
@@ -572,7 +879,7 @@ hipError_t launch_backward(const Dims &dm, const Plan &p, const Workspace &w, co
       const int rgu[3] = {F, F, 0};
       if ((e = tgemv(p, wgu, rgu, 2, H, sv.dgu, sv.part, sv.du, nullptr, false, s)) != hipSuccess)
         return e;
-      hipLaunchKernelGGL(k_rms_bwd, dim3(B), dim3(256), 0, s, x_mid, W.ffn_norm, sv.du, sv.dx,
+      hipLaunchKernelGGL(k_rms_bwd, dim3(B), dim3(1024), 0, s, x_mid, W.ffn_norm, sv.du, sv.dx,
                          sv.dxm, sv.dxmT, B, H, dm.eps);
       KVPRM_CHECK();
     }
@@ -609,10 +916,12 @@ hipError_t launch_backward(const Dims &dm, const Plan &p, const Workspace &w, co
       a.lse = lse;
       a.Dh = sv.Dh;
       a.dq_part = sv.dq_part;
+      constexpr int WB = 4;  // waves (chunks) per block of the matrix-core backward
+      const dim3 grid((chunks + WB - 1) / WB, B, nkv);
       if (D == 64)
-        hipLaunchKernelGGL(k_attn_bwd<64>, dim3(chunks, B, nkv), dim3(16 * 8), 0, s, a);
+        hipLaunchKernelGGL((k_attn_bwd_mx<64, WB>), grid, dim3(64 * WB), 0, s, a);
       else
-        hipLaunchKernelGGL(k_attn_bwd<128>, dim3(chunks, B, nkv), dim3(16 * 16), 0, s, a);
+        hipLaunchKernelGGL((k_attn_bwd_mx<128, WB>), grid, dim3(64 * WB), 0, s, a);
       KVPRM_CHECK();
       if (D == 64)
         hipLaunchKernelGGL(k_attn_bwd_merge<64>, dim3(B, nq + 2 * nkv), dim3(32), 0, s,
@@ -627,7 +936,7 @@ hipError_t launch_backward(const Dims &dm, const Plan &p, const Workspace &w, co
       const int rqkv[3] = {nq * D, nkv * D, nkv * D};
       if ((e = tgemv(p, wqkv, rqkv, 3, H, sv.dqkv, sv.part, sv.du, nullptr, false, s)) != hipSuccess)
         return e;
-      hipLaunchKernelGGL(k_rms_bwd, dim3(B), dim3(256), 0, s, x_in, W.attn_norm, sv.du, sv.dxm,
+      hipLaunchKernelGGL(k_rms_bwd, dim3(B), dim3(1024), 0, s, x_in, W.attn_norm, sv.du, sv.dxm,
                          sv.dx, sv.dxT, B, H, dm.eps);
       KVPRM_CHECK();
     }
