@@ -255,10 +255,10 @@ kvprm_status kvprm_score_ex(kvprm_handle h, const kvprm_kv_cache *cache, const k
  * reward head, final RMSNorm, and per layer (last to first) the FFN, the output projection,
  * the attention over the cache and the token's own key (softmax recomputed from the forward's
  * log-sum-exp), the rotary embedding, the q/k/v projections and the RMSNorms. Requires BF16
- * weights and a BF16 cache, batch <= 8, hidden size <= 16384, and candidates that do not share
- * cache pages (no prefix-sharing hint; a page read by two candidates would get one of the two
- * gradients):
- * KVPRM_E_UNSUPPORTED / KVPRM_E_INVALID otherwise. The workspace is
+ * weights and a BF16 cache, batch <= 8, hidden size <= 16384, ffn_dim and (n_q + 2 n_kv) d_h
+ * at most 73728, and candidates that do not share cache pages (no prefix-sharing hint; a page
+ * read by two candidates would get one of the two gradients): KVPRM_E_UNSUPPORTED /
+ * KVPRM_E_INVALID otherwise. The workspace is
  * kvprm_workspace_size_grad bytes (activations of every layer are kept). */
 kvprm_status kvprm_workspace_size_grad(kvprm_handle h, const kvprm_batch *batch, size_t *bytes);
 

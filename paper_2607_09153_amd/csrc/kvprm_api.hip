@@ -535,6 +535,10 @@ static kvprm_status check_grad(const kvprm_handle h, const kvprm_batch *b, const
   if (b->batch > 8) return fail(KVPRM_E_UNSUPPORTED, "%s: at most 8 candidates", fn);
   if (h->dm.H > kGradMaxHidden)
     return fail(KVPRM_E_UNSUPPORTED, "%s: hidden size above %d", fn, kGradMaxHidden);
+  // the row tiles of the transposed gate/up and q/k/v products must fit the splits
+  const int max_rows = kGradMaxSplits * kTgemvWindow * 8;
+  if (h->dm.F > max_rows || (h->dm.nq + 2 * h->dm.nkv) * h->dm.d > max_rows)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: ffn_dim or (n_q + 2 n_kv) d_h above %d", fn, max_rows);
   if (b->num_groups != 0)
     return fail(KVPRM_E_INVALID, "%s: candidates must not share cache pages (no prefix hint)", fn);
   return KVPRM_OK;

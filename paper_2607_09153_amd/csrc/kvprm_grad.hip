@@ -173,9 +173,12 @@ __global__ __launch_bounds__(1024) void k_rms_bwd(const float *x, const void *ga
 
 // y[b][k] = sum over the stacked rows r of W[r][k] d[r][b] for packed bf16 matrices (1 KiB
 // blocks, block kb * (rows_i / 16) + t, lane l holding W[16 t + l % 16][32 kb + 8 (l / 16) + i]).
-// One wave per (32-input block kb, row split): it streams the contiguous blocks of its row
-// tiles, each lane multiplying its 8 weights by the d values of its row, then the 16 lanes of
-// an input group add their sums. Partials: part[split][b][k].
+// A lane holds 8 inputs of one row, so the contraction (over rows) is not a matrix-core shape
+// without a transpose; the vector ALUs do it: each lane multiplies its 8 weights by the d values
+// of its row, and the 16 lanes of an input group add their sums at the end. Block = 4 waves on
+// 4 consecutive 32-input blocks kb of one row split (kTgemvWindow tiles at most); the split's d
+// rows are staged once in LDS, and each wave streams the contiguous weight blocks of its kb with
+// two batches of U tiles in flight. Partials: part[split][b][k].
 struct TgemvArgs {
   const void *w[3];
   int seg_tiles[3];  // row tiles of each segment
@@ -189,48 +192,67 @@ struct TgemvArgs {
 
 template <int BMAX>
 __global__ __launch_bounds__(256) void k_tgemv(TgemvArgs a) {
-  constexpr int U = 8;  // tiles whose loads are in flight together
-  const int lane = threadIdx.x & 63;
-  const int wg = blockIdx.x * 4 + (threadIdx.x >> 6);
+  constexpr int U = 8;  // tiles per load batch
+  __shared__ float4 d_s[kTgemvWindow * 16][2];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nkb = a.K >> 5;
-  const int kb = wg % nkb, split = wg / nkb;
-  if (split >= a.nsplit) return;
+  const int bps = (nkb + 3) >> 2;  // blocks per split
+  const int split = blockIdx.x / bps;
+  const int kb = (blockIdx.x - split * bps) * 4 + w;
+  const bool act = kb < nkb;  // wave-uniform
   const int n = lane & 15, c = lane >> 4;
   const int t0 = split * a.tps, t1 = min(a.tiles, t0 + a.tps);
   // first stacked tile of segments 1 and 2 (past the end when absent)
   const int cum1 = a.nseg > 1 ? a.seg_tiles[0] : a.tiles;
   const int cum2 = a.nseg > 2 ? a.seg_tiles[0] + a.seg_tiles[1] : a.tiles;
+  auto load = [&](int t, uint4 *wv) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int tt = min(t + u, t1 - 1);  // past the end: repeat the last tile (not used)
+      const int sg = tt >= cum2 ? 2 : (tt >= cum1 ? 1 : 0);
+      const int base = sg == 0 ? 0 : (sg == 1 ? cum1 : cum2);
+      wv[u] = ld_nt((const uint4 *)a.w[sg] + ((size_t)kb * a.seg_tiles[sg] + (tt - base)) * 64 + lane);
+    }
+  };
   float acc[BMAX][8];
 #pragma unroll
   for (int b = 0; b < BMAX; ++b)
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[b][i] = 0.f;
-  for (int t = t0; t < t1; t += U) {
-    uint4 wv[U];
-    float dv[U][BMAX];
+  auto comp = [&](int t, const uint4 *wv) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const bool in = t + u < t1;
-      const int tt = in ? t + u : t1 - 1;  // past the end: repeat the last tile, weight 0
-      const int sg = tt >= cum2 ? 2 : (tt >= cum1 ? 1 : 0);
-      const int base = sg == 0 ? 0 : (sg == 1 ? cum1 : cum2);
-      wv[u] = ld_nt((const uint4 *)a.w[sg] + ((size_t)kb * a.seg_tiles[sg] + (tt - base)) * 64 + lane);
-      const float4 *dr = (const float4 *)(a.d + (size_t)(tt * 16 + n) * kDPad);
-      const float4 d0 = dr[0], d1 = dr[1];
-      const float dd[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+      if (t + u < t1) {
+        const float4 d0 = d_s[(t + u - t0) * 16 + n][0], d1 = d_s[(t + u - t0) * 16 + n][1];
+        const float dd[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+        const float w8[8] = {bf(wv[u].x & 0xFFFFu), bf(wv[u].x >> 16), bf(wv[u].y & 0xFFFFu),
+                             bf(wv[u].y >> 16),     bf(wv[u].z & 0xFFFFu), bf(wv[u].z >> 16),
+                             bf(wv[u].w & 0xFFFFu), bf(wv[u].w >> 16)};
 #pragma unroll
-      for (int b = 0; b < BMAX; ++b) dv[u][b] = in ? dd[b] : 0.f;
+        for (int b = 0; b < BMAX; ++b)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[b][i] += w8[i] * dd[b];
+      }
     }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float w8[8] = {bf(wv[u].x & 0xFFFFu), bf(wv[u].x >> 16), bf(wv[u].y & 0xFFFFu),
-                           bf(wv[u].y >> 16),     bf(wv[u].z & 0xFFFFu), bf(wv[u].z >> 16),
-                           bf(wv[u].w & 0xFFFFu), bf(wv[u].w >> 16)};
-#pragma unroll
-      for (int b = 0; b < BMAX; ++b)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[b][i] += w8[i] * dv[u][b];
-    }
+  };
+  uint4 wa[U], wb[U];
+  if (act) load(t0, wa);  // in flight while the d rows are staged
+  for (int e = threadIdx.x; e < (t1 - t0) * 16; e += 256) {
+    const float4 *dr = (const float4 *)(a.d + (size_t)(t0 * 16 + e) * kDPad);
+    d_s[e][0] = dr[0];
+    d_s[e][1] = dr[1];
+  }
+  __syncthreads();
+  if (!act) return;
+  for (int t = t0; t < t1; t += 2 * U) {
+    load(t + U, wb);
+    __builtin_amdgcn_sched_barrier(0);
+    comp(t, wa);
+    __builtin_amdgcn_sched_barrier(0);
+    load(t + 2 * U, wa);
+    __builtin_amdgcn_sched_barrier(0);
+    comp(t + U, wb);
+    __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
   for (int b = 0; b < BMAX; ++b)
@@ -320,179 +342,9 @@ struct AttnBwdArgs {
   float *dq_part;              // [B][nq][nch][D]
 };
 
-// Attention backward over one chunk of one candidate's pages for one kv-head (bf16 cache):
-// thread (token s, dims 8 c .. 8 c + 7) of each page. The page's V tile is re-laid in LDS as
-// [token][dim] (its storage interleaves slots), the scores and the dot products with do are
-// added across the 16 lanes of a token, and each thread keeps its dq sums over the chunk's
-// pages for every head; those are added over the 16 tokens at the end. Slots at or beyond L
-// get zero gradient (and are left untouched by a steering step).
-template <int D>
-__global__ __launch_bounds__(16 * (D / 8)) void k_attn_bwd(AttnBwdArgs a) {
-  constexpr int NS = D / 8;      // dim slices
-  constexpr int NT = 16 * NS;    // threads
-  constexpr int GMAX = 16;
-  constexpr int TILE = kPage * D;  // elements of a tile
-  static_assert(TILE / 8 == NT, "one 16-byte piece of the V tile per thread");
-  __shared__ float q_s[GMAX][D], do_s[GMAX][D];
-  __shared__ uint16_t v_s[TILE];
-  __shared__ float dv_s[TILE];
-  __shared__ float dq_red[16][D];
-  const int c = blockIdx.x, b = blockIdx.y, j = blockIdx.z;
-  const int t = threadIdx.x;
-  const int s = t / NS, sl = t - s * NS;  // token, dim slice
-  const int m0 = sl * 8;
-  const int g = a.nq / a.nkv;
-  const int L = a.lengths[b];
-  const int npages = (L + kPage - 1) / kPage;
-  const int p0 = c * a.CP;
-  if (p0 >= npages) return;
-  const int np = min(npages, p0 + a.CP) - p0;
-  const float sc = 1.0f / sqrtf((float)D);
-  for (int e = t; e < g * D; e += NT) {
-    const int hh = e / D, m = e - hh * D;
-    const size_t r = ((size_t)b * a.nq + j * g + hh) * D + m;
-    q_s[hh][m] = a.q[r];
-    do_s[hh][m] = a.dout[r];
-  }
-  float lse_h[GMAX], Dh_h[GMAX];
-#pragma unroll
-  for (int hh = 0; hh < GMAX; ++hh) {
-    lse_h[hh] = hh < g ? a.lse[(size_t)b * a.nq + j * g + hh] : 0.f;
-    Dh_h[hh] = hh < g ? a.Dh[(size_t)b * a.nq + j * g + hh] : 0.f;
-  }
-  float dq[GMAX][8];
-#pragma unroll
-  for (int hh = 0; hh < GMAX; ++hh)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) dq[hh][i] = 0.f;
-  __syncthreads();
-  // element (slot s, dim m) of a V tile (bf16: x = 8, r = 2)
-  auto v_index = [](int ss, int m) {
-    return ((((m >> 5) * 4 + (ss >> 2)) * 16 + (m & 15)) * 2 + ((m >> 4) & 1)) * 4 + (ss & 3);
-  };
-  const int kidx = ((m0 >> 3) * 16 + s) * 8;  // K tile: ((m / 8) * 16 + s) * 8 + m % 8
-  // thread t holds 16 bytes of a page's V tile (TILE / 8 == NT entries) and its own K slice;
-  // the next page's are loaded while the current one is computed
-  auto tile_off = [&](int pi) {
-    const int pg = a.page_table[(size_t)b * a.max_pages + p0 + pi];
-    return ((size_t)pg * a.nkv + j) * TILE;
-  };
-  size_t toff_next = tile_off(0);
-  uint4 knext = *(const uint4 *)((const uint16_t *)a.kp + toff_next + kidx);
-  uint4 vnext = ((const uint4 *)((const uint16_t *)a.vp + toff_next))[t];
-  for (int pi = 0; pi < np; ++pi) {
-    const size_t toff = toff_next;
-    uint16_t *kt = (uint16_t *)a.kp + toff;
-    uint16_t *vt = (uint16_t *)a.vp + toff;
-    const uint4 kraw = knext;
-    ((uint4 *)v_s)[t] = vnext;  // V tile -> LDS, read below in [token][dim] order
-    if (pi + 1 < np) {
-      toff_next = tile_off(pi + 1);
-      knext = *(const uint4 *)((const uint16_t *)a.kp + toff_next + kidx);
-      vnext = ((const uint4 *)((const uint16_t *)a.vp + toff_next))[t];
-    }
-    const bool valid = (p0 + pi) * kPage + s < L;
-    float kv[8];
-    kv[0] = bf(kraw.x & 0xFFFFu); kv[1] = bf(kraw.x >> 16);
-    kv[2] = bf(kraw.y & 0xFFFFu); kv[3] = bf(kraw.y >> 16);
-    kv[4] = bf(kraw.z & 0xFFFFu); kv[5] = bf(kraw.z >> 16);
-    kv[6] = bf(kraw.w & 0xFFFFu); kv[7] = bf(kraw.w >> 16);
-    __syncthreads();
-    float vv[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) vv[i] = bf(v_s[v_index(s, m0 + i)]);
-    if (!valid) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) kv[i] = vv[i] = 0.f;  // the slot may hold anything
-    }
-    float dk[8], dvv[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) dk[i] = dvv[i] = 0.f;
-#pragma unroll
-    for (int hh = 0; hh < GMAX; ++hh) {
-      if (hh < g) {
-        float sp = 0.f, dp = 0.f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          sp += q_s[hh][m0 + i] * kv[i];
-          dp += do_s[hh][m0 + i] * vv[i];
-        }
-        sp = sum_lanes<NS>(sp);  // the NS lanes of a token hold its NS dim slices
-        dp = sum_lanes<NS>(dp);
-        const float p = valid ? expf(sp * sc - lse_h[hh]) : 0.f;
-        const float ds = p * (dp - Dh_h[hh]);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          dk[i] += ds * q_s[hh][m0 + i] * sc;
-          dvv[i] += p * do_s[hh][m0 + i];
-          dq[hh][i] += ds * kv[i] * sc;
-        }
-      }
-    }
-    // dV through LDS into the V layout, then out with the K gradient
-#pragma unroll
-    for (int i = 0; i < 8; ++i) dv_s[v_index(s, m0 + i)] = dvv[i];
-    __syncthreads();
-    if (a.gk) {
-      float *gk = a.gk + toff + kidx;
-      *(float4 *)gk = make_float4(dk[0], dk[1], dk[2], dk[3]);
-      *(float4 *)(gk + 4) = make_float4(dk[4], dk[5], dk[6], dk[7]);
-      for (int e = t; e < TILE / 4; e += NT) ((float4 *)(a.gv + toff))[e] = ((const float4 *)dv_s)[e];
-    } else {
-      if (valid) {
-        uint32_t w[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          w[i] = (uint32_t)bf16_round(kv[2 * i] - a.eta * dk[2 * i]) |
-                 ((uint32_t)bf16_round(kv[2 * i + 1] - a.eta * dk[2 * i + 1]) << 16);
-        *(uint4 *)(kt + kidx) = make_uint4(w[0], w[1], w[2], w[3]);
-      }
-      // V: thread t rewrites elements 8 t .. 8 t + 7 of the tile; element e holds slot
-      // ((e >> 7) & 3) * 4 + (e & 3) (inverse of v_index); slots past L keep their bits
-      {
-        const uint4 vo = ((const uint4 *)v_s)[t];
-        const uint32_t vw[4] = {vo.x, vo.y, vo.z, vo.w};
-        uint32_t nw[4];
-#pragma unroll
-        for (int q2 = 0; q2 < 4; ++q2) {
-          uint32_t out = 0;
-#pragma unroll
-          for (int hb = 0; hb < 2; ++hb) {
-            const int e = 8 * t + 2 * q2 + hb;
-            const int ss = ((e >> 7) & 3) * 4 + (e & 3);
-            const uint32_t old16 = (vw[q2] >> (16 * hb)) & 0xFFFFu;
-            const uint32_t new16 = (p0 + pi) * kPage + ss < L
-                                       ? bf16_round(bf(old16) - a.eta * dv_s[e])
-                                       : old16;
-            out |= new16 << (16 * hb);
-          }
-          nw[q2] = out;
-        }
-        ((uint4 *)vt)[t] = make_uint4(nw[0], nw[1], nw[2], nw[3]);
-      }
-    }
-    __syncthreads();
-  }
-  // dq partial of this chunk: add the 16 tokens' sums per (head, dim)
-#pragma unroll
-  for (int hh = 0; hh < GMAX; ++hh) {
-    if (hh < g) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) dq_red[s][m0 + i] = dq[hh][i];
-      __syncthreads();
-      for (int m = t; m < D; m += NT) {
-        float acc = 0.f;
-        for (int ss = 0; ss < 16; ++ss) acc += dq_red[ss][m];
-        a.dq_part[(((size_t)b * a.nq + j * g + hh) * a.nch + c) * D + m] = acc;
-      }
-      __syncthreads();
-    }
-  }
-}
-
-// The same on the matrix cores. Block = W waves of one (candidate b, kv-head j); wave w walks
-// the CP pages of chunk W x + w of b. Per page of 16 cached tokens, with the g q-heads of j as
-// the other side of every product (padded to 16):
+// Attention backward over the cache on the matrix cores (bf16 cache). Block = W waves of one
+// (candidate b, kv-head j); wave w walks the CP pages of chunk W x + w of b. Per page of 16
+// cached tokens, with the g q-heads of j as the other side of every product (padded to 16):
 //   S^T = Q K^T              16x16x32 over the dims (A = q in three bf16 terms, B = the K tile
 //                            as loaded)
 //   dP^T = dO V^T            over the dims (B = the V tile read back from LDS token-major)
@@ -805,11 +657,16 @@ __global__ __launch_bounds__(D / 2) void k_attn_bwd_merge(const float *dq_part, 
 
 // ------------------------------------------------------------------------------- sequencing
 
+// Row splits of a transposed product: about 2048 waves (8 per compute unit, one round) and at
+// most kTgemvWindow tiles per split; the tile count per split is then evened out.
 int grad_tgemv_splits(int K, int tiles) {
   const int nkb = K / 32;
-  int nsplit = (2048 + nkb - 1) / nkb;
+  int nsplit = 2048 / nkb;
+  const int need = (tiles + kTgemvWindow - 1) / kTgemvWindow;
+  if (nsplit < need) nsplit = need;
   if (nsplit > tiles) nsplit = tiles;
   if (nsplit > kGradMaxSplits) nsplit = kGradMaxSplits;
+  if (nsplit < 1) nsplit = 1;
   const int tps = (tiles + nsplit - 1) / nsplit;
   return (tiles + tps - 1) / tps;
 }
@@ -835,8 +692,9 @@ static hipError_t tgemv(const Plan &p, const void *const w[3], const int rows[3]
   a.nsplit = grad_tgemv_splits(K, tiles);
   a.tps = (tiles + a.nsplit - 1) / a.nsplit;
   a.part = part;
-  const int waves = (K / 32) * a.nsplit;
-  hipLaunchKernelGGL(k_tgemv<8>, dim3((waves + 3) / 4), dim3(256), 0, s, a);
+  if (a.tps > kTgemvWindow) return hipErrorInvalidValue;  // more rows than the splits allow
+  const int bps = (K / 32 + 3) / 4;
+  hipLaunchKernelGGL(k_tgemv<8>, dim3(bps * a.nsplit), dim3(256), 0, s, a);
   const int n = p.B * K;
   if (swiglu)
     hipLaunchKernelGGL(k_tgemv_sum<true>, dim3((n + 255) / 256), dim3(256), 0, s, part, a.nsplit,

@@ -95,6 +95,8 @@ enum { LORA_QKV = 0, LORA_O = 1, LORA_GU = 2, LORA_DOWN = 3 };
 constexpr int kGradMaxSplits = 64;  // row splits of a transposed product
 constexpr int kDPad = 8;            // columns of a transposed product's d rows (batch <= 8)
 constexpr int kGradMaxHidden = 16384;  // hidden size the RMSNorm backward holds in registers
+constexpr int kTgemvWindow = 144;      // row tiles of one split of a transposed product (its d
+                                        // rows, 72 KiB, are staged in LDS)
 struct GradSave {
   float *x_in, *x_mid;           // [N_L][B][H] residual stream entering the layer / after attention
   float *q, *ks, *vs, *o;        // [N_L][B][n_q | n_kv][d] (q, k_self after rotary)
