@@ -134,11 +134,17 @@ def time_depth(kv, dw, h, batch, depth, steps, warmup):
             "verify_tokens_per_s": w.batch * depth / (ms * 1e-3)}
 
 
+STEER_ETA = 20.0
+
+
 def time_steer(kv, dw, h, batch, steps):
-    """KV Steering on the workload's cache (kvprm_steer, eta = 0.1): one call of one step and
-    one call of 1 + steps steps, each between two synchronisations; a step (forward with the
-    activations kept, backward through every layer, in-place update of every cached key and
-    value) costs the difference divided by steps. The cache is rewritten."""
+    """KV Steering on the workload's cache (kvprm_steer): one call of one step and one call of
+    1 + steps steps, each between two synchronisations; a step (forward with the activations
+    kept, backward through every layer, in-place update of every cached key and value) costs the
+    difference divided by steps. The cache is rewritten. eta = 20: with these random weights the
+    gradient is ~1e-6 per cached value, and a step moves a stored bf16 value only where eta |g|
+    exceeds half its spacing; much smaller steps change P(+) by less than the scoring pass
+    resolves (activations enter the matrix cores with 16 significant bits)."""
     import torch
     w = dw.w
     n = kv.kvprm_workspace_size_grad(h, batch)
@@ -149,7 +155,7 @@ def time_steer(kv, dw, h, batch, steps):
     cache, ro = dw.cache(kv), dw.readout(kv)
 
     def call(k):
-        kv.kvprm_steer(h, cache, batch, ro, 0.1, k, ws.data_ptr(), n, before.data_ptr(),
+        kv.kvprm_steer(h, cache, batch, ro, STEER_ETA, k, ws.data_ptr(), n, before.data_ptr(),
                        after.data_ptr(), stream.cuda_stream)
 
     call(1)  # warm-up
@@ -162,7 +168,7 @@ def time_steer(kv, dw, h, batch, steps):
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     one, many = (t1 - t0) * 1e3, (t2 - t1) * 1e3
-    return {"eta": 0.1, "ms_one_step_call": one, "ms_per_step": (many - one) / steps,
+    return {"eta": STEER_ETA, "ms_one_step_call": one, "ms_per_step": (many - one) / steps,
             "p_before": before.cpu().tolist(), "p_after": after.cpu().tolist(),
             "workspace_bytes": n}
 
