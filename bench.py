@@ -173,6 +173,29 @@ def time_steer(kv, dw, h, batch, steps):
             "workspace_bytes": n}
 
 
+def read_bandwidth(kv, nbytes=4 << 30, reps=10):
+    """Streaming-read ceiling on this GPU: the library's plain read kernel (kvprm_stream_read:
+    the 16-byte non-temporal loads of the cache and weight streams, no arithmetic) over nbytes,
+    timed with events on the stream it runs on; the measured ceiling the kernels' HBM fractions
+    are set against, beside the 8 TB/s nominal figure."""
+    import torch
+    a = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda")
+    a.fill_(1)
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream()
+    kv.kvprm_stream_read(a.data_ptr(), nbytes, sink.data_ptr(), st.cuda_stream)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record(st)
+    for _ in range(reps):
+        kv.kvprm_stream_read(a.data_ptr(), nbytes, sink.data_ptr(), st.cuda_stream)
+    e.record(st)
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    del a
+    return nbytes / (ms * 1e-3) / 1e9
+
+
 def copy_bandwidth(nbytes=4 << 30, reps=10):
     """Streaming reference on this GPU: a device-to-device copy of nbytes (read + write bytes
     counted), timed with events; context for the HBM fraction, not a kernel of the path."""
@@ -351,6 +374,8 @@ def main():
     kv.kvprm_destroy(h)
     copy_gbps = copy_bandwidth()
     _log(f"device copy reference: {copy_gbps:.0f} GB/s")
+    read_gbps = read_bandwidth(kv)
+    _log(f"streaming read reference: {read_gbps:.0f} GB/s")
 
     out = {
         "metric": "verify-token scores/sec + achieved KV-read HBM GB/s at L=32k, B=8",
@@ -385,6 +410,7 @@ def main():
         "per_call_ms": {"median": per_call[len(per_call) // 2], "min": per_call[0],
                         "max": per_call[-1]},
         "copy_reference_gbps": copy_gbps,
+        "read_reference_gbps": read_gbps,
     }
     if lora is not None:
         out["lora_readout"] = lora

@@ -289,6 +289,16 @@ kvprm_status kvprm_steer(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
  * Enqueued on `stream`; a one-time preparation of static weights, not part of scoring. */
 kvprm_status kvprm_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, void *stream);
 
+/* Diagnostic (measurement, not part of scoring): read `bytes` of device memory at `buf` once,
+ * with the access pattern of the cache and weight streams (16-byte non-temporal loads, 512
+ * blocks of 256 threads striding over the buffer), and XOR all its 32-bit words into the device
+ * word *sink (one atomic per wave; the result keeps the reads from being removed and lets a
+ * caller check that every word was read once). The elapsed time gives the streaming-read
+ * ceiling of the GPU that the kernels' HBM fractions are compared with. buf 16-byte aligned,
+ * bytes a positive multiple of 16, sink 4-byte aligned: KVPRM_E_INVALID otherwise. Nothing is
+ * allocated; enqueued on `stream`. */
+kvprm_status kvprm_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream);
+
 /* Text of the last error on the calling thread ("" if none). Valid until the next call on
  * this thread. */
 const char *kvprm_last_error(void);

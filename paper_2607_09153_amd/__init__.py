@@ -24,7 +24,7 @@ EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_scor
             "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
             "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
             "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer",
-            "kvprm_last_error"]
+            "kvprm_stream_read", "kvprm_last_error"]
 LORA_PROJECTIONS = ("q", "k", "v", "o", "gate", "up", "down")
 
 
@@ -115,6 +115,7 @@ def _load():
     lib.kvprm_attention_partials.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
                                              ctypes.c_int32, vp, vp, sz, vp]
     lib.kvprm_pack_weight.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, vp]
+    lib.kvprm_stream_read.argtypes = [vp, sz, vp, vp]
     lib.kvprm_workspace_size_lora.argtypes = [vp, ctypes.POINTER(Batch), ctypes.c_int32,
                                               ctypes.POINTER(sz)]
     lib.kvprm_score_lora.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
@@ -134,7 +135,8 @@ def _load():
     for f in ("kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_score",
               "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
               "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
-              "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer"):
+              "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer",
+              "kvprm_stream_read"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kvprm_last_error.argtypes = []
     lib.kvprm_last_error.restype = ctypes.c_char_p
@@ -296,6 +298,10 @@ def kvprm_score(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeigh
                 stream: int = 0) -> None:
     _check(lib.kvprm_score(handle, ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(weights),
                            workspace_ptr, ws_bytes, scores_ptr, logits_ptr or None, stream or None))
+
+
+def kvprm_stream_read(buf_ptr: int, nbytes: int, sink_ptr: int, stream: int = 0) -> None:
+    _check(lib.kvprm_stream_read(buf_ptr, nbytes, sink_ptr, stream or None))
 
 
 def kvprm_pack_weight(src_ptr: int, dst_ptr: int, rows: int, K: int, stream: int = 0) -> None:

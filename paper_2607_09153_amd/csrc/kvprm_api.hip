@@ -645,6 +645,17 @@ kvprm_status kvprm_pack_weight(const void *src, void *dst, int64_t rows, int64_t
   return ok();
 }
 
+kvprm_status kvprm_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream) {
+  const char *fn = "kvprm_stream_read";
+  if (!buf || !sink) return fail(KVPRM_E_INVALID, "%s: null pointer", fn);
+  if (bytes == 0 || bytes % 16 != 0)
+    return fail(KVPRM_E_INVALID, "%s: bytes must be a positive multiple of 16", fn);
+  if ((uintptr_t)buf & 15) return fail(KVPRM_E_INVALID, "%s: buf must be 16-byte aligned", fn);
+  if ((uintptr_t)sink & 3) return fail(KVPRM_E_INVALID, "%s: sink must be 4-byte aligned", fn);
+  HIP_TRY(launch_stream_read(buf, bytes, sink, (hipStream_t)stream), "stream read");
+  return ok();
+}
+
 kvprm_status kvprm_attention(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
                              int32_t layer, const float *q, const float *k_self,
                              const float *v_self, void *workspace, size_t ws_bytes, float *o,

@@ -739,4 +739,39 @@ hipError_t launch_head(const Dims &dm, const Plan &p, const Workspace &w, const 
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------------------- diagnostics
+
+// Streaming read of n16 16-byte words: grid-stride, four non-temporal loads in flight per
+// thread, the words folded into an XOR that each wave adds to *sink with one atomic, so that the
+// loads cannot be removed (and a test can check that every word was read once). The reference
+// ceiling for the kernels' HBM fractions.
+__global__ __launch_bounds__(256) void k_stream_read(const uint4 *buf, size_t n16, uint32_t *sink) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const size_t stride = (size_t)gridDim.x * 256;
+  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    u32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = __builtin_nontemporal_load((const u32x4 *)(buf + i + u * stride));
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  for (; i < n16; i += stride) {
+    const u32x4 v = __builtin_nontemporal_load((const u32x4 *)(buf + i));
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, off, 64);
+  if ((threadIdx.x & 63) == 0) atomicXor(sink, acc);
+}
+
+hipError_t launch_stream_read(const void *buf, size_t bytes, uint32_t *sink, hipStream_t s) {
+  // 512 blocks of 4 waves: the fastest shape of a plain streaming read on this chip (256 blocks
+  // leave the memory system short of requests, 1024 and more add contention)
+  hipLaunchKernelGGL(k_stream_read, dim3(512), dim3(256), 0, s, (const uint4 *)buf, bytes / 16,
+                     sink);
+  return hipGetLastError();
+}
+
 }  // namespace kvprm

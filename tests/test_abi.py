@@ -167,6 +167,14 @@ def test_pack_weight_validation():
         assert e.value.status == kv.KVPRM_E_INVALID
 
 
+def test_stream_read_validation():
+    for args in [(0, 1024, FAKE), (FAKE, 1024, 0), (FAKE, 0, FAKE), (FAKE, 1000, FAKE),
+                 (FAKE + 8, 1024, FAKE), (FAKE, 1024, FAKE + 2)]:
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_stream_read(*args)
+        assert e.value.status == kv.KVPRM_E_INVALID
+
+
 def _lora(nl=2, rank=32, scale=1.0, drop=None, half=None):
     layers = []
     for l in range(nl):
@@ -276,6 +284,13 @@ def test_grad_and_steer_validation():
         assert e.value.status == kv.KVPRM_E_UNSUPPORTED
     finally:
         kv.kvprm_destroy(h8)
+    hw = kv.kvprm_create(_desc(weight_dtype="bf16", kv_dtype="bf16", hidden=16448))
+    try:  # the RMSNorm backward holds a candidate's hidden vector in one block's registers
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_workspace_size_grad(hw, kv.make_batch(1, FAKE, 4, FAKE))
+        assert e.value.status == kv.KVPRM_E_UNSUPPORTED
+    finally:
+        kv.kvprm_destroy(hw)
     h = kv.kvprm_create(_desc(weight_dtype="bf16", kv_dtype="bf16"))
     try:
         batch = kv.make_batch(2, FAKE, 4, FAKE, [10, 64])

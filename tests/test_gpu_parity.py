@@ -324,3 +324,24 @@ def test_debug_mode_rejects_out_of_range_page_ids():
         assert e.value.status == m.KVPRM_E_INVALID and "page_table" in m.kvprm_last_error()
     finally:
         m.kvprm_destroy(h)
+
+
+@pytest.mark.parametrize("nwords", [4, 4 * 1000003, 16 << 20])
+def test_stream_read_touches_every_word_once(nwords):
+    """The streaming-read diagnostic XORs every 32-bit word of the buffer into its sink: the
+    result equals the host's XOR of the buffer, so every word was read exactly once (a word read
+    twice or skipped changes the XOR unless it is zero, which the seeded values rule out), and a
+    second call restores the sink."""
+    _say(f"case: stream read, {nwords} words")
+    g = np.random.default_rng(77 + nwords)
+    host = g.integers(1, 2**32, size=nwords, dtype=np.uint64).astype(np.uint32)
+    buf = torch.from_numpy(host.view(np.int32)).cuda()
+    x = int(np.bitwise_xor.reduce(host))
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    kv().kvprm_stream_read(buf.data_ptr(), nwords * 4, sink.data_ptr(), st)
+    torch.cuda.synchronize()
+    assert int(sink.cpu().numpy().view(np.uint32)[0]) == x
+    kv().kvprm_stream_read(buf.data_ptr(), nwords * 4, sink.data_ptr(), st)
+    torch.cuda.synchronize()
+    assert int(sink.cpu().numpy().view(np.uint32)[0]) == 0
