@@ -236,7 +236,7 @@ def test_score_parity_7b_two_layers_bf16():
 
 @pytest.mark.parametrize("B", [9, 17, 40, 64])
 def test_score_parity_batch_sizes_bf16(B):
-    """One, two, four, six and eight operand column tiles (fused and split-K projections)."""
+    """One, two, four, six and eight operand column tiles (per-wave and shared-operand kernels)."""
     _say(f"case: score 7B shape, 2 layers, bf16, B={B}")
     import dataclasses
     shape = dataclasses.replace(synth.B7, num_layers=2)
