@@ -685,6 +685,138 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   }
 }
 
+// Gate/up + SwiGLU for larger batches (NT >= 4 column tiles). There every input block brings
+// NT KiB of operand for 2 KiB of gate/up weights, and k_gemv_fused, whose waves split the input
+// range, reads each operand tile from L2 once per wave. Here the waves of a block own whole row
+// tiles over the full input range instead (waves 0 .. WPB/2 - 1 gate tiles t0 + w, the others
+// the matching up tiles) and share every input block's operand tiles through LDS, read from L2
+// once per block. Batches of U input blocks are double buffered: while the matrix cores work on
+// batch i (operand from one LDS buffer, weights in registers), batch i+1's operand tiles go into
+// the other buffer and batch i+2's loads are issued. Each output is a complete sum over the
+// input (added in a different order than k_gemv_fused's); the up waves hand their sums to the
+// gate waves through LDS for the SwiGLU epilogue.
+template <int NT, int WPB, int U>
+__global__ __launch_bounds__(64 * WPB) void k_gateup_wide(FusedArgs a) {
+  constexpr int NG = NT / 2;         // candidate groups of 16
+  constexpr int HALF = WPB / 2;      // gate/up tile pairs per block
+  constexpr int PER = U * NT / WPB;  // operand pieces per thread and batch
+  static_assert(PER * WPB == U * NT, "operand batch split evenly over the block");
+  static_assert(2 * U * NT >= HALF * NG * 4, "the up sums fit in the operand buffers");
+  __shared__ uint4 op_s[2][U * NT * 64];
+  __shared__ float part_s[64 * WPB];
+  __shared__ float inv_s[64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int B = a.B;
+  const int ntf = a.F / 16;
+  const bool up = wave >= HALF;
+  const int pair = (int)blockIdx.x * HALF + (up ? wave - HALF : wave);
+  const bool own = pair < ntf;
+  const int tl = own ? pair : ntf - 1;  // past the end: repeat the last tile (results unused)
+  const size_t kstride = (size_t)ntf * 64;
+  const uint4 *wp = (const uint4 *)a.w[up ? 1 : 0] + (size_t)tl * 64 + lane;
+  const int nbat = (a.K >> 5) / U;  // the launcher guarantees K / 32 % U == 0
+  RmsLoads rl;
+  rms_load<64 * WPB>(a.ss, a.nss, B, rl);
+  floatx4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  uint4 wa[U], wb[U];
+  u32x4 ov[PER];
+  auto load_w = [&](int bat, uint4(&w)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) w[u] = ld_stream(&wp[(size_t)(bat * U + u) * kstride]);
+  };
+  // (the staging registers are plain vectors passed explicitly: as uint4 captured by reference
+  // they were kept in scratch memory)
+  auto load_op = [&](int bat, u32x4(&o)[PER]) {  // operand [K/32][NT][64]: a batch is U * NT * 64
+    const u32x4 *src = (const u32x4 *)a.act + (size_t)bat * U * NT * 64 + threadIdx.x;  // pieces
+#pragma unroll
+    for (int i = 0; i < PER; ++i) o[i] = src[i * 64 * WPB];
+  };
+  auto store_op = [&](int buf, const u32x4(&o)[PER]) {
+    u32x4 *dst = (u32x4 *)&op_s[buf][0] + threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) dst[i * 64 * WPB] = o[i];
+  };
+  auto mma = [&](int buf, const uint4(&w)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = mfma16(w[u], op_s[buf][(u * NT + t) * 64 + lane], acc[t]);
+  };
+  // batch i's operand is loaded into registers one batch before it is stored to LDS, and its
+  // weights two batches before they are used, so that each load has a whole batch of products
+  // and a barrier to arrive
+  load_op(0, ov);
+  store_op(0, ov);
+  load_w(0, wa);
+  if (nbat > 1) {
+    load_op(1, ov);
+    load_w(1, wb);
+  }
+  __syncthreads();
+  for (int bat = 0; bat < nbat; bat += 2) {  // block-uniform trip counts and barriers
+    mma(0, wa);
+    if (bat + 1 < nbat) store_op(1, ov);  // buffer 1 was last read before the previous barrier
+    if (bat + 2 < nbat) {
+      load_op(bat + 2, ov);
+      load_w(bat + 2, wa);
+    }
+    __syncthreads();
+    if (bat + 1 >= nbat) break;
+    mma(1, wb);
+    if (bat + 2 < nbat) store_op(0, ov);
+    if (bat + 3 < nbat) {
+      load_op(bat + 3, ov);
+      load_w(bat + 3, wb);
+    }
+    __syncthreads();
+  }
+  // adapter tail: B_seg (scale * A_seg u) of this wave's segment, operands from L2
+  const int seg = up ? 1 : 0;
+  if (a.tkb > 0 && a.tw[seg]) {
+    const uint4 *bw = (const uint4 *)a.tw[seg] + (size_t)tl * 64 + lane;
+    const uint4 *tp = a.tact + (size_t)seg * a.tstride + lane;
+    for (int kb = 0; kb < a.tkb; ++kb) {
+      const uint4 av = ld_stream(&bw[(size_t)kb * kstride]);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = mfma16(av, tp[((size_t)kb * NT + t) * 64], acc[t]);
+    }
+  }
+  // hi + lo per candidate group; the up waves leave theirs in LDS (the operand buffers are free:
+  // the last barrier of the loop follows their last read)
+  float4 *xch = (float4 *)&op_s[0][0];  // [HALF][NG][64]
+  if (up) {
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi)
+      xch[((wave - HALF) * NG + gi) * 64 + lane] =
+          make_float4(acc[gi][0] + acc[gi + NG][0], acc[gi][1] + acc[gi + NG][1],
+                      acc[gi][2] + acc[gi + NG][2], acc[gi][3] + acc[gi + NG][3]);
+  }
+  rms_finish<64 * WPB>(a.ss, a.nss, B, a.H, a.eps, rl, part_s, inv_s);  // has barriers
+  if (up || !own) return;
+  const int n = lane & 15, cq = lane >> 4;
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi) {
+    const int cand = 16 * gi + n;
+    if (cand >= B) continue;
+    const float inv = inv_s[cand];
+    const float4 uvv = xch[(wave * NG + gi) * 64 + lane];
+    const float uv4[4] = {uvv.x, uvv.y, uvv.z, uvv.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int f = tl * 16 + 4 * cq + i;
+      const float gv = (acc[gi][i] + acc[gi + NG][i]) * inv;
+      const float uv = uv4[i] * inv;
+      store_operand(a.op, a.NT, a.Bp, f, cand, gv / (1.0f + expf(-gv)) * uv);
+      if (a.save) {
+        a.save[(size_t)cand * 2 * a.F + f] = gv;
+        a.save[(size_t)cand * 2 * a.F + a.F + f] = uv;
+      }
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void k_pack_weight(const uint4 *src, uint4 *dst, int64_t rows,
                                                      int64_t K) {
   const int64_t ngroups = rows * K / 8;
@@ -1487,12 +1619,24 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
   a.nseg = 2;
   a.op = w.opD;
   const dim3 grid(dm.F / 16);
+  constexpr int WW = 8, UW = 4;  // waves and batch depth of the shared-operand kernel
+  const dim3 wgrid((dm.F / 16 + WW / 2 - 1) / (WW / 2));
+  const bool wide = (dm.H / 32) % UW == 0;
   switch (p.nt) {
     case 1: hipLaunchKernelGGL((k_gemv_fused<2, 1, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_gemv_fused<2, 2, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_gemv_fused<2, 4, 4, 2, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
-    case 6: hipLaunchKernelGGL((k_gemv_fused<2, 6, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((k_gemv_fused<2, 8, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
+    case 4:
+      if (wide) hipLaunchKernelGGL((k_gateup_wide<4, WW, UW>), wgrid, dim3(64 * WW), 0, s, a);
+      else hipLaunchKernelGGL((k_gemv_fused<2, 4, 4, 2, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
+      break;
+    case 6:
+      if (wide) hipLaunchKernelGGL((k_gateup_wide<6, WW, UW>), wgrid, dim3(64 * WW), 0, s, a);
+      else hipLaunchKernelGGL((k_gemv_fused<2, 6, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
+      break;
+    case 8:
+      if (wide) hipLaunchKernelGGL((k_gateup_wide<8, WW, UW>), wgrid, dim3(64 * WW), 0, s, a);
+      else hipLaunchKernelGGL((k_gemv_fused<2, 8, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
