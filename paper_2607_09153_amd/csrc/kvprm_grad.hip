@@ -596,30 +596,36 @@ __global__ __launch_bounds__(64 * W) void k_attn_bwd_mx(AttnBwdArgs a) {
         a.dq_part[((hb + 4 * c + i) * a.nch + chunk) * D + 16 * nb + n] = dq[nb][i] * sc;
 }
 
-// dq of every head (chunk partials in order, then the own-key term), the rotary backward of
+// dq of every head (the own-key term, then the chunk partials: four groups of consecutive
+// chunks, each added in order by its own threads, the groups in order), the rotary backward of
 // dq and dk_self (the transposed rotation by the same angles), and the stacked d vector of the
 // q/k/v products: rows [0, nq d) dq, then n_kv d of dk, then n_kv d of dv; layout
 // [row][kDPad].
 template <int D>
-__global__ __launch_bounds__(D / 2) void k_attn_bwd_merge(const float *dq_part, int nch,
+__global__ __launch_bounds__(2 * D) void k_attn_bwd_merge(const float *dq_part, int nch,
                                                           const int32_t *lengths, int CP,
                                                           const float *dq_self,
                                                           const float *dk_self,
                                                           const float *dv_self, const float *rope,
                                                           int nq, int nkv, int B, float *dqkv) {
-  const int b = blockIdx.x, h = blockIdx.y, i = threadIdx.x;  // h < nq: q-head; else kv-head
-  constexpr int HD = D / 2;
+  constexpr int HD = D / 2, NGRP = 4;  // threads: NGRP groups of HD (dims i and i + HD)
+  __shared__ float red_s[NGRP][2][HD];
+  const int b = blockIdx.x, h = blockIdx.y;  // h < nq: q-head; else kv-head (block-uniform)
+  const int i = threadIdx.x % HD, grp = threadIdx.x / HD;
   const float cs = rope[((size_t)b * HD + i) * 2], sn = rope[((size_t)b * HD + i) * 2 + 1];
   float y1, y2;
   size_t row;
   if (h < nq) {
+    // chunk partials: group grp adds its quarter of the chunks in order, eight loads in flight;
+    // then the quarters are added in group order
     const int L = lengths[b];
     const int nc = ((L + kPage - 1) / kPage + CP - 1) / CP;
-    y1 = dq_self[((size_t)b * nq + h) * D + i];
-    y2 = dq_self[((size_t)b * nq + h) * D + i + HD];
+    const int per = (nc + NGRP - 1) / NGRP;
+    const int c0 = min(nc, grp * per), c1 = min(nc, c0 + per);
     const float *pp = dq_part + ((size_t)b * nq + h) * nch * D;
-    int c = 0;
-    for (; c + 8 <= nc; c += 8) {  // eight partials in flight, added in chunk order
+    float a1 = 0.f, a2 = 0.f;
+    int c = c0;
+    for (; c + 8 <= c1; c += 8) {
       float u1[8], u2[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -628,15 +634,28 @@ __global__ __launch_bounds__(D / 2) void k_attn_bwd_merge(const float *dq_part, 
       }
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        y1 += u1[k];
-        y2 += u2[k];
+        a1 += u1[k];
+        a2 += u2[k];
       }
     }
-    for (; c < nc; ++c) {
-      y1 += pp[(size_t)c * D + i];
-      y2 += pp[(size_t)c * D + i + HD];
+    for (; c < c1; ++c) {
+      a1 += pp[(size_t)c * D + i];
+      a2 += pp[(size_t)c * D + i + HD];
+    }
+    red_s[grp][0][i] = a1;
+    red_s[grp][1][i] = a2;
+    __syncthreads();
+    if (grp != 0) return;
+    y1 = dq_self[((size_t)b * nq + h) * D + i];
+    y2 = dq_self[((size_t)b * nq + h) * D + i + HD];
+#pragma unroll
+    for (int k = 0; k < NGRP; ++k) {
+      y1 += red_s[k][0][i];
+      y2 += red_s[k][1][i];
     }
     row = (size_t)h * D;
+  } else if (grp != 0) {
+    return;
   } else if (h < nq + nkv) {
     const int j = h - nq;
     y1 = dk_self[((size_t)b * nkv + j) * D + i];
@@ -782,11 +801,11 @@ hipError_t launch_backward(const Dims &dm, const Plan &p, const Workspace &w, co
         hipLaunchKernelGGL((k_attn_bwd_mx<128, WB>), grid, dim3(64 * WB), 0, s, a);
       KVPRM_CHECK();
       if (D == 64)
-        hipLaunchKernelGGL(k_attn_bwd_merge<64>, dim3(B, nq + 2 * nkv), dim3(32), 0, s,
+        hipLaunchKernelGGL(k_attn_bwd_merge<64>, dim3(B, nq + 2 * nkv), dim3(128), 0, s,
                            sv.dq_part, p.nch, lengths, CP, sv.dq_self, sv.dk_self, sv.dv_self,
                            w.rope, nq, nkv, B, sv.dqkv);
       else
-        hipLaunchKernelGGL(k_attn_bwd_merge<128>, dim3(B, nq + 2 * nkv), dim3(64), 0, s,
+        hipLaunchKernelGGL(k_attn_bwd_merge<128>, dim3(B, nq + 2 * nkv), dim3(256), 0, s,
                            sv.dq_part, p.nch, lengths, CP, sv.dq_self, sv.dk_self, sv.dv_self,
                            w.rope, nq, nkv, B, sv.dqkv);
       KVPRM_CHECK();
