@@ -696,7 +696,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
 // input (added in a different order than k_gemv_fused's); the up waves hand their sums to the
 // gate waves through LDS for the SwiGLU epilogue.
 template <int NT, int WPB, int U>
-__global__ __launch_bounds__(64 * WPB) void k_gateup_wide(FusedArgs a) {
+__global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
   constexpr int NG = NT / 2;         // candidate groups of 16
   constexpr int HALF = WPB / 2;      // gate/up tile pairs per block
   constexpr int PER = U * NT / WPB;  // operand pieces per thread and batch
