@@ -1570,7 +1570,7 @@ static hipError_t launch_resid_fused(const Plan &p, const FusedArgs &a, int tile
     case 2: hipLaunchKernelGGL((k_gemv_fused<1, 2, 8, 4, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
     case 4: hipLaunchKernelGGL((k_gemv_fused<1, 4, 8, 2, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
     case 6: hipLaunchKernelGGL((k_gemv_fused<1, 6, 8, 1, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((k_gemv_fused<1, 8, 8, 1, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_gemv_fused<1, 8, 16, 1, EPI_RESID>), grid, dim3(64 * 16), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
