@@ -76,6 +76,36 @@ def time_attention(kv, dw, h, batch, ws, n, reps):
     return timed(partials), timed(step)
 
 
+def time_graph(kv, h, cache, batch, readout, ws, n, scores, steps):
+    """One kvprm_score call captured in a HIP graph (the library enqueues kernels only: no
+    allocation, synchronisation or memset), replayed `steps` times between two synchronisations:
+    the per-call time a caller that replays captured calls sees."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+
+    def call():
+        kv.kvprm_score(h, cache, batch, readout, ws.data_ptr(), n, scores.data_ptr(), 0,
+                       torch.cuda.current_stream().cuda_stream)
+
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call()
+    g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    del g
+    return {"ms_per_call": ms, "scores_per_s": scores.numel() / (ms * 1e-3)}
+
+
 def time_lora(kv, dw, h, batch, rank, steps, warmup):
     """Whole scoring calls with the base weights and an unmerged adapter of this rank on every
     projection (kvprm_score_lora): the same workload, K calls between two synchronisations."""
@@ -351,6 +381,8 @@ def main():
     ms = dt * 1e3 / args.steps
     _log(f"timed {args.steps} steps: {ms:.3f} ms/step")
 
+    graph = time_graph(kv, h, cache, batch, readout, ws, n, scores, args.steps)
+    _log(f"graph replay: {graph['ms_per_call']:.3f} ms/call")
     lora = None
     if args.lora_rank > 0:
         lora = time_lora(kv, dw, h, batch, args.lora_rank, args.steps, args.warmup)
@@ -412,6 +444,7 @@ def main():
         "copy_reference_gbps": copy_gbps,
         "read_reference_gbps": read_gbps,
     }
+    out["graph_replay"] = graph
     if lora is not None:
         out["lora_readout"] = lora
     if depth is not None:
