@@ -121,6 +121,16 @@ def test_cache_gradient_7b_two_layers():
     _grad_case(w)
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_cache_gradient_sixteen_heads_per_kv_head(head_dim):
+    """g = 16 (the most q-heads per kv-head the kernels take): every column of the matrix-core
+    products is a head."""
+    _say(f"case: cache gradient, 16 q-heads over 1 kv-head, d_h = {head_dim}")
+    shape = synth.ModelShape(2, 512, 16, 1, head_dim, 1024)
+    w = synth.make_workload("custom", shape=shape, lengths=[333, 16, 1], seed=404 + head_dim)
+    _grad_case(w)
+
+
 def test_kv_steering_matches_the_oracle():
     _say("case: KV steering, 3 steps, small bf16 shape")
     w = synth.make_workload("custom", shape=SMALL, lengths=[150, 33, 64], seed=403)
