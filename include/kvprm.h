@@ -11,8 +11,10 @@
  * Conventions for every entry point
  *   - All tensor pointers are DEVICE pointers unless the name ends in _host. The caller owns
  *     every buffer; the library never frees, never writes the cache (except kvprm_steer, which
- *     exists to update it), the page table or the weights, and never allocates device memory inside kvprm_score / kvprm_attention (the
- *     caller passes a workspace sized by kvprm_workspace_size).
+ *     exists to update it), the page table or the weights, and never allocates device memory
+ *     in any call (the caller passes a workspace sized by the matching kvprm_workspace_size*
+ *     query), so every scoring call can be captured in a HIP graph (no memset nodes either;
+ *     not in the KVPRM_DEBUG mode below, which synchronises).
  *   - Calls only enqueue work on `stream` (a hipStream_t; NULL = the null stream) and never
  *     synchronise the host. Outputs are valid once the stream reaches that point.
  *   - Arguments are validated on the host before anything is enqueued; on any error nothing
