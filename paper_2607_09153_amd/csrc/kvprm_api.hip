@@ -322,19 +322,16 @@ static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
     LoraTail t{{b0, b1, b2}, (b0 || b1 || b2) ? tkb : 0};
     return t;
   };
-  HIP_TRY(launch_init_mx(dm, p, w, wts->verify_embed, wts->layers[0].attn_norm, b->lengths, s),
+  HIP_TRY(launch_init_mx(dm, p, w, wts->verify_embed, wts->layers[0].attn_norm, b->lengths, s,
+                         sv ? sv->x_in : nullptr),
           "init");
-  const size_t xb = (size_t)p.B * dm.H * sizeof(float);
   const size_t qd = (size_t)p.B * dm.nq * dm.d, kd = (size_t)p.B * dm.nkv * dm.d;
   for (int l = 0; l < dm.layers; ++l) {
     const kvprm_layer_weights &W = wts->layers[l];
     const void *gamma_next = l + 1 < dm.layers ? wts->layers[l + 1].attn_norm : nullptr;
     Workspace wl = w;  // with sv: q, k_self, v_self written to the layer's saved copies
     float *o_save = nullptr, *lse_save = nullptr, *gu_save = nullptr;
-    if (sv) {
-      HIP_TRY(hipMemcpyAsync(sv->x_in + (size_t)l * p.B * dm.H, w.x, xb, hipMemcpyDeviceToDevice,
-                             s),
-              "save");
+    if (sv) {  // (the residual stream entering the layer was saved by the previous epilogue)
       wl.q = sv->q + l * qd;
       wl.kself = sv->ks + l * kd;
       wl.vself = sv->vs + l * kd;
@@ -364,11 +361,9 @@ static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
       const void *a_o[3] = {lora->layers[l].o.a, nullptr, nullptr};
       HIP_TRY(launch_lora_a(dm, p, w, LORA_O, a_o, lora->scale, w.opO, s), "output adapter");
     }
-    HIP_TRY(launch_oproj_fused(dm, p, w, W.wo, W.ffn_norm, t_o, s), "output projection");
-    if (sv)
-      HIP_TRY(hipMemcpyAsync(sv->x_mid + (size_t)l * p.B * dm.H, w.x, xb,
-                             hipMemcpyDeviceToDevice, s),
-              "save");
+    HIP_TRY(launch_oproj_fused(dm, p, w, W.wo, W.ffn_norm, t_o, s,
+                               sv ? sv->x_mid + (size_t)l * p.B * dm.H : nullptr),
+            "output projection");
     if (lora && t_gu.tkb) {
       const void *a_gu[3] = {lora->layers[l].gate.a, lora->layers[l].up.a, nullptr};
       HIP_TRY(launch_lora_a(dm, p, w, LORA_GU, a_gu, lora->scale, w.opA, s), "gate/up adapter");
@@ -379,7 +374,10 @@ static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
       const void *a_d[3] = {lora->layers[l].down.a, nullptr, nullptr};
       HIP_TRY(launch_lora_a(dm, p, w, LORA_DOWN, a_d, lora->scale, w.opD, s), "down adapter");
     }
-    HIP_TRY(launch_down_fused(dm, p, w, W.w_down, gamma_next, t_d, s), "down projection");
+    HIP_TRY(launch_down_fused(dm, p, w, W.w_down, gamma_next, t_d, s,
+                              sv && l + 1 < dm.layers ? sv->x_in + (size_t)(l + 1) * p.B * dm.H
+                                                      : nullptr),
+            "down projection");
   }
   HIP_TRY(launch_head(dm, p, w, wts->final_norm, wts->reward_w, wts->reward_b, scores, logits, s),
           "reward head");

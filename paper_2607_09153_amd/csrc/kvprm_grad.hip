@@ -793,7 +793,7 @@ hipError_t launch_backward(const Dims &dm, const Plan &p, const Workspace &w, co
       a.lse = lse;
       a.Dh = sv.Dh;
       a.dq_part = sv.dq_part;
-      constexpr int WB = 4;  // waves (chunks) per block of the matrix-core backward
+      constexpr int WB = 8;  // waves (chunks) per block of the matrix-core backward
       const dim3 grid((chunks + WB - 1) / WB, B, nkv);
       if (D == 64)
         hipLaunchKernelGGL((k_attn_bwd_mx<64, WB>), grid, dim3(64 * WB), 0, s, a);

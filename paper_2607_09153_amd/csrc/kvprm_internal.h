@@ -147,8 +147,10 @@ hipError_t launch_gemv(const Dims &dm, const Plan &p, const GemvSegs &segs, int 
                        int ksplit, const float *in, const void *gamma, const float *ss,
                        float *part, hipStream_t s);
 // matrix-core pipeline (bf16 weights)
+// xsave (optional): a copy of the residual stream x as initialised
 hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *ev,
-                          const void *gamma0, const int32_t *lengths, hipStream_t s);
+                          const void *gamma0, const int32_t *lengths, hipStream_t s,
+                          float *xsave = nullptr);
 hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
                          const void *wk, const void *wv, const LoraTail &tail, hipStream_t s);
 // scale * A u of one projection group's adapters into the operand slots w.topd (slot i =
@@ -157,13 +159,16 @@ hipError_t launch_lora_a(const Dims &dm, const Plan &p, const Workspace &w, int 
                          const void *const a[3], float scale, const uint16_t *act, hipStream_t s);
 // fused projections: no split-K partials, the element-wise step after the output, gate/up and
 // down projections runs in the epilogue
+// xsave (optional, output and down projections): a copy of the updated residual stream
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
-                              const void *gamma_ffn, const LoraTail &tail, hipStream_t s);
+                              const void *gamma_ffn, const LoraTail &tail, hipStream_t s,
+                              float *xsave = nullptr);
 hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wg,
                                const void *wu, const LoraTail &tail, hipStream_t s,
                                float *save_gu = nullptr);
 hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
-                             const void *gamma_next, const LoraTail &tail, hipStream_t s);
+                             const void *gamma_next, const LoraTail &tail, hipStream_t s,
+                             float *xsave = nullptr);
 hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, const char *kp,
                           const char *vp, const float *ksc, const float *vsc,
                           const int32_t *page_table, const int32_t *lengths, const GroupTable &gt,

@@ -136,7 +136,7 @@ __global__ __launch_bounds__(256) void k_init_mx(float *x, float *ss, int RB, co
                                                  const void *gamma0, int wdt, int B, int H,
                                                  uint16_t *opA, int NT, int Bp,
                                                  const int32_t *lengths, int kq, float theta,
-                                                 int d, float *rope) {
+                                                 int d, float *rope, float *xsave) {
   __shared__ float red[4];
   const int r0 = blockIdx.x * RB;
   const int nr = min(RB, H - r0);
@@ -148,6 +148,7 @@ __global__ __launch_bounds__(256) void k_init_mx(float *x, float *ss, int RB, co
     const float u = v * ld_w(gamma0, r, wdt);
     for (int b = 0; b < B; ++b) {
       x[(size_t)b * H + r] = v;
+      if (xsave) xsave[(size_t)b * H + r] = v;
       store_operand(opA, NT, Bp, r, b, u);
     }
   }
@@ -471,6 +472,7 @@ struct FusedArgs {
   int B;
   // epilogue
   float *x;                  // residual [B][H] (RESID)
+  float *xsave;              // a copy of the updated residual (RESID, may be null)
   int H;
   float *ss;                 // sums of squares: written per 16-row tile (RESID), read (SWIGLU)
   int nss;
@@ -644,6 +646,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
       if (cand_ok) {
         xv = a.x[(size_t)b * a.H + r] + y[0][i];
         a.x[(size_t)b * a.H + r] = xv;
+        if (a.xsave) a.xsave[(size_t)b * a.H + r] = xv;
         if (a.gamma) store_operand(a.op, a.NT, a.Bp, r, b, xv * ld_bf16(a.gamma, r));
       }
       sq += xv * xv;
@@ -1401,9 +1404,10 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
 }
 
 hipError_t launch_init_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *ev,
-                          const void *gamma0, const int32_t *lengths, hipStream_t s) {
+                          const void *gamma0, const int32_t *lengths, hipStream_t s,
+                          float *xsave) {
   hipLaunchKernelGGL(k_init_mx, dim3(p.nss), dim3(256), 0, s, w.x, w.ss, p.rb, ev, gamma0, dm.wdt,
-                     p.B, dm.H, w.opA, p.nt, p.bp, lengths, p.kq, dm.theta, dm.d, w.rope);
+                     p.B, dm.H, w.opA, p.nt, p.bp, lengths, p.kq, dm.theta, dm.d, w.rope, xsave);
   return hipGetLastError();
 }
 
@@ -1595,8 +1599,10 @@ static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, i
 }
 
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
-                              const void *gamma_ffn, const LoraTail &tail, hipStream_t s) {
+                              const void *gamma_ffn, const LoraTail &tail, hipStream_t s,
+                              float *xsave) {
   FusedArgs a = fused_args(dm, p, w, dm.nq * dm.d, w.opO);
+  a.xsave = xsave;
   set_tail(a, p, w, tail);
   a.w[0] = wo;
   a.seg_rows[0] = dm.H;
@@ -1643,8 +1649,10 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
 }
 
 hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
-                             const void *gamma_next, const LoraTail &tail, hipStream_t s) {
+                             const void *gamma_next, const LoraTail &tail, hipStream_t s,
+                             float *xsave) {
   FusedArgs a = fused_args(dm, p, w, dm.F, w.opD);
+  a.xsave = xsave;
   set_tail(a, p, w, tail);
   a.w[0] = wd;
   a.seg_rows[0] = dm.H;
