@@ -13,8 +13,7 @@ P(+) = softmax([z_-, z_+]) taken at the "+" entry. Everything runs in float64
 on exactly decoded inputs (fp32, bf16 and e4m3 * scale all convert to float64
 without rounding).
 
-Readings where the paper is silent (each is listed with its reason in the
-design notes of the repository):
+Readings where the paper is silent:
   * the decoder block is the standard pre-norm one: RMSNorm -> Q/K/V ->
     rotary -> grouped-query attention -> output projection -> residual;
     RMSNorm -> SwiGLU -> residual; a final RMSNorm; no biases, no q/k norm;
