@@ -281,7 +281,19 @@ def cpu_baseline(w, layers_sample, min_seconds=10.0):
             "sample": (f"{w.name}: all {w.batch} candidates through the first {layers_sample} of "
                        f"{s.num_layers} layers, {reps} passes in {dt:.1f} s (fp64 numpy, inputs "
                        f"pre-generated), scaled by {s.num_layers}/{layers_sample} to one full "
-                       f"call")}
+                       f"call"),
+            "host": {"logical_cpus": os.cpu_count(), "cpu_model": _cpu_model()}}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_ragged_32k_traffic.txt")
