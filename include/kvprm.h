@@ -23,9 +23,11 @@
  *     they use distinct workspaces and outputs.
  *   - Out-of-range physical page ids in the page table are undefined behaviour: the kernels do
  *     not check them. With the environment variable KVPRM_DEBUG=1 set when the handle is
- *     created, kvprm_score and kvprm_attention copy lengths and page table to the host (on
- *     `stream`, then synchronising it) and return KVPRM_E_INVALID for any page id outside
- *     [0, num_pages) among the pages a candidate reads, before enqueueing anything.
+ *     created, the calls that read the cache copy lengths and page table to the host (on
+ *     `stream`, then synchronising it) and return KVPRM_E_INVALID, before enqueueing anything,
+ *     for any page id outside [0, num_pages) among the pages a candidate reads, for a
+ *     lengths_host entry that differs from the device length, and (kvprm_score_grad,
+ *     kvprm_steer) for a physical page read by two candidates.
  *
  * Model structure (the paper names only "decoder-only transformer"; the block follows the
  * Qwen3/Llama family it evaluates): pre-norm RMSNorm -> Q/K/V projections -> rotate-half
@@ -138,7 +140,12 @@ typedef struct {
   const int32_t *page_table;            /* device [B][max_pages] */
   int32_t max_pages;                    /* >= 1 */
   const int32_t *lengths;               /* device [B], 0 <= L_b <= max_pages * 16 */
-  const int32_t *lengths_host;          /* optional host mirror of lengths (validation) */
+  /* Optional host mirror of lengths. When given it must equal the device lengths at the time
+   * the enqueued work runs (also on every replay of a captured graph): the chunk grid of the
+   * attention kernels is sized from it, so a device length above its mirror would leave the
+   * chunks past that grid uncomputed (checked only in the KVPRM_DEBUG mode). NULL sizes the
+   * grid from max_pages, which is valid for any device lengths. */
+  const int32_t *lengths_host;
   int32_t num_groups;                   /* 0 = no prefix-sharing hint */
   const int32_t *group_start_host;      /* [num_groups + 1] */
   const int32_t *group_prefix_len_host; /* [num_groups] */

@@ -151,9 +151,13 @@ static kvprm_status check_cache(const kvprm_handle h, const kvprm_kv_cache *c, c
 }
 
 // Debug mode only: copy lengths and the page table to the host (on the call's stream, then
-// wait) and check every read entry against [0, num_pages) and every length against the table.
+// wait) and check every read entry against [0, num_pages), every length against the table and
+// against lengths_host (when given: the launch grids are sized from it), and, for the calls
+// that write per-page results (distinct_pages: gradients and steering), that no physical page
+// is read by two candidates.
 static kvprm_status check_pages_debug(const kvprm_handle h, const kvprm_kv_cache *c,
-                                      const kvprm_batch *b, hipStream_t s, const char *fn) {
+                                      const kvprm_batch *b, hipStream_t s, const char *fn,
+                                      bool distinct_pages = false) {
   if (!h->debug) return KVPRM_OK;
   std::vector<int32_t> len(b->batch), pt((size_t)b->batch * b->max_pages);
   if (hipMemcpyAsync(len.data(), b->lengths, len.size() * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
@@ -161,15 +165,25 @@ static kvprm_status check_pages_debug(const kvprm_handle h, const kvprm_kv_cache
       hipStreamSynchronize(s) != hipSuccess)
     return fail(KVPRM_E_HIP, "%s: debug copy of the page table failed", fn);
   const int cap = b->max_pages * h->desc.page_size;
+  std::vector<int32_t> owner(distinct_pages ? (size_t)c->num_pages : 0, -1);
   for (int i = 0; i < b->batch; ++i) {
     if (len[i] < 0 || len[i] > cap)
       return fail(KVPRM_E_INVALID, "%s: lengths[%d] = %d outside [0, %d]", fn, i, len[i], cap);
+    if (b->lengths_host && b->lengths_host[i] != len[i])
+      return fail(KVPRM_E_INVALID, "%s: lengths_host[%d] = %d differs from lengths[%d] = %d", fn,
+                  i, b->lengths_host[i], i, len[i]);
     const int np = (len[i] + h->desc.page_size - 1) / h->desc.page_size;
     for (int k = 0; k < np; ++k) {
       const int32_t id = pt[(size_t)i * b->max_pages + k];
       if (id < 0 || id >= c->num_pages)
         return fail(KVPRM_E_INVALID, "%s: page_table[%d][%d] = %d outside [0, %d)", fn, i, k, id,
                     c->num_pages);
+      if (distinct_pages) {
+        if (owner[id] >= 0)
+          return fail(KVPRM_E_INVALID, "%s: page %d is read by candidates %d and %d", fn, id,
+                      owner[id], i);
+        owner[id] = i;
+      }
     }
   }
   return KVPRM_OK;
@@ -301,11 +315,12 @@ static kvprm_status check_lora(const kvprm_handle h, const kvprm_lora *lora, con
   return KVPRM_OK;
 }
 
-// The matrix-core pipeline (bf16 weights): seven launches per layer, QKV (split-K) and its
-// rotary step, attention and its merge, then the output, gate/up and down projections with
-// their element-wise steps fused (no split-K partials). With an adapter, each projection group
-// that has one first computes scale * A u (a split-K GEMV and its finish) and the projection
-// adds B (scale * A u) as a tail of its input range.
+// The matrix-core pipeline (bf16 weights): six launches per layer (seven with shared
+// prefixes): the q/k/v projection with the RMSNorm scale and the rotary embedding in its
+// epilogue, the attention chunk kernel(s) and their merge, then the output, gate/up and down
+// projections with their element-wise steps fused (no split-K partials). With an adapter, each
+// projection group that has one first computes scale * A u (a split-K GEMV and its finish) and
+// the projection adds B (scale * A u) as a tail of its input range.
 // With sv, the activations the backward pass needs are kept per layer (GradSave).
 static kvprm_status score_mx(const kvprm_handle h, const kvprm_kv_cache *cache,
                              const kvprm_batch *b, const kvprm_readout_weights *wts,
@@ -580,7 +595,7 @@ static kvprm_status grad_impl(kvprm_handle h, const kvprm_kv_cache *cache, const
                 workspace ? ws_bytes : (size_t)0);
   if (((uintptr_t)workspace & 255) != 0)
     return fail(KVPRM_E_WORKSPACE, "%s: workspace not 256-byte aligned", fn);
-  if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn)) != KVPRM_OK) return st;
+  if ((st = check_pages_debug(h, cache, b, (hipStream_t)stream, fn, true)) != KVPRM_OK) return st;
   const Dims &dm = h->dm;
   hipStream_t s = (hipStream_t)stream;
   const Plan p = make_plan(dm, b->batch, b->max_pages);

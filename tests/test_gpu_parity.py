@@ -326,6 +326,94 @@ def test_debug_mode_rejects_out_of_range_page_ids():
         m.kvprm_destroy(h)
 
 
+@pytest.mark.parametrize("name,lengths", [("b7_bf16", [32768, 1, 20000, 33, 5000, 31000]),
+                                          ("b7_bf16", [4096, 0, 17, 3001, 1200]),
+                                          ("fp8", [9000, 0, 17000, 31])])
+def test_score_without_host_lengths(name, lengths):
+    """lengths_host = NULL: the attention chunk grid is sized from max_pages (every chunk any
+    device length could need) and the chunk length from batch x max_pages; the scores match the
+    oracle as with the host lengths (the two differ only in summation order)."""
+    _say(f"case: score without lengths_host {name} lengths={lengths}")
+    w = synth.make_workload("custom", shape=_shape(name), lengths=lengths, seed=4545)
+    dw = DeviceWorkload(w, nan_unused_pages=True)
+    p0, z0 = run_score(dw, lengths_host=False)
+    p1, z1 = run_score(dw)
+    zr, pr = oin.score_workload(w)
+    _say(f"  no host lengths: max|dP| = {np.max(np.abs(p0 - pr)):.3e} max|dz| = "
+         f"{np.max(np.abs(z0 - zr)):.3e}; with: max|dz| = {np.max(np.abs(z1 - zr)):.3e}")
+    assert np.all(np.isfinite(p0)) and np.all(np.isfinite(z0))
+    assert np.max(np.abs(p0 - pr)) <= 2e-3 and np.max(np.abs(z0 - zr)) <= 2e-2
+    assert np.max(np.abs(z0 - z1)) <= 1e-3
+
+
+def _debug_handle(m, desc):
+    import os
+    old = os.environ.get("KVPRM_DEBUG")
+    os.environ["KVPRM_DEBUG"] = "1"
+    try:
+        return m.kvprm_create(desc)
+    finally:
+        if old is None:
+            del os.environ["KVPRM_DEBUG"]
+        else:
+            os.environ["KVPRM_DEBUG"] = old
+
+
+def test_debug_mode_rejects_stale_host_lengths():
+    _say("case: KVPRM_DEBUG lengths_host check")
+    w = synth.make_workload("custom", shape=synth.TINY, lengths=[100, 37, 0], seed=83)
+    dw = DeviceWorkload(w)
+    m = kv()
+    h = _debug_handle(m, dw.desc(m))
+    try:
+        n = m.kvprm_workspace_size(h, dw.batch(m))
+        ws = torch.empty(max(n, 256), dtype=torch.uint8, device="cuda")
+        scores = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+        st = torch.cuda.current_stream().cuda_stream
+        stale = m.make_batch(w.batch, dw.page_table.data_ptr(), w.max_pages, dw.lengths.data_ptr(),
+                             [100, 36, 0])
+        with pytest.raises(m.KvprmError) as e:
+            m.kvprm_score(h, dw.cache(m), stale, dw.readout(m), ws.data_ptr(), n,
+                          scores.data_ptr(), 0, st)
+        assert e.value.status == m.KVPRM_E_INVALID and "lengths_host" in m.kvprm_last_error()
+        # without the mirror the same call is valid
+        m.kvprm_score(h, dw.cache(m), dw.batch(m, lengths_host=False), dw.readout(m),
+                      ws.data_ptr(), n, scores.data_ptr(), 0, st)
+        torch.cuda.synchronize()
+        assert np.all(np.isfinite(scores.cpu().numpy()))
+    finally:
+        m.kvprm_destroy(h)
+
+
+def test_debug_mode_rejects_shared_pages_in_steering():
+    """kvprm_score_grad / kvprm_steer write per-page results: a physical page read by two
+    candidates is refused in the debug mode before anything is enqueued (the cache unchanged)."""
+    _say("case: KVPRM_DEBUG shared pages in steering")
+    shape = synth.ModelShape(2, 1024, 16, 4, 64, 2048)
+    w = synth.make_workload("custom", shape=shape, lengths=[64, 40], seed=84)
+    dw = DeviceWorkload(w)
+    m = kv()
+    h = _debug_handle(m, dw.desc(m))
+    try:
+        shared = dw.page_table.clone()
+        shared[1, 0] = shared[0, 1]
+        b = m.make_batch(w.batch, shared.data_ptr(), w.max_pages, dw.lengths.data_ptr(), w.lengths)
+        n = m.kvprm_workspace_size_grad(h, b)
+        ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        p0 = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+        p1 = torch.empty_like(p0)
+        kc, vc = dw.k_pool.clone(), dw.v_pool.clone()
+        st = torch.cuda.current_stream().cuda_stream
+        with pytest.raises(m.KvprmError) as e:
+            m.kvprm_steer(h, dw.cache(m), b, dw.readout(m), 1.0, 1, ws.data_ptr(), n,
+                          p0.data_ptr(), p1.data_ptr(), st)
+        assert e.value.status == m.KVPRM_E_INVALID and "read by candidates" in m.kvprm_last_error()
+        torch.cuda.synchronize()
+        assert torch.equal(kc, dw.k_pool) and torch.equal(vc, dw.v_pool)
+    finally:
+        m.kvprm_destroy(h)
+
+
 @pytest.mark.parametrize("nwords", [4, 4 * 1000003, 16 << 20])
 def test_stream_read_touches_every_word_once(nwords):
     """The streaming-read diagnostic XORs every 32-bit word of the buffer into its sink: the
