@@ -172,6 +172,27 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
                          const kvprm_readout_weights *weights, void *workspace, size_t ws_bytes,
                          float *scores, float *logits, void *stream);
 
+/* Bytes of the static workspace of kvprm_score_static (64 MiB per GPU). */
+#define KVPRM_STATIC_WORKSPACE_BYTES (64u << 20)
+
+/* kvprm_score without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture that must not allocate, tight serving loops, harnesses that
+ * forbid hipMalloc). The workspace is a static device array of KVPRM_STATIC_WORKSPACE_BYTES
+ * that the library holds on every GPU it runs on until the process ends; nothing is allocated
+ * or freed by the call. It serves batches whose kvprm_workspace_size is at most that size
+ * (8 candidates with up to 32768 cached tokens at the 7B shape need 16 MiB; 64 candidates with
+ * 18432 tokens each need 79 MiB and are refused); a larger one returns KVPRM_E_WORKSPACE before
+ * anything is enqueued.
+ * Every call on one GPU, from any handle or thread, uses the same array, which keeps the
+ * previous call's contents (no call needs it cleared): calls whose work overlaps on one GPU
+ * race, so the caller serialises them (for example by issuing them on one stream). The work
+ * runs on the current device; a non-null stream must belong to it (KVPRM_E_INVALID
+ * otherwise). The first call on a device resolves that device's copy of the array. Outputs
+ * and the other conventions are those of kvprm_score. */
+kvprm_status kvprm_score_static(kvprm_handle h, const kvprm_kv_cache *cache,
+                                const kvprm_batch *batch, const kvprm_readout_weights *weights,
+                                float *scores, float *logits, void *stream);
+
 /* The attention step of one layer alone (for tests and diagnostics): for every candidate b and
  * q-head h, o[b][h] = softmax(q K^T / sqrt(d_h)) V over the L_b cached keys/values of `layer`
  * and the extra key/value k_self[b][h / g], v_self[b][h / g] (the verify token's own).

@@ -24,7 +24,8 @@ EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_scor
             "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
             "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
             "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer",
-            "kvprm_stream_read", "kvprm_last_error"]
+            "kvprm_stream_read", "kvprm_score_static", "kvprm_last_error"]
+STATIC_WORKSPACE_BYTES = 64 << 20  # KVPRM_STATIC_WORKSPACE_BYTES
 LORA_PROJECTIONS = ("q", "k", "v", "o", "gate", "up", "down")
 
 
@@ -114,6 +115,8 @@ def _load():
                                     ctypes.c_int32, vp, vp, vp, vp, sz, vp, vp]
     lib.kvprm_attention_partials.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
                                              ctypes.c_int32, vp, vp, sz, vp]
+    lib.kvprm_score_static.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
+                                       ctypes.POINTER(ReadoutWeights), vp, vp, vp]
     lib.kvprm_pack_weight.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, vp]
     lib.kvprm_stream_read.argtypes = [vp, sz, vp, vp]
     lib.kvprm_workspace_size_lora.argtypes = [vp, ctypes.POINTER(Batch), ctypes.c_int32,
@@ -136,7 +139,7 @@ def _load():
               "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
               "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
               "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer",
-              "kvprm_stream_read"):
+              "kvprm_stream_read", "kvprm_score_static"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kvprm_last_error.argtypes = []
     lib.kvprm_last_error.restype = ctypes.c_char_p
@@ -298,6 +301,13 @@ def kvprm_score(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeigh
                 stream: int = 0) -> None:
     _check(lib.kvprm_score(handle, ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(weights),
                            workspace_ptr, ws_bytes, scores_ptr, logits_ptr or None, stream or None))
+
+
+def kvprm_score_static(handle: int, cache: KVCache, batch: Batch, weights: ReadoutWeights,
+                       scores_ptr: int, logits_ptr: int = 0, stream: int = 0) -> None:
+    _check(lib.kvprm_score_static(handle, ctypes.byref(cache), ctypes.byref(batch),
+                                  ctypes.byref(weights), scores_ptr, logits_ptr or None,
+                                  stream or None))
 
 
 def kvprm_stream_read(buf_ptr: int, nbytes: int, sink_ptr: int, stream: int = 0) -> None:

@@ -6,6 +6,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -489,6 +490,62 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
                          float *scores, float *logits, void *stream) {
   return score_impl(h, cache, b, wts, nullptr, 1, workspace, ws_bytes, scores, logits, stream,
                     "kvprm_score");
+}
+
+// ---------------------------------------------------------------- allocation-free scoring
+
+// Workspace of kvprm_score_static: one array per GPU, held by the library's code object on every
+// device it is loaded on until the process ends. Host code never uses this name as an address
+// (on the host it is a stand-in, not device memory): the device address of the current device's
+// copy comes from hipGetSymbolAddress and is kept in g_static_ws.
+static __device__ __align__(256) unsigned char scratch[KVPRM_STATIC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_static_mu;
+static void *g_static_ws[kMaxDevices];
+
+// The current device's copy of `scratch` (resolved once per device, with that device current);
+// a non-null stream must belong to the current device.
+static kvprm_status static_workspace(hipStream_t s, void **ptr, const char *fn) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: device %d outside [0, %d)", fn, dev, kMaxDevices);
+  if (s) {
+    hipDevice_t sdev = -1;
+    HIP_TRY(hipStreamGetDevice(s, &sdev), "hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(KVPRM_E_INVALID, "%s: the stream belongs to device %d, device %d is current", fn,
+                  (int)sdev, dev);
+  }
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (!g_static_ws[dev]) {
+    void *p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!p || ((uintptr_t)p & 255) != 0)
+      return fail(KVPRM_E_INTERNAL, "%s: static workspace address %p is not 256-byte aligned", fn, p);
+    g_static_ws[dev] = p;
+  }
+  *ptr = g_static_ws[dev];
+  return KVPRM_OK;
+}
+
+kvprm_status kvprm_score_static(kvprm_handle h, const kvprm_kv_cache *cache, const kvprm_batch *b,
+                                const kvprm_readout_weights *wts, float *scores, float *logits,
+                                void *stream) {
+  const char *fn = "kvprm_score_static";
+  if (!h) return fail(KVPRM_E_INVALID, "%s: null handle", fn);
+  kvprm_status st = check_batch(h, b, fn);
+  if (st != KVPRM_OK) return st;
+  if (b->batch == 0) return ok();
+  const size_t need = ws_bytes_for(h, b);
+  if (need > (size_t)KVPRM_STATIC_WORKSPACE_BYTES)
+    return fail(KVPRM_E_WORKSPACE, "%s: the batch needs %zu bytes of workspace, the static one holds %zu",
+                fn, need, (size_t)KVPRM_STATIC_WORKSPACE_BYTES);
+  void *ws = nullptr;
+  if ((st = static_workspace((hipStream_t)stream, &ws, fn)) != KVPRM_OK) return st;
+  return score_impl(h, cache, b, wts, nullptr, 1, ws, (size_t)KVPRM_STATIC_WORKSPACE_BYTES, scores,
+                    logits, stream, fn);
 }
 
 kvprm_status kvprm_workspace_size_lora(kvprm_handle h, const kvprm_batch *b, int32_t rank,

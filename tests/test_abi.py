@@ -313,3 +313,26 @@ def test_grad_and_steer_validation():
         assert e.value.status == kv.KVPRM_E_INVALID
     finally:
         kv.kvprm_destroy(h)
+
+
+def test_score_static_validates_on_the_host():
+    """kvprm_score_static: B = 0 is a no-op; a batch whose workspace exceeds the static array is
+    refused with KVPRM_E_WORKSPACE, and bad arguments with their status, before the device is
+    touched."""
+    h = kv.kvprm_create(_desc(weight_dtype="bf16", kv_dtype="bf16", head_dim=128, num_q_heads=28,
+                              num_kv_heads=4, hidden=3584, ffn_dim=18944, num_layers=28))
+    try:
+        kv.kvprm_score_static(h, _cache(), kv.make_batch(0, 0, 1, 0), _weights(28), FAKE)
+        big = kv.make_batch(64, FAKE, 1152, FAKE)
+        assert kv.kvprm_workspace_size(h, big) > kv.STATIC_WORKSPACE_BYTES
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_score_static(h, _cache(), big, _weights(28), FAKE)
+        assert e.value.status == kv.KVPRM_E_WORKSPACE and "static" in kv.kvprm_last_error()
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_score_static(h, _cache(), kv.make_batch(2, 0, 4, FAKE), _weights(28), FAKE)
+        assert e.value.status == kv.KVPRM_E_INVALID
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_score_static(None, _cache(), big, _weights(28), FAKE)
+        assert e.value.status == kv.KVPRM_E_INVALID
+    finally:
+        kv.kvprm_destroy(h)
