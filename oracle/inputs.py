@@ -109,3 +109,40 @@ def score_workload(w: synth.Workload, candidates=None, return_hidden: bool = Fal
         return ko.verify_pass_depth(w.shape, ro, cache, lens, pt, depth,
                                     return_hidden=return_hidden)
     return ko.verify_pass(w.shape, ro, cache, lens, pt, return_hidden=return_hidden)
+
+
+def embed_table(shape: synth.ModelShape, seed: int, vocab: int = synth.VOCAB) -> np.ndarray:
+    """Token embedding table [vocab][H] of a synthetic model, N(0, 1) in the weight storage
+    precision, widened to float64."""
+    raw = synth.host_normal(vocab * shape.hidden, seed,
+                            synth.stream_id(synth.GLOBAL, synth.G_EMBED_TABLE), 0, 0.0, 1.0,
+                            _DT[shape.weight_dtype])
+    return ko.decode_storage(raw, shape.weight_dtype).reshape(vocab, shape.hidden)
+
+
+def reencode_batch(shape: synth.ModelShape, seed: int, lengths, mixed: bool = False):
+    """The re-encode mode of a workload: candidate b is a sequence of lengths[b] token ids (from
+    the seed's token stream, offset b * 4096) followed by the verify token (id VERIFY_ID), run
+    causally through the model by kvprm_oracle.reencode. The cached positions use the weights
+    of `seed` (adapter off, as during generation); the verify token uses the same weights, or,
+    with mixed, those of seed + ADAPTER_SEED_OFFSET (adapter on the verify token only).
+
+    Returns a dict: z, p [B] (the last position's logit and P(+)), K, V (per candidate
+    [N_L][n_kv][L_b][d_h] float64: the cache the causal pass wrote, keys after rotation),
+    verify_embed (the verify token's embedding row) and the two readouts (base, verify)."""
+    base = readout_from_synth(shape, seed, layer_cache=max(2, shape.num_layers))
+    ver = (readout_from_synth(shape, seed + synth.ADAPTER_SEED_OFFSET,
+                              layer_cache=max(2, shape.num_layers)) if mixed else base)
+    E = embed_table(shape, seed)
+    ev = E[synth.VERIFY_ID]
+    zs, Ks, Vs = [], [], []
+    for b, n in enumerate(lengths):
+        toks = synth.token_ids(seed, int(n), offset=4096 * b)
+        z, _, _, K, V = ko.reencode(shape, base.layer, ver.layer, E, toks, ev, ver.final_norm,
+                                    ver.reward_w, ver.reward_b)
+        zs.append(z)
+        Ks.append(K)
+        Vs.append(V)
+    z = np.array(zs)
+    return {"z": z, "p": ko.sigmoid(z), "K": Ks, "V": Vs, "verify_embed": ev, "base": base,
+            "verify": ver}

@@ -440,10 +440,17 @@ def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional
                     k_std=k_std)
 
 
-def token_ids(seed: int, n: int, vocab: int = 1000) -> List[int]:
-    """Random token ids in [0, vocab) for the re-encode workload."""
+# Re-encode mode of the tiny workload: token ids from a 1000-word vocabulary, the verify token is
+# the last word of it.
+VOCAB = 1000
+VERIFY_ID = 999
+
+
+def token_ids(seed: int, n: int, vocab: int = VOCAB, offset: int = 0) -> List[int]:
+    """Random token ids in [0, vocab) for the re-encode workload (counter words offset ..
+    offset + n - 1 of the seed's token stream)."""
     k = key(seed, stream_id(RECIPE, R_TOKENS))
-    return [uniform_int(k, i, 0, vocab - 1) for i in range(n)]
+    return [uniform_int(k, offset + i, 0, vocab - 1) for i in range(n)]
 
 
 def kv_pool_elems(shape: ModelShape, num_pages: int) -> int:

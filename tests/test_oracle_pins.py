@@ -273,6 +273,25 @@ def test_verify_pass_equals_causal_reencode(mixed):
     assert np.allclose(p2, ko.sigmoid(np.array(zs)), rtol=0, atol=1e-12)
 
 
+@pytest.mark.parametrize("mixed", [False, True])
+def test_tiny_reencode_mode_at_full_length(mixed):
+    """The tiny workload's re-encode mode at its own size (2 layers, H = 256, 4/2 heads, d_h 64,
+    FFN 1024, fp32): four sequences of 512 token ids from the 1000-word vocabulary, verify id
+    999, written causally (section 5.1, the Text-PRM re-encode of [x; v]); the verify pass over
+    the cache that pass wrote equals its last position. mixed: the verify token alone runs
+    other weights (adapter on the verify token only, section 4.1)."""
+    shape = synth.TINY
+    lens = [512] * 4
+    r = inputs.reencode_batch(shape, 1000, lens, mixed=mixed)
+    cache, pt = _dense_cache(r["K"], r["V"], shape.page_size)
+    ver = r["verify"]
+    ro = ko.Readout(ver.layer, r["verify_embed"], ver.final_norm, ver.reward_w, ver.reward_b)
+    z2, p2 = ko.verify_pass(shape, ro, cache, lens, pt)
+    assert np.allclose(z2, r["z"], rtol=0, atol=1e-12)
+    assert np.allclose(p2, r["p"], rtol=0, atol=1e-12)
+    assert np.ptp(r["z"]) > 1e-3  # the four sequences score differently
+
+
 def test_empty_cache_is_one_token_forward():
     shape = _tiny_small()
     ro = _readout(shape, 5)
