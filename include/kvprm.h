@@ -319,6 +319,26 @@ kvprm_status kvprm_steer(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
  * Enqueued on `stream`; a one-time preparation of static weights, not part of scoring. */
 kvprm_status kvprm_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, void *stream);
 
+/* Which pool kvprm_pack_kv writes: the K and V tiles have different stored layouts. */
+typedef enum { KVPRM_KEYS = 0, KVPRM_VALUES = 1 } kvprm_kv_part;
+
+/* Converts cache tiles written token by token into the stored tile layout of kvprm_kv_cache
+ * (section 2: the generator caches the key and value of every token at every layer; this is
+ * the bridge from a token-major paged cache to the layout the scoring kernels stream).
+ * src: num_tiles tiles of page_size (16) x head_dim values of `dtype` in token-major order,
+ *      element (slot s, dim m) of tile t at t * 16 * head_dim + s * head_dim + m, i.e. a pool
+ *      [num_layers][num_pages][num_kv_heads][16][head_dim] when num_tiles = num_layers *
+ *      num_pages * num_kv_heads;
+ * dst: the same tiles in the K (part = KVPRM_KEYS) or V (KVPRM_VALUES) tile layout described at
+ *      kvprm_kv_cache, in the same tile order (fp8 per-tile scales therefore keep their order
+ *      and are not touched).
+ * The bytes are moved unchanged (slots past a sequence's end may hold anything, NaN included).
+ * dtype F32, BF16 or FP8_E4M3; head_dim 64 or 128 (KVPRM_E_UNSUPPORTED otherwise); src and dst
+ * device pointers, 16-byte aligned, not overlapping (KVPRM_E_INVALID otherwise); num_tiles = 0
+ * does nothing. Nothing is allocated; enqueued on `stream`. */
+kvprm_status kvprm_pack_kv(const void *src, void *dst, int64_t num_tiles, int32_t head_dim,
+                           kvprm_dtype dtype, kvprm_kv_part part, void *stream);
+
 /* Diagnostic (measurement, not part of scoring): read `bytes` of device memory at `buf` once,
  * with the access pattern of the cache and weight streams (16-byte non-temporal loads, 512
  * blocks of 256 threads striding over the buffer), and XOR all its 32-bit words into the device

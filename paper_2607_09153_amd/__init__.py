@@ -24,7 +24,8 @@ EXPORTED = ["kvprm_create", "kvprm_destroy", "kvprm_workspace_size", "kvprm_scor
             "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
             "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
             "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer",
-            "kvprm_stream_read", "kvprm_score_static", "kvprm_last_error"]
+            "kvprm_stream_read", "kvprm_score_static", "kvprm_pack_kv", "kvprm_last_error"]
+KVPRM_KEYS, KVPRM_VALUES = 0, 1
 STATIC_WORKSPACE_BYTES = 64 << 20  # KVPRM_STATIC_WORKSPACE_BYTES
 LORA_PROJECTIONS = ("q", "k", "v", "o", "gate", "up", "down")
 
@@ -118,6 +119,8 @@ def _load():
     lib.kvprm_score_static.argtypes = [vp, ctypes.POINTER(KVCache), ctypes.POINTER(Batch),
                                        ctypes.POINTER(ReadoutWeights), vp, vp, vp]
     lib.kvprm_pack_weight.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, vp]
+    lib.kvprm_pack_kv.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int,
+                                  ctypes.c_int, vp]
     lib.kvprm_stream_read.argtypes = [vp, sz, vp, vp]
     lib.kvprm_workspace_size_lora.argtypes = [vp, ctypes.POINTER(Batch), ctypes.c_int32,
                                               ctypes.POINTER(sz)]
@@ -139,7 +142,7 @@ def _load():
               "kvprm_attention", "kvprm_attention_partials", "kvprm_pack_weight",
               "kvprm_workspace_size_lora", "kvprm_score_lora", "kvprm_workspace_size_ex",
               "kvprm_score_ex", "kvprm_workspace_size_grad", "kvprm_score_grad", "kvprm_steer",
-              "kvprm_stream_read", "kvprm_score_static"):
+              "kvprm_stream_read", "kvprm_score_static", "kvprm_pack_kv"):
         getattr(lib, f).restype = ctypes.c_int
     lib.kvprm_last_error.argtypes = []
     lib.kvprm_last_error.restype = ctypes.c_char_p
@@ -316,6 +319,13 @@ def kvprm_stream_read(buf_ptr: int, nbytes: int, sink_ptr: int, stream: int = 0)
 
 def kvprm_pack_weight(src_ptr: int, dst_ptr: int, rows: int, K: int, stream: int = 0) -> None:
     _check(lib.kvprm_pack_weight(src_ptr, dst_ptr, rows, K, stream or None))
+
+
+def kvprm_pack_kv(src_ptr: int, dst_ptr: int, num_tiles: int, head_dim: int, dtype: str,
+                  part: int, stream: int = 0) -> None:
+    """Token-major cache tiles -> the stored K (part = KVPRM_KEYS) or V tile layout."""
+    _check(lib.kvprm_pack_kv(src_ptr or None, dst_ptr or None, num_tiles, head_dim,
+                             DTYPE_CODE[dtype], part, stream or None))
 
 
 def kvprm_attention_partials(handle: int, cache: KVCache, batch: Batch, layer: int, q_ptr: int,

@@ -715,6 +715,29 @@ kvprm_status kvprm_pack_weight(const void *src, void *dst, int64_t rows, int64_t
   return ok();
 }
 
+kvprm_status kvprm_pack_kv(const void *src, void *dst, int64_t num_tiles, int32_t head_dim,
+                           kvprm_dtype dtype, kvprm_kv_part part, void *stream) {
+  const char *fn = "kvprm_pack_kv";
+  if (num_tiles < 0) return fail(KVPRM_E_INVALID, "%s: num_tiles < 0", fn);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(KVPRM_E_UNSUPPORTED, "%s: head_dim must be 64 or 128", fn);
+  if (dtype != KVPRM_F32 && dtype != KVPRM_BF16 && dtype != KVPRM_FP8_E4M3)
+    return fail(KVPRM_E_INVALID, "%s: unknown dtype %d", fn, (int)dtype);
+  if (part != KVPRM_KEYS && part != KVPRM_VALUES)
+    return fail(KVPRM_E_INVALID, "%s: part must be KVPRM_KEYS or KVPRM_VALUES", fn);
+  if (num_tiles == 0) return ok();
+  if (!src || !dst) return fail(KVPRM_E_INVALID, "%s: null pointer", fn);
+  const int eb = dtype == KVPRM_F32 ? 4 : (dtype == KVPRM_BF16 ? 2 : 1);
+  const uintptr_t a = (uintptr_t)src, b = (uintptr_t)dst;
+  const uintptr_t n = (uintptr_t)num_tiles * 16 * (uintptr_t)head_dim * (uintptr_t)eb;
+  if (a < b + n && b < a + n) return fail(KVPRM_E_INVALID, "%s: src and dst overlap", fn);
+  if ((a | b) & 15) return fail(KVPRM_E_INVALID, "%s: pointers must be 16-byte aligned", fn);
+  HIP_TRY(launch_pack_kv(src, dst, num_tiles, head_dim, eb, part == KVPRM_VALUES,
+                         (hipStream_t)stream),
+          "pack kv");
+  return ok();
+}
+
 kvprm_status kvprm_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream) {
   const char *fn = "kvprm_stream_read";
   if (!buf || !sink) return fail(KVPRM_E_INVALID, "%s: null pointer", fn);

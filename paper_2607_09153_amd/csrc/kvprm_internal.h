@@ -129,6 +129,9 @@ int gemv_bp(int B);
 int gemv_mt(int nt, int rows);
 hipError_t launch_pack_weight(const void *src, void *dst, int64_t rows, int64_t K, hipStream_t s);
 hipError_t launch_stream_read(const void *buf, size_t bytes, uint32_t *sink, hipStream_t s);
+// token-major cache tiles -> the stored K (v = false) or V tile layout; eb = element bytes
+hipError_t launch_pack_kv(const void *src, void *dst, int64_t ntiles, int d, int eb, bool v,
+                          hipStream_t s);
 
 Plan make_plan(const Dims &dm, int B, int max_pages, int lora_rank = 0, int depth = 1);
 Workspace carve(const Dims &dm, const Plan &p, void *base);

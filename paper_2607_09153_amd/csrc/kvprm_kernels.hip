@@ -739,6 +739,69 @@ hipError_t launch_head(const Dims &dm, const Plan &p, const Workspace &w, const 
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------------------- cache packing
+
+// Token-major cache tiles ([page_size][d] values, slot-major) -> the stored K or V tile layout.
+// One block per tile (grid-stride over tiles): the tile is read into LDS with 16-byte loads,
+// then every thread assembles 16-byte output groups in output order and stores them, so both
+// the reads and the writes are contiguous. EB = element bytes; x = 16 / EB values per group.
+//   K group (m / x) * 16 + s holds dims m .. m + x - 1 of slot s (a contiguous source run);
+//   V group ((m / (16 r)) * 4 + s / 4) * 16 + m % 16 holds slots 4 (s / 4) .. + 3 of the r dims
+//   m % 16 + 16 i (i < r) of the 16 r-dim block, as [i][slot % 4] (r = x / 4).
+template <int EB, bool V>
+__global__ __launch_bounds__(256) void k_pack_kv(const uint4 *__restrict__ src, uint4 *__restrict__ dst,
+                                                 int64_t ntiles, int d) {
+  extern __shared__ uint4 tile_s[];
+  constexpr int X = 16 / EB, R = X / 4;
+  const int groups = 16 * d / X;  // 16-byte groups per tile
+  const unsigned char *tb = (const unsigned char *)tile_s;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const uint4 *sp = src + t * groups;
+    for (int i = threadIdx.x; i < groups; i += 256) tile_s[i] = sp[i];
+    __syncthreads();
+    for (int gi = threadIdx.x; gi < groups; gi += 256) {
+      uint4 out;
+      if (!V) {
+        const int s = gi & 15, mb = gi >> 4;  // slot, x-dim block
+        out = tile_s[s * (d / X) + mb];
+      } else {
+        const int mm = gi & 15, sq = (gi >> 4) & 3, blk = gi >> 6;
+        unsigned char *ob = (unsigned char *)&out;
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int m = blk * 16 * R + i * 16 + mm, sl = 4 * sq + k;
+#pragma unroll
+            for (int e = 0; e < EB; ++e) ob[(i * 4 + k) * EB + e] = tb[(sl * d + m) * EB + e];
+          }
+      }
+      dst[t * groups + gi] = out;
+    }
+    __syncthreads();
+  }
+}
+
+hipError_t launch_pack_kv(const void *src, void *dst, int64_t ntiles, int d, int eb, bool v,
+                          hipStream_t s) {
+  const size_t lds = (size_t)16 * d * eb;
+  int64_t blocks = ntiles < 65536 ? ntiles : 65536;
+  const dim3 grid((unsigned)blocks), block(256);
+  const uint4 *a = (const uint4 *)src;
+  uint4 *b = (uint4 *)dst;
+#define KVPRM_PK(E_)                                                                    \
+  if (v) hipLaunchKernelGGL((k_pack_kv<E_, true>), grid, block, lds, s, a, b, ntiles, d); \
+  else hipLaunchKernelGGL((k_pack_kv<E_, false>), grid, block, lds, s, a, b, ntiles, d)
+  switch (eb) {
+    case 4: KVPRM_PK(4); break;
+    case 2: KVPRM_PK(2); break;
+    case 1: KVPRM_PK(1); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef KVPRM_PK
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------------------- diagnostics
 
 // Streaming read of n16 16-byte words: grid-stride, four non-temporal loads in flight per

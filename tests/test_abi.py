@@ -336,3 +336,16 @@ def test_score_static_validates_on_the_host():
         assert e.value.status == kv.KVPRM_E_INVALID
     finally:
         kv.kvprm_destroy(h)
+
+
+def test_pack_kv_validates_on_the_host():
+    kv.kvprm_pack_kv(0, 0, 0, 128, "bf16", kv.KVPRM_KEYS)  # nothing to do
+    for args, status in [((FAKE, FAKE + (1 << 30), 4, 96, "bf16", kv.KVPRM_KEYS), kv.KVPRM_E_UNSUPPORTED),
+                         ((FAKE, FAKE + 4096, 4, 128, "bf16", kv.KVPRM_VALUES), kv.KVPRM_E_INVALID),
+                         ((FAKE + 8, FAKE + (1 << 30), 4, 128, "fp8", kv.KVPRM_KEYS), kv.KVPRM_E_INVALID),
+                         ((FAKE, 0, 4, 64, "f32", kv.KVPRM_KEYS), kv.KVPRM_E_INVALID),
+                         ((FAKE, FAKE + (1 << 30), 4, 64, "f32", 2), kv.KVPRM_E_INVALID),
+                         ((FAKE, FAKE + (1 << 30), -1, 64, "f32", kv.KVPRM_KEYS), kv.KVPRM_E_INVALID)]:
+        with pytest.raises(kv.KvprmError) as e:
+            kv.kvprm_pack_kv(*args)
+        assert e.value.status == status, args
