@@ -8,11 +8,14 @@ generator) and resident in HBM before the timed region.
 
 Prints one JSON line: scores/s (value), the end-to-end KV-read rate, the roofline of the
 dominant kernel (the split-L attention chunk kernel, timed live with HIP events on its stream;
-the whole attention step with its merge is reported beside it), the same workload scored with
-the base weights and an unmerged rank-256 adapter on every projection (kvprm_score_lora,
-`lora_readout`) and with two verify tokens per candidate (the depth-k readout, kvprm_score_ex,
-`depth_readout`), KV steering steps on its cache (kvprm_steer, `kv_steering`), and the fp64
-CPU oracle timed on a bounded sample of the same workload.
+the whole attention step with its merge is reported beside it), the parity of the timed call's
+scores against stored fp64 oracle values (`parity`), the other benchmark workloads measured the
+same way (`workloads`: the 7B batch of 16 at L = 4096, the fixed L = 32768 batch of 8, the
+64-candidate beam batch with a shared 16k prefix, the large fp8-cache model), the same ragged
+workload scored with the base weights and an unmerged rank-256 adapter on every projection
+(kvprm_score_lora, `lora_readout`) and with two verify tokens per candidate (the depth-k
+readout, kvprm_score_ex, `depth_readout`), KV steering steps on its cache (kvprm_steer,
+`kv_steering`), and the fp64 CPU oracle timed on one full call of the same workload.
 """
 import argparse
 import json
@@ -246,43 +249,51 @@ def copy_bandwidth(nbytes=4 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
-def cpu_baseline(w, layers_sample, min_seconds=10.0):
-    """The fp64 oracle, untuned, on all candidates of the workload through its first
-    `layers_sample` layers, repeated until at least `min_seconds` of CPU work; input generation
-    is done before the clock starts. Scaled to scores/s of the full-depth model."""
-    import dataclasses
-
+def cpu_baseline(w):
+    """The fp64 oracle as it stands (kvprm_oracle.verify_pass, untuned) on one whole call of the
+    workload: every candidate through every layer. Its inputs are generated lazily inside the
+    call (one layer of weights and the pages it reads at a time, so that host memory stays
+    bounded); the time spent in the generator is measured around each generator call and
+    subtracted, so the figure is the oracle's own arithmetic. numpy's BLAS runs the projections
+    on its threads; the per-candidate, per-head attention loop runs on one thread. Returns the
+    baseline record and the oracle's (z, P(+)) of every candidate."""
     from threadpoolctl import threadpool_info
 
     from oracle import inputs as oin
     from oracle import kvprm_oracle as ko
 
     s = w.shape
-    sub = dataclasses.replace(s, num_layers=layers_sample)
-    ro = oin.readout_from_synth(sub, w.seed, layer_cache=layers_sample)
+    ro = oin.readout_from_synth(s, w.seed, layer_cache=1)
     npages = sum(-(-L // s.page_size) for L in w.lengths)
-    cache = oin.cache_from_synth(w, page_cache=2 * layers_sample * npages + 16)
-    for l in range(layers_sample):  # materialise inputs outside the timed region
-        ro.layer(l)
-        for b in range(w.batch):
-            for i in range(-(-w.lengths[b] // s.page_size)):
-                cache.tiles(l, "k", w.page_table[b][i])
-                cache.tiles(l, "v", w.page_table[b][i])
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        ko.verify_pass(sub, ro, cache, w.lengths, w.page_table)
-        reps += 1
-        dt = time.perf_counter() - t0
-        if dt >= min_seconds:
-            break
-    per_call = dt / reps * s.num_layers / layers_sample
+    cache = oin.cache_from_synth(w, page_cache=2 * npages + 16)
+    gen = [0.0]
+
+    def timed_layer(l):
+        t = time.perf_counter()
+        r = ro.layer(l)
+        gen[0] += time.perf_counter() - t
+        return r
+
+    def timed_tiles(l, which, page):
+        t = time.perf_counter()
+        r = cache.tiles(l, which, page)
+        gen[0] += time.perf_counter() - t
+        return r
+
+    ro_t = ko.Readout(timed_layer, ro.verify_embed, ro.final_norm, ro.reward_w, ro.reward_b)
+    t0 = time.perf_counter()
+    z, p = ko.verify_pass(s, ro_t, ko.PagedCache(timed_tiles), w.lengths, w.page_table)
+    wall = time.perf_counter() - t0
+    oracle_s = wall - gen[0]
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": w.batch / per_call, "unit": "scores/s", "cores": threads, "kind": "oracle",
-            "sample": (f"{w.name}: all {w.batch} candidates through the first {layers_sample} of "
-                       f"{s.num_layers} layers, {reps} passes in {dt:.1f} s (fp64 numpy, inputs "
-                       f"pre-generated), scaled by {s.num_layers}/{layers_sample} to one full "
-                       f"call"),
-            "host": {"logical_cpus": os.cpu_count(), "cpu_model": _cpu_model()}}
+    rec = {"value": w.batch / oracle_s, "unit": "scores/s", "cores": threads, "kind": "oracle",
+           "sample": (f"{w.name}: one whole call, all {w.batch} candidates through all "
+                      f"{s.num_layers} layers (fp64 numpy verify_pass): {wall:.1f} s of wall "
+                      f"time, of which {gen[0]:.1f} s in the input generator (subtracted)"),
+           "threads": {"blas_projections": threads, "attention_loop": 1},
+           "seconds_per_call": oracle_s,
+           "host": {"logical_cpus": os.cpu_count(), "cpu_model": _cpu_model()}}
+    return rec, z, p
 
 
 def _cpu_model():
@@ -326,16 +337,108 @@ def measured_traffic(workload):
     return float(kv["traffic_bytes_per_launch"])
 
 
+GOLDEN_DIR = os.path.join(ROOT, "tests", "golden")
+
+
+def golden_parity(name, p, z):
+    """max |dP(+)| and |dz| of a call's scores against the fp64 oracle values stored for this
+    workload in tests/golden/ (written by tests/golden/make_golden.py, which calls only the
+    oracle), on the candidates stored there; None when there are none."""
+    import numpy as np
+    path = os.path.join(GOLDEN_DIR, f"{name}.json")
+    if not os.path.exists(path):
+        return None
+    ref = json.load(open(path))
+    cand = ref["candidates"]
+    dp = float(np.max(np.abs(np.asarray(p, dtype=np.float64)[cand] - np.array(ref["p"]))))
+    dz = float(np.max(np.abs(np.asarray(z, dtype=np.float64)[cand] - np.array(ref["z"]))))
+    return {"reference": os.path.relpath(path, ROOT), "candidates": cand, "max_abs_dp": dp,
+            "max_abs_dz": dz, "tolerance": {"dp": 2e-3, "dz": 2e-2},
+            "ok": dp <= 2e-3 and dz <= 2e-2}
+
+
+def measure_workload(kv, name, steps, warmup, attn_reps):
+    """One benchmark workload measured like the headline: whole kvprm_score calls (inputs
+    resident in HBM, K calls between two synchronisations, per-call HIP events), the attention
+    chunk kernel(s) alone (kvprm_attention_partials: the dominant HBM stream), end-to-end and
+    dominant-kernel fractions of the 8 TB/s HBM peak, and parity against the stored oracle
+    values. Frees its device memory before returning."""
+    import torch
+    import synth
+    from synth.device import DeviceWorkload
+
+    w = synth.make_workload(name)
+    _log(f"workload {name}: B={w.batch} layers={w.shape.num_layers} kv={w.shape.kv_dtype}")
+    dw = DeviceWorkload(w)
+    torch.cuda.synchronize()
+    kv_bytes, w_bytes = algorithmic_bytes(w, dw)
+    h = kv.kvprm_create(dw.desc(kv))
+    try:
+        batch = dw.batch(kv)
+        n = kv.kvprm_workspace_size(h, batch)
+        ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        scores = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+        logits = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+        stream = torch.cuda.current_stream()
+        cache, readout = dw.cache(kv), dw.readout(kv)
+
+        def step():
+            kv.kvprm_score(h, cache, batch, readout, ws.data_ptr(), n, scores.data_ptr(),
+                           logits.data_ptr(), stream.cuda_stream)
+
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        t0 = time.perf_counter()
+        evs[0].record(stream)
+        for i in range(steps):
+            step()
+            evs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        per_call = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(steps))
+        kernel_ms, step_ms = time_attention(kv, dw, h, batch, ws, n, attn_reps)
+        p, z = scores.cpu().numpy(), logits.cpu().numpy()
+    finally:
+        kv.kvprm_destroy(h)
+    kv_layer = kv_bytes / w.shape.num_layers
+    e2e = (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9
+    attn = kv_layer / (kernel_ms * 1e-3) / 1e9
+    out = {"batch": w.batch, "layers": w.shape.num_layers, "hidden": w.shape.hidden,
+           "kv_dtype": w.shape.kv_dtype, "cached_tokens": sum(w.lengths),
+           "unique_cached_tokens": w.unique_tokens(),
+           "ms_per_call": ms, "scores_per_s": w.batch / (ms * 1e-3),
+           "per_call_ms": {"median": per_call[len(per_call) // 2], "min": per_call[0],
+                           "max": per_call[-1]},
+           "bytes_per_call": {"kv": kv_bytes, "weights": w_bytes},
+           "end_to_end_gbps": e2e, "end_to_end_frac": e2e / HBM_PEAK_GBPS,
+           "dominant_kernel": {"kernel": ("attention chunk kernels, one layer (shared-prefix + "
+                                          "private)" if w.group_start else
+                                          "k_attn_mx: attention chunk kernel, one layer"),
+                               "avg_us": kernel_ms * 1e3, "bytes_per_launch": kv_layer,
+                               "achieved_gbps": attn, "frac": attn / HBM_PEAK_GBPS,
+                               "with_merge_us": step_ms * 1e3},
+           "parity": golden_parity(name, p, z)}
+    if w.shape.kv_dtype == "fp8":
+        out["fp8_scale"] = w.fp8_scale
+    del dw, ws
+    torch.cuda.empty_cache()
+    _log(f"  {ms:.3f} ms/call, end to end {e2e:.0f} GB/s, attention {kernel_ms * 1e3:.1f} us "
+         f"({attn:.0f} GB/s), parity {out['parity']}")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="ragged_32k")
-    ap.add_argument("--cpu-layers", type=int, default=2,
-                    help="layers of the oracle sample for the CPU baseline (0 = skip)")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="minimum CPU work of the oracle sample (repeated passes)")
+    ap.add_argument("--no-cpu", action="store_true",
+                    help="skip the CPU oracle baseline (one whole oracle call)")
+    ap.add_argument("--other-workloads", default="b7_bf16,fixed_32k,beam_prefix,large_fp8",
+                    help="comma-separated workloads measured after the headline ('' = none)")
     ap.add_argument("--attn-reps", type=int, default=56)
     ap.add_argument("--lora-rank", type=int, default=256,
                     help="rank of the unmerged adapter of the second timed line (0 = skip)")
@@ -370,12 +473,13 @@ def main():
     n = kv.kvprm_workspace_size(h, batch)
     ws = torch.empty(n, dtype=torch.uint8, device="cuda")
     scores = torch.empty(w.batch, dtype=torch.float32, device="cuda")
+    logits = torch.empty(w.batch, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
     cache, readout = dw.cache(kv), dw.readout(kv)
 
     def step():
-        kv.kvprm_score(h, cache, batch, readout, ws.data_ptr(), n, scores.data_ptr(), 0,
-                       stream.cuda_stream)
+        kv.kvprm_score(h, cache, batch, readout, ws.data_ptr(), n, scores.data_ptr(),
+                       logits.data_ptr(), stream.cuda_stream)
 
     for _ in range(args.warmup):
         step()
@@ -392,6 +496,9 @@ def main():
     per_call = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
     ms = dt * 1e3 / args.steps
     _log(f"timed {args.steps} steps: {ms:.3f} ms/step")
+    timed_p, timed_z = scores.cpu().numpy(), logits.cpu().numpy()
+    parity = golden_parity(w.name, timed_p, timed_z)
+    _log(f"parity of the timed call: {parity}")
 
     graph = time_graph(kv, h, cache, batch, readout, ws, n, scores, args.steps)
     _log(f"graph replay: {graph['ms_per_call']:.3f} ms/call")
@@ -416,6 +523,11 @@ def main():
         steer = time_steer(kv, dw, h, batch, args.steer_steps)
         _log(f"KV steering: {steer['ms_per_step']:.3f} ms per step")
     kv.kvprm_destroy(h)
+    del dw, ws
+    torch.cuda.empty_cache()
+    others = {}
+    for name in [x for x in args.other_workloads.split(",") if x]:
+        others[name] = measure_workload(kv, name, args.steps, args.warmup, max(args.attn_reps, 1))
     copy_gbps = copy_bandwidth()
     _log(f"device copy reference: {copy_gbps:.0f} GB/s")
     read_gbps = read_bandwidth(kv)
@@ -453,6 +565,8 @@ def main():
                            "kv_gbps": kv_per_layer / (step_ms * 1e-3) / 1e9},
         "per_call_ms": {"median": per_call[len(per_call) // 2], "min": per_call[0],
                         "max": per_call[-1]},
+        "end_to_end_frac": (kv_bytes + w_bytes) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "parity": parity,
         "copy_reference_gbps": copy_gbps,
         "read_reference_gbps": read_gbps,
     }
@@ -463,9 +577,22 @@ def main():
         out["depth_readout"] = depth
     if steer is not None:
         out["kv_steering"] = steer
-    if args.cpu_layers > 0:
-        _log("timing the oracle on the CPU sample ...")
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers, args.cpu_seconds)
+    if others:
+        out["workloads"] = others
+    if not args.no_cpu:
+        import numpy as np
+        _log("timing one whole oracle call on the CPU ...")
+        base, oz, op = cpu_baseline(w)
+        out["cpu_baseline"] = base
+        # the timed GPU call against that oracle call, every candidate
+        if out["parity"] is None:
+            out["parity"] = {}
+        out["parity"]["vs_oracle_call"] = {
+            "candidates": list(range(w.batch)),
+            "max_abs_dp": float(np.max(np.abs(timed_p.astype(np.float64) - op))),
+            "max_abs_dz": float(np.max(np.abs(timed_z.astype(np.float64) - oz)))}
+        _log(f"oracle: {base['seconds_per_call']:.1f} s per call; "
+             f"vs GPU {out['parity']['vs_oracle_call']}")
     print(json.dumps(out), flush=True)
 
 

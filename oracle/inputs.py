@@ -74,7 +74,8 @@ def cache_from_synth(w: synth.Workload, nan_pages=(), page_cache: int = 4096) ->
         stream = synth.kv_stream(layer, which)
         std = w.k_std if which == "k" else w.v_std
         if s.kv_dtype == "fp8":
-            codes, scales = synth.host_fp8_tiles(nkv, T, w.seed, stream, page * nkv)
+            codes, scales = synth.host_fp8_tiles(nkv, T, w.seed, stream, page * nkv,
+                                                 scale=w.fp8_scale)
             vals = ko.e4m3fn_to_f64(codes).reshape(nkv, T) * scales.astype(np.float64)[:, None]
         else:
             raw = synth.host_normal(nkv * T, w.seed, stream, page * nkv * T, 0.0, std,

@@ -107,7 +107,7 @@ def _load_host():
         lib.synth_fill_normal.restype = None
         lib.synth_fill_fp8_tiles.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                              ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint64,
-                                             ctypes.c_int64]
+                                             ctypes.c_int64, ctypes.c_int]
         lib.synth_fill_fp8_tiles.restype = None
         lib.synth_words.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
                                     ctypes.c_uint64, ctypes.c_int64]
@@ -140,7 +140,7 @@ def _load_dev():
         lib.synth_dev_fill_normal.restype = ctypes.c_int
         lib.synth_dev_fill_fp8_tiles.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                                  ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint64,
-                                                 ctypes.c_int64, ctypes.c_void_p]
+                                                 ctypes.c_int64, ctypes.c_int, ctypes.c_void_p]
         lib.synth_dev_fill_fp8_tiles.restype = ctypes.c_int
         _dev = lib
     return _dev
@@ -158,13 +158,19 @@ def host_normal(n: int, seed: int, stream: int, offset: int = 0, mean: float = 0
     return out
 
 
-def host_fp8_tiles(ntiles: int, tile: int, seed: int, stream: int, tile0: int = 0):
+# fp8 tile scales: powers of two, or amax / 448 (the largest value of a tile at the top of the
+# e4m3 range; not a power of two)
+FP8_SCALE_MODES = {"pow2": 0, "amax": 1}
+
+
+def host_fp8_tiles(ntiles: int, tile: int, seed: int, stream: int, tile0: int = 0,
+                   scale: str = "pow2"):
     """(codes uint8 [ntiles*tile], scales fp32 [ntiles]) for tiles tile0 .. tile0+ntiles."""
     codes = np.empty(ntiles * tile, dtype=np.uint8)
     scales = np.empty(ntiles, dtype=np.float32)
     if ntiles:
         _load_host().synth_fill_fp8_tiles(codes.ctypes.data, scales.ctypes.data, ntiles, tile,
-                                          seed, stream, tile0)
+                                          seed, stream, tile0, FP8_SCALE_MODES[scale])
     return codes, scales
 
 
@@ -178,9 +184,9 @@ def device_normal(ptr: int, n: int, seed: int, stream: int, offset: int = 0, mea
 
 
 def device_fp8_tiles(codes_ptr: int, scales_ptr: int, ntiles: int, tile: int, seed: int,
-                     stream: int, tile0: int = 0, hip_stream: int = 0) -> None:
+                     stream: int, tile0: int = 0, hip_stream: int = 0, scale: str = "pow2") -> None:
     rc = _load_dev().synth_dev_fill_fp8_tiles(codes_ptr, scales_ptr, ntiles, tile, seed, stream,
-                                              tile0, hip_stream)
+                                              tile0, FP8_SCALE_MODES[scale], hip_stream)
     if rc != 0:
         raise RuntimeError(f"synth_dev_fill_fp8_tiles failed with hipError {rc}")
 
@@ -235,6 +241,7 @@ class Workload:
     group_prefix_len: List[int] = field(default_factory=list)
     k_std: float = 1.0  # test variants scale K to make the softmax peaked
     v_std: float = 1.0
+    fp8_scale: str = "amax"  # fp8 tile scales: "amax" (amax / 448) or "pow2" (powers of two)
 
     @property
     def batch(self) -> int:
@@ -380,7 +387,8 @@ LARGE_FP8 = ModelShape(64, 8192, 64, 8, 128, 28672, kv_dtype="fp8")
 def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional[int] = None,
                   lengths: Optional[Sequence[int]] = None, seed: Optional[int] = None,
                   k_std: float = 1.0,
-                  groups: Optional[Tuple[Sequence[int], Sequence[int]]] = None) -> Workload:
+                  groups: Optional[Tuple[Sequence[int], Sequence[int]]] = None,
+                  fp8_scale: str = "amax") -> Workload:
     """The five workloads of the benchmark plan, plus custom ones for tests.
 
     tiny_fp32    B=4, 2 layers, H=256, 4/2 heads, d_h=64, FFN 1024, fp32, L=512 each
@@ -389,8 +397,12 @@ def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional
     beam_prefix  7B shape, B=64, one shared 16384-token prefix + private U[512, 2048]
     large_fp8    B=16, 64 layers, H=8192, 64/8 heads, FFN 28672, bf16 weights,
                  e4m3 K/V with per-(layer, page, kv-head) scales, L_b ~ U[8192, 16384]
+    fixed_32k    7B shape, B=8, every L_b = 32768 (the fixed-length point beside ragged_32k)
     custom       any shape with explicit lengths (tests); ``groups`` = (group starts, prefix
                  lengths in tokens, multiples of the page size) makes members share prefix pages
+
+    fp8 caches get per-(layer, page, kv-head) scales amax / 448 by default (``fp8_scale``
+    "pow2": the smallest power of two that fits the tile instead).
     """
     presets = {
         "tiny_fp32": (TINY, 1000),
@@ -398,6 +410,7 @@ def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional
         "ragged_32k": (B7, 1002),
         "beam_prefix": (B7, 1003),
         "large_fp8": (LARGE_FP8, 1004),
+        "fixed_32k": (B7, 1005),
     }
     if name in presets:
         shp, sd = presets[name]
@@ -426,6 +439,8 @@ def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional
         groups_start, groups_prefix = [0, B], [prefix]
     elif name == "large_fp8":
         lens = [uniform_int(klen, i, 8192, 16384) for i in range(batch or 16)]
+    elif name == "fixed_32k":
+        lens = [32768] * (batch or 8)
     else:
         raise ValueError(f"workload {name!r} needs explicit lengths")
     if groups_start:
@@ -436,8 +451,9 @@ def make_workload(name: str, shape: Optional[ModelShape] = None, batch: Optional
             assert all(lens[b] >= pl for b in range(groups_start[gi], groups_start[gi + 1]))
     rows, num_pages = _assign_pages(seed, lens, ps, groups_start,
                                     [pl // ps for pl in groups_prefix])
+    assert fp8_scale in FP8_SCALE_MODES
     return Workload(name, shape, seed, lens, rows, num_pages, groups_start, groups_prefix,
-                    k_std=k_std)
+                    k_std=k_std, fp8_scale=fp8_scale)
 
 
 # Re-encode mode of the tiny workload: token ids from a 1000-word vocabulary, the verify token is

@@ -1,8 +1,8 @@
 // Seeded synthetic input generator, GPU implementation.
 //
 // Same definition as synth_host.c (SplitMix64 counter words, Irwin-Hall
-// normals, round-to-nearest-even storage rounding, power-of-two fp8 tile
-// scales); it exists so that multi-GB inputs can be written straight into
+// normals, round-to-nearest-even storage rounding, fp8 tile scales as powers
+// of two or amax / 448); it exists so that multi-GB inputs can be written straight into
 // HBM. It holds no arithmetic of the scoring method. The test suite checks
 // that both implementations produce identical bits.
 //
@@ -93,7 +93,7 @@ __device__ static uint8_t syn_e4m3_rne(double x) {
 
 // One 64-lane wave per tile: amax by a wave reduction (max is order-free), then codes.
 __global__ void syn_fill_fp8_kernel(uint8_t *codes, float *scales, int64_t ntiles, int64_t T,
-                                    uint64_t key, int64_t tile0) {
+                                    uint64_t key, int64_t tile0, int scale_mode) {
   const int lane = threadIdx.x & 63;
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
@@ -102,6 +102,13 @@ __global__ void syn_fill_fp8_kernel(uint8_t *codes, float *scales, int64_t ntile
     double amax = 0.0;
     for (int64_t i = lane; i < T; i += 64) amax = fmax(amax, fabs(syn_normal(key, base + i)));
     for (int off = 32; off > 0; off >>= 1) amax = fmax(amax, __shfl_xor(amax, off, 64));
+    if (scale_mode == 1) {
+      const float sf = amax > 0.0 ? (float)(amax / 448.0) : 1.0f;
+      if (lane == 0) scales[t] = sf;
+      for (int64_t i = lane; i < T; i += 64)
+        codes[t * T + i] = syn_e4m3_rne(syn_normal(key, base + i) / (double)sf);
+      continue;
+    }
     int e = -30;
     if (amax > 0.0) {
       int ea;
@@ -129,13 +136,13 @@ int synth_dev_fill_normal(void *out, int64_t n, uint64_t seed, uint64_t stream, 
 }
 
 int synth_dev_fill_fp8_tiles(uint8_t *codes, float *scales, int64_t ntiles, int64_t T, uint64_t seed,
-                             uint64_t stream, int64_t tile0, void *stream_handle) {
+                             uint64_t stream, int64_t tile0, int scale_mode, void *stream_handle) {
   if (ntiles <= 0) return 0;
   int64_t blocks = (ntiles + 3) / 4;  // 4 waves per block
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL(syn_fill_fp8_kernel, dim3((unsigned)blocks), dim3(256), 0,
                      (hipStream_t)stream_handle, codes, scales, ntiles, T, syn_key(seed, stream),
-                     tile0);
+                     tile0, scale_mode);
   return (int)hipGetLastError();
 }
 

@@ -23,9 +23,12 @@
  *                storage type: fp32 by round-to-nearest-even, bf16 by
  *                round-to-nearest-even from that fp32.
  *   fp8 tiles    a tile of T consecutive normals z_i (index t*T + i) gets a
- *                power-of-two scale s = 2^e, the smallest with
- *                amax / s <= 448, and codes q_i = E4M3FN(z_i / s) rounded
- *                to nearest even (saturating at 448; no NaN is produced).
+ *                scale s and codes q_i = E4M3FN(z_i / s) rounded to nearest
+ *                even (saturating at 448; no NaN is produced). Scale mode 0:
+ *                s = 2^e, the smallest power of two with amax / s <= 448;
+ *                mode 1: s = fp32(amax / 448) (1 for an all-zero tile), so
+ *                that the tile's largest value maps to the top of the e4m3
+ *                range; z_i / s is one correctly rounded double division.
  *
  * Only integer operations and correctly rounded IEEE basic operations are
  * used, so every platform that follows IEEE 754 gives identical bits.
@@ -130,9 +133,10 @@ static uint8_t syn_e4m3_rne(double x) {
   return sign | (uint8_t)((exp_field << 3) | mf);
 }
 
-/* Tiles t in [tile0, tile0 + ntiles), each of T elements: codes and power-of-two scales. */
+/* Tiles t in [tile0, tile0 + ntiles), each of T elements: codes and scales (scale_mode 0:
+ * powers of two; 1: amax / 448). */
 void synth_fill_fp8_tiles(uint8_t *codes, float *scales, int64_t ntiles, int64_t T, uint64_t seed,
-                          uint64_t stream, int64_t tile0) {
+                          uint64_t stream, int64_t tile0, int scale_mode) {
   uint64_t key = synth_key(seed, stream);
 #pragma omp parallel for schedule(static)
   for (int64_t t = 0; t < ntiles; ++t) {
@@ -141,6 +145,13 @@ void synth_fill_fp8_tiles(uint8_t *codes, float *scales, int64_t ntiles, int64_t
     for (int64_t i = 0; i < T; ++i) {
       double a = fabs(syn_normal(key, base + (uint64_t)i));
       if (a > amax) amax = a;
+    }
+    if (scale_mode == 1) {
+      float sf = amax > 0.0 ? (float)(amax / 448.0) : 1.0f;
+      scales[t] = sf;
+      for (int64_t i = 0; i < T; ++i)
+        codes[t * T + i] = syn_e4m3_rne(syn_normal(key, base + (uint64_t)i) / (double)sf);
+      continue;
     }
     /* smallest e with amax <= 448 * 2^e; 448 = 0.875 * 2^9 and amax = f * 2^ea, f in [0.5, 1) */
     int e = -30;

@@ -59,7 +59,7 @@ class DeviceWorkload:
                     sc = self.k_scale if which == "k" else self.v_scale
                     synth.device_fp8_tiles(pool[l].data_ptr(), sc[l].data_ptr(), ntiles,
                                            s.tile_elems, w.seed, synth.kv_stream(l, which), 0,
-                                           stream)
+                                           stream, scale=w.fp8_scale)
                 else:
                     synth.device_normal(pool[l].data_ptr(), per_layer, w.seed,
                                         synth.kv_stream(l, which), 0, 0.0, std, _DT[s.kv_dtype],

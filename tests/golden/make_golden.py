@@ -20,11 +20,14 @@ import synth  # noqa: E402
 from oracle import inputs as oin  # noqa: E402
 from oracle import kvprm_oracle as ko  # noqa: E402
 
+# sampled candidates of each batch: the first, the longest and the shortest cached sequence among
+# them (ragged: 2 is the longest at 31832 tokens and fills the most chunk slots, 1 the shortest;
+# beam: 2 the longest suffix, 0 the shortest; large fp8: 0 the longest, 14 the shortest at 8834)
 SAMPLES = {
     "b7_bf16": [0, 7, 15],
-    "ragged_32k": [0, 1, 5],
-    "beam_prefix": [0, 33, 63],
-    "large_fp8": [0, 9],
+    "ragged_32k": [0, 1, 2, 5],
+    "beam_prefix": [0, 2, 33, 63],
+    "large_fp8": [0, 9, 14],
 }
 
 
@@ -56,6 +59,7 @@ def make(name, lora_rank=0):
         "z": [float(v) for v in z],
         "p": [float(v) for v in p],
         "source": "fp64 oracle (oracle/kvprm_oracle.py verify_pass), Eq. (score) of section 4.1",
+        "fp8_scale": w.fp8_scale if w.shape.kv_dtype == "fp8" else None,
         "oracle_seconds": round(time.time() - t0, 1),
     }
     if lora_rank:

@@ -41,17 +41,20 @@ def test_device_generator_matches_host_bits():
             dev = dev.numpy()
         assert np.array_equal(dev.view(np.uint8), host.view(np.uint8))
     T, nt = 2048, 333
-    codes = torch.empty(nt * T, dtype=torch.uint8, device="cuda")
-    scales = torch.empty(nt, dtype=torch.float32, device="cuda")
-    synth.device_fp8_tiles(codes.data_ptr(), scales.data_ptr(), nt, T, 9, 3, 50, 0)
-    torch.cuda.synchronize()
-    hc, hs = synth.host_fp8_tiles(nt, T, 9, 3, 50)
-    assert np.array_equal(codes.cpu().numpy(), hc)
-    assert np.array_equal(scales.cpu().numpy(), hs)
+    for mode in ("pow2", "amax"):
+        codes = torch.empty(nt * T, dtype=torch.uint8, device="cuda")
+        scales = torch.empty(nt, dtype=torch.float32, device="cuda")
+        synth.device_fp8_tiles(codes.data_ptr(), scales.data_ptr(), nt, T, 9, 3, 50, 0,
+                               scale=mode)
+        torch.cuda.synchronize()
+        hc, hs = synth.host_fp8_tiles(nt, T, 9, 3, 50, scale=mode)
+        assert np.array_equal(codes.cpu().numpy(), hc)
+        assert np.array_equal(scales.cpu().numpy(), hs)
 
 
 ATTN_CASES = [
-    # name, lengths (incl. empty, one token, page edges, ragged tails), K scale
+    # name, lengths (incl. empty, one token, page edges, ragged tails), K scale; fp8 caches have
+    # per-tile scales amax / 448 (not powers of two) unless the name ends in _pow2
     ("tiny_fp32", [512, 0, 1, 15, 16, 17, 700, 1025], 1.0),
     ("b7_bf16", [4096, 0, 1, 17, 5000, 9000], 1.0),
     ("b7_bf16_spiky", [3000, 33, 16], 30.0),
@@ -64,6 +67,8 @@ ATTN_CASES = [
     ("b7_bf16", [16384, 300, 17, 9000, 0, 12000], 1.0),
     ("b7_bf16", [32768, 1, 20000, 33, 5000, 31000], 1.0),
     ("fp8", [32768, 16, 17000, 4000, 29999, 2], 1.0),
+    ("fp8_pow2", [2049, 0, 31, 8192], 1.0),
+    ("fp8", [3000, 33, 16], 30.0),
 ]
 
 
@@ -73,7 +78,7 @@ def _shape(name):
         return synth.TINY
     if name.startswith("b7"):
         return dataclasses.replace(synth.B7, num_layers=2)
-    if name == "fp8":
+    if name in ("fp8", "fp8_pow2"):
         return dataclasses.replace(synth.LARGE_FP8, num_layers=2)
     if name == "g16_bf16":
         return synth.ModelShape(2, 1024, 16, 1, 64, 2048)
@@ -86,7 +91,8 @@ def _shape(name):
 def test_attention_parity(name, lengths, k_std):
     _say(f"case: attention {name} lengths={lengths}")
     shape = _shape(name)
-    w = synth.make_workload("custom", shape=shape, lengths=lengths, seed=4242, k_std=k_std)
+    w = synth.make_workload("custom", shape=shape, lengths=lengths, seed=4242, k_std=k_std,
+                            fp8_scale="pow2" if name.endswith("_pow2") else "amax")
     dw = DeviceWorkload(w, nan_unused_pages=True, fill_weights=False)
     q, ks, vs = host_activations(w, 0xABC, scale=1.0)
     layer = 1
@@ -224,6 +230,36 @@ def test_score_parity_tiny_spiky_keys():
     w = synth.make_workload("custom", shape=synth.TINY, lengths=[300, 64, 129], seed=78,
                             k_std=30.0)
     _parity(w, 1e-5, 4e-5)
+
+
+@pytest.mark.parametrize("kv_dtype,fp8_scale", [("bf16", None), ("fp8", "amax"), ("fp8", "pow2")])
+def test_score_parity_two_layers_cache_dtypes(kv_dtype, fp8_scale):
+    """Whole scoring pass over bf16 and e4m3 caches (scales amax / 448, or powers of two)."""
+    _say(f"case: score 7B shape, 2 layers, {kv_dtype} cache {fp8_scale or ''}")
+    import dataclasses
+    shape = dataclasses.replace(synth.B7, num_layers=2, kv_dtype=kv_dtype)
+    w = synth.make_workload("custom", shape=shape, lengths=[4100, 0, 17, 3001, 1200], seed=85,
+                            fp8_scale=fp8_scale or "amax")
+    _parity(w, 2e-3, 2e-2)
+
+
+def test_score_long_peaked_softmax_moves_z():
+    """L ~ 32k over 2 layers of the 7B shape with K scaled x30: one cached key dominates each
+    head's softmax, so the attention output is an O(1) cached value row and the cache moves z by
+    more than 1 (against the same model with an empty cache): a wrong page, chunk or merge at
+    long L would show far above the |dz| bar, which is held at 2e-2 here too."""
+    import dataclasses
+    shape = dataclasses.replace(synth.B7, num_layers=2)
+    lens = [32768, 30001, 16385]
+    _say(f"case: score long peaked softmax lengths={lens}")
+    w = synth.make_workload("custom", shape=shape, lengths=lens, seed=4601, k_std=30.0)
+    p, z = _parity(w, 2e-3, 2e-2)
+    z_empty, _ = oin.score_workload(
+        synth.make_workload("custom", shape=shape, lengths=[0] * len(lens), seed=4601))
+    zr, _ = oin.score_workload(w)
+    _say(f"  oracle z {np.round(zr, 4)}; with an empty cache {np.round(z_empty, 4)}")
+    assert np.max(np.abs(zr - z_empty)) > 1.0
+    assert np.ptp(zr) > 0.5
 
 
 def test_score_parity_7b_two_layers_bf16():

@@ -67,13 +67,33 @@ def test_fp8_tiles_scale_and_rounding():
     assert np.array_equal(codes.reshape(64, T), ref.view(torch.uint8).numpy())
 
 
+def test_fp8_tiles_amax_scale_and_rounding():
+    """Scale mode "amax": s = fp32(amax / 448) (not a power of two in general), codes the
+    round-to-nearest-even e4m3fn of z / s, saturating; the largest value of each tile decodes
+    to within one e4m3 step of 448 * s."""
+    import torch
+    T = 2048
+    codes, scales = synth.host_fp8_tiles(64, T, 21, 9, 10, scale="amax")
+    z = synth.host_normal(64 * T, 21, 9, 10 * T).reshape(64, T)
+    amax = np.abs(z).max(axis=1)
+    assert np.array_equal(scales, (amax / 448.0).astype(np.float32))
+    e = np.log2(scales.astype(np.float64))
+    assert np.sum(e != np.round(e)) >= 60  # essentially never a power of two
+    scaled = z / scales[:, None].astype(np.float64)
+    ref = torch.from_numpy(np.clip(scaled, -448.0, 448.0)).to(torch.float8_e4m3fn)
+    assert np.array_equal(codes.reshape(64, T), ref.view(torch.uint8).numpy())
+    top = np.abs(ref.to(torch.float64).numpy()).max(axis=1)
+    assert np.all(top >= 416.0) and np.all(top <= 448.0)
+
+
 def test_permutation_is_bijection():
     p = synth.permutation(5, 1, 1000)
     assert sorted(p) == list(range(1000))
     assert p != list(range(1000))
 
 
-@pytest.mark.parametrize("name", ["tiny_fp32", "b7_bf16", "ragged_32k", "beam_prefix", "large_fp8"])
+@pytest.mark.parametrize("name", ["tiny_fp32", "b7_bf16", "ragged_32k", "beam_prefix", "large_fp8",
+                                  "fixed_32k"])
 def test_workload_structure(name):
     w = synth.make_workload(name)
     ps = w.shape.page_size
