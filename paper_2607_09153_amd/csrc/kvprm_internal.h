@@ -84,6 +84,10 @@ struct Plan {
   // output, gate/up and down groups
   int lora_rank;
   GemvPlan g_la[4];
+  // q/k/v as a split-K product and a finish kernel (RMSNorm scale, rotary) instead of the fused
+  // kernel, for shapes with more rotary tile pairs than compute units (no adapter)
+  int qkv_split;
+  GemvPlan g_qkv;
   size_t part_elems;
 };
 

@@ -122,6 +122,15 @@ Plan make_plan(const Dims &dm, int Breal, int max_pages, int lora_rank, int dept
       p.g_la[LORA_DOWN] = gemv_plan(lora_rank, dm.F, B);
       for (const GemvPlan &g : p.g_la) m = partial_elems(g) > m ? partial_elems(g) : m;
     }
+    // the fused q/k/v kernel has one block per rotary tile pair; with more pairs than compute
+    // units (320 at H = 8192, 64/8 heads) a second round leaves most of the chip idle, and the
+    // split-K product with its finish kernel measured faster (28.3 vs 29.1 ms per call there)
+    const int pairs = (dm.nq + 2 * dm.nkv) * (dm.d / 32);
+    if (pairs > 256 && lora_rank == 0) {
+      p.qkv_split = 1;
+      p.g_qkv = gemv_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B);
+      m = partial_elems(p.g_qkv) > m ? partial_elems(p.g_qkv) : m;
+    }
   } else {
     // vector-ALU GEMV: the activation slice of all B candidates is staged in LDS (<= 32 KiB)
     p.rb = 256;

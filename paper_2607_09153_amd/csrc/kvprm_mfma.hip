@@ -1502,9 +1502,66 @@ static hipError_t launch_qkv_rope_fused(const Dims &dm, const Plan &p, const Wor
   return hipGetLastError();
 }
 
+// q, k_self, v_self from the split-K partials of the stacked q/k/v product: the k-partials of
+// rows r and r + d/2 of a head (the two halves of a rotary pair) added in k order, the RMSNorm
+// scale of the candidate, the rotation (q and k heads) at the candidate's position. One thread
+// per (row pair, candidate).
+template <int NMAX>
+__global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ part, int ksp,
+                                                    int ksplit, const float *__restrict__ ss,
+                                                    int nss, int H, float eps, int B, int nq,
+                                                    int nkv, int d, const float *__restrict__ rope,
+                                                    float *__restrict__ q, float *__restrict__ ks,
+                                                    float *__restrict__ vs) {
+  __shared__ float part_s[256], inv_s[64];
+  const int hd = d / 2;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  const bool act = e < (nq + 2 * nkv) * hd * B;
+  const int ec = act ? e : 0;
+  const int pr = ec / B, b = ec - pr * B;
+  const int head = pr / hd, i = pr - head * hd;
+  const int r = head * d + i;
+  const size_t i1 = (size_t)r * B + b, i2 = (size_t)(r + hd) * B + b;
+  float4 v1[NMAX], v2[NMAX];
+  ksum_load<NMAX>(part, ksp, i1, v1);
+  ksum_load<NMAX>(part, ksp, i2, v2);
+  const float2 csn = *(const float2 *)(rope + ((size_t)b * hd + i) * 2);
+  RmsLoads rl;
+  rms_load<256>(ss, nss, B, rl);
+  rms_finish<256>(ss, nss, B, H, eps, rl, part_s, inv_s);  // has barriers: every thread
+  const float x1 = ksum_add<NMAX>(part, ksp, ksplit, i1, v1);
+  const float x2 = ksum_add<NMAX>(part, ksp, ksplit, i2, v2);
+  if (!act) return;
+  const float inv = inv_s[b];
+  const float y1 = x1 * inv, y2 = x2 * inv;
+  const bool rot = head < nq + nkv;
+  float *dst = head < nq ? q + ((size_t)b * nq + head) * d
+               : head < nq + nkv ? ks + ((size_t)b * nkv + (head - nq)) * d
+                                 : vs + ((size_t)b * nkv + (head - nq - nkv)) * d;
+  dst[i] = rot ? y1 * csn.x - y2 * csn.y : y1;
+  dst[i + hd] = rot ? y2 * csn.x + y1 * csn.y : y2;
+}
+
 hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
                          const void *wk, const void *wv, const LoraTail &tail, hipStream_t s) {
-  return launch_qkv_rope_fused(dm, p, w, wq, wk, wv, tail, s);
+  if (!p.qkv_split || tail.tkb > 0) return launch_qkv_rope_fused(dm, p, w, wq, wk, wv, tail, s);
+  hipError_t e = launch_gemv_mx(p, p.g_qkv, wq, dm.nq * dm.d, wk, dm.nkv * dm.d, wv,
+                                dm.nkv * dm.d, w.opA, w.part, s);
+  if (e != hipSuccess) return e;
+  const int n = (dm.nq + 2 * dm.nkv) * (dm.d / 2) * p.B;
+  const int ksp = ksp_of(p.g_qkv);
+#define KVPRM_F(NM)                                                                           \
+  hipLaunchKernelGGL(k_qkv_fin_mx<NM>, dim3((n + 255) / 256), dim3(256), 0, s, w.part, ksp,   \
+                     p.g_qkv.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.nq, dm.nkv, dm.d,     \
+                     w.rope, w.q, w.kself, w.vself)
+  switch (ksum_nmax(ksp)) {
+    case 1: KVPRM_F(1); break;
+    case 2: KVPRM_F(2); break;
+    case 4: KVPRM_F(4); break;
+    default: KVPRM_F(8); break;
+  }
+#undef KVPRM_F
+  return hipGetLastError();
 }
 
 // scale * (sum of the k-partials) of adapter row r (segment r / rank, index r % rank) for
