@@ -31,6 +31,7 @@
 // candidates 0..7; otherwise columns [0, Bp) are hi and [Bp, 2 Bp) lo (Bp = batch rounded up
 // to 16). Columns of absent candidates only ever reach outputs that are discarded.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "kvprm_internal.h"
@@ -505,6 +506,9 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   // global row tiles of this block
   int tile[MT];
   tile[0] = blockIdx.x;
+  if (EPI == EPI_RESID)  // MT consecutive row tiles
+#pragma unroll
+    for (int m = 0; m < MT; ++m) tile[m] = blockIdx.x * MT + m;
   if (EPI == EPI_SWIGLU && MT > 1) tile[MT - 1] = blockIdx.x + a.F / 16;
   if (EPI == EPI_ROPE) {  // block = (head, tile of the head's first half)
     const int half = a.d / 32;
@@ -638,23 +642,26 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   const bool cand_ok = NT == 1 ? (n < 8 && n < B) : cand < B;
   const int b = cand_ok ? cand : 0;
   if (EPI == EPI_RESID) {
-    float sq = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = tile[0] * 16 + 4 * cq + i;
-      float xv = 0.f;
-      if (cand_ok) {
-        xv = a.x[(size_t)b * a.H + r] + y[0][i];
-        a.x[(size_t)b * a.H + r] = xv;
-        if (a.xsave) a.xsave[(size_t)b * a.H + r] = xv;
-        if (a.gamma) store_operand(a.op, a.NT, a.Bp, r, b, xv * ld_bf16(a.gamma, r));
+    for (int m = 0; m < MT; ++m) {
+      float sq = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = tile[m] * 16 + 4 * cq + i;
+        float xv = 0.f;
+        if (cand_ok) {
+          xv = a.x[(size_t)b * a.H + r] + y[m][i];
+          a.x[(size_t)b * a.H + r] = xv;
+          if (a.xsave) a.xsave[(size_t)b * a.H + r] = xv;
+          if (a.gamma) store_operand(a.op, a.NT, a.Bp, r, b, xv * ld_bf16(a.gamma, r));
+        }
+        sq += xv * xv;
       }
-      sq += xv * xv;
+      // rows of the tile: the 4 lane groups cq, in a fixed order
+      sq += __shfl_xor(sq, 16, 64);
+      sq += __shfl_xor(sq, 32, 64);
+      if (cand_ok && cq == 0) a.ss[(size_t)tile[m] * B + b] = sq;
     }
-    // rows of the tile: the 4 lane groups cq, in a fixed order
-    sq += __shfl_xor(sq, 16, 64);
-    sq += __shfl_xor(sq, 32, 64);
-    if (cand_ok && cq == 0) a.ss[(size_t)tile[0] * B + b] = sq;
   } else if (EPI == EPI_ROPE) {
     const float inv = NT == 1 ? wave_rms_finish(a.ss, a.nss, B, b, a.H, a.eps, wl) : inv_s[b];
     const int d = a.d, hd = d / 2;
@@ -1626,6 +1633,13 @@ static void set_tail(FusedArgs &a, const Plan &p, const Workspace &w, const Lora
 // fused projections
 static hipError_t launch_resid_fused(const Plan &p, const FusedArgs &a, int tiles, hipStream_t s) {
   const dim3 grid(tiles);
+  // two row tiles per wave, one operand read for both, when that still leaves a block for every
+  // compute unit: two candidate tiles (9 to 16 candidates) and at least 512 row tiles (H = 8192:
+  // 28.9 -> 26.7 ms per call of the large fp8 workload)
+  if (p.nt == 2 && tiles % 2 == 0 && tiles >= 512) {
+    hipLaunchKernelGGL((k_gemv_fused<2, 2, 8, 4, EPI_RESID>), dim3(tiles / 2), dim3(512), 0, s, a);
+    return hipGetLastError();
+  }
   switch (p.nt) {
     case 1: hipLaunchKernelGGL((k_gemv_fused<1, 1, 16, 4, EPI_RESID>), grid, dim3(64 * 16), 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_gemv_fused<1, 2, 8, 4, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
@@ -1685,6 +1699,12 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
   constexpr int WW = 8, UW = 4;  // waves and batch depth of the shared-operand kernel
   const dim3 wgrid((dm.F / 16 + WW / 2 - 1) / (WW / 2));
   const bool wide = (dm.H / 32) % UW == 0;
+  // 9 to 16 candidates: the shared-operand kernel pays for long inputs (H = 8192: 26.8 -> 24.8 ms
+  // per call of the large fp8 workload), not at H = 3584 (4.2 -> 4.4 ms on the 7B batch of 16)
+  if (p.nt == 2 && wide && dm.H >= 8192) {
+    hipLaunchKernelGGL((k_gateup_wide<2, WW, UW>), wgrid, dim3(64 * WW), 0, s, a);
+    return hipGetLastError();
+  }
   switch (p.nt) {
     case 1: hipLaunchKernelGGL((k_gemv_fused<2, 1, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_gemv_fused<2, 2, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
