@@ -18,7 +18,9 @@ struct Dims {
 
 // Prefix-sharing groups, passed by value to the attention kernels (no host->device copy).
 constexpr int kMaxGroups = 64;
-constexpr int kPrefixWaves = 8;  // waves per shared-prefix block (16 columns each)
+constexpr int kPrefixWaves = 7;  // waves per shared-prefix block (16 columns each; 7 x 16 = 112
+                                 // columns = 16 members x 7 heads at the 7B shape, so the 448
+                                 // columns of a 64-candidate beam fill 4 blocks exactly)
 struct GroupTable {
   int n;                               // 0 = no sharing
   int start[kMaxGroups + 1];           // candidate ranges
