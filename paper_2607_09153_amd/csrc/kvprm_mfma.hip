@@ -708,9 +708,12 @@ template <int NT, int WPB, int U>
 __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
   constexpr int NG = NT / 2;         // candidate groups of 16
   constexpr int HALF = WPB / 2;      // gate/up tile pairs per block
-  constexpr int PER = U * NT / WPB;  // operand pieces per thread and batch
-  static_assert(PER * WPB == U * NT, "operand batch split evenly over the block");
-  static_assert(2 * U * NT >= HALF * NG * 4, "the up sums fit in the operand buffers");
+  constexpr int PIECES = U * NT * 64;                     // 16-byte operand pieces per batch
+  constexpr int PER = (PIECES + 64 * WPB - 1) / (64 * WPB);  // per thread (the last partly)
+  constexpr bool EVEN = PER * 64 * WPB == PIECES;
+  // the up waves' sums (HALF x NG x 64 float4) go through the two operand buffers (2 x U x NT x
+  // 64 16-byte entries)
+  static_assert(2 * U * NT >= HALF * NG, "the up sums fit in the operand buffers");
   __shared__ uint4 op_s[2][U * NT * 64];
   __shared__ float part_s[64 * WPB];
   __shared__ float inv_s[64];
@@ -738,14 +741,20 @@ __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
   // (the staging registers are plain vectors passed explicitly: as uint4 captured by reference
   // they were kept in scratch memory)
   auto load_op = [&](int bat, u32x4(&o)[PER]) {  // operand [K/32][NT][64]: a batch is U * NT * 64
-    const u32x4 *src = (const u32x4 *)a.act + (size_t)bat * U * NT * 64 + threadIdx.x;  // pieces
+    const u32x4 *src = (const u32x4 *)a.act + (size_t)bat * PIECES;  // pieces
 #pragma unroll
-    for (int i = 0; i < PER; ++i) o[i] = src[i * 64 * WPB];
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 64 * WPB;
+      o[i] = src[EVEN || e < PIECES ? e : PIECES - 1];  // (a piece past the batch is not stored)
+    }
   };
   auto store_op = [&](int buf, const u32x4(&o)[PER]) {
-    u32x4 *dst = (u32x4 *)&op_s[buf][0] + threadIdx.x;
+    u32x4 *dst = (u32x4 *)&op_s[buf][0];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) dst[i * 64 * WPB] = o[i];
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 64 * WPB;
+      if (EVEN || e < PIECES) dst[e] = o[i];
+    }
   };
   auto mma = [&](int buf, const uint4(&w)[U]) {
 #pragma unroll
@@ -1696,32 +1705,48 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
   a.nseg = 2;
   a.op = w.opD;
   const dim3 grid(dm.F / 16);
-  constexpr int WW = 8, UW = 4;  // waves and batch depth of the shared-operand kernel
-  const dim3 wgrid((dm.F / 16 + WW / 2 - 1) / (WW / 2));
+  // Shared-operand kernel (k_gateup_wide): HALF gate/up tile pairs per block (2 HALF waves),
+  // chosen so that every compute unit gets at most one block where possible: with 4 pairs, the
+  // 1184 pairs of the 7B shape make 296 blocks, and the 40 compute units holding two set the
+  // kernel's length (beam: 5 pairs, 237 blocks: 8.42 -> 7.90 ms per call).
+  constexpr int UW = 4;  // batch depth
+  const int pairs = dm.F / 16;
+  int half = (pairs + 255) / 256;
+  half = half < 4 ? 4 : (half > 8 ? 8 : half);
+  const dim3 wgrid((pairs + half - 1) / half);
   const bool wide = (dm.H / 32) % UW == 0;
+#define KVPRM_GW(NT_)                                                                                \
+  switch (half) {                                                                                 \
+    case 4: hipLaunchKernelGGL((k_gateup_wide<NT_, 8, UW>), wgrid, dim3(512), 0, s, a); break;     \
+    case 5: hipLaunchKernelGGL((k_gateup_wide<NT_, 10, UW>), wgrid, dim3(640), 0, s, a); break;    \
+    case 6: hipLaunchKernelGGL((k_gateup_wide<NT_, 12, UW>), wgrid, dim3(768), 0, s, a); break;    \
+    case 7: hipLaunchKernelGGL((k_gateup_wide<NT_, 14, UW>), wgrid, dim3(896), 0, s, a); break;    \
+    default: hipLaunchKernelGGL((k_gateup_wide<NT_, 16, UW>), wgrid, dim3(1024), 0, s, a); break;  \
+  }
   // 9 to 16 candidates: the shared-operand kernel pays for long inputs (H = 8192: 26.8 -> 24.8 ms
   // per call of the large fp8 workload), not at H = 3584 (4.2 -> 4.4 ms on the 7B batch of 16)
   if (p.nt == 2 && wide && dm.H >= 8192) {
-    hipLaunchKernelGGL((k_gateup_wide<2, WW, UW>), wgrid, dim3(64 * WW), 0, s, a);
+    KVPRM_GW(2);
     return hipGetLastError();
   }
   switch (p.nt) {
     case 1: hipLaunchKernelGGL((k_gemv_fused<2, 1, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_gemv_fused<2, 2, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
     case 4:
-      if (wide) hipLaunchKernelGGL((k_gateup_wide<4, WW, UW>), wgrid, dim3(64 * WW), 0, s, a);
+      if (wide) KVPRM_GW(4)
       else hipLaunchKernelGGL((k_gemv_fused<2, 4, 4, 2, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
       break;
     case 6:
-      if (wide) hipLaunchKernelGGL((k_gateup_wide<6, WW, UW>), wgrid, dim3(64 * WW), 0, s, a);
+      if (wide) KVPRM_GW(6)
       else hipLaunchKernelGGL((k_gemv_fused<2, 6, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
       break;
     case 8:
-      if (wide) hipLaunchKernelGGL((k_gateup_wide<8, WW, UW>), wgrid, dim3(64 * WW), 0, s, a);
+      if (wide) KVPRM_GW(8)
       else hipLaunchKernelGGL((k_gemv_fused<2, 8, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
       break;
     default: return hipErrorInvalidValue;
   }
+#undef KVPRM_GW
   return hipGetLastError();
 }
 
