@@ -694,19 +694,22 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   }
 }
 
-// Gate/up + SwiGLU for larger batches (NT >= 4 column tiles). There every input block brings
-// NT KiB of operand for 2 KiB of gate/up weights, and k_gemv_fused, whose waves split the input
-// range, reads each operand tile from L2 once per wave. Here the waves of a block own whole row
-// tiles over the full input range instead (waves 0 .. WPB/2 - 1 gate tiles t0 + w, the others
-// the matching up tiles) and share every input block's operand tiles through LDS, read from L2
-// once per block. Batches of U input blocks are double buffered: while the matrix cores work on
+// Gate/up + SwiGLU (every batch size whose input is a whole number of batches). Every input
+// block brings NT KiB of operand for 2 KiB of gate/up weights, and k_gemv_fused, whose waves
+// split the input range, reads each operand tile from L2 once per wave. Here the waves of a block
+// own whole row tiles over the full input range instead (waves 0 .. WPB/2 - 1 gate tiles t0 + w,
+// the others the matching up tiles) and share every input block's operand tiles through LDS,
+// read from L2 once per block; the launcher sizes blocks so that each compute unit holds at most
+// one where possible. Batches of U input blocks are double buffered: while the matrix cores work on
 // batch i (operand from one LDS buffer, weights in registers), batch i+1's operand tiles go into
 // the other buffer and batch i+2's loads are issued. Each output is a complete sum over the
 // input (added in a different order than k_gemv_fused's); the up waves hand their sums to the
 // gate waves through LDS for the SwiGLU epilogue.
 template <int NT, int WPB, int U>
 __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
-  constexpr int NG = NT / 2;         // candidate groups of 16
+  // candidate groups: with one column tile (B <= 8) columns b and 8 + b hold the hi and lo
+  // halves of candidate b; otherwise tiles g and NT/2 + g those of candidates 16 g .. 16 g + 15
+  constexpr int NG = NT == 1 ? 1 : NT / 2;
   constexpr int HALF = WPB / 2;      // gate/up tile pairs per block
   constexpr int PIECES = U * NT * 64;                     // 16-byte operand pieces per batch
   constexpr int PER = (PIECES + 64 * WPB - 1) / (64 * WPB);  // per thread (the last partly)
@@ -804,27 +807,31 @@ __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
   // hi + lo per candidate group; the up waves leave theirs in LDS (the operand buffers are free:
   // the last barrier of the loop follows their last read)
   float4 *xch = (float4 *)&op_s[0][0];  // [HALF][NG][64]
+  float hl[NG][4];  // hi + lo (every lane, before any branch: the one-tile case shuffles)
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      hl[gi][i] = NT == 1 ? acc[0][i] + __shfl_xor(acc[0][i], 8, 64) : acc[gi][i] + acc[gi + NG][i];
   if (up) {
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi)
-      xch[((wave - HALF) * NG + gi) * 64 + lane] =
-          make_float4(acc[gi][0] + acc[gi + NG][0], acc[gi][1] + acc[gi + NG][1],
-                      acc[gi][2] + acc[gi + NG][2], acc[gi][3] + acc[gi + NG][3]);
+      xch[((wave - HALF) * NG + gi) * 64 + lane] = make_float4(hl[gi][0], hl[gi][1], hl[gi][2], hl[gi][3]);
   }
   rms_finish<64 * WPB>(a.ss, a.nss, B, a.H, a.eps, rl, part_s, inv_s);  // has barriers
   if (up || !own) return;
   const int n = lane & 15, cq = lane >> 4;
 #pragma unroll
   for (int gi = 0; gi < NG; ++gi) {
-    const int cand = 16 * gi + n;
-    if (cand >= B) continue;
+    const int cand = NT == 1 ? n : 16 * gi + n;
+    if (cand >= B || (NT == 1 && n >= 8)) continue;
     const float inv = inv_s[cand];
     const float4 uvv = xch[(wave * NG + gi) * 64 + lane];
     const float uv4[4] = {uvv.x, uvv.y, uvv.z, uvv.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int f = tl * 16 + 4 * cq + i;
-      const float gv = (acc[gi][i] + acc[gi + NG][i]) * inv;
+      const float gv = hl[gi][i] * inv;
       const float uv = uv4[i] * inv;
       store_operand(a.op, a.NT, a.Bp, f, cand, gv / (1.0f + expf(-gv)) * uv);
       if (a.save) {
@@ -1723,10 +1730,11 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
     case 7: hipLaunchKernelGGL((k_gateup_wide<NT_, 14, UW>), wgrid, dim3(896), 0, s, a); break;    \
     default: hipLaunchKernelGGL((k_gateup_wide<NT_, 16, UW>), wgrid, dim3(1024), 0, s, a); break;  \
   }
-  // 9 to 16 candidates: the shared-operand kernel pays for long inputs (H = 8192: 26.8 -> 24.8 ms
-  // per call of the large fp8 workload), not at H = 3584 (4.2 -> 4.4 ms on the 7B batch of 16)
-  if (p.nt == 2 && wide && dm.H >= 8192) {
-    KVPRM_GW(2);
+  // with balanced blocks it is also the faster choice for 16 candidates or fewer (7B batch of 16:
+  // 4.15 -> 3.86 ms per call; ragged batch of 8: about 2% faster)
+  if (wide && p.nt <= 2) {
+    if (p.nt == 1) KVPRM_GW(1)
+    else KVPRM_GW(2)
     return hipGetLastError();
   }
   switch (p.nt) {
