@@ -1330,16 +1330,17 @@ __global__ __launch_bounds__(64 * kPrefixWaves) void k_prefix_mx(AttnArgs a) {
 // Log-sum-exp merge of the chunk partials of one (candidate b, q-head h) with the token's own
 // key/value: m = max(s_self, m_c),
 //   o = (e^{s_self - m} v_self + sum_c e^{m_c - m} acc_c) / (e^{s_self - m} + sum_c e^{m_c - m} l_c).
-// One block of 512 threads per (b, h): thread (s, d) owns output dimension d for the chunks
-// c = s, s + S, ... (S = 512 / D subsets). Every load is issued at entry (the first 16 chunk
+// One block of NTHR threads per (b, h): thread (s, d) owns output dimension d for the chunks
+// c = s, s + S, ... (S = NTHR / D subsets). Every load is issued at entry (the first 16 chunk
 // rows of each subset go to registers), so the merge costs about one memory round trip; the
 // subsets are added in a fixed order. Writes o (fp32) and/or the output projection's operand.
-template <int D>
-__global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
-  constexpr int S = 512 / D;
+template <int D, int NTHR>
+__global__ __launch_bounds__(NTHR) void k_merge_mx(AttnArgs a) {
+  constexpr int S = NTHR / D;   // chunk subsets
+  constexpr int NW = NTHR / 64;  // waves
   constexpr int R = 16;
   __shared__ float m_s[kMaxChunks], f_s[kMaxChunks];
-  __shared__ float red[3][8];
+  __shared__ float red[3][NW];
   __shared__ float sub_s[S][D];
   __shared__ float sself_s[16];
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;  // row (candidate, verify token)
@@ -1363,7 +1364,7 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
     rv[i] = c < nc ? base[(size_t)c * (D + 2) + dd] : 0.f;
   }
   float mx = -INFINITY;
-  for (int c = t; c < nc; c += 512) {
+  for (int c = t; c < nc; c += NTHR) {
     const float m = base[(size_t)c * (D + 2) + D];
     m_s[c] = m;
     f_s[c] = base[(size_t)c * (D + 2) + D + 1];  // l_c for now
@@ -1373,7 +1374,7 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
   // (rows cand kq + i); s_i = q . k_self_i / sqrt(D), one wave per key
   const size_t row0 = (size_t)cand * kq;
   const float *qr = a.q + ((size_t)b * a.nq + h) * D;
-  for (int i = wave; i <= tok; i += 8) {
+  for (int i = wave; i <= tok; i += NW) {
     const float *kr = a.kself + ((row0 + i) * a.nkv + j) * D;
     float dot = 0.f;
 #pragma unroll
@@ -1387,9 +1388,9 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
   float M = -INFINITY;
   for (int i = 0; i <= tok; ++i) M = fmaxf(M, sself_s[i]);
 #pragma unroll
-  for (int w = 0; w < 8; ++w) M = fmaxf(M, red[1][w]);
+  for (int w = 0; w < NW; ++w) M = fmaxf(M, red[1][w]);
   float ls = 0.f;
-  for (int c = t; c < nc; c += 512) {
+  for (int c = t; c < nc; c += NTHR) {
     const float f = expf(m_s[c] - M);
     ls += f * f_s[c];
     f_s[c] = f;
@@ -1399,7 +1400,7 @@ __global__ __launch_bounds__(512) void k_merge_mx(AttnArgs a) {
   __syncthreads();
   float lsum = 0.f;
 #pragma unroll
-  for (int w = 0; w < 8; ++w) lsum += red[2][w];
+  for (int w = 0; w < NW; ++w) lsum += red[2][w];
   float acc = 0.f;
 #pragma unroll
   for (int i = 0; i < R; ++i) {
@@ -1828,10 +1829,17 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
 #undef KVPRM_A
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !merge) return e;
-  if (dm.d == 64)
-    hipLaunchKernelGGL(k_merge_mx<64>, dim3(p.B, dm.nq), dim3(512), 0, s, a);
-  else
-    hipLaunchKernelGGL(k_merge_mx<128>, dim3(p.B, dm.nq), dim3(512), 0, s, a);
+  // 512 threads per (row, q-head); 256 when there are more rows than four 512-thread blocks per
+  // compute unit hold (the 64-candidate beam: 1792 rows), so that they all run in one round
+  const bool small = p.B * dm.nq > 1024;
+  const dim3 mgrid(p.B, dm.nq);
+  if (dm.d == 64) {
+    if (small) hipLaunchKernelGGL((k_merge_mx<64, 256>), mgrid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_merge_mx<64, 512>), mgrid, dim3(512), 0, s, a);
+  } else {
+    if (small) hipLaunchKernelGGL((k_merge_mx<128, 256>), mgrid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_merge_mx<128, 512>), mgrid, dim3(512), 0, s, a);
+  }
   return hipGetLastError();
 }
 
