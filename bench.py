@@ -509,7 +509,9 @@ def main():
         lora["end_to_end_gbps"] = (kv_bytes + w_bytes + lora["adapter_bytes_per_call"]) / (
             lora["ms_per_call"] * 1e-3) / 1e9
     depth = None
-    if args.depth > 1:
+    if args.depth > 1 and w.batch * args.depth > 64:  # a pass holds at most 64 rows
+        _log(f"depth-{args.depth} readout skipped: {w.batch} x {args.depth} rows exceed 64")
+    elif args.depth > 1:
         depth = time_depth(kv, dw, h, batch, args.depth, args.steps, args.warmup)
         _log(f"depth-{args.depth} readout: {depth['ms_per_call']:.3f} ms/call")
         depth["end_to_end_gbps"] = (kv_bytes + w_bytes) / (depth["ms_per_call"] * 1e-3) / 1e9

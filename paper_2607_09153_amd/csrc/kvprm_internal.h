@@ -90,6 +90,11 @@ struct Plan {
   // kernel, for shapes with more rotary tile pairs than compute units (no adapter)
   int qkv_split;
   GemvPlan g_qkv;
+  // output and down projections as split-K products whose blocks share each operand batch in
+  // LDS (k_resid_split: rs_wpb row tiles per block, kslice / 32 input blocks per slice) and a
+  // residual finish kernel, for more than 16 rows (no adapter); 0 = the fused kernel
+  int rs_wpb;
+  GemvPlan g_rs_o, g_rs_d;
   size_t part_elems;
 };
 

@@ -82,6 +82,22 @@ static GemvPlan gemv_plan(int rows, int K, int B) {
   return g;
 }
 
+// Split-K plan of k_resid_split (wpb row tiles per block, batches of 4 input blocks): as many
+// input slices as leave about one block per compute unit, each slice a whole number of batches.
+static GemvPlan resid_split_plan(int rows, int K, int wpb) {
+  GemvPlan g;
+  g.rows = rows;
+  g.K = K;
+  const int groups = (rows / 16 + wpb - 1) / wpb;
+  const int nkb = K / 32;
+  int want = 256 / groups;
+  if (want < 1) want = 1;
+  const int kb_per = ((nkb + want - 1) / want + 3) & ~3;
+  g.kslice = kb_per * 32;
+  g.ksplit = (nkb + kb_per - 1) / kb_per;
+  return g;
+}
+
 static size_t partial_elems(const GemvPlan &g) {
   return (size_t)((g.ksplit + 3) & ~3) * g.rows;
 }
@@ -130,6 +146,19 @@ Plan make_plan(const Dims &dm, int Breal, int max_pages, int lora_rank, int dept
       p.qkv_split = 1;
       p.g_qkv = gemv_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B);
       m = partial_elems(p.g_qkv) > m ? partial_elems(p.g_qkv) : m;
+    }
+    // more than 16 rows: the fused output and down kernels would read NT KiB of operand from L2
+    // per 1 KiB weight tile in each of their H / 16 blocks
+    if (p.nt >= 4 && lora_rank == 0 && (dm.nq * dm.d / 32) % 4 == 0 && (dm.F / 32) % 4 == 0) {
+      // (8 row tiles per block measured faster than 16: 6.74 against 6.79 ms per call of the
+      // 64-candidate beam, 7.92 with the fused kernels)
+      p.rs_wpb = 8;
+      p.g_rs_o = resid_split_plan(dm.H, dm.nq * dm.d, p.rs_wpb);
+      p.g_rs_d = resid_split_plan(dm.H, dm.F, p.rs_wpb);
+      for (const GemvPlan *g : {&p.g_rs_o, &p.g_rs_d}) {
+        const size_t e = (size_t)g->ksplit * g->rows;
+        m = e > m ? e : m;
+      }
     }
   } else {
     // vector-ALU GEMV: the activation slice of all B candidates is staged in LDS (<= 32 KiB)

@@ -842,6 +842,132 @@ __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
   }
 }
 
+// Split-K residual projection (output, down) for more than 16 candidates. At NT >= 4 column
+// tiles every input block brings NT KiB of operand for each 1 KiB weight tile, and a block that
+// owns one row tile over the whole input (k_gemv_fused) pulls its whole operand from L2 for 1/224
+// of the weights. Here block (g, ks) owns row tiles g WPB .. g WPB + WPB - 1 (one per wave) over
+// input slice ks: each batch of U input blocks of the operand is staged once in LDS and read by
+// all WPB waves (double buffered, loaded one batch ahead; the weights two batches ahead, as in
+// k_gateup_wide), and the plan sizes the grid at about one block per compute unit. Each wave
+// writes its tile's slice sums (hi + lo) to part[ks][candidate][row]; k_resid_split_fin adds the
+// slices in order and runs the residual epilogue.
+struct SplitArgs {
+  const void *w;     // packed weights, rows x K
+  int rows, nkb;     // row count, input blocks of 32
+  int kb_per;        // input blocks per slice (a multiple of U)
+  const uint4 *act;  // operand [K / 32][NT][64]
+  int B;
+  float *part;       // [ksplit][B][rows]
+};
+
+template <int NT, int WPB, int U>
+__global__ __launch_bounds__(64 * WPB) void k_resid_split(SplitArgs a) {
+  constexpr int NG = NT / 2;  // candidate groups of 16 (tiles g and NG + g: hi and lo)
+  constexpr int PIECES = U * NT * 64;  // 16-byte operand pieces per batch
+  constexpr int PER = PIECES / (64 * WPB);
+  static_assert(NT >= 2 && PER * 64 * WPB == PIECES, "operand batch split evenly over the block");
+  __shared__ uint4 op_s[2][U * NT * 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ks = blockIdx.y;
+  const int kb0 = ks * a.kb_per;
+  const int nbat = min(a.kb_per, a.nkb - kb0) / U;
+  const int ntiles = a.rows / 16;
+  const int tile = (int)blockIdx.x * WPB + wave;
+  const bool own = tile < ntiles;
+  const int tl = own ? tile : ntiles - 1;  // past the end: repeat the last tile (not stored)
+  const size_t kstride = (size_t)ntiles * 64;
+  const uint4 *wp = (const uint4 *)a.w + ((size_t)kb0 * ntiles + tl) * 64 + lane;
+  const u32x4 *src = (const u32x4 *)a.act + (size_t)kb0 * NT * 64 + threadIdx.x;
+  floatx4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  uint4 wa[U], wb[U];
+  u32x4 ov[PER];
+  auto load_w = [&](int bat, uint4(&w)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) w[u] = ld_stream(&wp[(size_t)(bat * U + u) * kstride]);
+  };
+  auto load_op = [&](int bat, u32x4(&o)[PER]) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) o[i] = src[(size_t)bat * PIECES + i * 64 * WPB];
+  };
+  auto store_op = [&](int buf, const u32x4(&o)[PER]) {
+    u32x4 *dst = (u32x4 *)&op_s[buf][0] + threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) dst[i * 64 * WPB] = o[i];
+  };
+  auto mma = [&](int buf, const uint4(&w)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = mfma16(w[u], op_s[buf][(u * NT + t) * 64 + lane], acc[t]);
+  };
+  if (nbat > 0) {
+    load_op(0, ov);
+    store_op(0, ov);
+    load_w(0, wa);
+    if (nbat > 1) {
+      load_op(1, ov);
+      load_w(1, wb);
+    }
+  }
+  __syncthreads();
+  for (int bat = 0; bat < nbat; bat += 2) {  // block-uniform trip counts and barriers
+    mma(0, wa);
+    if (bat + 1 < nbat) store_op(1, ov);  // buffer 1 was last read before the previous barrier
+    if (bat + 2 < nbat) {
+      load_op(bat + 2, ov);
+      load_w(bat + 2, wa);
+    }
+    __syncthreads();
+    if (bat + 1 >= nbat) break;
+    mma(1, wb);
+    if (bat + 2 < nbat) store_op(0, ov);
+    if (bat + 3 < nbat) {
+      load_op(bat + 3, ov);
+      load_w(bat + 3, wb);
+    }
+    __syncthreads();
+  }
+  if (!own) return;
+  // lane (n, cq) holds rows 4 cq .. 4 cq + 3 of the tile for candidate 16 gi + n
+  const int n = lane & 15, cq = lane >> 4;
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi) {
+    const int cand = 16 * gi + n;
+    if (cand >= a.B) continue;
+    const float4 v = make_float4(acc[gi][0] + acc[gi + NG][0], acc[gi][1] + acc[gi + NG][1],
+                                 acc[gi][2] + acc[gi + NG][2], acc[gi][3] + acc[gi + NG][3]);
+    *(float4 *)(a.part + ((size_t)ks * a.B + cand) * a.rows + tile * 16 + 4 * cq) = v;
+  }
+}
+
+// Residual epilogue of k_resid_split, one output (candidate b, row r) per thread, e = b H + r:
+// y = the slice sums added in slice order, x += y, the next operand x * gamma (if gamma), and the
+// sum of squares of the new x over each 16-row tile (16 consecutive lanes, a fixed shuffle order).
+__global__ __launch_bounds__(256) void k_resid_split_fin(const float *__restrict__ part, int ksplit,
+                                                         float *x, float *xsave, float *ss, int H,
+                                                         int B, const void *gamma, uint16_t *op,
+                                                         int NT, int Bp) {
+  const int e = (int)blockIdx.x * 256 + threadIdx.x;
+  if (e >= B * H) return;  // (whole 16-lane groups: H is a multiple of 16)
+  const int b = e / H, r = e - b * H;
+  const size_t stride = (size_t)B * H;
+  float y = 0.f;
+#pragma unroll 8
+  for (int k = 0; k < ksplit; ++k) y += part[(size_t)k * stride + e];
+  const float xv = x[e] + y;
+  x[e] = xv;
+  if (xsave) xsave[e] = xv;
+  if (gamma) store_operand(op, NT, Bp, r, b, xv * ld_bf16(gamma, r));
+  float sq = xv * xv;
+  sq += __shfl_xor(sq, 1, 64);
+  sq += __shfl_xor(sq, 2, 64);
+  sq += __shfl_xor(sq, 4, 64);
+  sq += __shfl_xor(sq, 8, 64);
+  if ((r & 15) == 0) ss[(size_t)(r >> 4) * B + b] = sq;
+}
+
 __global__ __launch_bounds__(256) void k_pack_weight(const uint4 *src, uint4 *dst, int64_t rows,
                                                      int64_t K) {
   const int64_t ngroups = rows * K / 8;
@@ -1668,6 +1794,35 @@ static hipError_t launch_resid_fused(const Plan &p, const FusedArgs &a, int tile
   return hipGetLastError();
 }
 
+// k_resid_split over the plan's slices, then k_resid_split_fin (next operand into w.opA)
+static hipError_t launch_resid_split(const Dims &dm, const Plan &p, const Workspace &w,
+                                     const GemvPlan &g, const void *wt, const uint16_t *act,
+                                     const void *gamma, float *xsave, hipStream_t s) {
+  SplitArgs a;
+  a.w = wt;
+  a.rows = g.rows;
+  a.nkb = g.K / 32;
+  a.kb_per = g.kslice / 32;
+  a.act = (const uint4 *)act;
+  a.B = p.B;
+  a.part = w.part;
+  constexpr int U = 4, WPB = 8;  // (the plan's slices are whole batches of U input blocks)
+  if (p.rs_wpb != WPB) return hipErrorInvalidValue;
+  const dim3 grid((g.rows / 16 + WPB - 1) / WPB, g.ksplit);
+  switch (p.nt) {
+    case 4: hipLaunchKernelGGL((k_resid_split<4, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
+    case 6: hipLaunchKernelGGL((k_resid_split<6, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_resid_split<8, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int n = p.B * dm.H;
+  hipLaunchKernelGGL(k_resid_split_fin, dim3((n + 255) / 256), dim3(256), 0, s, w.part, g.ksplit,
+                     w.x, xsave, w.ss, dm.H, p.B, gamma, w.opA, p.nt, p.bp);
+  return hipGetLastError();
+}
+
 static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, int K,
                             const uint16_t *act) {
   FusedArgs a;
@@ -1689,6 +1844,8 @@ static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, i
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
                               const void *gamma_ffn, const LoraTail &tail, hipStream_t s,
                               float *xsave) {
+  if (p.rs_wpb && tail.tkb == 0)
+    return launch_resid_split(dm, p, w, p.g_rs_o, wo, w.opO, gamma_ffn, xsave, s);
   FusedArgs a = fused_args(dm, p, w, dm.nq * dm.d, w.opO);
   a.xsave = xsave;
   set_tail(a, p, w, tail);
@@ -1762,6 +1919,8 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
 hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
                              const void *gamma_next, const LoraTail &tail, hipStream_t s,
                              float *xsave) {
+  if (p.rs_wpb && tail.tkb == 0)
+    return launch_resid_split(dm, p, w, p.g_rs_d, wd, w.opD, gamma_next, xsave, s);
   FusedArgs a = fused_args(dm, p, w, dm.F, w.opD);
   a.xsave = xsave;
   set_tail(a, p, w, tail);
