@@ -309,7 +309,7 @@ def _cpu_model():
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_ragged_32k_traffic.txt")
 ATTN_SOURCES = [os.path.join(ROOT, "paper_2607_09153_amd", "csrc", f)
-                for f in ("kvprm_mfma.hip", "kvprm_internal.h")]
+                for f in ("kvprm_attn.hip", "kvprm_mx_common.h")]
 
 
 def attention_source_hash():
@@ -323,8 +323,8 @@ def attention_source_hash():
 def measured_traffic(workload):
     """HBM bytes per launch of the attention chunk kernel from the committed FETCH_SIZE /
     WRITE_SIZE summary, scaled by the copy-kernel calibration recorded there; None when the
-    summary is for another workload or the attention sources have changed since the counters
-    were taken."""
+    summary is for another workload or the attention kernel's sources (kvprm_attn.hip and the
+    device helpers it includes) have changed since the counters were taken."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     kv = {}

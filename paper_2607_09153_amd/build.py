@@ -6,7 +6,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 LIB = os.path.join(HERE, "libkvprm.so")
-SOURCES = ["kvprm_api.hip", "kvprm_kernels.hip", "kvprm_mfma.hip", "kvprm_grad.hip"]
+SOURCES = ["kvprm_api.hip", "kvprm_kernels.hip", "kvprm_mfma.hip", "kvprm_attn.hip", "kvprm_grad.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-shared", "-std=c++17",
          # packed fp32 instructions are disabled on purpose for this target
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

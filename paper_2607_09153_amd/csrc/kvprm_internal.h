@@ -134,7 +134,7 @@ hipError_t launch_backward(const Dims &dm, const Plan &p, const Workspace &w, co
                            int CP, int chunks, float *grad_k, float *grad_v, float eta,
                            hipStream_t s);
 
-// matrix-core helpers (kvprm_mfma.hip)
+// matrix-core helpers (kvprm_mfma.hip; the attention launcher is in kvprm_attn.hip)
 int gemv_nt(int B);
 int gemv_bp(int B);
 int gemv_mt(int nt, int rows);

@@ -1,5 +1,6 @@
 // HIP kernels of the verify-token pass (gfx950). Vector-ALU versions for every dtype; the
-// matrix-core (MFMA) kernels for bf16 weights and bf16/fp8 caches live in kvprm_mfma.hip.
+// matrix-core (MFMA) kernels for bf16 weights and bf16/fp8 caches live in kvprm_mfma.hip
+// (projections) and kvprm_attn.hip (attention).
 //
 // Per layer the pass runs: RMSNorm+QKV projection (split-K partials) -> sum partials + rotary
 // -> split-L paged attention partials -> log-sum-exp merge with the token's own key -> output
