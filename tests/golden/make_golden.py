@@ -22,10 +22,12 @@ from oracle import kvprm_oracle as ko  # noqa: E402
 
 # sampled candidates of each batch: the first, the longest and the shortest cached sequence among
 # them (ragged: 2 is the longest at 31832 tokens and fills the most chunk slots, 1 the shortest;
-# beam: 2 the longest suffix, 0 the shortest; large fp8: 0 the longest, 14 the shortest at 8834)
+# beam: 2 the longest suffix, 0 the shortest; large fp8: 0 the longest, 14 the shortest at 8834;
+# fixed 32k: every candidate holds 32768 tokens, so the first and the last)
 SAMPLES = {
     "b7_bf16": [0, 7, 15],
     "ragged_32k": [0, 1, 2, 5],
+    "fixed_32k": [0, 7],
     "beam_prefix": [0, 2, 33, 63],
     "large_fp8": [0, 9, 14],
 }

@@ -18,7 +18,7 @@ from gpu_common import run_score
 pytestmark = pytest.mark.gpu
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
-WORKLOADS = ["b7_bf16", "ragged_32k", "beam_prefix", "large_fp8"]
+WORKLOADS = ["b7_bf16", "ragged_32k", "fixed_32k", "beam_prefix", "large_fp8"]
 
 
 @pytest.mark.parametrize("name", WORKLOADS)
