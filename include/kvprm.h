@@ -181,7 +181,7 @@ kvprm_status kvprm_score(kvprm_handle h, const kvprm_kv_cache *cache, const kvpr
  * that the library holds on every GPU it runs on until the process ends; nothing is allocated
  * or freed by the call. It serves batches whose kvprm_workspace_size is at most that size
  * (8 candidates with up to 32768 cached tokens at the 7B shape need 16 MiB; 64 candidates with
- * 18432 tokens each need 79 MiB and are refused); a larger one returns KVPRM_E_WORKSPACE before
+ * 18432 tokens each need 87 MiB and are refused); a larger one returns KVPRM_E_WORKSPACE before
  * anything is enqueued.
  * Every call on one GPU, from any handle or thread, uses the same array, which keeps the
  * previous call's contents (no call needs it cleared): calls whose work overlaps on one GPU
