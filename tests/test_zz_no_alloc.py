@@ -55,6 +55,24 @@ def test_static_workspace_equals_caller_workspace_twice_then_smaller():
         torch.cuda.empty_cache()
 
 
+def test_static_workspace_more_than_16_rows():
+    """More than 16 candidates: the output and down projections run as split-K products whose
+    slice partials live in the workspace; two calls in a row, the second with fewer rows."""
+    shape = dataclasses.replace(synth.B7, num_layers=2)
+    for B, seed in ((40, 5152), (20, 5153)):
+        lengths = [(53 * i * i + 7 * i) % 1500 for i in range(B)]
+        w = synth.make_workload("custom", shape=shape, lengths=lengths, seed=seed)
+        _say(f"case: static workspace, B={w.batch} (split-K output/down)")
+        dw = DeviceWorkload(w, nan_unused_pages=True)
+        p_s, z_s = _static_scores(dw)
+        p_r, z_r = run_score(dw)
+        _say(f"  max|dP| vs caller workspace {np.max(np.abs(p_s - p_r)):.2e}")
+        assert np.all(np.isfinite(p_s)) and np.all(np.isfinite(z_s))
+        assert np.array_equal(p_s, p_r) and np.array_equal(z_s, z_r)
+        del dw
+        torch.cuda.empty_cache()
+
+
 def test_static_workspace_fp32_tiny_and_refusal():
     w = synth.make_workload("tiny_fp32")
     _say(f"case: static workspace tiny fp32 B={w.batch}")
