@@ -320,8 +320,8 @@ static kvprm_status check_lora(const kvprm_handle h, const kvprm_lora *lora, con
 // prefixes): the q/k/v projection with the RMSNorm scale and the rotary embedding in its
 // epilogue, the attention chunk kernel(s) and their merge, then the output, gate/up and down
 // projections with their element-wise steps fused (no split-K partials; with more than 16 rows
-// and no adapter the output and down projections are split-K products with a residual finish
-// kernel each, eight launches per layer). With an adapter, each
+// and no adapter the q/k/v, output and down projections are split-K products with a finish
+// kernel each, nine launches per layer). With an adapter, each
 // projection group that has one first computes scale * A u (a split-K GEMV and its finish) and
 // the projection adds B (scale * A u) as a tail of its input range.
 // With sv, the activations the backward pass needs are kept per layer (GradSave).

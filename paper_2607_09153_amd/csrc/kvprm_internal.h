@@ -95,6 +95,8 @@ struct Plan {
   // residual finish kernel, for more than 16 rows (no adapter); 0 = the fused kernel
   int rs_wpb;
   GemvPlan g_rs_o, g_rs_d;
+  int rs_qkv;  // the q/k/v product the same way, with a rotary finish (k_qkv_split_fin)
+  GemvPlan g_rs_qkv;
   size_t part_elems;
 };
 

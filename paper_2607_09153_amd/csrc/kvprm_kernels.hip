@@ -156,7 +156,11 @@ Plan make_plan(const Dims &dm, int Breal, int max_pages, int lora_rank, int dept
       p.rs_wpb = 8;
       p.g_rs_o = resid_split_plan(dm.H, dm.nq * dm.d, p.rs_wpb);
       p.g_rs_d = resid_split_plan(dm.H, dm.F, p.rs_wpb);
-      for (const GemvPlan *g : {&p.g_rs_o, &p.g_rs_d}) {
+      if ((dm.H / 32) % 4 == 0 && (dm.nq + 2 * dm.nkv) * (dm.d / 2) >= 64) {
+        p.rs_qkv = 1;
+        p.g_rs_qkv = resid_split_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, p.rs_wpb);
+      }
+      for (const GemvPlan *g : {&p.g_rs_o, &p.g_rs_d, &p.g_rs_qkv}) {
         const size_t e = (size_t)g->ksplit * g->rows;
         m = e > m ? e : m;
       }

@@ -768,8 +768,10 @@ __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
 // writes its tile's slice sums (hi + lo) to part[ks][candidate][row]; k_resid_split_fin adds the
 // slices in order and runs the residual epilogue.
 struct SplitArgs {
-  const void *w;     // packed weights, rows x K
-  int rows, nkb;     // row count, input blocks of 32
+  const void *w[3];  // packed weight segments (e.g. q, k, v), stacked rows
+  int seg_rows[3];
+  int nseg;
+  int rows, nkb;     // row count (all segments), input blocks of 32
   int kb_per;        // input blocks per slice (a multiple of U)
   const uint4 *act;  // operand [K / 32][NT][64]
   int B;
@@ -787,12 +789,14 @@ __global__ __launch_bounds__(64 * WPB) void k_resid_split(SplitArgs a) {
   const int ks = blockIdx.y;
   const int kb0 = ks * a.kb_per;
   const int nbat = min(a.kb_per, a.nkb - kb0) / U;
-  const int ntiles = a.rows / 16;
   const int tile = (int)blockIdx.x * WPB + wave;
-  const bool own = tile < ntiles;
-  const int tl = own ? tile : ntiles - 1;  // past the end: repeat the last tile (not stored)
-  const size_t kstride = (size_t)ntiles * 64;
-  const uint4 *wp = (const uint4 *)a.w + ((size_t)kb0 * ntiles + tl) * 64 + lane;
+  const bool own = tile < a.rows / 16;
+  const int tl = own ? tile : a.rows / 16 - 1;  // past the end: repeat the last tile (not stored)
+  int seg = 0, base = 0;  // the tile's weight segment
+  while (seg < a.nseg - 1 && tl * 16 >= base + a.seg_rows[seg]) base += a.seg_rows[seg++];
+  const size_t ntiles = (size_t)a.seg_rows[seg] / 16;
+  const size_t kstride = ntiles * 64;
+  const uint4 *wp = (const uint4 *)a.w[seg] + ((size_t)kb0 * ntiles + (tl - base / 16)) * 64 + lane;
   const u32x4 *src = (const u32x4 *)a.act + (size_t)kb0 * NT * 64 + threadIdx.x;
   floatx4 acc[NT];
 #pragma unroll
@@ -882,6 +886,59 @@ __global__ __launch_bounds__(256) void k_resid_split_fin(const float *__restrict
   sq += __shfl_xor(sq, 4, 64);
   sq += __shfl_xor(sq, 8, 64);
   if ((r & 15) == 0) ss[(size_t)(r >> 4) * B + b] = sq;
+}
+
+// Rotary epilogue of the split q/k/v product (k_resid_split over the stacked q, k, v rows), one
+// rotary pair (candidate b, head, i < d/2) per thread, consecutive threads on consecutive i: the
+// slice sums of rows r and r + d/2 of the head added in slice order, times the candidate's
+// RMSNorm scale (its sums of squares added by one wave: lane-strided, then a fixed butterfly),
+// rotated (q and k heads; v heads are not) and stored as q, k_self or v_self (fp32).
+__global__ __launch_bounds__(256) void k_qkv_split_fin(const float *__restrict__ part, int ksplit,
+                                                       const float *__restrict__ ss, int nss,
+                                                       int H, float eps, int B, int nq, int nkv,
+                                                       int d, const float *__restrict__ rope,
+                                                       float *__restrict__ q, float *__restrict__ ks,
+                                                       float *__restrict__ vs) {
+  const int hd = d / 2, nh = nq + 2 * nkv, rows = nh * d;
+  const int e = (int)blockIdx.x * 256 + threadIdx.x;
+  const bool act = e < B * nh * hd;
+  const int ec = act ? e : 0;
+  const int b = ec / (nh * hd), rem = ec - b * (nh * hd);
+  const int head = rem / hd, i = rem - head * hd;
+  const int r = head * d + i;
+  // the wave's candidates: b of its first and last active lanes (a wave spans at most two, as
+  // nh * hd >= 64); the sums of squares of both are added lane-strided by the whole wave
+  const size_t stride = (size_t)B * rows;
+  float y1 = 0.f, y2 = 0.f;
+  const float *p1 = part + (size_t)b * rows + r;
+#pragma unroll 8
+  for (int k = 0; k < ksplit; ++k) {
+    y1 += p1[(size_t)k * stride];
+    y2 += p1[(size_t)k * stride + hd];
+  }
+  // (the wave's lanes hold nondecreasing candidates; the inactive tail takes the first one)
+  int b1 = act ? b : 0;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) b1 = max(b1, __shfl_xor(b1, off, 64));
+  const int lane = threadIdx.x & 63;
+  const int b0 = __shfl(b, 0, 64);
+  float s0 = 0.f, s1 = 0.f;
+  for (int t = lane; t < nss; t += 64) {
+    s0 += ss[(size_t)t * B + b0];
+    if (b1 != b0) s1 += ss[(size_t)t * B + b1];
+  }
+  s0 = wsum(s0);
+  s1 = wsum(s1);
+  const float inv = 1.0f / sqrtf((b == b0 ? s0 : s1) / (float)H + eps);
+  if (!act) return;
+  const float2 csn = *(const float2 *)(rope + ((size_t)b * hd + i) * 2);
+  const float x1 = y1 * inv, x2 = y2 * inv;
+  const bool rot = head < nq + nkv;
+  float *dst = head < nq ? q + ((size_t)b * nq + head) * d
+               : head < nq + nkv ? ks + ((size_t)b * nkv + (head - nq)) * d
+                                 : vs + ((size_t)b * nkv + (head - nq - nkv)) * d;
+  dst[i] = rot ? x1 * csn.x - x2 * csn.y : x1;
+  dst[i + hd] = rot ? x2 * csn.x + x1 * csn.y : x2;
 }
 
 __global__ __launch_bounds__(256) void k_pack_weight(const uint4 *src, uint4 *dst, int64_t rows,
@@ -1045,8 +1102,22 @@ __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ pa
   dst[i + hd] = rot ? y2 * csn.x + y1 * csn.y : y2;
 }
 
+static hipError_t launch_split(const Plan &p, const GemvPlan &g, const void *w0, int r0,
+                               const void *w1, int r1, const void *w2, int r2,
+                               const uint16_t *act, float *part, hipStream_t s);
+
 hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
                          const void *wk, const void *wv, const LoraTail &tail, hipStream_t s) {
+  if (p.rs_qkv && tail.tkb == 0) {  // more than 16 rows: split-K product + rotary finish
+    hipError_t e = launch_split(p, p.g_rs_qkv, wq, dm.nq * dm.d, wk, dm.nkv * dm.d, wv,
+                                dm.nkv * dm.d, w.opA, w.part, s);
+    if (e != hipSuccess) return e;
+    const int n = p.B * (dm.nq + 2 * dm.nkv) * (dm.d / 2);
+    hipLaunchKernelGGL(k_qkv_split_fin, dim3((n + 255) / 256), dim3(256), 0, s, w.part,
+                       p.g_rs_qkv.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.nq, dm.nkv, dm.d,
+                       w.rope, w.q, w.kself, w.vself);
+    return hipGetLastError();
+  }
   if (!p.qkv_split || tail.tkb > 0) return launch_qkv_rope_fused(dm, p, w, wq, wk, wv, tail, s);
   hipError_t e = launch_gemv_mx(p, p.g_qkv, wq, dm.nq * dm.d, wk, dm.nkv * dm.d, wv,
                                 dm.nkv * dm.d, w.opA, w.part, s);
@@ -1149,17 +1220,23 @@ static hipError_t launch_resid_fused(const Plan &p, const FusedArgs &a, int tile
 }
 
 // k_resid_split over the plan's slices, then k_resid_split_fin (next operand into w.opA)
-static hipError_t launch_resid_split(const Dims &dm, const Plan &p, const Workspace &w,
-                                     const GemvPlan &g, const void *wt, const uint16_t *act,
-                                     const void *gamma, float *xsave, hipStream_t s) {
+static hipError_t launch_split(const Plan &p, const GemvPlan &g, const void *w0, int r0,
+                               const void *w1, int r1, const void *w2, int r2,
+                               const uint16_t *act, float *part, hipStream_t s) {
   SplitArgs a;
-  a.w = wt;
+  a.w[0] = w0;
+  a.w[1] = w1;
+  a.w[2] = w2;
+  a.seg_rows[0] = r0;
+  a.seg_rows[1] = r1;
+  a.seg_rows[2] = r2;
+  a.nseg = w2 ? 3 : (w1 ? 2 : 1);
   a.rows = g.rows;
   a.nkb = g.K / 32;
   a.kb_per = g.kslice / 32;
   a.act = (const uint4 *)act;
   a.B = p.B;
-  a.part = w.part;
+  a.part = part;
   constexpr int U = 4, WPB = 8;  // (the plan's slices are whole batches of U input blocks)
   if (p.rs_wpb != WPB) return hipErrorInvalidValue;
   const dim3 grid((g.rows / 16 + WPB - 1) / WPB, g.ksplit);
@@ -1169,7 +1246,13 @@ static hipError_t launch_resid_split(const Dims &dm, const Plan &p, const Worksp
     case 8: hipLaunchKernelGGL((k_resid_split<8, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+static hipError_t launch_resid_split(const Dims &dm, const Plan &p, const Workspace &w,
+                                     const GemvPlan &g, const void *wt, const uint16_t *act,
+                                     const void *gamma, float *xsave, hipStream_t s) {
+  hipError_t e = launch_split(p, g, wt, dm.H, nullptr, 0, nullptr, 0, act, w.part, s);
   if (e != hipSuccess) return e;
   const int n = p.B * dm.H;
   hipLaunchKernelGGL(k_resid_split_fin, dim3((n + 255) / 256), dim3(256), 0, s, w.part, g.ksplit,
