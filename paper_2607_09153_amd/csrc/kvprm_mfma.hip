@@ -758,15 +758,16 @@ __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
   }
 }
 
-// Split-K residual projection (output, down) for more than 16 candidates. At NT >= 4 column
-// tiles every input block brings NT KiB of operand for each 1 KiB weight tile, and a block that
-// owns one row tile over the whole input (k_gemv_fused) pulls its whole operand from L2 for 1/224
-// of the weights. Here block (g, ks) owns row tiles g WPB .. g WPB + WPB - 1 (one per wave) over
-// input slice ks: each batch of U input blocks of the operand is staged once in LDS and read by
-// all WPB waves (double buffered, loaded one batch ahead; the weights two batches ahead, as in
-// k_gateup_wide), and the plan sizes the grid at about one block per compute unit. Each wave
-// writes its tile's slice sums (hi + lo) to part[ks][candidate][row]; k_resid_split_fin adds the
-// slices in order and runs the residual epilogue.
+// Split-K projection (q/k/v, output, down) for more than 16 candidates. At NT >= 4 column tiles
+// every input block brings NT KiB of operand for each 1 KiB weight tile, and a block that owns
+// one row tile (or tile pair) over the whole input (k_gemv_fused) pulls its whole operand from
+// L2 for a few hundredth of the weights. Here block (g, ks) owns row tiles g WPB .. g WPB + WPB
+// - 1 (one per wave; the rows may stack up to three weight segments) over input slice ks: each
+// batch of U input blocks of the operand is staged once in LDS and read by all WPB waves (double
+// buffered, loaded one batch ahead; the weights two batches ahead, as in k_gateup_wide), and the
+// plan sizes the grid at about one block per compute unit. Each wave writes its tile's slice
+// sums (hi + lo) to part[ks][candidate][row]; k_resid_split_fin (output, down: the residual
+// epilogue) or k_qkv_split_fin (q/k/v: RMSNorm scale and rotation) adds the slices in order.
 struct SplitArgs {
   const void *w[3];  // packed weight segments (e.g. q, k, v), stacked rows
   int seg_rows[3];
