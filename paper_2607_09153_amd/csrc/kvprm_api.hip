@@ -316,12 +316,12 @@ static kvprm_status check_lora(const kvprm_handle h, const kvprm_lora *lora, con
   return KVPRM_OK;
 }
 
-// The matrix-core pipeline (bf16 weights): six launches per layer (seven with shared
-// prefixes): the q/k/v projection with the RMSNorm scale and the rotary embedding in its
-// epilogue, the attention chunk kernel(s) and their merge, then the output, gate/up and down
-// projections with their element-wise steps fused (no split-K partials; with more than 16 rows
-// and no adapter the q/k/v, output and down projections are split-K products with a finish
-// kernel each, nine launches per layer). With an adapter, each
+// The matrix-core pipeline (bf16 weights), per layer: the q/k/v projection with the RMSNorm
+// scale and the rotary embedding in its epilogue, the attention chunk kernel(s) and their merge,
+// then the output, gate/up and down projections with their element-wise steps fused. The down
+// projection (all batch sizes), q/k/v (more than 8 rows) and the output projection (more than 16
+// rows, or large shapes) run instead as split-K products with a finish kernel each: seven to
+// nine launches per layer (one more with shared prefixes). With an adapter, each
 // projection group that has one first computes scale * A u (a split-K GEMV and its finish) and
 // the projection adds B (scale * A u) as a tail of its input range.
 // With sv, the activations the backward pass needs are kept per layer (GradSave).

@@ -90,10 +90,11 @@ struct Plan {
   // kernel, for shapes with more rotary tile pairs than compute units (no adapter)
   int qkv_split;
   GemvPlan g_qkv;
-  // output and down projections as split-K products whose blocks share each operand batch in
-  // LDS (k_resid_split: rs_wpb row tiles per block, kslice / 32 input blocks per slice) and a
-  // residual finish kernel, for more than 16 rows (no adapter); 0 = the fused kernel
+  // projections as split-K products whose blocks share each operand batch in LDS
+  // (k_resid_split: rs_wpb row tiles per block, kslice / 32 input blocks per slice, an adapter's
+  // B-factor tail as one more slice) and a finish kernel, by batch size; 0 = the fused kernels
   int rs_wpb;
+  int rs_o, rs_d;  // output / down projection split
   GemvPlan g_rs_o, g_rs_d;
   int rs_qkv;  // the q/k/v product the same way, with a rotary finish (k_qkv_split_fin)
   GemvPlan g_rs_qkv;

@@ -83,9 +83,9 @@ static GemvPlan gemv_plan(int rows, int K, int B) {
   return g;
 }
 
-// Split-K plan of k_resid_split (wpb row tiles per block, batches of 4 input blocks): as many
+// Split-K plan of k_resid_split (wpb row tiles per block, batches of U input blocks): as many
 // input slices as leave about one block per compute unit, each slice a whole number of batches.
-static GemvPlan resid_split_plan(int rows, int K, int wpb) {
+static GemvPlan resid_split_plan(int rows, int K, int wpb, int U) {
   GemvPlan g;
   g.rows = rows;
   g.K = K;
@@ -93,7 +93,7 @@ static GemvPlan resid_split_plan(int rows, int K, int wpb) {
   const int nkb = K / 32;
   int want = 256 / groups;
   if (want < 1) want = 1;
-  const int kb_per = ((nkb + want - 1) / want + 3) & ~3;
+  const int kb_per = ((nkb + want - 1) / want + U - 1) / U * U;
   g.kslice = kb_per * 32;
   g.ksplit = (nkb + kb_per - 1) / kb_per;
   return g;
@@ -148,21 +148,35 @@ Plan make_plan(const Dims &dm, int Breal, int max_pages, int lora_rank, int dept
       p.g_qkv = gemv_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, B);
       m = partial_elems(p.g_qkv) > m ? partial_elems(p.g_qkv) : m;
     }
-    // more than 16 rows: the fused output and down kernels would read NT KiB of operand from L2
-    // per 1 KiB weight tile in each of their H / 16 blocks
-    if (p.nt >= 4 && lora_rank == 0 && (dm.nq * dm.d / 32) % 4 == 0 && (dm.F / 32) % 4 == 0) {
-      // (8 row tiles per block measured faster than 16: 6.74 against 6.79 ms per call of the
-      // 64-candidate beam, 7.92 with the fused kernels)
-      p.rs_wpb = 8;
-      p.g_rs_o = resid_split_plan(dm.H, dm.nq * dm.d, p.rs_wpb);
-      p.g_rs_d = resid_split_plan(dm.H, dm.F, p.rs_wpb);
-      if ((dm.H / 32) % 4 == 0 && (dm.nq + 2 * dm.nkv) * (dm.d / 2) >= 64) {
-        p.rs_qkv = 1;
-        p.g_rs_qkv = resid_split_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, p.rs_wpb);
-      }
-      for (const GemvPlan *g : {&p.g_rs_o, &p.g_rs_d, &p.g_rs_qkv}) {
-        const size_t e = (size_t)g->ksplit * g->rows;
-        m = e > m ? e : m;
+    // Split-K projections (k_resid_split + a finish kernel): a fused kernel's block owns whole
+    // rows over the whole input and reads the whole operand (NT KiB per input block) from L2,
+    // for H / 16 row tiles (224 at the 7B shape, under one block per compute unit); the split
+    // blocks share each operand batch over 8 row tiles and cover all compute units, at the cost
+    // of one more launch. Measured per call: the down projection for every batch size (ragged
+    // 32k 4.79-4.82 -> 4.73-4.76 ms, 7B batch of 16 3.86 -> 3.59), q/k/v too for 9-16 rows (3.57),
+    // all three for 9-16 rows with at least 512 row tiles (large fp8 24.6 -> 23.7) and for more
+    // than 16 rows (beam 7.92 -> 6.74 with output and down, 6.8 -> 6.75 with q/k/v).
+    {
+      const int U = p.nt == 1 ? 8 : 4;  // input blocks per batch of k_resid_split
+      // bits: 1 down, 2 output, 4 q/k/v
+      const int mask = p.nt >= 4 ? 7 : p.nt == 2 ? (dm.H / 16 >= 512 ? 7 : 5) : 1;
+      if ((dm.nq * dm.d / 32) % U == 0 && (dm.F / 32) % U == 0) {
+        // (8 row tiles per block measured faster than 16: 6.74 against 6.79 ms per call of the
+        // 64-candidate beam)
+        p.rs_wpb = 8;
+        p.rs_d = mask & 1;
+        p.rs_o = (mask >> 1) & 1;
+        p.g_rs_o = resid_split_plan(dm.H, dm.nq * dm.d, p.rs_wpb, U);
+        p.g_rs_d = resid_split_plan(dm.H, dm.F, p.rs_wpb, U);
+        if ((mask & 4) && (dm.H / 32) % U == 0 && (dm.nq + 2 * dm.nkv) * (dm.d / 2) >= 64) {
+          p.rs_qkv = 1;
+          p.g_rs_qkv = resid_split_plan((dm.nq + 2 * dm.nkv) * dm.d, dm.H, p.rs_wpb, U);
+        }
+        for (const GemvPlan *g : {&p.g_rs_o, &p.g_rs_d, &p.g_rs_qkv}) {
+          // (with an adapter, one more slice: its B-factor tail)
+          const size_t e = (size_t)(g->ksplit + (lora_rank > 0 ? 1 : 0)) * g->rows;
+          m = e > m ? e : m;
+        }
       }
     }
   } else {

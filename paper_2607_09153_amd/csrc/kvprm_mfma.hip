@@ -776,15 +776,24 @@ struct SplitArgs {
   int kb_per;        // input blocks per slice (a multiple of U)
   const uint4 *act;  // operand [K / 32][NT][64]
   int B;
-  float *part;       // [ksplit][B][rows]
+  float *part;       // [ksplit (+ 1 with an adapter)][B][rows]
+  // adapter tail (tkb > 0): slice ksplit (the grid's last) runs the tkb input blocks of the
+  // segments' B factors (packed [rows_i][32 tkb], null = no adapter) against operand slot i of
+  // tact, as k_gemv_fused's tail does
+  int ksplit;
+  const void *tw[3];
+  const uint4 *tact;
+  int tkb, tstride;
 };
 
 template <int NT, int WPB, int U>
 __global__ __launch_bounds__(64 * WPB) void k_resid_split(SplitArgs a) {
-  constexpr int NG = NT / 2;  // candidate groups of 16 (tiles g and NG + g: hi and lo)
+  // candidate groups: one column tile (B <= 8) holds the hi and lo halves of candidate b in
+  // columns b and 8 + b; otherwise tiles g and NG + g those of candidates 16 g .. 16 g + 15
+  constexpr int NG = NT == 1 ? 1 : NT / 2;
   constexpr int PIECES = U * NT * 64;  // 16-byte operand pieces per batch
   constexpr int PER = PIECES / (64 * WPB);
-  static_assert(NT >= 2 && PER * 64 * WPB == PIECES, "operand batch split evenly over the block");
+  static_assert(PER >= 1 && PER * 64 * WPB == PIECES, "operand batch split evenly over the block");
   __shared__ uint4 op_s[2][U * NT * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ks = blockIdx.y;
@@ -802,6 +811,18 @@ __global__ __launch_bounds__(64 * WPB) void k_resid_split(SplitArgs a) {
   floatx4 acc[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (ks == a.ksplit) {  // the adapter tail slice (block-uniform: no barriers on this path)
+    const uint4 *bw = (const uint4 *)a.tw[seg];
+    if (bw && own) {
+      bw += (size_t)(tl - base / 16) * 64 + lane;
+      const uint4 *tp = a.tact + (size_t)seg * a.tstride + lane;
+      for (int kb = 0; kb < a.tkb; ++kb) {
+        const uint4 av = ld_stream(&bw[(size_t)kb * kstride]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t] = mfma16(av, tp[((size_t)kb * NT + t) * 64], acc[t]);
+      }
+    }
+  } else {
   uint4 wa[U], wb[U];
   u32x4 ov[PER];
   auto load_w = [&](int bat, uint4(&w)[U]) {
@@ -850,16 +871,20 @@ __global__ __launch_bounds__(64 * WPB) void k_resid_split(SplitArgs a) {
     }
     __syncthreads();
   }
-  if (!own) return;
-  // lane (n, cq) holds rows 4 cq .. 4 cq + 3 of the tile for candidate 16 gi + n
+  }
+  if (!own) return;  // (whole waves)
+  // lane (n, cq) holds rows 4 cq .. 4 cq + 3 of the tile for column n
   const int n = lane & 15, cq = lane >> 4;
 #pragma unroll
   for (int gi = 0; gi < NG; ++gi) {
-    const int cand = 16 * gi + n;
-    if (cand >= a.B) continue;
-    const float4 v = make_float4(acc[gi][0] + acc[gi + NG][0], acc[gi][1] + acc[gi + NG][1],
-                                 acc[gi][2] + acc[gi + NG][2], acc[gi][3] + acc[gi + NG][3]);
-    *(float4 *)(a.part + ((size_t)ks * a.B + cand) * a.rows + tile * 16 + 4 * cq) = v;
+    float hl[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      hl[i] = NT == 1 ? acc[0][i] + __shfl_xor(acc[0][i], 8, 64) : acc[gi][i] + acc[gi + NG][i];
+    const int cand = NT == 1 ? n : 16 * gi + n;
+    if (cand >= a.B || (NT == 1 && n >= 8)) continue;
+    *(float4 *)(a.part + ((size_t)ks * a.B + cand) * a.rows + tile * 16 + 4 * cq) =
+        make_float4(hl[0], hl[1], hl[2], hl[3]);
   }
 }
 
@@ -1103,20 +1128,20 @@ __global__ __launch_bounds__(256) void k_qkv_fin_mx(const float *__restrict__ pa
   dst[i + hd] = rot ? y2 * csn.x + y1 * csn.y : y2;
 }
 
-static hipError_t launch_split(const Plan &p, const GemvPlan &g, const void *w0, int r0,
-                               const void *w1, int r1, const void *w2, int r2,
-                               const uint16_t *act, float *part, hipStream_t s);
+static hipError_t launch_split(const Plan &p, const Workspace &w, const GemvPlan &g,
+                               const void *w0, int r0, const void *w1, int r1, const void *w2,
+                               int r2, const uint16_t *act, const LoraTail &tail, hipStream_t s);
 
 hipError_t launch_qkv_mx(const Dims &dm, const Plan &p, const Workspace &w, const void *wq,
                          const void *wk, const void *wv, const LoraTail &tail, hipStream_t s) {
-  if (p.rs_qkv && tail.tkb == 0) {  // more than 16 rows: split-K product + rotary finish
-    hipError_t e = launch_split(p, p.g_rs_qkv, wq, dm.nq * dm.d, wk, dm.nkv * dm.d, wv,
-                                dm.nkv * dm.d, w.opA, w.part, s);
+  if (p.rs_qkv) {  // split-K product (+ the adapter tail slice) and the rotary finish
+    hipError_t e = launch_split(p, w, p.g_rs_qkv, wq, dm.nq * dm.d, wk, dm.nkv * dm.d, wv,
+                                dm.nkv * dm.d, w.opA, tail, s);
     if (e != hipSuccess) return e;
     const int n = p.B * (dm.nq + 2 * dm.nkv) * (dm.d / 2);
     hipLaunchKernelGGL(k_qkv_split_fin, dim3((n + 255) / 256), dim3(256), 0, s, w.part,
-                       p.g_rs_qkv.ksplit, w.ss, p.nss, dm.H, dm.eps, p.B, dm.nq, dm.nkv, dm.d,
-                       w.rope, w.q, w.kself, w.vself);
+                       p.g_rs_qkv.ksplit + (tail.tkb > 0 ? 1 : 0), w.ss, p.nss, dm.H, dm.eps,
+                       p.B, dm.nq, dm.nkv, dm.d, w.rope, w.q, w.kself, w.vself);
     return hipGetLastError();
   }
   if (!p.qkv_split || tail.tkb > 0) return launch_qkv_rope_fused(dm, p, w, wq, wk, wv, tail, s);
@@ -1221,10 +1246,11 @@ static hipError_t launch_resid_fused(const Plan &p, const FusedArgs &a, int tile
 }
 
 // k_resid_split over the plan's slices, then k_resid_split_fin (next operand into w.opA)
-static hipError_t launch_split(const Plan &p, const GemvPlan &g, const void *w0, int r0,
-                               const void *w1, int r1, const void *w2, int r2,
-                               const uint16_t *act, float *part, hipStream_t s) {
+static hipError_t launch_split(const Plan &p, const Workspace &w, const GemvPlan &g,
+                               const void *w0, int r0, const void *w1, int r1, const void *w2,
+                               int r2, const uint16_t *act, const LoraTail &tail, hipStream_t s) {
   SplitArgs a;
+  memset(&a, 0, sizeof a);
   a.w[0] = w0;
   a.w[1] = w1;
   a.w[2] = w2;
@@ -1237,11 +1263,19 @@ static hipError_t launch_split(const Plan &p, const GemvPlan &g, const void *w0,
   a.kb_per = g.kslice / 32;
   a.act = (const uint4 *)act;
   a.B = p.B;
-  a.part = part;
-  constexpr int U = 4, WPB = 8;  // (the plan's slices are whole batches of U input blocks)
+  a.part = w.part;
+  a.ksplit = g.ksplit;
+  for (int i = 0; i < 3; ++i) a.tw[i] = tail.b[i];
+  a.tact = (const uint4 *)w.topd;
+  a.tkb = tail.tkb;
+  a.tstride = tail.tkb * p.nt * 64;
+  constexpr int U = 4, WPB = 8;  // (the plan's slices are whole batches of U input blocks; 2 U
+                                 // with one column tile)
   if (p.rs_wpb != WPB) return hipErrorInvalidValue;
-  const dim3 grid((g.rows / 16 + WPB - 1) / WPB, g.ksplit);
+  const dim3 grid((g.rows / 16 + WPB - 1) / WPB, g.ksplit + (tail.tkb > 0 ? 1 : 0));
   switch (p.nt) {
+    case 1: hipLaunchKernelGGL((k_resid_split<1, WPB, 2 * U>), grid, dim3(64 * WPB), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_resid_split<2, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
     case 4: hipLaunchKernelGGL((k_resid_split<4, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
     case 6: hipLaunchKernelGGL((k_resid_split<6, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
     case 8: hipLaunchKernelGGL((k_resid_split<8, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
@@ -1252,12 +1286,14 @@ static hipError_t launch_split(const Plan &p, const GemvPlan &g, const void *w0,
 
 static hipError_t launch_resid_split(const Dims &dm, const Plan &p, const Workspace &w,
                                      const GemvPlan &g, const void *wt, const uint16_t *act,
-                                     const void *gamma, float *xsave, hipStream_t s) {
-  hipError_t e = launch_split(p, g, wt, dm.H, nullptr, 0, nullptr, 0, act, w.part, s);
+                                     const LoraTail &tail, const void *gamma, float *xsave,
+                                     hipStream_t s) {
+  hipError_t e = launch_split(p, w, g, wt, dm.H, nullptr, 0, nullptr, 0, act, tail, s);
   if (e != hipSuccess) return e;
   const int n = p.B * dm.H;
-  hipLaunchKernelGGL(k_resid_split_fin, dim3((n + 255) / 256), dim3(256), 0, s, w.part, g.ksplit,
-                     w.x, xsave, w.ss, dm.H, p.B, gamma, w.opA, p.nt, p.bp);
+  hipLaunchKernelGGL(k_resid_split_fin, dim3((n + 255) / 256), dim3(256), 0, s, w.part,
+                     g.ksplit + (tail.tkb > 0 ? 1 : 0), w.x, xsave, w.ss, dm.H, p.B, gamma,
+                     w.opA, p.nt, p.bp);
   return hipGetLastError();
 }
 
@@ -1282,8 +1318,7 @@ static FusedArgs fused_args(const Dims &dm, const Plan &p, const Workspace &w, i
 hipError_t launch_oproj_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wo,
                               const void *gamma_ffn, const LoraTail &tail, hipStream_t s,
                               float *xsave) {
-  if (p.rs_wpb && tail.tkb == 0)
-    return launch_resid_split(dm, p, w, p.g_rs_o, wo, w.opO, gamma_ffn, xsave, s);
+  if (p.rs_o) return launch_resid_split(dm, p, w, p.g_rs_o, wo, w.opO, tail, gamma_ffn, xsave, s);
   FusedArgs a = fused_args(dm, p, w, dm.nq * dm.d, w.opO);
   a.xsave = xsave;
   set_tail(a, p, w, tail);
@@ -1357,8 +1392,7 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
 hipError_t launch_down_fused(const Dims &dm, const Plan &p, const Workspace &w, const void *wd,
                              const void *gamma_next, const LoraTail &tail, hipStream_t s,
                              float *xsave) {
-  if (p.rs_wpb && tail.tkb == 0)
-    return launch_resid_split(dm, p, w, p.g_rs_d, wd, w.opD, gamma_next, xsave, s);
+  if (p.rs_d) return launch_resid_split(dm, p, w, p.g_rs_d, wd, w.opD, tail, gamma_next, xsave, s);
   FusedArgs a = fused_args(dm, p, w, dm.F, w.opD);
   a.xsave = xsave;
   set_tail(a, p, w, tail);
