@@ -1232,7 +1232,9 @@ static hipError_t launch_resid_fused(const Plan &p, const FusedArgs &a, int tile
     return hipGetLastError();
   }
   switch (p.nt) {
-    case 1: hipLaunchKernelGGL((k_gemv_fused<1, 1, 16, 4, EPI_RESID>), grid, dim3(64 * 16), 0, s, a); break;
+    // (8 waves with batches of 2 input blocks: 9.2 -> 8.7 us per output projection of the
+    // ragged batch of 8, against 16 x 4, 8 x 4, 16 x 2 and 16 x 1)
+    case 1: hipLaunchKernelGGL((k_gemv_fused<1, 1, 8, 2, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
     // batches of 2 input blocks (74 registers): 4.20 -> 4.15 ms per call of the 7B batch of 16
     case 2: hipLaunchKernelGGL((k_gemv_fused<1, 2, 8, 2, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
     case 4: hipLaunchKernelGGL((k_gemv_fused<1, 4, 8, 2, EPI_RESID>), grid, dim3(64 * 8), 0, s, a); break;
