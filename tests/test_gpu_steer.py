@@ -121,6 +121,15 @@ def test_cache_gradient_7b_two_layers():
     _grad_case(w)
 
 
+def test_cache_gradient_7b_long_multi_chunk():
+    """Long caches against the oracle: 8192 tokens (32 chunks of the backward's 16-page
+    chunks) and 3001 (a partial last page), 7B shape, 2 layers."""
+    _say("case: cache gradient, 7B shape, 2 layers, L = 8192 and 3001")
+    shape = dataclasses.replace(synth.B7, num_layers=2)
+    w = synth.make_workload("custom", shape=shape, lengths=[8192, 3001], seed=405)
+    _grad_case(w)
+
+
 @pytest.mark.parametrize("head_dim", [64, 128])
 def test_cache_gradient_sixteen_heads_per_kv_head(head_dim):
     """g = 16 (the most q-heads per kv-head the kernels take): every column of the matrix-core
@@ -176,6 +185,43 @@ def test_kv_steering_matches_the_oracle():
         for pg in range(w.num_pages):
             if pg not in used:
                 assert torch.equal(a[:, pg], o[:, pg])
+
+
+def test_kv_steering_7b_two_layers_matches_the_oracle():
+    """Two steering steps at the 7B shape (2 layers, 4096 and 999 cached tokens) with the step
+    size of the benchmark: the stored caches within 2 bf16 spacings of the oracle's steps, P(+)
+    before and after within 2e-3 of the oracle's."""
+    _say("case: KV steering, 2 steps, 7B shape, 2 layers")
+    shape = dataclasses.replace(synth.B7, num_layers=2)
+    w = synth.make_workload("custom", shape=shape, lengths=[4096, 999], seed=406)
+    dw = DeviceWorkload(w)
+    eta, steps = 20.0, 2
+    m = kv()
+    h = m.kvprm_create(dw.desc(m))
+    try:
+        batch = dw.batch(m)
+        n = m.kvprm_workspace_size_grad(h, batch)
+        ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        before = torch.full((w.batch,), float("nan"), device="cuda")
+        after = torch.full((w.batch,), float("nan"), device="cuda")
+        m.kvprm_steer(h, dw.cache(m), batch, dw.readout(m), eta, steps, ws.data_ptr(), n,
+                      before.data_ptr(), after.data_ptr(), torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+    finally:
+        m.kvprm_destroy(h)
+    ro = oin.readout_from_synth(w.shape, w.seed, layer_cache=64)
+    K, V = ksr.dense_cache(oin.cache_from_synth(w), w.shape, w.lengths, w.page_table)
+    K2, V2, losses = ksr.steer(w.shape, ro, K, V, w.lengths, eta, steps, "bf16")
+    pb, pa = before.cpu().numpy(), after.cpu().numpy()
+    p_ref0 = np.exp(-np.array(losses[0]))
+    p_ref1 = np.exp(-np.array(losses[-1]))
+    _say(f"  P before {pb} (oracle {p_ref0}), after {pa} (oracle {p_ref1})")
+    assert np.max(np.abs(pb - p_ref0)) < 2e-3 and np.max(np.abs(pa - p_ref1)) < 2e-3
+    GK, GV = _dense_from_pools(w, dw.k_pool.view(torch.bfloat16), dw.v_pool.view(torch.bfloat16))
+    for b in range(w.batch):
+        for got, want in ((GK[b], K2[b]), (GV[b], V2[b])):
+            ulp = np.abs(want) * 2.0 ** -7 + 1e-30
+            assert np.all(np.abs(got - want) <= 2 * ulp + 1e-6)
 
 
 # ---------------------------------------------------------------------------------------------
