@@ -608,7 +608,7 @@ __global__ __launch_bounds__(64 * WPB) void k_gemv_fused(FusedArgs a) {
   }
 }
 
-// Gate/up + SwiGLU (every batch size whose input is a whole number of batches). Every input
+// Gate/up + SwiGLU for 16 candidates or fewer whose input is a whole number of batches. Every input
 // block brings NT KiB of operand for 2 KiB of gate/up weights, and k_gemv_fused, whose waves
 // split the input range, reads each operand tile from L2 once per wave. Here the waves of a block
 // own whole row tiles over the full input range instead (waves 0 .. WPB/2 - 1 gate tiles t0 + w,
@@ -747,6 +747,143 @@ __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
       const int f = tl * 16 + 4 * cq + i;
       const float gv = hl[gi][i] * inv;
       const float uv = uv4[i] * inv;
+      store_operand(a.op, a.NT, a.Bp, f, cand, gv / (1.0f + expf(-gv)) * uv);
+      if (a.save) {
+        a.save[(size_t)cand * 2 * a.F + f] = gv;
+        a.save[(size_t)cand * 2 * a.F + a.F + f] = uv;
+      }
+    }
+  }
+}
+
+// Gate/up + SwiGLU for 32 candidates or more (NT >= 4 column tiles). With NT operand tiles per
+// input block a wave that owns one row tile reads NT KiB of operand from LDS for each KiB of
+// weights; here wave w of the block owns gate/up tile pair blockIdx.x WPB + w whole, so each
+// operand tile it reads from LDS feeds two products (the gate's and the up's) and the SwiGLU
+// epilogue needs no exchange between waves. Staging as in k_gateup_wide: batches of U input
+// blocks of the operand double buffered in LDS, the weights two batches ahead in registers.
+template <int NT, int WPB, int U>
+__global__ __launch_bounds__(64 * WPB, 1) void k_gateup_pair(FusedArgs a) {
+  constexpr int NG = NT / 2;
+  constexpr int PIECES = U * NT * 64;
+  constexpr int PER = (PIECES + 64 * WPB - 1) / (64 * WPB);
+  constexpr bool EVEN = PER * 64 * WPB == PIECES;
+  __shared__ uint4 op_s[2][U * NT * 64];
+  __shared__ float part_s[64 * WPB];
+  __shared__ float inv_s[64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int B = a.B;
+  const int ntf = a.F / 16;
+  const int pair = (int)blockIdx.x * WPB + wave;
+  const bool own = pair < ntf;
+  const int tl = own ? pair : ntf - 1;  // past the end: repeat the last pair (results unused)
+  const size_t kstride = (size_t)ntf * 64;
+  const uint4 *wpg = (const uint4 *)a.w[0] + (size_t)tl * 64 + lane;
+  const uint4 *wpu = (const uint4 *)a.w[1] + (size_t)tl * 64 + lane;
+  const int nbat = (a.K >> 5) / U;  // the launcher guarantees K / 32 % U == 0
+  RmsLoads rl;
+  rms_load<64 * WPB>(a.ss, a.nss, B, rl);
+  floatx4 acc[2][NT];
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  uint4 wa[2][U], wb[2][U];
+  u32x4 ov[PER];
+  auto load_w = [&](int bat, uint4(&w)[2][U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      w[0][u] = ld_stream(&wpg[(size_t)(bat * U + u) * kstride]);
+      w[1][u] = ld_stream(&wpu[(size_t)(bat * U + u) * kstride]);
+    }
+  };
+  auto load_op = [&](int bat, u32x4(&o)[PER]) {
+    const u32x4 *src = (const u32x4 *)a.act + (size_t)bat * PIECES;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 64 * WPB;
+      o[i] = src[EVEN || e < PIECES ? e : PIECES - 1];
+    }
+  };
+  auto store_op = [&](int buf, const u32x4(&o)[PER]) {
+    u32x4 *dst = (u32x4 *)&op_s[buf][0];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 64 * WPB;
+      if (EVEN || e < PIECES) dst[e] = o[i];
+    }
+  };
+  // the products of batch buf with weights w; each input block's weight registers are reloaded
+  // with batch nb's as soon as its products are issued, so that the weight stream does not wait
+  // for the whole batch of products
+  // (the operand tiles of input block u + 1 are read from LDS while block u's products issue)
+  auto mma = [&](int buf, uint4(&w)[2][U], int nb) {
+    uint4 o[2][NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) o[0][t] = op_s[buf][t * 64 + lane];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (u + 1 < U) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) o[(u + 1) & 1][t] = op_s[buf][((u + 1) * NT + t) * 64 + lane];
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        acc[0][t] = mfma16(w[0][u], o[u & 1][t], acc[0][t]);
+        acc[1][t] = mfma16(w[1][u], o[u & 1][t], acc[1][t]);
+      }
+      if (nb < nbat) {
+        w[0][u] = ld_stream(&wpg[(size_t)(nb * U + u) * kstride]);
+        w[1][u] = ld_stream(&wpu[(size_t)(nb * U + u) * kstride]);
+      }
+    }
+  };
+  load_op(0, ov);
+  store_op(0, ov);
+  load_w(0, wa);
+  if (nbat > 1) {
+    load_op(1, ov);
+    load_w(1, wb);
+  }
+  __syncthreads();
+  for (int bat = 0; bat < nbat; bat += 2) {  // block-uniform trip counts and barriers
+    mma(0, wa, bat + 2);
+    if (bat + 1 < nbat) store_op(1, ov);
+    if (bat + 2 < nbat) load_op(bat + 2, ov);
+    __syncthreads();
+    if (bat + 1 >= nbat) break;
+    mma(1, wb, bat + 3);
+    if (bat + 2 < nbat) store_op(0, ov);
+    if (bat + 3 < nbat) load_op(bat + 3, ov);
+    __syncthreads();
+  }
+  // adapter tail: B_seg (scale * A_seg u) of each segment, operands from L2
+  if (a.tkb > 0) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      if (!a.tw[m]) continue;
+      const uint4 *bw = (const uint4 *)a.tw[m] + (size_t)tl * 64 + lane;
+      const uint4 *tp = a.tact + (size_t)m * a.tstride + lane;
+      for (int kb = 0; kb < a.tkb; ++kb) {
+        const uint4 av = ld_stream(&bw[(size_t)kb * kstride]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[m][t] = mfma16(av, tp[((size_t)kb * NT + t) * 64], acc[m][t]);
+      }
+    }
+  }
+  rms_finish<64 * WPB>(a.ss, a.nss, B, a.H, a.eps, rl, part_s, inv_s);  // has barriers
+  if (!own) return;
+  const int n = lane & 15, cq = lane >> 4;
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi) {
+    const int cand = 16 * gi + n;
+    if (cand >= B) continue;
+    const float inv = inv_s[cand];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int f = tl * 16 + 4 * cq + i;
+      const float gv = (acc[0][gi][i] + acc[0][gi + NG][i]) * inv;
+      const float uv = (acc[1][gi][i] + acc[1][gi + NG][i]) * inv;
       store_operand(a.op, a.NT, a.Bp, f, cand, gv / (1.0f + expf(-gv)) * uv);
       if (a.save) {
         a.save[(size_t)cand * 2 * a.F + f] = gv;
@@ -1353,6 +1490,23 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
   half = half < 4 ? 4 : (half > 8 ? 8 : half);
   const dim3 wgrid((pairs + half - 1) / half);
   const bool wide = (dm.H / 32) % UW == 0;
+  // 32 candidates or more: one gate/up pair per wave (k_gateup_pair), as many pairs per block
+  // as k_gateup_wide's (beam batch of 64: 6.75 -> 6.59 ms per call)
+  if (wide && p.nt >= 4) {
+#define KVPRM_GP(NT_)                                                                                 \
+  switch (half) {                                                                                  \
+    case 4: hipLaunchKernelGGL((k_gateup_pair<NT_, 4, UW>), wgrid, dim3(256), 0, s, a); break;      \
+    case 5: hipLaunchKernelGGL((k_gateup_pair<NT_, 5, UW>), wgrid, dim3(320), 0, s, a); break;      \
+    case 6: hipLaunchKernelGGL((k_gateup_pair<NT_, 6, UW>), wgrid, dim3(384), 0, s, a); break;      \
+    case 7: hipLaunchKernelGGL((k_gateup_pair<NT_, 7, UW>), wgrid, dim3(448), 0, s, a); break;      \
+    default: hipLaunchKernelGGL((k_gateup_pair<NT_, 8, UW>), wgrid, dim3(512), 0, s, a); break;     \
+  }
+    if (p.nt == 4) KVPRM_GP(4)
+    else if (p.nt == 6) KVPRM_GP(6)
+    else KVPRM_GP(8)
+#undef KVPRM_GP
+    return hipGetLastError();
+  }
 #define KVPRM_GW(NT_)                                                                                \
   switch (half) {                                                                                 \
     case 4: hipLaunchKernelGGL((k_gateup_wide<NT_, 8, UW>), wgrid, dim3(512), 0, s, a); break;     \
@@ -1362,8 +1516,9 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
     default: hipLaunchKernelGGL((k_gateup_wide<NT_, 16, UW>), wgrid, dim3(1024), 0, s, a); break;  \
   }
   // with balanced blocks it is also the faster choice for 16 candidates or fewer (7B batch of 16:
-  // 4.15 -> 3.86 ms per call; ragged batch of 8: about 2% faster)
-  if (wide && p.nt <= 2) {
+  // 4.15 -> 3.86 ms per call; ragged batch of 8: about 2% faster); an input that is not a whole
+  // number of batches takes k_gemv_fused
+  if (wide) {
     if (p.nt == 1) KVPRM_GW(1)
     else KVPRM_GW(2)
     return hipGetLastError();
@@ -1371,18 +1526,9 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
   switch (p.nt) {
     case 1: hipLaunchKernelGGL((k_gemv_fused<2, 1, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_gemv_fused<2, 2, 4, 4, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
-    case 4:
-      if (wide) KVPRM_GW(4)
-      else hipLaunchKernelGGL((k_gemv_fused<2, 4, 4, 2, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
-      break;
-    case 6:
-      if (wide) KVPRM_GW(6)
-      else hipLaunchKernelGGL((k_gemv_fused<2, 6, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
-      break;
-    case 8:
-      if (wide) KVPRM_GW(8)
-      else hipLaunchKernelGGL((k_gemv_fused<2, 8, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a);
-      break;
+    case 4: hipLaunchKernelGGL((k_gemv_fused<2, 4, 4, 2, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
+    case 6: hipLaunchKernelGGL((k_gemv_fused<2, 6, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_gemv_fused<2, 8, 4, 1, EPI_SWIGLU>), grid, dim3(64 * 4), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
 #undef KVPRM_GW
