@@ -15,9 +15,9 @@
 //               the same for the token's own key; rotary backward;
 //               du1 = [W_q; W_k; W_v]^T (dq, dk, dv); RMSNorm backward  -> dx_in
 //
-// The transposed products read the packed bf16 weight tiles and multiply on the vector ALUs
-// (a handful of candidates: two flops per weight byte per candidate, far below the rate the
-// ALUs sustain while the tiles stream from HBM). All reductions have a fixed order.
+// The transposed products read the packed bf16 weight tiles once and run on the matrix cores
+// (each tile turned around by a product with a 0/1 selector, then contracted with d in bf16
+// hi + lo terms). All reductions have a fixed order.
 #include <math.h>
 #include <string.h>
 
@@ -173,12 +173,9 @@ __global__ __launch_bounds__(1024) void k_rms_bwd(const float *x, const void *ga
 
 // y[b][k] = sum over the stacked rows r of W[r][k] d[r][b] for packed bf16 matrices (1 KiB
 // blocks, block kb * (rows_i / 16) + t, lane l holding W[16 t + l % 16][32 kb + 8 (l / 16) + i]).
-// A lane holds 8 inputs of one row, so the contraction (over rows) is not a matrix-core shape
-// without a transpose; the vector ALUs do it: each lane multiplies its 8 weights by the d values
-// of its row, and the 16 lanes of an input group add their sums at the end. Block = 4 waves on
-// 4 consecutive 32-input blocks kb of one row split (kTgemvWindow tiles at most); the split's d
-// rows are staged once in LDS, and each wave streams the contiguous weight blocks of its kb with
-// two batches of U tiles in flight. Partials: part[split][b][k].
+// Block = 4 waves on 4 consecutive 32-input blocks kb of one row split (kTgemvWindow tiles at
+// most); the split's d rows are staged once in LDS, and each wave streams the contiguous weight
+// blocks of its kb with two batches of U tiles in flight. Partials: part[split][b][k].
 struct TgemvArgs {
   const void *w[3];
   int seg_tiles[3];  // row tiles of each segment
@@ -190,10 +187,20 @@ struct TgemvArgs {
   float *part;       // [nsplit][B][K]
 };
 
-template <int BMAX>
-__global__ __launch_bounds__(256) void k_tgemv(TgemvArgs a) {
-  constexpr int U = 8;  // tiles per load batch
-  __shared__ float4 d_s[kTgemvWindow * 16][2];
+// The product runs on the matrix cores. Its contraction runs over rows while a tile lane holds
+// 8 inputs of one row, so each tile is first turned around by a product with a 0/1 selector:
+// S_h[k][n] = 1 where k = 16 h + n gives D[r][n] = W[r][16 h + n] exactly (one bf16 weight
+// times 1 per output), with lane (n, c) holding rows 4c .. 4c+3 of input 16 h + n, which is the
+// B operand of a 16x16x16 product over the tile's 16 rows. Its A operand holds d, staged once
+// per split in LDS in that layout: slot m < 8 the hi bf16 term of candidate m's d, slot 8 + m
+// the lo term (zero for candidates past B and for tiles past the split), so the tile costs four
+// matrix-core products instead of 64 FMAs per lane. The accumulator lane (n, c) holds slots
+// 4c .. 4c+3 of input 16 h + n; a candidate's hi and lo sums (lanes c and c + 2) are added at the
+// end.
+template <int U>
+__global__ __launch_bounds__(256) void k_tgemv_mx(TgemvArgs a) {
+  constexpr int NT = kTgemvWindow + 2 * U;  // staged tiles (the last 2U only ever zero)
+  __shared__ uint2 dop_s[NT][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nkb = a.K >> 5;
   const int bps = (nkb + 3) >> 2;  // blocks per split
@@ -202,48 +209,79 @@ __global__ __launch_bounds__(256) void k_tgemv(TgemvArgs a) {
   const bool act = kb < nkb;  // wave-uniform
   const int n = lane & 15, c = lane >> 4;
   const int t0 = split * a.tps, t1 = min(a.tiles, t0 + a.tps);
-  // first stacked tile of segments 1 and 2 (past the end when absent)
   const int cum1 = a.nseg > 1 ? a.seg_tiles[0] : a.tiles;
   const int cum2 = a.nseg > 2 ? a.seg_tiles[0] + a.seg_tiles[1] : a.tiles;
   auto load = [&](int t, uint4 *wv) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int tt = min(t + u, t1 - 1);  // past the end: repeat the last tile (not used)
+      const int tt = min(t + u, t1 - 1);  // past the end: repeat the last tile (its d is zero)
       const int sg = tt >= cum2 ? 2 : (tt >= cum1 ? 1 : 0);
       const int base = sg == 0 ? 0 : (sg == 1 ? cum1 : cum2);
       wv[u] = ld_nt((const uint4 *)a.w[sg] + ((size_t)kb * a.seg_tiles[sg] + (tt - base)) * 64 + lane);
     }
   };
-  float acc[BMAX][8];
-#pragma unroll
-  for (int b = 0; b < BMAX; ++b)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[b][i] = 0.f;
-  auto comp = [&](int t, const uint4 *wv) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (t + u < t1) {
-        const float4 d0 = d_s[(t + u - t0) * 16 + n][0], d1 = d_s[(t + u - t0) * 16 + n][1];
-        const float dd[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-        const float w8[8] = {bf(wv[u].x & 0xFFFFu), bf(wv[u].x >> 16), bf(wv[u].y & 0xFFFFu),
-                             bf(wv[u].y >> 16),     bf(wv[u].z & 0xFFFFu), bf(wv[u].z >> 16),
-                             bf(wv[u].w & 0xFFFFu), bf(wv[u].w >> 16)};
-#pragma unroll
-        for (int b = 0; b < BMAX; ++b)
-#pragma unroll
-          for (int i = 0; i < 8; ++i) acc[b][i] += w8[i] * dd[b];
-      }
-    }
-  };
   uint4 wa[U], wb[U];
-  if (act) load(t0, wa);  // in flight while the d rows are staged
-  for (int e = threadIdx.x; e < (t1 - t0) * 16; e += 256) {
-    const float4 *dr = (const float4 *)(a.d + (size_t)(t0 * 16 + e) * kDPad);
-    d_s[e][0] = dr[0];
-    d_s[e][1] = dr[1];
+  if (act) load(t0, wa);  // in flight while d is staged
+  // staging: item (tile tl, row group q) reads rows 16 (t0 + tl) + 4q .. + 3 and writes the hi
+  // and lo operands of every candidate for lanes 16 q + m and 16 q + 8 + m
+  for (int it = threadIdx.x; it < NT * 4; it += 256) {
+    const int tl = it >> 2, q = it & 3;
+    float dv[4][8];
+    const bool live = tl < t1 - t0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float4 v0 = make_float4(0.f, 0.f, 0.f, 0.f), v1 = v0;
+      if (live) {
+        const float4 *dr = (const float4 *)(a.d + ((size_t)(t0 + tl) * 16 + 4 * q + i) * kDPad);
+        v0 = dr[0];
+        v1 = dr[1];
+      }
+      dv[i][0] = v0.x; dv[i][1] = v0.y; dv[i][2] = v0.z; dv[i][3] = v0.w;
+      dv[i][4] = v1.x; dv[i][5] = v1.y; dv[i][6] = v1.z; dv[i][7] = v1.w;
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      uint32_t hi[4], lo[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = m < a.B ? dv[i][m] : 0.f;
+        hi[i] = bf16_round(v);
+        lo[i] = bf16_round(v - bf(hi[i]));
+      }
+      dop_s[tl][16 * q + m] = make_uint2(hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16));
+      dop_s[tl][16 * q + 8 + m] = make_uint2(lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16));
+    }
   }
   __syncthreads();
   if (!act) return;
+  // selector operands: B lane (n, c) holds slots 8c .. 8c+7 of column n; 1.0 where 8c + i = 16 h + n
+  uint4 sel[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t wd[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t e0 = (8 * c + 2 * j == 16 * h + n) ? 0x3F80u : 0u;
+      const uint32_t e1 = (8 * c + 2 * j + 1 == 16 * h + n) ? 0x3F80u : 0u;
+      wd[j] = e0 | (e1 << 16);
+    }
+    sel[h] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+  }
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  floatx4 acc[2] = {zero, zero};
+  auto comp = [&](int t, const uint4 *wv) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint2 aop = dop_s[t + u - t0][lane];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const floatx4 tr = mma32(wv[u], sel[h], zero);  // exact: one weight per output
+        const uint2 bop = make_uint2((__float_as_uint(tr[0]) >> 16) | (__float_as_uint(tr[1]) & 0xFFFF0000u),
+                                     (__float_as_uint(tr[2]) >> 16) | (__float_as_uint(tr[3]) & 0xFFFF0000u));
+        acc[h] = mma16(aop, bop, acc[h]);
+      }
+    }
+  };
   for (int t = t0; t < t1; t += 2 * U) {
     load(t + U, wb);
     __builtin_amdgcn_sched_barrier(0);
@@ -254,17 +292,19 @@ __global__ __launch_bounds__(256) void k_tgemv(TgemvArgs a) {
     comp(t + U, wb);
     __builtin_amdgcn_sched_barrier(0);
   }
+  // hi + lo of candidate 4c + i (c < 2) from lanes c and c + 2
 #pragma unroll
-  for (int b = 0; b < BMAX; ++b)
+  for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[b][i] = sum_lanes<16>(acc[b][i]);
-  if (n == 0) {
+    for (int i = 0; i < 4; ++i) acc[h][i] += __shfl_xor(acc[h][i], 32, 64);
+  if (c < 2) {
 #pragma unroll
-    for (int b = 0; b < BMAX; ++b) {
+    for (int i = 0; i < 4; ++i) {
+      const int b = 4 * c + i;
       if (b < a.B) {
-        float *dst = a.part + ((size_t)split * a.B + b) * a.K + kb * 32 + c * 8;
-        *(float4 *)dst = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
-        *(float4 *)(dst + 4) = make_float4(acc[b][4], acc[b][5], acc[b][6], acc[b][7]);
+        float *dst = a.part + ((size_t)split * a.B + b) * a.K + kb * 32 + n;
+        dst[0] = acc[0][i];
+        dst[16] = acc[1][i];
       }
     }
   }
@@ -713,7 +753,7 @@ static hipError_t tgemv(const Plan &p, const void *const w[3], const int rows[3]
   a.part = part;
   if (a.tps > kTgemvWindow) return hipErrorInvalidValue;  // more rows than the splits allow
   const int bps = (K / 32 + 3) / 4;
-  hipLaunchKernelGGL(k_tgemv<8>, dim3(bps * a.nsplit), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_tgemv_mx<8>, dim3(bps * a.nsplit), dim3(256), 0, s, a);
   const int n = p.B * K;
   if (swiglu)
     hipLaunchKernelGGL(k_tgemv_sum<true>, dim3((n + 255) / 256), dim3(256), 0, s, part, a.nsplit,
