@@ -12,6 +12,7 @@ import torch
 
 import synth
 from oracle import inputs as oin
+from oracle import kv_steering as ksr
 from oracle import kvprm_oracle as ko
 from synth.device import DeviceWorkload
 
@@ -105,6 +106,46 @@ def test_attention_parity(name, lengths, k_std):
     scale = max(1.0, float(np.max(np.abs(ref))))
     _say(f"  max|do| = {err:.3e} (max|o| = {np.max(np.abs(ref)):.3e})")
     assert err <= 2e-5 * scale
+
+
+@pytest.mark.parametrize("name", ["b7_bf16", "fp8"])
+def test_attention_sink_key(name):
+    """A key the query points straight at (an attention sink): every q-head of kv-head j of a
+    candidate is a multiple of one cached key of that head, so its score stands ~30 above the
+    rest and the softmax is one-hot to fp32 precision. Sinks at token 0, mid-cache (not on a
+    page or chunk boundary) and at the last token of a partial page; the other kv-heads keep
+    random queries."""
+    import dataclasses
+    _say(f"case: attention sink key {name}")
+    shape = _shape(name)
+    lengths = [4100, 20000, 3001]
+    sinks = [0, 12345, 3000]
+    w = synth.make_workload("custom", shape=shape, lengths=lengths, seed=4747)
+    dw = DeviceWorkload(w, nan_unused_pages=True, fill_weights=False)
+    q, ks, vs = host_activations(w, 0xABE, scale=1.0)
+    layer = 1
+    cache = oin.cache_from_synth(w)
+    K, _ = ksr.dense_cache(cache, shape, w.lengths, w.page_table)
+    g = shape.num_q_heads // shape.num_kv_heads
+    for b, t in enumerate(sinks):
+        j = b % shape.num_kv_heads
+        key = K[b][layer][j][t]
+        alpha = 4.0 * np.sqrt(shape.head_dim) / float(np.dot(key, key)) * np.sqrt(shape.head_dim)
+        q[b, j * g:(j + 1) * g] = (alpha * key).astype(np.float32)
+    o = run_attention(dw, layer, q, ks, vs)
+    ref = ko.attention_layer(shape, cache, layer, w.lengths, w.page_table, q.astype(np.float64),
+                             ks.astype(np.float64), vs.astype(np.float64))
+    assert np.all(np.isfinite(o))
+    err = np.max(np.abs(o - ref))
+    scale = max(1.0, float(np.max(np.abs(ref))))
+    _say(f"  max|do| = {err:.3e} (max|o| = {np.max(np.abs(ref)):.3e})")
+    assert err <= 2e-5 * scale
+    # the sink heads' outputs are the sink's value row (to the softmax's rounding)
+    _, V = ksr.dense_cache(cache, shape, w.lengths, w.page_table)
+    for b, t in enumerate(sinks):
+        j = b % shape.num_kv_heads
+        for h in range(j * g, (j + 1) * g):
+            assert np.max(np.abs(ref[b, h] - V[b][layer][j][t])) < 1e-6 * max(1.0, np.max(np.abs(V[b][layer][j][t])))
 
 
 @pytest.mark.parametrize("name,lengths", [("b7_bf16", [32768, 1, 20000, 33, 5000, 31000]),
