@@ -14,9 +14,11 @@ namespace kvprm {
 
 template <bool HIGH>
 __device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t word) {
-  // two OCP e4m3 codes -> two fp32 (exact) -> upper halves are the exact bf16 values
-  const auto f = __builtin_amdgcn_cvt_pk_f32_fp8((int)word, HIGH);
-  return (__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xFFFF0000u);
+  // two OCP e4m3 codes (bytes 0, 1 or 2, 3) -> two bf16 in one instruction; every e4m3 value is
+  // a bf16 value and the scale is 1, so the conversion is exact
+  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+  const bf16x2v v = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(word, 1.0f, HIGH);
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // Lane i's value of v, for a wave-uniform i (a scalar read of one lane: no LDS round trip).
