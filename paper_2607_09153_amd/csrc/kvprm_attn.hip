@@ -5,6 +5,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "kvprm_internal.h"
 #include "kvprm_mx_common.h"
 
@@ -132,9 +134,10 @@ __device__ __forceinline__ void load_query_ops(const float *qr, bool present, in
 // query's hi, mid, lo bf16 terms, three MFMAs per 32-dim block), running max and sum, then
 // O^T += V^T P^T with P split hi + lo (two MFMAs per 16-dim block). Scores arrive scaled by
 // log2(e) (sca, scb include it), so the running max m_run is in log2 units and p = 2^(s - m).
-// ok[] marks valid tokens: masked tokens get p = 0 and their V entries are zeroed, since their
-// slots may hold NaN. vsa / vsb scale P for fp8 V.
-template <int D>
+// ok[] marks valid tokens: masked tokens get p = 0 and, with MASKV, their V entries are zeroed,
+// since slots past a candidate's length may hold NaN (a caller that knows every masked slot holds
+// finite data passes MASKV = false). vsa / vsb scale P for fp8 V.
+template <int D, bool MASKV = true>
 __device__ __forceinline__ void online_step(const uint4 *KA, const uint4 *KB, const uint2 *VA,
                                             const uint2 *VB, const uint4 *q0, const uint4 *q1,
                                             const uint4 *q2, const bool *ok, float sca, float scb,
@@ -195,7 +198,8 @@ __device__ __forceinline__ void online_step(const uint4 *KA, const uint4 *KB, co
   const uint32_t mb1 = (ok[6] ? 0xFFFFu : 0u) | (ok[7] ? 0xFFFF0000u : 0u);
 #pragma unroll
   for (int nb = 0; nb < NDB; ++nb) {
-    const uint4 vop = make_uint4(VA[nb].x & ma0, VA[nb].y & ma1, VB[nb].x & mb0, VB[nb].y & mb1);
+    const uint4 vop = MASKV ? make_uint4(VA[nb].x & ma0, VA[nb].y & ma1, VB[nb].x & mb0, VB[nb].y & mb1)
+                            : make_uint4(VA[nb].x, VA[nb].y, VB[nb].x, VB[nb].y);
     acc[nb] = mfma16(vop, Phi, acc[nb]);
     acc[nb] = mfma16(vop, Plo, acc[nb]);
   }
@@ -297,7 +301,7 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
 #pragma unroll
   for (int nb = 0; nb < NDB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute_pair = [&](int pp, const PairRaw<D> &r) {
+  auto compute_pair = [&](int pp, const PairRaw<D> &r, auto maskv) {
     const int la = min(2 * pp, np - 1), lb = 2 * pp + 1;
     const bool hasA = 2 * pp < np, hasB = lb < np;
     uint4 KA[NKB], KB[NKB];
@@ -315,23 +319,35 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
     const float scb = (KVT == 2) ? lane_value(ksc_l, lbc) * rs : rs;
     const float vsa = (KVT == 2) ? lane_value(vsc_l, la) : 1.f;
     const float vsb = (KVT == 2) ? lane_value(vsc_l, lbc) : 1.f;
-    online_step<D>(KA, KB, VA, VB, q0, q1, q2, ok, sca, scb, vsa, vsb, m_run, l_run, acc);
+    online_step<D, decltype(maskv)::value>(KA, KB, VA, VB, q0, q1, q2, ok, sca, scb, vsa, vsb,
+                                           m_run, l_run, acc);
   };
   // a branch-free loop over an even number of pairs: the pair past the end (if any) is fully
   // masked, and loads past the end repeat the last page (an L2 hit), so that wait counts never
   // cover the loads in flight for the next pair
   // (scheduling barriers keep each pair's loads ahead of the previous pair's arithmetic, so that
   // the waits inside a compute step cover only its own, older loads)
-  for (int pp = 0; pp < npairs; pp += 2) {
-    load_pair(pp + 1, r1);
-    __builtin_amdgcn_sched_barrier(0);
-    compute_pair(pp, r0);
-    __builtin_amdgcn_sched_barrier(0);
-    load_pair(pp + 2, r0);
-    __builtin_amdgcn_sched_barrier(0);
-    compute_pair(pp + 1, r1);
-    __builtin_amdgcn_sched_barrier(0);
-  }
+  // Only the chunk holding the candidate's last page can hold slots past L_b (which may be
+  // NaN); every page of the other chunks is full, and their pairs past the end repeat a full
+  // page (finite, with p = 0), so their V operands need no masking. fp8 pages, whose step is
+  // bound by vector instructions rather than HBM, get a loop copy without it (for bf16 the
+  // second copy would cost more registers than the masking costs time).
+  auto chunk_loop = [&](auto maskv) {
+    for (int pp = 0; pp < npairs; pp += 2) {
+      load_pair(pp + 1, r1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_pair(pp, r0, maskv);
+      __builtin_amdgcn_sched_barrier(0);
+      load_pair(pp + 2, r0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_pair(pp + 1, r1, maskv);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  if (KVT == 2 && p0 + np < npages)
+    chunk_loop(std::integral_constant<bool, false>{});
+  else
+    chunk_loop(std::integral_constant<bool, true>{});
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
   if (colv)
