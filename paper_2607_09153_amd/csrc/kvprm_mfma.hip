@@ -756,7 +756,7 @@ __global__ __launch_bounds__(64 * WPB, 4) void k_gateup_wide(FusedArgs a) {
   }
 }
 
-// Gate/up + SwiGLU for 32 candidates or more (NT >= 4 column tiles). With NT operand tiles per
+// Gate/up + SwiGLU for more than 16 candidates (NT >= 4 column tiles). With NT operand tiles per
 // input block a wave that owns one row tile reads NT KiB of operand from LDS for each KiB of
 // weights; here wave w of the block owns gate/up tile pair blockIdx.x WPB + w whole, so each
 // operand tile it reads from LDS feeds two products (the gate's and the up's) and the SwiGLU
@@ -1490,7 +1490,7 @@ hipError_t launch_gateup_fused(const Dims &dm, const Plan &p, const Workspace &w
   half = half < 4 ? 4 : (half > 8 ? 8 : half);
   const dim3 wgrid((pairs + half - 1) / half);
   const bool wide = (dm.H / 32) % UW == 0;
-  // 32 candidates or more: one gate/up pair per wave (k_gateup_pair), as many pairs per block
+  // more than 16 candidates: one gate/up pair per wave (k_gateup_pair), as many pairs per block
   // as k_gateup_wide's (beam batch of 64: 6.75 -> 6.59 ms per call)
   if (wide && p.nt >= 4) {
 #define KVPRM_GP(NT_)                                                                                 \
