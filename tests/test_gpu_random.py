@@ -14,6 +14,7 @@ from oracle import inputs as oin
 from synth.device import DeviceWorkload
 
 from gpu_common import run_score
+from test_gpu_steer import _grad_case
 
 pytestmark = pytest.mark.gpu
 
@@ -68,3 +69,32 @@ def test_random_configuration(case):
     assert np.all(np.isfinite(p)) and np.all(np.isfinite(z))
     tol_p, tol_z = (1e-5, 4e-5) if shape.weight_dtype == "f32" else (2e-3, 2e-2)
     assert dp <= tol_p and dz <= tol_z
+
+
+GRAD_CASES = 8
+
+
+def _draw_grad(case: int):
+    rng = np.random.default_rng(7500 + case)
+    d = int(rng.choice([64, 128]))
+    nkv = int(rng.choice([1, 2, 4, 8]))
+    g = int(rng.choice([1, 2, 4, 7, 8, 16]))
+    H = 64 * int(rng.integers(2, 9))
+    F = 64 * int(rng.integers(4, 17))
+    shape = synth.ModelShape(2, H, nkv * g, nkv, d, F)
+    B = int(rng.integers(1, 5))
+    lengths = [int(rng.choice(EDGE_LENGTHS)) if rng.random() < 0.4 else int(rng.integers(0, 401))
+               for _ in range(B)]
+    return shape, lengths
+
+
+@pytest.mark.parametrize("case", range(GRAD_CASES))
+def test_random_cache_gradient(case):
+    """The KV Steering gradient (appendix, KV Steering algorithm) element by element against
+    the oracle's reverse mode on seeded random shapes (bf16 weights and cache, 1-4 candidates):
+    the transposed products over hidden, FFN and n_q d_h inputs of every size the library takes."""
+    shape, lengths = _draw_grad(case)
+    _say(f"grad case {case}: H={shape.hidden} heads={shape.num_q_heads}/{shape.num_kv_heads} "
+         f"d_h={shape.head_dim} F={shape.ffn_dim} B={len(lengths)} lengths={lengths}")
+    w = synth.make_workload("custom", shape=shape, lengths=lengths, seed=7600 + case)
+    _grad_case(w)
