@@ -753,7 +753,9 @@ static hipError_t tgemv(const Plan &p, const void *const w[3], const int rows[3]
   a.part = part;
   if (a.tps > kTgemvWindow) return hipErrorInvalidValue;  // more rows than the splits allow
   const int bps = (K / 32 + 3) / 4;
-  hipLaunchKernelGGL(k_tgemv_mx<8>, dim3(bps * a.nsplit), dim3(256), 0, s, a);
+  // batches of 2 tiles (ragged 32k steering step: 15.02-15.05 ms; 4: 15.12-15.15, 8: 15.21-15.22,
+  // 1: 15.68, 16: 16.5)
+  hipLaunchKernelGGL(k_tgemv_mx<2>, dim3(bps * a.nsplit), dim3(256), 0, s, a);
   const int n = p.B * K;
   if (swiglu)
     hipLaunchKernelGGL(k_tgemv_sum<true>, dim3((n + 255) / 256), dim3(256), 0, s, part, a.nsplit,
