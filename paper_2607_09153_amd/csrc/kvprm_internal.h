@@ -94,6 +94,7 @@ struct Plan {
   // (k_resid_split: rs_wpb row tiles per block, kslice / 32 input blocks per slice, an adapter's
   // B-factor tail as one more slice) and a finish kernel, by batch size; 0 = the fused kernels
   int rs_wpb;
+  int rs_u;        // input blocks per operand batch of k_resid_split (4, or 8 / 16 at one column tile)
   int rs_o, rs_d;  // output / down projection split
   GemvPlan g_rs_o, g_rs_d;
   int rs_qkv;  // the q/k/v product the same way, with a rotary finish (k_qkv_split_fin)

@@ -157,13 +157,17 @@ Plan make_plan(const Dims &dm, int Breal, int max_pages, int lora_rank, int dept
     // all three for 9-16 rows with at least 512 row tiles (large fp8 24.6 -> 23.7) and for more
     // than 16 rows (beam 7.92 -> 6.74 with output and down, 6.8 -> 6.75 with q/k/v).
     {
-      const int U = p.nt == 1 ? 8 : 4;  // input blocks per batch of k_resid_split
+      // input blocks per batch of k_resid_split; with one column tile 16 where the input widths
+      // divide (ragged 32k 4.75 -> 4.69 ms per call against 8), else 8
+      int U = 4;
+      if (p.nt == 1) U = (dm.nq * dm.d / 32) % 16 == 0 && (dm.F / 32) % 16 == 0 ? 16 : 8;
       // bits: 1 down, 2 output, 4 q/k/v
       const int mask = p.nt >= 4 ? 7 : p.nt == 2 ? (dm.H / 16 >= 512 ? 7 : 5) : 1;
       if ((dm.nq * dm.d / 32) % U == 0 && (dm.F / 32) % U == 0) {
         // (8 row tiles per block measured faster than 16: 6.74 against 6.79 ms per call of the
         // 64-candidate beam)
         p.rs_wpb = 8;
+        p.rs_u = U;
         p.rs_d = mask & 1;
         p.rs_o = (mask >> 1) & 1;
         p.g_rs_o = resid_split_plan(dm.H, dm.nq * dm.d, p.rs_wpb, U);

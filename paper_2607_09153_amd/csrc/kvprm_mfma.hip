@@ -1406,12 +1406,19 @@ static hipError_t launch_split(const Plan &p, const Workspace &w, const GemvPlan
   a.tact = (const uint4 *)w.topd;
   a.tkb = tail.tkb;
   a.tstride = tail.tkb * p.nt * 64;
-  constexpr int U = 4, WPB = 8;  // (the plan's slices are whole batches of U input blocks; 2 U
-                                 // with one column tile)
-  if (p.rs_wpb != WPB) return hipErrorInvalidValue;
+  // (the plan's slices are whole batches of p.rs_u input blocks: U, or 8 or 16 with one column tile)
+  constexpr int U = 4, WPB = 8;
+  if (p.rs_wpb != WPB || (p.nt > 1 && p.rs_u != U)) return hipErrorInvalidValue;
   const dim3 grid((g.rows / 16 + WPB - 1) / WPB, g.ksplit + (tail.tkb > 0 ? 1 : 0));
   switch (p.nt) {
-    case 1: hipLaunchKernelGGL((k_resid_split<1, WPB, 2 * U>), grid, dim3(64 * WPB), 0, s, a); break;
+    case 1:
+      if (p.rs_u == 16)
+        hipLaunchKernelGGL((k_resid_split<1, WPB, 16>), grid, dim3(64 * WPB), 0, s, a);
+      else if (p.rs_u == 8)
+        hipLaunchKernelGGL((k_resid_split<1, WPB, 8>), grid, dim3(64 * WPB), 0, s, a);
+      else
+        return hipErrorInvalidValue;
+      break;
     case 2: hipLaunchKernelGGL((k_resid_split<2, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
     case 4: hipLaunchKernelGGL((k_resid_split<4, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
     case 6: hipLaunchKernelGGL((k_resid_split<6, WPB, U>), grid, dim3(64 * WPB), 0, s, a); break;
