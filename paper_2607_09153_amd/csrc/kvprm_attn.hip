@@ -256,25 +256,21 @@ __global__ __launch_bounds__(64 * kMaxKvHeadsMx) void k_attn_mx(AttnArgs a) {
   const int c = blockIdx.x, b = blockIdx.y;  // chunk, candidate
   const int j = threadIdx.x >> 6;
   const int nkv = a.nkv, g = a.g, nq = a.nq, kq = a.kq;
-  const int lane = threadIdx.x & 63;
-  const int n = lane & 15, cq = lane >> 4;
+  const int L = a.lengths[b];
+  const int npages = (L + kPage - 1) / kPage;
   int first = 0;
   for (int gi = 0; gi < a.gt.n; ++gi)
     if (b * kq >= a.gt.start[gi] && b * kq < a.gt.start[gi + 1]) first = a.gt.prefix_pages[gi];
   const int CP = 1 << a.gt.cshift_private;
   const int ncp = (first + (1 << a.gt.cshift_prefix) - 1) >> a.gt.cshift_prefix;  // prefix chunks
   const int p0 = first + c * CP;
-  // each wave reads the chunk's page ids itself into lane registers (lane i holds page i and,
-  // for fp8, its scales) and fetches them with scalar lane reads: no LDS, no barrier. The ids
-  // are loaded together with the candidate's length (the chunk's slots of the page-table row,
-  // within the row): entries at or past the candidate's last page are never used
-  const int pid_pre =
-      lane < CP && p0 + lane < a.max_pages ? a.page_table[(size_t)b * a.max_pages + p0 + lane] : 0;
-  const int L = a.lengths[b];
-  const int npages = (L + kPage - 1) / kPage;
   if (p0 >= npages) return;
   const int np = min(npages, p0 + CP) - p0;
-  const int ph_l = lane < np ? pid_pre : 0;
+  const int lane = threadIdx.x & 63;
+  const int n = lane & 15, cq = lane >> 4;
+  // each wave reads the chunk's page ids itself into lane registers (lane i holds page i and,
+  // for fp8, its scales) and fetches them with scalar lane reads: no LDS, no barrier
+  const int ph_l = lane < np ? a.page_table[(size_t)b * a.max_pages + p0 + lane] : 0;
   float ksc_l = 0.f, vsc_l = 0.f;
   if (KVT == 2 && lane < np) {
     ksc_l = a.ksc[(size_t)ph_l * nkv + j];
@@ -516,20 +512,6 @@ __global__ __launch_bounds__(NTHR) void k_merge_mx(AttnArgs a) {
   const int sub = t / D, dd = t - sub * D;
   const int j = h / a.g;
   const int kq = a.kq, cand = b / kq, tok = b - cand * kq;
-  // the partials of the row's first chunk slots, its first chunk states and its own first value
-  // are loaded together with the candidate's length (every slot up to nch is within the buffer;
-  // slots at or past the row's chunk count are never used)
-  const float *base = a.apart + ((size_t)b * a.nq + h) * a.nch * (D + 2);
-  float rv[R];
-#pragma unroll
-  for (int i = 0; i < R; ++i) {
-    const int c = sub + S * i;
-    rv[i] = c < a.nch ? base[(size_t)c * (D + 2) + dd] : 0.f;
-  }
-  const float m_pre = t < a.nch ? base[(size_t)t * (D + 2) + D] : 0.f;
-  const float l_pre = t < a.nch ? base[(size_t)t * (D + 2) + D + 1] : 0.f;
-  const size_t row0 = (size_t)cand * kq;
-  const float v0 = sub == 0 ? a.vself[(row0 * a.nkv + j) * D + dd] : 0.f;
   const int L = a.lengths[cand];
   const int npages = (L + kPage - 1) / kPage;
   int first = 0;
@@ -538,20 +520,23 @@ __global__ __launch_bounds__(NTHR) void k_merge_mx(AttnArgs a) {
   // shared-prefix chunks, then private chunks
   const int sp = a.gt.cshift_prefix, sv = a.gt.cshift_private;
   const int nc = ((first + (1 << sp) - 1) >> sp) + ((npages - first + (1 << sv) - 1) >> sv);
-  float mx = -INFINITY;
-  if (t < nc) {
-    m_s[t] = m_pre;
-    f_s[t] = l_pre;  // l_c for now
-    mx = m_pre;
+  const float *base = a.apart + ((size_t)b * a.nq + h) * a.nch * (D + 2);
+  float rv[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int c = sub + S * i;
+    rv[i] = c < nc ? base[(size_t)c * (D + 2) + dd] : 0.f;
   }
-  for (int c = t + NTHR; c < nc; c += NTHR) {
+  float mx = -INFINITY;
+  for (int c = t; c < nc; c += NTHR) {
     const float m = base[(size_t)c * (D + 2) + D];
     m_s[c] = m;
-    f_s[c] = base[(size_t)c * (D + 2) + D + 1];
+    f_s[c] = base[(size_t)c * (D + 2) + D + 1];  // l_c for now
     mx = fmaxf(mx, m);
   }
   // the verify tokens' own keys: this row's token attends to tokens 0..tok of its candidate
   // (rows cand kq + i); s_i = q . k_self_i / sqrt(D), one wave per key
+  const size_t row0 = (size_t)cand * kq;
   const float *qr = a.q + ((size_t)b * a.nq + h) * D;
   for (int i = wave; i <= tok; i += NW) {
     const float *kr = a.kself + ((row0 + i) * a.nkv + j) * D;
@@ -597,7 +582,7 @@ __global__ __launch_bounds__(NTHR) void k_merge_mx(AttnArgs a) {
   for (int i = 0; i <= tok; ++i) {
     const float es = expf(sself_s[i] - M);
     es_sum += es;
-    tot += es * (i == 0 ? v0 : a.vself[((row0 + i) * a.nkv + j) * D + dd]);
+    tot += es * a.vself[((row0 + i) * a.nkv + j) * D + dd];
   }
   const float ov = tot / (lsum + es_sum);
   if (a.lse && dd == 0) a.lse[(size_t)b * a.nq + h] = M + logf(lsum + es_sum);
