@@ -4,6 +4,8 @@ depends on the keys and values its page-table row names, in row order, and on no
 * Physical placement: moving every page of the pool to another physical slot (pools, fp8
   scales and page-table entries permuted together) leaves every score and logit bit for bit
   unchanged, with and without a shared-prefix group; unused pages hold NaN throughout.
+* The same for the KV Steering gradient (appendix, KV Steering algorithm), which is written per
+  physical page: after the move it equals the first gradient moved the same way, bit for bit.
 * Candidate independence: each candidate scored alone (a batch of one, same pools and row)
   equals its score inside the batch up to the summation order of the attention chunks, which
   the plan sizes from the batch.
@@ -18,7 +20,7 @@ import torch
 import synth
 from synth.device import DeviceWorkload
 
-from gpu_common import run_score
+from gpu_common import kv, run_score
 
 pytestmark = pytest.mark.gpu
 
@@ -30,29 +32,49 @@ def _say(*a):
     sys.stdout.flush()
 
 
-def _permute_pages(dw: DeviceWorkload, seed: int):
+def _moved(t: torch.Tensor, perm: torch.Tensor, layers: int, per_page: int) -> torch.Tensor:
+    """t ([layers][pages ...] in page-major order) with page p moved to slot perm[p]."""
+    raw = t.view(torch.uint8).view(layers, perm.numel(), -1)
+    assert raw.shape[2] == per_page
+    out = torch.empty_like(raw)
+    out[:, perm] = raw
+    return out.view(-1).view(t.dtype).view(t.shape)
+
+
+def _permute_pages(dw: DeviceWorkload, seed: int) -> torch.Tensor:
     """Move physical page p to slot perm[p] in both pools (and the fp8 scales), and rewrite
-    the page table to match."""
+    the page table to match; returns perm."""
     s, P = dw.w.shape, dw.w.num_pages
     perm = torch.from_numpy(np.random.default_rng(seed).permutation(P)).to(dw.device)
-
-    def moved(t: torch.Tensor, per_page: int) -> torch.Tensor:
-        raw = t.view(torch.uint8).view(s.num_layers, P, -1)
-        assert raw.shape[2] == per_page
-        out = torch.empty_like(raw)
-        out[:, perm] = raw
-        return out.view(-1).view(t.dtype).view(t.shape)
-
-    eb = dw.k_pool.element_size()
-    tile = s.num_kv_heads * s.tile_elems * eb
-    dw.k_pool = moved(dw.k_pool, tile)
-    dw.v_pool = moved(dw.v_pool, tile)
+    tile = s.num_kv_heads * s.tile_elems * dw.k_pool.element_size()
+    dw.k_pool = _moved(dw.k_pool, perm, s.num_layers, tile)
+    dw.v_pool = _moved(dw.v_pool, perm, s.num_layers, tile)
     if dw.k_scale is not None:
-        dw.k_scale = moved(dw.k_scale, s.num_kv_heads * 4)
-        dw.v_scale = moved(dw.v_scale, s.num_kv_heads * 4)
+        dw.k_scale = _moved(dw.k_scale, perm, s.num_layers, s.num_kv_heads * 4)
+        dw.v_scale = _moved(dw.v_scale, perm, s.num_layers, s.num_kv_heads * 4)
     pt = dw.page_table
     dw.page_table = torch.where(pt >= 0, perm[pt.clamp(min=0).long()].to(torch.int32), pt)
     assert not torch.equal(dw.page_table, pt)
+    return perm
+
+
+def _cache_gradient(dw: DeviceWorkload):
+    m = kv()
+    h = m.kvprm_create(dw.desc(m))
+    try:
+        batch = dw.batch(m)
+        n = m.kvprm_workspace_size_grad(h, batch)
+        ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        scores = torch.full((dw.w.batch,), float("nan"), device="cuda")
+        gk = torch.zeros(dw.k_pool.shape, dtype=torch.float32, device="cuda")
+        gv = torch.zeros(dw.v_pool.shape, dtype=torch.float32, device="cuda")
+        m.kvprm_score_grad(h, dw.cache(m), batch, dw.readout(m), ws.data_ptr(), n,
+                           scores.data_ptr(), gk.data_ptr(), gv.data_ptr(),
+                           torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+    finally:
+        m.kvprm_destroy(h)
+    return scores.cpu().numpy(), gk, gv
 
 
 @pytest.mark.parametrize("kv_dtype,groups", [("bf16", False), ("fp8", False), ("bf16", True)])
@@ -93,3 +115,20 @@ def test_candidate_scored_alone_matches_the_batch():
             assert abs(pb[0] - p[b]) <= 1e-5 and abs(zb[0] - z[b]) <= 5e-5
     finally:
         dw.page_table, dw.lengths, dw.w = pt_full, len_full, w_full
+
+
+def test_cache_gradient_moves_with_the_pages():
+    lengths = [3000, 17, 0, 1100, 64]
+    _say(f"case: cache gradient under a page move, lengths={lengths}")
+    w = synth.make_workload("custom", shape=SHAPE, lengths=lengths, seed=8300)
+    dw = DeviceWorkload(w, nan_unused_pages=True)
+    p0, gk0, gv0 = _cache_gradient(dw)
+    perm = _permute_pages(dw, seed=8301)
+    p1, gk1, gv1 = _cache_gradient(dw)
+    s = w.shape
+    per_page = s.num_kv_heads * s.tile_elems * 4
+    assert np.all(np.isfinite(p0)) and np.array_equal(p0, p1)
+    assert torch.count_nonzero(gk0) > 0 and torch.count_nonzero(gv0) > 0
+    assert torch.equal(_moved(gk0, perm, s.num_layers, per_page), gk1)
+    assert torch.equal(_moved(gv0, perm, s.num_layers, per_page), gv1)
+    _say(f"  P(+) = {np.round(p0, 5)}; gradients moved with their pages, bit for bit")
