@@ -646,14 +646,15 @@ hipError_t launch_attn_mx(const Dims &dm, const Plan &p, const Workspace &w, con
 #undef KVPRM_A
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !merge) return e;
-  // 256 threads per (row, q-head) when their registers hold every chunk of a row (256 / D
-  // subsets of 16 chunks: 32 at d_h = 128; the 7B batch of 16 3.566 -> 3.556 ms per call, the
-  // ragged 32k batch unchanged) or when there are more rows than four 512-thread blocks per
-  // compute unit hold (the 64-candidate beam: 1792 rows), so that they all run in one round;
-  // 512 otherwise (a row's chunks: its group prefix's and its private pages'; without host
-  // lengths, the plan's chunk slots)
+  // 256 threads per (row, q-head) when each of their 256 / D chunk subsets has at most 8 of the
+  // row's chunks (16 at d_h = 128: per merge 5.2 -> 5.1 us for the 7B batch of 16, 6.4 -> 5.9 us
+  // for the large fp8 batch; rows of 32 chunks, as in the ragged 32k batch, take 5.3 us against
+  // 5.0-5.1 with 512) or when there are more rows than four 512-thread blocks per compute unit
+  // hold (the 64-candidate beam: 1792 rows), so that they all run in one round; 512 otherwise
+  // (a row's chunks: its group prefix's and its private pages'; without host lengths, the
+  // plan's chunk slots)
   const int row_chunks = gt.private_chunks > 0 ? gt.prefix_chunks + gt.private_chunks : p.nch;
-  const bool small = p.B * dm.nq > 1024 || row_chunks <= (256 / dm.d) * 16;
+  const bool small = p.B * dm.nq > 1024 || row_chunks <= (256 / dm.d) * 8;
   const dim3 mgrid(p.B, dm.nq);
   if (dm.d == 64) {
     if (small) hipLaunchKernelGGL((k_merge_mx<64, 256>), mgrid, dim3(256), 0, s, a);
